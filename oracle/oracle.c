@@ -1,0 +1,153 @@
+/*
+ * Oracle for the sparse-embedding hot path -- TEST INFRASTRUCTURE ONLY.
+ * Plain single-threaded C; see oracle.h for the contract of each function and
+ * the passage of the paper it follows.  Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load this code.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Forward lookup, Sec. 4.1.1. */
+int64_t orc_gather(const float *W, int64_t V, int64_t D,
+                   const int32_t *ids, int64_t T, float *out) {
+    int64_t bad = 0;
+    for (int64_t t = 0; t < T; ++t) {
+        int64_t id = ids[t];
+        for (int64_t j = 0; j < D; ++j)
+            out[t * D + j] = (id >= 0 && id < V) ? W[id * D + j] : 0.0f;
+        if (id < 0 || id >= V) ++bad;
+    }
+    return bad;
+}
+
+/* A COO coordinate: (row index, token position). */
+typedef struct {
+    int64_t id;
+    int64_t t;
+} orc_coord;
+
+static int orc_coord_cmp(const void *a, const void *b) {
+    const orc_coord *x = (const orc_coord *)a, *y = (const orc_coord *)b;
+    if (x->id != y->id) return x->id < y->id ? -1 : 1;
+    if (x->t != y->t) return x->t < y->t ? -1 : 1;
+    return 0;
+}
+
+/* Exact widening of one gradient element to fp64. */
+static double orc_grad_elem(const void *grad, int32_t is_bf16, int64_t idx) {
+    if (is_bf16) {
+        uint32_t bits = (uint32_t)((const uint16_t *)grad)[idx] << 16;
+        float f;
+        memcpy(&f, &bits, sizeof f);
+        return (double)f;
+    }
+    return (double)((const float *)grad)[idx];
+}
+
+/* COALESCE and UNIQUE of Algorithm 1, Sec. 4.2.2: sort the coordinates by
+ * (index, position), then sum each run of equal index. */
+int64_t orc_coalesce(const int32_t *ids, int64_t T, const void *grad,
+                     int32_t grad_is_bf16, int64_t D, int64_t V,
+                     int32_t *uniq_ids, int32_t *seg_offsets, float *uniq_grad,
+                     double *sum_f64, double *absum, int64_t *n_invalid) {
+    orc_coord *c = (orc_coord *)malloc(sizeof(orc_coord) * (size_t)(T > 0 ? T : 1));
+    double *acc = (double *)malloc(sizeof(double) * (size_t)(D > 0 ? D : 1));
+    double *aab = (double *)malloc(sizeof(double) * (size_t)(D > 0 ? D : 1));
+    int64_t n = 0, bad = 0;
+    for (int64_t t = 0; t < T; ++t) {
+        if (ids[t] < 0 || ids[t] >= V) { ++bad; continue; }
+        c[n].id = ids[t];
+        c[n].t = t;
+        ++n;
+    }
+    qsort(c, (size_t)n, sizeof(orc_coord), orc_coord_cmp);
+
+    int64_t U = 0;
+    for (int64_t s = 0; s < n;) {
+        int64_t e = s;
+        while (e < n && c[e].id == c[s].id) ++e;
+        for (int64_t j = 0; j < D; ++j) { acc[j] = 0.0; aab[j] = 0.0; }
+        for (int64_t i = s; i < e; ++i) {
+            for (int64_t j = 0; j < D; ++j) {
+                double g = orc_grad_elem(grad, grad_is_bf16, c[i].t * D + j);
+                acc[j] += g;
+                aab[j] += fabs(g);
+            }
+        }
+        uniq_ids[U] = (int32_t)c[s].id;
+        seg_offsets[U] = (int32_t)s;
+        for (int64_t j = 0; j < D; ++j) {
+            uniq_grad[U * D + j] = (float)acc[j];
+            if (sum_f64) sum_f64[U * D + j] = acc[j];
+            if (absum) absum[U * D + j] = aab[j];
+        }
+        ++U;
+        s = e;
+    }
+    seg_offsets[U] = (int32_t)n;
+    if (n_invalid) *n_invalid = bad;
+    free(c);
+    free(acc);
+    free(aab);
+    return U;
+}
+
+/* Pack by owner for the gradient AlltoAll, Sec. 4.1.1 / 4.1.2. */
+int64_t orc_pack_by_owner(const int32_t *uniq_ids, const float *uniq_grad,
+                          int64_t U, int64_t D, const int32_t *row_owner,
+                          int64_t V, int32_t P, int32_t *send_ids,
+                          float *send_rows, int32_t *send_counts,
+                          int32_t *send_offsets) {
+    int64_t bad = 0;
+    int32_t *own = (int32_t *)malloc(sizeof(int32_t) * (size_t)(U > 0 ? U : 1));
+    int32_t *run = (int32_t *)calloc((size_t)P, sizeof(int32_t));
+    for (int32_t p = 0; p < P; ++p) send_counts[p] = 0;
+    for (int64_t k = 0; k < U; ++k) {
+        int64_t id = uniq_ids[k];
+        own[k] = -1;
+        if (id < 0 || id >= V || row_owner[id] < 0 || row_owner[id] >= P) { ++bad; continue; }
+        own[k] = row_owner[id];
+        send_counts[own[k]] += 1;
+    }
+    send_offsets[0] = 0;
+    for (int32_t p = 0; p < P; ++p) send_offsets[p + 1] = send_offsets[p] + send_counts[p];
+    for (int64_t k = 0; k < U; ++k) {
+        if (own[k] < 0) continue;
+        int64_t pos = (int64_t)send_offsets[own[k]] + run[own[k]]++;
+        send_ids[pos] = uniq_ids[k];
+        for (int64_t j = 0; j < D; ++j) send_rows[pos * D + j] = uniq_grad[k * D + j];
+    }
+    free(own);
+    free(run);
+    return bad;
+}
+
+/* Row-wise Adam, Sec. 4.1.1 and Sec. 5.7; Kingma & Ba, Algorithm 1. */
+int64_t orc_sparse_adam(float *W, float *m, float *v, int64_t V, int64_t D,
+                        const int32_t *row_ids, const float *rows,
+                        const int32_t *offsets, int32_t shard_begin,
+                        int32_t shard_end, double lr, double beta1,
+                        double beta2, double eps, int64_t step) {
+    const double bc1 = 1.0 - pow(beta1, (double)step);
+    const double bc2 = 1.0 - pow(beta2, (double)step);
+    int64_t bad = 0;
+    for (int64_t i = offsets[shard_begin]; i < offsets[shard_end]; ++i) {
+        int64_t r = row_ids[i];
+        if (r < 0 || r >= V) { ++bad; continue; }
+        for (int64_t j = 0; j < D; ++j) {
+            double g = rows[i * D + j];
+            double mm = beta1 * (double)m[r * D + j] + (1.0 - beta1) * g;
+            double vv = beta2 * (double)v[r * D + j] + (1.0 - beta2) * g * g;
+            double mhat = mm / bc1;
+            double vhat = vv / bc2;
+            double w = (double)W[r * D + j] - lr * mhat / (sqrt(vhat) + eps);
+            m[r * D + j] = (float)mm;
+            v[r * D + j] = (float)vv;
+            W[r * D + j] = (float)w;
+        }
+    }
+    return bad;
+}

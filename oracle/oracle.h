@@ -1,0 +1,78 @@
+/*
+ * Oracle for the sparse-embedding hot path -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, single-threaded CPU definition of what the hot path computes,
+ * used by the tests, the smoke check and the CPU-baseline leg of the benchmark
+ * to judge the GPU library.  Nothing in the product path may call it.  It
+ * shares no code, header, table or helper with the GPU library.
+ *
+ * Paper: EmbRace, "Accelerating Sparse Communication for Distributed Training
+ * of Deep Neural Networks" (ICPP '22).
+ *
+ * Floating point: sums and the optimizer arithmetic are carried in fp64 and
+ * rounded once to fp32 when stored (the paper fixes no precision).
+ * Integers (ids, counts, offsets) are exact.
+ */
+#ifndef EMB_ORACLE_H
+#define EMB_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Forward embedding lookup (Sec. 4.1.1: every process looks up its training
+ * data in the embedding table).  out[t][j] = W[ids[t]][j] for ids in [0, V);
+ * an id outside [0, V) yields a zero row.  Returns the number of such ids. */
+int64_t orc_gather(const float *W, int64_t V, int64_t D,
+                   const int32_t *ids, int64_t T, float *out);
+
+/* COALESCE + UNIQUE of Algorithm 1 (Sec. 4.2.2, "Coalescing Gradients"):
+ * the sparse COO gradient (Sec. 2.1) has one row per token; rows with the same
+ * index are summed into one.  Tokens with an id outside [0, V) are dropped.
+ *   uniq_ids[U]      the distinct ids, ascending
+ *   seg_offsets[U+1] exclusive scan of per-id multiplicities (seg_offsets[U]
+ *                    = number of valid tokens)
+ *   uniq_grad[U][D]  fp64 sum (tokens in increasing t) rounded once to fp32
+ *   sum_f64[U][D]    the same sums before rounding        (may be NULL)
+ *   absum[U][D]      sums of |G| (the error-bound scale)  (may be NULL)
+ * grad is fp32 [T][D] (grad_is_bf16 == 0) or bf16 bit patterns (uint16).
+ * Returns U; *n_invalid receives the number of dropped tokens (may be NULL). */
+int64_t orc_coalesce(const int32_t *ids, int64_t T, const void *grad,
+                     int32_t grad_is_bf16, int64_t D, int64_t V,
+                     int32_t *uniq_ids, int32_t *seg_offsets, float *uniq_grad,
+                     double *sum_f64, double *absum, int64_t *n_invalid);
+
+/* Pack the coalesced rows by owner shard (Sec. 4.1.1 / 4.1.2: the gradients
+ * are exchanged with an AlltoAll, each peer receiving the rows it owns).
+ *   owner(k)          = row_owner[uniq_ids[k]]
+ *   send_counts[p]    = #{k : owner(k) = p}
+ *   send_offsets[P+1] = exclusive scan of send_counts
+ *   rows are placed in owner-major order, ascending k inside an owner.
+ * Rows whose id is outside [0, V) or whose owner is outside [0, P) are not
+ * sent.  Returns the number of such rows. */
+int64_t orc_pack_by_owner(const int32_t *uniq_ids, const float *uniq_grad,
+                          int64_t U, int64_t D, const int32_t *row_owner,
+                          int64_t V, int32_t P, int32_t *send_ids,
+                          float *send_rows, int32_t *send_counts,
+                          int32_t *send_offsets);
+
+/* Row-wise (lazy) Adam on the received rows (Sec. 4.1.1: each process updates
+ * its embedding parameters with the new gradients; Sec. 5.7: Adam, with the
+ * global step counter passed in by the caller).  Kingma & Ba, Algorithm 1:
+ *   m <- b1 m + (1-b1) g ;  v <- b2 v + (1-b2) g^2
+ *   w <- w - lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
+ * applied to rows row_ids[i], i in [offsets[shard_begin], offsets[shard_end]).
+ * Rows not listed keep W, m, v unchanged.  Row ids outside [0, V) are skipped;
+ * returns their number. */
+int64_t orc_sparse_adam(float *W, float *m, float *v, int64_t V, int64_t D,
+                        const int32_t *row_ids, const float *rows,
+                        const int32_t *offsets, int32_t shard_begin,
+                        int32_t shard_end, double lr, double beta1,
+                        double beta2, double eps, int64_t step);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

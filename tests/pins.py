@@ -1,0 +1,298 @@
+"""Pins of the oracle against what the paper and the mathematics fix.
+
+Each `pin_*` function raises AssertionError when the oracle disagrees with an
+independent reference: a hand-worked fixture (tests/golden), brute force on
+tiny inputs (dense fp64 scatter-add over a V-row table, presence bitmaps,
+bincounts), invariants, special cases with exactly known results, closed forms
+of Adam, and PyTorch's dense Adam where lazy and dense Adam coincide.  The
+same functions run against mutated builds of the oracle (see
+test_oracle_mutations.py) to show that each planted mistake is caught.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+from golden import load as load_golden
+from workloads import gen
+
+ADAM = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8)
+
+
+def _rng_ids(seed, T, V):
+    return gen.uniform_ids(gen.stream_key(seed, 0, gen.PURPOSE_IDS), T, V)
+
+
+def _rng_normal(seed, n, sigma=1.0, purpose=gen.PURPOSE_GRADS):
+    return gen.normal_f32(gen.stream_key(seed, 0, purpose), n, sigma)
+
+
+# --------------------------------------------------------------------- gather
+def pin_gather():
+    """out[t] = W[ids[t]] (Sec. 4.1.1), checked against numpy fancy indexing."""
+    V, D, T = 37, 5, 200
+    W = _rng_normal(7, V * D).reshape(V, D)
+    ids = _rng_ids(8, T, V)
+    out, bad = oracle.gather(W, ids)
+    assert bad == 0
+    assert np.array_equal(out.view(np.uint32), W[ids].view(np.uint32))
+    ids2 = ids.copy()
+    ids2[[3, 50, 199]] = [-1, V, 1 << 30]
+    out2, bad2 = oracle.gather(W, ids2)
+    assert bad2 == 3
+    ok = np.ones(T, bool)
+    ok[[3, 50, 199]] = False
+    assert np.array_equal(out2[ok], W[ids2[ok]]) and not out2[~ok].any()
+
+
+# ------------------------------------------------------------------- coalesce
+def pin_coalesce_golden():
+    """Hand-worked example of COALESCE/UNIQUE (Algorithm 1, Sec. 4.2.2)."""
+    g = load_golden("coalesce_pack_worked.txt")
+    r = oracle.coalesce(np.array(g["ids"]), np.array(g["grad"], np.float32), g["V"])
+    assert r["uniq_ids"].tolist() == g["uniq_ids"]
+    assert r["seg_offsets"].tolist() == g["seg_offsets"]
+    assert r["uniq_grad"].tolist() == g["uniq_grad"]
+    assert r["absum"].tolist() == g["absum"]
+
+
+def pin_coalesce_bruteforce():
+    """Against a dense fp64 V x D scatter-add and a presence bitmap (tiny V)."""
+    seed = 100
+    for V in (1, 2, 8, 37, 64):
+        for T in (0, 1, 5, 100, 333):
+            for D in (1, 3, 8):
+                seed += 1
+                ids = _rng_ids(seed, T, V)
+                G = _rng_normal(seed, T * D).reshape(T, D)
+                dense = np.zeros((V, D), np.float64)
+                np.add.at(dense, ids, G.astype(np.float64))
+                dabs = np.zeros((V, D), np.float64)
+                np.add.at(dabs, ids, np.abs(G.astype(np.float64)))
+                present = np.zeros(V, bool)
+                present[ids] = True
+                cnt = np.bincount(ids, minlength=V)
+                r = oracle.coalesce(ids, G, V)
+                u = r["uniq_ids"]
+                assert r["U"] == int(present.sum())
+                assert np.array_equal(u, np.flatnonzero(present))
+                assert np.array_equal(np.diff(r["seg_offsets"]), cnt[u])
+                assert r["seg_offsets"][0] == 0 and r["seg_offsets"][-1] == T
+                # np.add.at accumulates in token order, as the oracle does: exact.
+                assert np.array_equal(r["sum_f64"], dense[u])
+                assert np.array_equal(r["absum"], dabs[u])
+                assert np.array_equal(r["uniq_grad"], dense[u].astype(np.float32))
+
+
+def pin_coalesce_invariants():
+    """Column sums preserved, multiplicities sum to T, ids strictly ascending (Zipf batch)."""
+    V, D, T = 5000, 16, 20000
+    ids = gen.zipf_ids(gen.stream_key(3, 0, gen.PURPOSE_IDS), T, V, 1.1)
+    G = _rng_normal(3, T * D).reshape(T, D)
+    r = oracle.coalesce(ids, G, V)
+    assert np.all(np.diff(r["uniq_ids"]) > 0)
+    assert set(r["uniq_ids"].tolist()) == set(np.unique(ids).tolist())
+    assert int(np.diff(r["seg_offsets"]).sum()) == T and np.all(np.diff(r["seg_offsets"]) > 0)
+    col = G.astype(np.float64).sum(axis=0)
+    got = r["sum_f64"].sum(axis=0)
+    assert np.all(np.abs(got - col) <= 1e-9 * np.abs(G).astype(np.float64).sum(axis=0))
+
+
+def pin_coalesce_special_cases():
+    """Cases whose fp32 result is known exactly."""
+    # all ids distinct: a pure permutation of the rows (bit copies)
+    V, D, T = 1000, 7, 300
+    perm = np.random.default_rng(5).permutation(V)[:T].astype(np.int32)
+    G = _rng_normal(11, T * D).reshape(T, D)
+    r = oracle.coalesce(perm, G, V)
+    order = np.argsort(perm, kind="stable")
+    assert np.array_equal(r["uniq_ids"], perm[order])
+    assert np.array_equal(r["uniq_grad"].view(np.uint32), G[order].view(np.uint32))
+    # every id exactly twice: one fp32 addition, correctly rounded, a + b in token order
+    half = perm[:150]
+    ids2 = np.concatenate([half, half[::-1]])
+    G2 = _rng_normal(12, 300 * D).reshape(300, D)
+    r2 = oracle.coalesce(ids2, G2, V)
+    first = {int(i): t for t, i in enumerate(ids2[:150])}
+    second = {int(i): 150 + t for t, i in enumerate(ids2[150:])}
+    exp = np.stack([G2[first[int(i)]] + G2[second[int(i)]] for i in r2["uniq_ids"]])
+    assert np.array_equal(r2["uniq_grad"].view(np.uint32), exp.view(np.uint32))
+    # bf16 gradients are widened exactly: same as the fp32 path on the widened values
+    ids3 = gen.zipf_ids(gen.stream_key(13, 0, gen.PURPOSE_IDS), 500, 300, 1.0)
+    h = gen.bf16_round(_rng_normal(13, 500 * D, 0.01)).reshape(500, D)
+    rb = oracle.coalesce(ids3, h, 300, grad_is_bf16=True)
+    rf = oracle.coalesce(ids3, gen.bf16_bits_to_f32(h).reshape(500, D), 300)
+    assert np.array_equal(rb["uniq_grad"], rf["uniq_grad"]) and np.array_equal(rb["uniq_ids"], rf["uniq_ids"])
+    # empty batch
+    r0 = oracle.coalesce(np.zeros(0, np.int32), np.zeros((0, 4), np.float32), 10)
+    assert r0["U"] == 0 and r0["seg_offsets"].tolist() == [0]
+    # out-of-range ids are dropped: same as coalescing the valid tokens alone
+    ids4 = ids3.copy()
+    ids4[[0, 10, 499]] = [-5, 300, 1 << 31 - 1]
+    G4 = gen.bf16_bits_to_f32(h).reshape(500, D)
+    r4 = oracle.coalesce(ids4, G4, 300)
+    keep = (ids4 >= 0) & (ids4 < 300)
+    r5 = oracle.coalesce(ids4[keep], G4[keep], 300)
+    assert r4["n_invalid"] == 3
+    assert np.array_equal(r4["uniq_ids"], r5["uniq_ids"]) and np.array_equal(r4["seg_offsets"], r5["seg_offsets"])
+    assert np.array_equal(r4["uniq_grad"], r5["uniq_grad"])
+
+
+# ----------------------------------------------------------------------- pack
+def pin_pack_golden():
+    g = load_golden("coalesce_pack_worked.txt")
+    V, P = g["V"], g["P"]
+    r = oracle.pack_by_owner(np.array(g["uniq_ids"]), np.array(g["uniq_grad"], np.float32),
+                             gen.owner_mod(V, P), P)
+    assert r["send_ids"].tolist() == g["send_ids"]
+    assert r["send_rows"].tolist() == g["send_rows"]
+    assert r["send_counts"].tolist() == g["send_counts"]
+    assert r["send_offsets"].tolist() == g["send_offsets"]
+
+
+def check_pack_result(r, uniq_ids, uniq_grad, row_owner, P):
+    """Invariants of an owner-major stable pack (shared by oracle pins and GPU tests)."""
+    own = row_owner[uniq_ids]
+    counts = np.bincount(own, minlength=P)
+    assert np.array_equal(r["send_counts"], counts)
+    assert np.array_equal(r["send_offsets"], np.concatenate([[0], np.cumsum(counts)]))
+    pos = {int(i): k for k, i in enumerate(uniq_ids)}
+    for p in range(P):
+        a, b = r["send_offsets"][p], r["send_offsets"][p + 1]
+        blk = r["send_ids"][a:b]
+        assert np.all(row_owner[blk] == p)
+        assert np.all(np.diff(blk) > 0)
+    assert sorted(r["send_ids"].tolist()) == sorted(uniq_ids.tolist())
+    src = np.array([pos[int(i)] for i in r["send_ids"]], dtype=np.int64)
+    assert np.array_equal(r["send_rows"].view(np.uint32), uniq_grad[src].view(np.uint32))
+
+
+def pin_pack_invariants():
+    for seed, (V, D, U, P, rule) in enumerate([(1000, 4, 300, 7, "mod"), (1000, 3, 999, 16, "range"),
+                                               (50, 2, 50, 1, "mod"), (4096, 5, 1000, 1024, "rand"),
+                                               (10, 1, 0, 3, "mod")]):
+        uid = np.sort(np.random.default_rng(seed).permutation(V)[:U]).astype(np.int32)
+        rows = _rng_normal(200 + seed, U * D).reshape(U, D)
+        if rule == "mod":
+            own = gen.owner_mod(V, P)
+        elif rule == "range":
+            own = gen.owner_range(V, P)
+        else:
+            own = np.random.default_rng(99).integers(0, P, V).astype(np.int32)
+        r = oracle.pack_by_owner(uid, rows, own, P)
+        assert r["n_dropped"] == 0
+        check_pack_result(r, uid, rows, own, P)
+        if P == 1 or rule == "range":  # owner-major order is already ascending-id order
+            assert np.array_equal(r["send_ids"], uid)
+            assert np.array_equal(r["send_rows"].view(np.uint32), rows.view(np.uint32))
+    # rows whose owner is out of range are not sent
+    V, P = 20, 4
+    own = gen.owner_mod(V, P)
+    own[[3, 7]] = [4, -1]
+    uid = np.arange(0, 20, 2, dtype=np.int32)
+    rows = _rng_normal(5, 10 * 2).reshape(10, 2)
+    r = oracle.pack_by_owner(uid, rows, own, P)
+    assert r["n_dropped"] == 0  # 3 and 7 are odd: not in uid
+    uid2 = np.arange(0, 20, 1, dtype=np.int32)
+    r2 = oracle.pack_by_owner(uid2, _rng_normal(6, 40).reshape(20, 2), own, P)
+    assert r2["n_dropped"] == 2 and r2["send_offsets"][-1] == 18
+    assert 3 not in r2["send_ids"].tolist() and 7 not in r2["send_ids"].tolist()
+
+
+# ----------------------------------------------------------------------- adam
+def _adam_tables(V, D, seed):
+    W = _rng_normal(seed, V * D, purpose=gen.PURPOSE_WEIGHTS).reshape(V, D)
+    return W, np.zeros((V, D), np.float32), np.zeros((V, D), np.float32)
+
+
+def pin_adam_golden():
+    """Hand-worked first step from zero moments (Kingma & Ba Algorithm 1, t = 1)."""
+    g = load_golden("adam_first_step.txt")
+    n = len(g["g"])
+    W = np.array(g["w0"], np.float32).reshape(n, 1).copy()
+    m = np.zeros((n, 1), np.float32)
+    v = np.zeros((n, 1), np.float32)
+    rows = np.array(g["g"], np.float32).reshape(n, 1)
+    oracle.sparse_adam(W, m, v, np.arange(n, dtype=np.int32), rows, np.array([0, n], np.int32), 0, 1,
+                       g["lr"], g["beta1"], g["beta2"], g["eps"], 1)
+    np.testing.assert_allclose(W[:, 0], np.array(g["w1"], np.float32), rtol=2e-7, atol=0)
+    np.testing.assert_allclose(m[:, 0], np.array(g["m1"], np.float32), rtol=2e-7, atol=0)
+    np.testing.assert_allclose(v[:, 0], np.array(g["v1"], np.float32), rtol=2e-7, atol=0)
+
+
+def pin_adam_closed_forms():
+    """Constant gradient: w_t = w_0 - t lr g/(|g|+eps).  Rows touched only at
+    steps 1 and 3 (lazy): m_hat_3 = (1+b1) g/(1+b1+b1^2), v_hat_3 =
+    (1+b2) g^2/(1+b2+b2^2).  Untouched rows stay bit-identical."""
+    lr, b1, b2, eps = ADAM["lr"], ADAM["beta1"], ADAM["beta2"], ADAM["eps"]
+    V, D = 12, 6
+    W, m, v = _adam_tables(V, D, 21)
+    W0 = W.copy()
+    rows_const = np.array([1, 4, 5], np.int32)
+    g = np.array([[0.3, -2.0, 1e-3, 5e-9, 1.0, -0.7]], np.float32).repeat(3, axis=0)
+    g[1] *= -3
+    g[2] *= 0.01
+    lazy_row = np.array([9], np.int32)
+    gl = np.array([[0.2, -0.4, 1e-8, 3.0, -1e-6, 0.05]], np.float32)
+    for t in range(1, 6):
+        oracle.sparse_adam(W, m, v, rows_const, g, np.array([0, 3], np.int32), 0, 1, lr, b1, b2, eps, t)
+        if t in (1, 3):
+            oracle.sparse_adam(W, m, v, lazy_row, gl, np.array([0, 1], np.int32), 0, 1, lr, b1, b2, eps, t)
+        if t == 3:
+            W_lazy3 = W[9].copy()
+    g64 = g.astype(np.float64)
+    exp = W0[rows_const].astype(np.float64) - 5 * lr * g64 / (np.abs(g64) + eps)
+    np.testing.assert_allclose(W[rows_const], exp, rtol=0, atol=4e-7 * np.abs(exp).max())
+    # lazy closed form at step 3
+    gl64 = gl[0].astype(np.float64)
+    w1 = W0[9].astype(np.float64) - lr * gl64 / (np.abs(gl64) + eps)
+    mh = (1 + b1) * gl64 / (1 + b1 + b1 * b1)
+    vh = (1 + b2) * gl64 * gl64 / (1 + b2 + b2 * b2)
+    w3 = w1 - lr * mh / (np.sqrt(vh) + eps)
+    np.testing.assert_allclose(W_lazy3, w3, rtol=0, atol=4e-7 * np.abs(w3).max())
+    untouched = np.setdiff1d(np.arange(V), np.concatenate([rows_const, lazy_row]))
+    assert np.array_equal(W[untouched].view(np.uint32), W0[untouched].view(np.uint32))
+    assert not m[untouched].any() and not v[untouched].any()
+
+
+def pin_adam_vs_torch_dense():
+    """When every row is touched at every step, lazy Adam is dense Adam: compare
+    with torch.optim.Adam (fp64) over 6 steps, gradients spanning 1e-9 .. 1."""
+    import torch
+    V, D, steps = 10, 8, 6
+    W, m, v = _adam_tables(V, D, 31)
+    p = torch.nn.Parameter(torch.tensor(W.astype(np.float64)))
+    opt = torch.optim.Adam([p], lr=ADAM["lr"], betas=(ADAM["beta1"], ADAM["beta2"]), eps=ADAM["eps"])
+    scale = np.logspace(-9, 0, V * D).reshape(V, D)
+    for t in range(1, steps + 1):
+        g = (_rng_normal(40 + t, V * D).reshape(V, D) * scale).astype(np.float32)
+        oracle.sparse_adam(W, m, v, np.arange(V, dtype=np.int32), g, np.array([0, V], np.int32), 0, 1,
+                           ADAM["lr"], ADAM["beta1"], ADAM["beta2"], ADAM["eps"], t)
+        p.grad = torch.tensor(g.astype(np.float64))
+        opt.step()
+    ref = p.detach().numpy()
+    st = opt.state[p]
+    np.testing.assert_allclose(W, ref, rtol=0, atol=2e-6 * np.abs(ref).max())
+    # m can cancel across steps: measure its error against the gradient scale.
+    mref = st["exp_avg"].numpy()
+    assert np.all(np.abs(m - mref) <= 2e-6 * (np.abs(mref) + 0.1 * scale))
+    np.testing.assert_allclose(v, st["exp_avg_sq"].numpy(), rtol=2e-6, atol=1e-38)
+
+
+def pin_adam_shard_ranges():
+    """Updating shards one by one equals one update over all of them; a prior
+    and a delayed part applied with the same step equal one apply on the union
+    (the step counter of Sec. 5.7 advances once per iteration)."""
+    V, D, P = 40, 3, 4
+    Wa, ma, va = _adam_tables(V, D, 51)
+    Wb, mb, vb = Wa.copy(), ma.copy(), va.copy()
+    ids = np.array([1, 5, 9, 13, 2, 6, 30, 3, 7, 11, 39], np.int32)
+    offs = np.array([0, 4, 7, 7, 11], np.int32)  # shard 2 empty
+    rows = _rng_normal(52, ids.size * D).reshape(ids.size, D)
+    for t in (1, 2):
+        oracle.sparse_adam(Wa, ma, va, ids, rows, offs, 0, P, ADAM["lr"], ADAM["beta1"], ADAM["beta2"], ADAM["eps"], t)
+        for s in range(P):
+            oracle.sparse_adam(Wb, mb, vb, ids, rows, offs, s, s + 1, ADAM["lr"], ADAM["beta1"], ADAM["beta2"],
+                               ADAM["eps"], t)
+    for a, b in ((Wa, Wb), (ma, mb), (va, vb)):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))

@@ -1,0 +1,59 @@
+"""Plant plausible mistakes in copies of the oracle (on the CPU) and check that
+the pins catch every one of them: a dropped term, a wrong sign, a wrong or
+transposed index, a wrong order, an off-by-one offset, and the usual Adam slips
+(no bias correction, eps inside the square root, the other eps placement, a
+swapped beta).  Each mutant is compiled with gcc into a temporary directory."""
+import os
+
+import pytest
+
+import oracle
+import pins
+
+SRC = open(oracle.SRC_PATH).read()
+
+MUTANTS = {
+    "gather_reversed_columns": ("W[id * D + j]", "W[id * D + (D - 1 - j)]", ["pin_gather"]),
+    "coalesce_dropped_first_term": ("for (int64_t i = s; i < e; ++i) {", "for (int64_t i = s + 1; i < e; ++i) {",
+                                    ["pin_coalesce_golden", "pin_coalesce_bruteforce"]),
+    "coalesce_wrong_sign": ("acc[j] += g;", "acc[j] -= g;", ["pin_coalesce_golden", "pin_coalesce_bruteforce"]),
+    "coalesce_index_by_id_not_token": ("c[i].t * D + j", "c[i].id * D + j",
+                                       ["pin_coalesce_golden", "pin_coalesce_bruteforce"]),
+    "coalesce_descending_ids": ("return x->id < y->id ? -1 : 1;", "return x->id < y->id ? 1 : -1;",
+                                ["pin_coalesce_golden", "pin_coalesce_invariants"]),
+    "coalesce_offsets_at_segment_end": ("seg_offsets[U] = (int32_t)s;", "seg_offsets[U] = (int32_t)e;",
+                                        ["pin_coalesce_golden", "pin_coalesce_bruteforce"]),
+    "pack_descending_inside_owner": ("int64_t pos = (int64_t)send_offsets[own[k]] + run[own[k]]++;",
+                                     "int64_t pos = (int64_t)send_offsets[own[k] + 1] - 1 - run[own[k]]++;",
+                                     ["pin_pack_golden", "pin_pack_invariants"]),
+    "pack_owner_shifted": ("own[k] = row_owner[id];", "own[k] = (row_owner[id] + 1) % P;",
+                           ["pin_pack_golden", "pin_pack_invariants"]),
+    "adam_no_bias_correction": ("double mhat = mm / bc1;", "double mhat = mm;",
+                                ["pin_adam_golden", "pin_adam_closed_forms", "pin_adam_vs_torch_dense"]),
+    "adam_eps_inside_sqrt": ("(sqrt(vhat) + eps)", "sqrt(vhat + eps)",
+                             ["pin_adam_golden", "pin_adam_closed_forms", "pin_adam_vs_torch_dense"]),
+    "adam_eps_on_uncorrected_v": ("lr * mhat / (sqrt(vhat) + eps)", "lr * sqrt(bc2) / bc1 * mm / (sqrt(vv) + eps)",
+                                  ["pin_adam_closed_forms", "pin_adam_vs_torch_dense"]),
+    "adam_swapped_beta": ("(1.0 - beta1) * g;", "(1.0 - beta2) * g;",
+                          ["pin_adam_golden", "pin_adam_closed_forms", "pin_adam_vs_torch_dense"]),
+    "adam_step_off_by_one": ("pow(beta1, (double)step)", "pow(beta1, (double)(step + 1))",
+                             ["pin_adam_golden", "pin_adam_closed_forms", "pin_adam_vs_torch_dense"]),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    find, repl, which = MUTANTS[name]
+    assert SRC.count(find) == 1, f"mutation site not unique: {find!r}"
+    lib = oracle.build_variant(SRC.replace(find, repl), os.path.join(str(tmp_path), f"lib_{name}.so"))
+    caught = []
+    try:
+        oracle.use_library(lib)
+        for pin in which:
+            try:
+                getattr(pins, pin)()
+            except AssertionError:
+                caught.append(pin)
+    finally:
+        oracle.use_library(None)
+    assert caught, f"mutant {name} survived pins {which}"
