@@ -1,0 +1,164 @@
+/*
+ * emb.h -- C ABI of the sparse-embedding hot path on one MI355X (gfx950).
+ *
+ * The path is one GPU's share of sparse embedding-table training in EmbRace
+ * (Li et al., "EmbRace: Accelerating Sparse Communication for Distributed
+ * Training of Deep Neural Networks", ICPP '22):
+ *
+ *   emb_gather             forward lookup of the batch's rows       (Sec. 4.1.1)
+ *   emb_grad_coalesce      COALESCE + UNIQUE of the sparse gradient (Sec. 4.2.2,
+ *                          Algorithm 1)
+ *   emb_pack_by_owner      per-owner send buffers, counts, offsets  (Sec. 4.1.1,
+ *                          Sec. 4.1.2: the payload of the gradient AlltoAll)
+ *   emb_sparse_adam_apply  row-wise Adam on the rows a shard owns   (Sec. 4.1.1,
+ *                          Sec. 5.7)
+ *
+ * Conventions for every call:
+ *  - Array arguments are DEVICE pointers (memory of the current HIP device);
+ *    scalars are passed by value.  The caller allocates and owns every buffer;
+ *    the library never allocates, frees or keeps a pointer after returning.
+ *  - Tables and gradient rows are dense row-major [rows][D] arrays.  Ids are
+ *    int32 row indices in [0, V).
+ *  - `stream` is a hipStream_t (NULL: the null stream).  Calls only enqueue
+ *    work on it and return without synchronising; outputs are valid once the
+ *    stream has reached that point.  Data-dependent sizes (the unique count,
+ *    per-owner counts) stay in device memory: later calls read them there, and
+ *    grids are sized by the caller's capacity arguments.
+ *  - The return value is a host status (EMB_OK or an EMB_ERR_* code).  Argument
+ *    errors are found on the host before anything is enqueued.  Errors that
+ *    depend on device data (an id or owner out of range) are OR-ed as
+ *    EMB_DEV_* flags into *dev_status (an optional int32 in device memory,
+ *    NULL to ignore); the caller clears it and reads it after synchronising.
+ *  - Calls are reentrant; concurrent calls need distinct outputs and
+ *    workspaces.
+ */
+#ifndef EMB_H
+#define EMB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EMB_ABI_VERSION 1
+
+/* host status codes */
+#define EMB_OK 0
+#define EMB_ERR_INVALID_ARG 1 /* null pointer, size or range out of bounds */
+#define EMB_ERR_WORKSPACE 2   /* workspace smaller than the size query */
+#define EMB_ERR_LAUNCH 3      /* the HIP runtime refused a launch */
+#define EMB_ERR_UNSUPPORTED 4 /* valid but not supported by this build */
+
+/* gradient element types */
+#define EMB_F32 0  /* IEEE binary32 */
+#define EMB_BF16 1 /* bfloat16 (upper half of a binary32), widened exactly */
+
+/* device status flags */
+#define EMB_DEV_ID_OUT_OF_RANGE 1    /* a token or row id was outside [0, V) */
+#define EMB_DEV_OWNER_OUT_OF_RANGE 2 /* row_owner[id] was outside [0, P) */
+
+int emb_abi_version(void);
+const char *emb_status_string(int status);
+
+/*
+ * Forward lookup (Sec. 4.1.1: each process looks up its batch in the
+ * embedding table).  out[t][j] = table[ids[t]][j] for t < T, j < D: a bit copy.
+ *   table [V][D] fp32, ids [T] int32, out [T][D] fp32.
+ * An id outside [0, V) yields a zero row and sets EMB_DEV_ID_OUT_OF_RANGE.
+ * T == 0 is a no-op.  Requires 1 <= V < 2^31, D >= 1, T >= 0.
+ */
+int emb_gather(const float *table, int64_t V, int32_t D, const int32_t *ids,
+               int32_t T, float *out, int32_t *dev_status, void *stream);
+
+/*
+ * COALESCE and UNIQUE of Algorithm 1 (Sec. 4.2.2, "Coalescing Gradients"):
+ * the embedding gradient is a sparse COO tensor (Sec. 2.1) with one row per
+ * token; rows with the same index are summed into one.
+ *   ids [T] int32, grad [T][D] fp32 (EMB_F32) or bf16 (EMB_BF16).
+ * Outputs, sized by the capacity T (the unique count U <= T):
+ *   uniq_ids    [T]     the U distinct valid ids, ascending
+ *   seg_offsets [T + 1] seg_offsets[k] = number of valid tokens whose id is
+ *                       below uniq_ids[k]; seg_offsets[U] = valid tokens
+ *   uniq_grad   [T][D]  fp32 per-id sums of the gradient rows
+ *   num_unique  [1]     U
+ * Entries past U are left unspecified.  Tokens with an id outside [0, V) are
+ * left out and set EMB_DEV_ID_OUT_OF_RANGE.
+ * Sums are accumulated in fp32 in a fixed order that depends only on the ids
+ * (sorted position order, in chunks of 32 tokens, then an ordered combine of
+ * the chunk partials): results are bitwise reproducible run to run.
+ * workspace: device memory of at least
+ * emb_grad_coalesce_workspace_bytes(T, V, D, grad_dtype) bytes, 256-byte
+ * aligned; its contents on entry do not matter.
+ * Requires 1 <= V < 2^31, D >= 1, T >= 0.  grad rows must be 4-byte aligned.
+ */
+size_t emb_grad_coalesce_workspace_bytes(int32_t T, int64_t V, int32_t D,
+                                         int32_t grad_dtype);
+int emb_grad_coalesce(const int32_t *ids, int32_t T, const void *grad,
+                      int32_t grad_dtype, int32_t D, int64_t V,
+                      int32_t *uniq_ids, int32_t *seg_offsets,
+                      float *uniq_grad, int32_t *num_unique, void *workspace,
+                      size_t workspace_bytes, int32_t *dev_status,
+                      void *stream);
+
+/*
+ * Pack the coalesced rows into per-owner send buffers (Sec. 4.1.1 / 4.1.2: the
+ * sparse gradients are exchanged with an AlltoAll; each of the P shards
+ * receives the rows it owns).  The P shards are partitions of one table on
+ * this device.
+ *   uniq_ids [cap_rows], uniq_grad [cap_rows][D], num_unique [1]: the rows
+ *   k < *num_unique (read on the device; must be <= cap_rows).
+ *   row_owner [V] int32: owner shard of each table row, in [0, P).
+ * Outputs:
+ *   send_counts  [P]     rows per owner
+ *   send_offsets [P + 1] exclusive scan of send_counts
+ *   send_ids     [cap_rows], send_rows [cap_rows][D]: owner p's rows at
+ *   [send_offsets[p], send_offsets[p + 1]), in the order of the input (so
+ *   ascending id when the input is emb_grad_coalesce output); rows are bit
+ *   copies.
+ * A row whose id is outside [0, V) or whose owner is outside [0, P) is not
+ * sent and sets EMB_DEV_ID_OUT_OF_RANGE / EMB_DEV_OWNER_OUT_OF_RANGE.
+ * workspace: at least emb_pack_by_owner_workspace_bytes(cap_rows, P) bytes.
+ * Requires 1 <= P <= 1024, cap_rows >= 0, D >= 1, 1 <= V < 2^31.
+ */
+size_t emb_pack_by_owner_workspace_bytes(int32_t cap_rows, int32_t P);
+int emb_pack_by_owner(const int32_t *uniq_ids, const float *uniq_grad,
+                      const int32_t *num_unique, int32_t cap_rows, int32_t D,
+                      const int32_t *row_owner, int64_t V, int32_t P,
+                      int32_t *send_ids, float *send_rows,
+                      int32_t *send_counts, int32_t *send_offsets,
+                      void *workspace, size_t workspace_bytes,
+                      int32_t *dev_status, void *stream);
+
+/*
+ * Row-wise (lazy) Adam on received rows (Sec. 4.1.1: each process updates its
+ * embedding rows with the exchanged gradients; Sec. 5.7: Adam with a global
+ * step counter that the caller owns and advances once per iteration).
+ * Kingma & Ba, Algorithm 1, for each listed row r and column j:
+ *   m <- b1 m + (1 - b1) g ;  v <- b2 v + (1 - b2) g^2
+ *   w <- w - lr * (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps)
+ * computed in fp32 (bias corrections formed in fp64 on the host).
+ *   table, exp_avg, exp_avg_sq [V][D] fp32, updated in place.
+ *   row_ids [cap_rows], rows [cap_rows][D]: the rows i in
+ *   [offsets[shard_begin], offsets[shard_end]) are applied, with offsets
+ *   [P + 1] in device memory (the send_offsets of emb_pack_by_owner);
+ *   that range must lie within [0, cap_rows).
+ * Rows not listed keep table, exp_avg and exp_avg_sq bit-unchanged.  Listed
+ * row ids must be distinct (true of pack output); an id outside [0, V) is
+ * skipped and sets EMB_DEV_ID_OUT_OF_RANGE.
+ * Requires 1 <= P <= 1024, 0 <= shard_begin <= shard_end <= P, step >= 1,
+ * 0 <= beta1, beta2 < 1, eps >= 0.
+ */
+int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
+                          int64_t V, int32_t D, const int32_t *row_ids,
+                          const float *rows, const int32_t *offsets, int32_t P,
+                          int32_t shard_begin, int32_t shard_end,
+                          int32_t cap_rows, double lr, double beta1,
+                          double beta2, double eps, int64_t step,
+                          int32_t *dev_status, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EMB_H */

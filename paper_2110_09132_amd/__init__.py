@@ -1,0 +1,193 @@
+"""Python binding of libemb (the C ABI in include/emb.h).
+
+Argument marshalling only: every step of the hot path runs in the HIP kernels
+of libemb.so.  PyTorch supplies device memory and the stream
+(torch.cuda.current_stream()).  There is no fallback: if the library is not
+built, importing this package raises.
+
+torch is imported before the library is loaded so that the process maps a
+single HIP runtime (the one torch ships), which the library then shares.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # noqa: F401  (must be loaded before libemb.so; see module docstring)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libemb.so")
+
+EMB_OK = 0
+EMB_ERR_INVALID_ARG = 1
+EMB_ERR_WORKSPACE = 2
+EMB_ERR_LAUNCH = 3
+EMB_ERR_UNSUPPORTED = 4
+EMB_F32 = 0
+EMB_BF16 = 1
+EMB_DEV_ID_OUT_OF_RANGE = 1
+EMB_DEV_OWNER_OUT_OF_RANGE = 2
+
+# (name, restype, argtypes) of every symbol include/emb.h declares.
+_P, _I32, _I64, _SZ, _D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_double
+SIGNATURES = {
+    "emb_abi_version": (ctypes.c_int, []),
+    "emb_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "emb_gather": (ctypes.c_int, [_P, _I64, _I32, _P, _I32, _P, _P, _P]),
+    "emb_grad_coalesce_workspace_bytes": (_SZ, [_I32, _I64, _I32, _I32]),
+    "emb_grad_coalesce": (ctypes.c_int, [_P, _I32, _P, _I32, _I32, _I64, _P, _P, _P, _P, _P, _SZ, _P, _P]),
+    "emb_pack_by_owner_workspace_bytes": (_SZ, [_I32, _I32]),
+    "emb_pack_by_owner": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _P, _P, _SZ, _P, _P]),
+    "emb_sparse_adam_apply": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _P, _P, _P, _I32, _I32, _I32, _I32,
+                                             _D, _D, _D, _D, _I64, _P, _P]),
+}
+
+
+class EmbError(RuntimeError):
+    pass
+
+
+def _load_library():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run paper_2110_09132_amd/build.py (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load_library()
+
+
+def abi_version() -> int:
+    return lib.emb_abi_version()
+
+
+def status_string(status: int) -> str:
+    return lib.emb_status_string(status).decode()
+
+
+def _check(status: int, what: str):
+    if status != EMB_OK:
+        raise EmbError(f"{what}: {status_string(status)} ({status})")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return EMB_F32
+    if t.dtype == torch.bfloat16:
+        return EMB_BF16
+    raise EmbError(f"gradient dtype {t.dtype} is not float32 or bfloat16")
+
+
+def _need(t, dtype, what):
+    if t.dtype != dtype or not t.is_cuda or not t.is_contiguous():
+        raise EmbError(f"{what} must be a contiguous {dtype} CUDA tensor (got {t.dtype}, {t.device})")
+
+
+def new_status(device=None):
+    """A zeroed device status word for the dev_status argument."""
+    return torch.zeros(1, dtype=torch.int32, device=device or "cuda")
+
+
+def gather(table, ids, out=None, dev_status=None, stream=None):
+    """out[t] = table[ids[t]] (emb_gather)."""
+    _need(table, torch.float32, "table")
+    _need(ids, torch.int32, "ids")
+    V, D = table.shape
+    T = ids.numel()
+    if out is None:
+        out = torch.empty((T, D), dtype=torch.float32, device=table.device)
+    _check(lib.emb_gather(_ptr(table), V, D, _ptr(ids), T, _ptr(out), _ptr(dev_status), _stream(stream)),
+           "emb_gather")
+    return out
+
+
+def grad_coalesce_workspace_bytes(T, V, D, grad_dtype=EMB_F32) -> int:
+    return int(lib.emb_grad_coalesce_workspace_bytes(T, V, D, grad_dtype))
+
+
+def new_workspace(nbytes, device=None):
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device or "cuda")
+
+
+def grad_coalesce(ids, grad, V, out=None, workspace=None, dev_status=None, stream=None):
+    """COALESCE + UNIQUE (emb_grad_coalesce).
+
+    Returns (uniq_ids [T], seg_offsets [T+1], uniq_grad [T, D], num_unique [1]); the
+    first num_unique entries are meaningful.  `out` may pass those four tensors in.
+    """
+    _need(ids, torch.int32, "ids")
+    code = _dtype_code(grad)
+    if not grad.is_cuda or not grad.is_contiguous():
+        raise EmbError("grad must be a contiguous CUDA tensor")
+    T = ids.numel()
+    D = grad.shape[1]
+    dev = ids.device
+    if out is None:
+        out = (torch.empty(T, dtype=torch.int32, device=dev), torch.empty(T + 1, dtype=torch.int32, device=dev),
+               torch.empty((T, D), dtype=torch.float32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
+    uniq_ids, seg_offsets, uniq_grad, num_unique = out
+    nbytes = grad_coalesce_workspace_bytes(T, V, D, code)
+    if workspace is None:
+        workspace = new_workspace(nbytes, dev)
+    _check(lib.emb_grad_coalesce(_ptr(ids), T, _ptr(grad), code, D, V, _ptr(uniq_ids), _ptr(seg_offsets),
+                                 _ptr(uniq_grad), _ptr(num_unique), _ptr(workspace), workspace.numel(),
+                                 _ptr(dev_status), _stream(stream)), "emb_grad_coalesce")
+    return out
+
+
+def pack_by_owner_workspace_bytes(cap_rows, P) -> int:
+    return int(lib.emb_pack_by_owner_workspace_bytes(cap_rows, P))
+
+
+def pack_by_owner(uniq_ids, uniq_grad, num_unique, row_owner, P, out=None, workspace=None, dev_status=None,
+                  stream=None):
+    """Owner-major send buffers (emb_pack_by_owner).
+
+    Returns (send_ids [cap], send_rows [cap, D], send_counts [P], send_offsets [P+1]).
+    """
+    _need(uniq_ids, torch.int32, "uniq_ids")
+    _need(uniq_grad, torch.float32, "uniq_grad")
+    _need(num_unique, torch.int32, "num_unique")
+    _need(row_owner, torch.int32, "row_owner")
+    cap = uniq_ids.numel()
+    D = uniq_grad.shape[1]
+    V = row_owner.numel()
+    dev = uniq_ids.device
+    if out is None:
+        out = (torch.empty(cap, dtype=torch.int32, device=dev), torch.empty((cap, D), dtype=torch.float32, device=dev),
+               torch.empty(P, dtype=torch.int32, device=dev), torch.empty(P + 1, dtype=torch.int32, device=dev))
+    send_ids, send_rows, send_counts, send_offsets = out
+    if workspace is None:
+        workspace = new_workspace(pack_by_owner_workspace_bytes(cap, P), dev)
+    _check(lib.emb_pack_by_owner(_ptr(uniq_ids), _ptr(uniq_grad), _ptr(num_unique), cap, D, _ptr(row_owner), V, P,
+                                 _ptr(send_ids), _ptr(send_rows), _ptr(send_counts), _ptr(send_offsets),
+                                 _ptr(workspace), workspace.numel(), _ptr(dev_status), _stream(stream)),
+           "emb_pack_by_owner")
+    return out
+
+
+def sparse_adam_apply(table, exp_avg, exp_avg_sq, row_ids, rows, offsets, P, shard_begin, shard_end, lr, beta1,
+                      beta2, eps, step, dev_status=None, stream=None):
+    """Row-wise Adam on rows [offsets[shard_begin], offsets[shard_end]) (emb_sparse_adam_apply)."""
+    for t, n in ((table, "table"), (exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq"), (rows, "rows")):
+        _need(t, torch.float32, n)
+    _need(row_ids, torch.int32, "row_ids")
+    _need(offsets, torch.int32, "offsets")
+    V, D = table.shape
+    _check(lib.emb_sparse_adam_apply(_ptr(table), _ptr(exp_avg), _ptr(exp_avg_sq), V, D, _ptr(row_ids), _ptr(rows),
+                                     _ptr(offsets), P, shard_begin, shard_end, row_ids.numel(), float(lr),
+                                     float(beta1), float(beta2), float(eps), int(step), _ptr(dev_status),
+                                     _stream(stream)), "emb_sparse_adam_apply")

@@ -1,0 +1,109 @@
+// C ABI entry points: host-side argument checks, workspace checks, and the
+// launches of each stage on the caller's stream.  Contract: include/emb.h.
+#include <cmath>
+
+#include "common.h"
+#include "launch.h"
+
+namespace {
+
+constexpr int64_t kMaxV = (int64_t{1} << 31) - 1;
+constexpr int kMaxOwners = 1024;
+
+int launch_status(hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_ERR_LAUNCH; }
+
+bool bad_table_dims(int64_t V, int32_t D) { return V < 1 || V > kMaxV || D < 1; }
+
+}  // namespace
+
+extern "C" {
+
+int emb_abi_version(void) { return EMB_ABI_VERSION; }
+
+const char* emb_status_string(int status) {
+  switch (status) {
+    case EMB_OK: return "ok";
+    case EMB_ERR_INVALID_ARG: return "invalid argument";
+    case EMB_ERR_WORKSPACE: return "workspace too small";
+    case EMB_ERR_LAUNCH: return "kernel launch failed";
+    case EMB_ERR_UNSUPPORTED: return "unsupported";
+    default: return "unknown status";
+  }
+}
+
+int emb_gather(const float* table, int64_t V, int32_t D, const int32_t* ids, int32_t T, float* out,
+               int32_t* dev_status, void* stream) {
+  if (bad_table_dims(V, D) || T < 0) return EMB_ERR_INVALID_ARG;
+  if (T == 0) return EMB_OK;
+  if (!table || !ids || !out) return EMB_ERR_INVALID_ARG;
+  return launch_status(emb::launch_gather(table, V, D, ids, T, out, dev_status, static_cast<hipStream_t>(stream)));
+}
+
+size_t emb_grad_coalesce_workspace_bytes(int32_t T, int64_t V, int32_t D, int32_t grad_dtype) {
+  if (T < 0 || bad_table_dims(V, D) || (grad_dtype != EMB_F32 && grad_dtype != EMB_BF16)) return 0;
+  return emb::coalesce_workspace_bytes(T, V, D);
+}
+
+int emb_grad_coalesce(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D, int64_t V,
+                      int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad, int32_t* num_unique,
+                      void* workspace, size_t workspace_bytes, int32_t* dev_status, void* stream) {
+  if (T < 0 || bad_table_dims(V, D) || (grad_dtype != EMB_F32 && grad_dtype != EMB_BF16)) return EMB_ERR_INVALID_ARG;
+  if (!seg_offsets || !num_unique) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && (!ids || !grad || !uniq_ids || !uniq_grad || !workspace)) return EMB_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(grad) % (grad_dtype == EMB_BF16 ? 2 : 4) != 0) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return EMB_ERR_INVALID_ARG;
+  if (workspace_bytes < emb::coalesce_workspace_bytes(T, V, D) && T > 0) return EMB_ERR_WORKSPACE;
+  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, uniq_ids, seg_offsets,
+                                            uniq_grad, num_unique, workspace, dev_status,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+size_t emb_pack_by_owner_workspace_bytes(int32_t cap_rows, int32_t P) {
+  if (cap_rows < 0 || P < 1 || P > kMaxOwners) return 0;
+  return emb::pack_workspace_bytes(cap_rows, P);
+}
+
+int emb_pack_by_owner(const int32_t* uniq_ids, const float* uniq_grad, const int32_t* num_unique, int32_t cap_rows,
+                      int32_t D, const int32_t* row_owner, int64_t V, int32_t P, int32_t* send_ids, float* send_rows,
+                      int32_t* send_counts, int32_t* send_offsets, void* workspace, size_t workspace_bytes,
+                      int32_t* dev_status, void* stream) {
+  if (cap_rows < 0 || bad_table_dims(V, D) || P < 1 || P > kMaxOwners) return EMB_ERR_INVALID_ARG;
+  if (!send_counts || !send_offsets) return EMB_ERR_INVALID_ARG;
+  if (cap_rows > 0 && (!uniq_ids || !uniq_grad || !num_unique || !row_owner || !send_ids || !send_rows ||
+                       !workspace))
+    return EMB_ERR_INVALID_ARG;
+  if (cap_rows > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return EMB_ERR_INVALID_ARG;
+  if (cap_rows > 0 && workspace_bytes < emb::pack_workspace_bytes(cap_rows, P)) return EMB_ERR_WORKSPACE;
+  return launch_status(emb::launch_pack(uniq_ids, uniq_grad, num_unique, cap_rows, D, row_owner, V, P, send_ids,
+                                        send_rows, send_counts, send_offsets, workspace, dev_status,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+int emb_sparse_adam_apply(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int32_t D,
+                          const int32_t* row_ids, const float* rows, const int32_t* offsets, int32_t P,
+                          int32_t shard_begin, int32_t shard_end, int32_t cap_rows, double lr, double beta1,
+                          double beta2, double eps, int64_t step, int32_t* dev_status, void* stream) {
+  if (bad_table_dims(V, D) || P < 1 || P > kMaxOwners || cap_rows < 0) return EMB_ERR_INVALID_ARG;
+  if (shard_begin < 0 || shard_begin > shard_end || shard_end > P) return EMB_ERR_INVALID_ARG;
+  if (step < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0) ||
+      !std::isfinite(lr) || !std::isfinite(eps))
+    return EMB_ERR_INVALID_ARG;
+  if (cap_rows == 0 || shard_begin == shard_end) return EMB_OK;
+  if (!table || !exp_avg || !exp_avg_sq || !row_ids || !rows || !offsets) return EMB_ERR_INVALID_ARG;
+  // bias corrections in fp64 on the host, then the fp32 coefficients of the kernel
+  const double bc1 = 1.0 - std::pow(beta1, static_cast<double>(step));
+  const double bc2 = 1.0 - std::pow(beta2, static_cast<double>(step));
+  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return EMB_ERR_INVALID_ARG;  // beta == 0 edge cases stay valid: bc == 1
+  emb::AdamCoeffs c;
+  c.beta1 = static_cast<float>(beta1);
+  c.one_minus_beta1 = static_cast<float>(1.0 - beta1);
+  c.beta2 = static_cast<float>(beta2);
+  c.one_minus_beta2 = static_cast<float>(1.0 - beta2);
+  c.step_size = static_cast<float>(lr / bc1);
+  c.inv_bc2 = static_cast<float>(1.0 / bc2);
+  c.eps = static_cast<float>(eps);
+  return launch_status(emb::launch_adam(table, exp_avg, exp_avg_sq, V, D, row_ids, rows, offsets, shard_begin,
+                                        shard_end, cap_rows, c, dev_status, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

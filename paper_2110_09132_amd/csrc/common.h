@@ -1,0 +1,171 @@
+// Device helpers shared by the kernels of the library (wave64, gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "emb.h"
+
+namespace emb {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
+
+// Mask of the lanes below this one.
+__device__ __forceinline__ uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
+
+__device__ __forceinline__ void raise_flag(int32_t* status, int32_t flag) {
+  if (status != nullptr) atomicOr(status, flag);
+}
+
+// Wave-uniform value as an SGPR (lets the compiler use scalar loads).
+__device__ __forceinline__ int32_t uniform(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Inclusive prefix sum across the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    uint32_t y = __shfl_up(x, o, kWave);
+    if (lane_id() >= static_cast<uint32_t>(o)) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
+  return x;
+}
+
+// Exclusive scan, in place, of a[0..n) in LDS by a block of NT threads.
+// `wsum` is LDS scratch of NT/64 words.  Returns the total.  Ends with a barrier.
+template <int NT>
+__device__ uint32_t block_exclusive_scan(uint32_t* a, int n, uint32_t* wsum) {
+  const int per = (n + NT - 1) / NT;
+  const int beg = min(static_cast<int>(threadIdx.x) * per, n);
+  const int end = min(beg + per, n);
+  uint32_t s = 0;
+  for (int i = beg; i < end; ++i) s += a[i];
+  const uint32_t inc = wave_inclusive_scan(s);
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == kWave - 1) wsum[w] = inc;
+  __syncthreads();
+  uint32_t base = 0, total = 0;
+#pragma unroll
+  for (int i = 0; i < NT / kWave; ++i) {
+    const uint32_t v = wsum[i];
+    base += (i < w) ? v : 0u;
+    total += v;
+  }
+  uint32_t run = base + inc - s;
+  for (int i = beg; i < end; ++i) {
+    const uint32_t v = a[i];
+    a[i] = run;
+    run += v;
+  }
+  __syncthreads();
+  return total;
+}
+
+// Stable ranking of small integer digits inside one tile of NT*ITEMS keys.
+//
+// Key (wave w, round r, lane l) of the tile is input element
+// w*ITEMS*64 + r*64 + l, so walking waves, then rounds, then lanes visits the
+// keys in input order.  Within a round, lanes holding the same digit are found
+// with one ballot per digit bit; the lowest such lane advances the wave's
+// counter for that digit.  After all rounds the per-wave counters are turned
+// into exclusive offsets across waves and digits, which gives each key its
+// position in the tile's stable digit order.
+//
+// cnt: LDS [NT/64][bins]; dstart: LDS [bins]; wsum: LDS [NT/64].
+// On return dstart[d] is the tile-local start of digit d, lpos[] the tile
+// position of each valid key, and the function returns the number of valid keys.
+template <int NT, int ITEMS>
+__device__ uint32_t tile_stable_rank(const uint32_t (&dig)[ITEMS], const bool (&valid)[ITEMS], int bins,
+                                     int bits, uint32_t* cnt, uint32_t* dstart, uint32_t* wsum,
+                                     uint32_t (&lpos)[ITEMS]) {
+  constexpr int NW = NT / kWave;
+  const int w = threadIdx.x / kWave;
+  for (int i = threadIdx.x; i < NW * bins; i += NT) cnt[i] = 0;
+  __syncthreads();
+  uint32_t* mine = cnt + w * bins;
+  uint32_t rank[ITEMS];
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) {
+    const uint32_t d = dig[r];
+    uint64_t peers = __ballot(valid[r]);
+    for (int b = 0; b < bits; ++b) {
+      const bool set = (d >> b) & 1u;
+      const uint64_t m = __ballot(set);
+      peers &= set ? m : ~m;
+    }
+    const uint32_t below = __popcll(peers & lanemask_lt());
+    const uint32_t old = valid[r] ? mine[d] : 0u;
+    // all lanes have read the counter before the group leader writes it
+    __builtin_amdgcn_wave_barrier();
+    if (valid[r] && below == 0) mine[d] = old + static_cast<uint32_t>(__popcll(peers));
+    __builtin_amdgcn_wave_barrier();
+    rank[r] = old + below;
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < bins; d += NT) {
+    uint32_t s = 0;
+    for (int ww = 0; ww < NW; ++ww) {
+      const uint32_t v = cnt[ww * bins + d];
+      cnt[ww * bins + d] = s;
+      s += v;
+    }
+    dstart[d] = s;
+  }
+  __syncthreads();
+  const uint32_t total = block_exclusive_scan<NT>(dstart, bins, wsum);
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r)
+    lpos[r] = valid[r] ? dstart[dig[r]] + cnt[w * bins + dig[r]] + rank[r] : 0xFFFFFFFFu;
+  return total;
+}
+
+// For each digit d < bins, over the per-tile histograms hist[ntiles][bins]:
+//   colall[d] = sum over all tiles of hist[t][d]
+//   gbase[d]  = sum over all tiles of digits d' < d  +  sum over tiles t < tile of hist[t][d]
+// i.e. where this tile's keys of digit d start in the stably sorted output.
+// before: LDS scratch [bins].  Returns the grand total.  Ends with a barrier.
+template <int NT>
+__device__ uint32_t tile_global_bases(const uint32_t* __restrict__ hist, int ntiles, int tile, int bins,
+                                      uint32_t* colall, uint32_t* gbase, uint32_t* before, uint32_t* wsum) {
+  for (int d = threadIdx.x; d < bins; d += NT) {
+    uint32_t all = 0, bef = 0;
+    for (int t = 0; t < ntiles; ++t) {
+      const uint32_t v = hist[static_cast<size_t>(t) * bins + d];
+      all += v;
+      bef += (t < tile) ? v : 0u;
+    }
+    colall[d] = all;
+    gbase[d] = all;
+    before[d] = bef;
+  }
+  __syncthreads();
+  const uint32_t total = block_exclusive_scan<NT>(gbase, bins, wsum);
+  for (int d = threadIdx.x; d < bins; d += NT) gbase[d] += before[d];
+  __syncthreads();
+  return total;
+}
+
+// Rows of D elements are processed by groups of lanes: a row gets
+// L = min(64, 2^ceil(log2(ncols))) lanes and a wave covers 64 / L rows at once.
+struct RowLanes {
+  int log2_lanes;  // log2 L
+  __host__ __device__ int lanes() const { return 1 << log2_lanes; }
+  __host__ __device__ int rows_per_wave() const { return kWave >> log2_lanes; }
+};
+
+inline RowLanes row_lanes_for(int ncols) {
+  int l = 0;
+  while ((1 << l) < ncols && l < 6) ++l;
+  return RowLanes{l};
+}
+
+}  // namespace emb

@@ -71,3 +71,13 @@ def test_workload_shapes_small():
     spec4 = configs.WORKLOADS["lm_large_vocab_bf16"].tables[0]
     g4 = configs.make_grads(spec4, 0, T=8)
     assert g4.dtype == np.uint16 and g4.shape == (8, 1024)
+
+
+def test_compiled_normals_match_reference():
+    key = gen.stream_key(9, 3, gen.PURPOSE_GRADS)
+    for n in (0, 1, 2, 7, 10001):
+        a = gen.normal_f32(key, n, 0.5)
+        b = gen.normal_f32_reference(key, n, 0.5)
+        assert a.shape == b.shape
+        # same definition; libm and numpy may differ in the last fp64 bit
+        assert np.all(np.abs(a.astype(np.float64) - b) <= np.spacing(np.abs(b)))

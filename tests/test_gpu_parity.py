@@ -1,0 +1,245 @@
+"""Parity of each C ABI call with the oracle at sizes the oracle finishes in
+seconds: several sort tiles (2048 keys) and reduction chunks (32 tokens) with
+ragged tails, every gradient width path (vector and scalar), bf16 gradients,
+hot rows spanning many chunks, empty and degenerate inputs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2110_09132_amd as emb
+import tolerance
+from gpu_helpers import (check_adam, check_coalesce, check_pack, gpu_coalesce, gpu_gather, host, to_dev)
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+HP = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8)
+
+
+def ids_for(law, seed, T, V, s=1.1):
+    key = gen.stream_key(seed, 0, gen.PURPOSE_IDS)
+    return gen.uniform_ids(key, T, V) if law == "uniform" else gen.zipf_ids(key, T, V, s)
+
+
+def grads_for(seed, T, D, sigma=1.0, bf16=False):
+    g = gen.normal_f32(gen.stream_key(seed, 0, gen.PURPOSE_GRADS), T * D, sigma).reshape(T, D)
+    return gen.bf16_round(g).reshape(T, D) if bf16 else g
+
+
+# ---------------------------------------------------------------------- gather
+@pytest.mark.parametrize("D", [1, 3, 64, 65, 256, 1024])
+@pytest.mark.parametrize("T", [1, 2047, 2049, 5000])
+def test_gather_parity(D, T):
+    V = 3000
+    W = gen.normal_f32(gen.stream_key(D, T, gen.PURPOSE_WEIGHTS), V * D).reshape(V, D)
+    ids = ids_for("zipf", D + T, T, V)
+    out, st = gpu_gather(to_dev(W), ids)
+    ref, bad = oracle.gather(W, ids)
+    assert bad == 0 and st == 0
+    assert np.array_equal(out.view(np.uint32), ref.view(np.uint32))
+
+
+def test_gather_out_of_range_ids_give_zero_rows_and_flag():
+    V, D, T = 100, 8, 300
+    W = gen.normal_f32(gen.stream_key(1, 0, 1), V * D).reshape(V, D)
+    ids = ids_for("uniform", 2, T, V)
+    ids[[0, 17, 299]] = [-1, V, 1 << 30]
+    out, st = gpu_gather(to_dev(W), ids)
+    ref, bad = oracle.gather(W, ids)
+    assert bad == 3 and st == emb.EMB_DEV_ID_OUT_OF_RANGE
+    assert np.array_equal(out.view(np.uint32), ref.view(np.uint32))
+
+
+def test_gather_empty():
+    W = to_dev(np.ones((4, 4), np.float32))
+    out = emb.gather(W, to_dev(np.zeros(0, np.int32)))
+    torch.cuda.synchronize()
+    assert out.shape == (0, 4)
+
+
+# -------------------------------------------------------------------- coalesce
+@pytest.mark.parametrize("law,V,T,D", [
+    ("zipf", 1000, 512, 64),         # the tiny workload's shape
+    ("zipf", 5000, 2048, 8),         # exactly one sort tile
+    ("zipf", 5000, 2049, 3),         # ragged second tile, scalar width path
+    ("uniform", 1 << 20, 10000, 16),  # 21 key bits: three radix passes
+    ("zipf", 32768, 25000, 65),      # odd width (scalar path), many chunks
+    ("zipf", 300, 4001, 256),        # very heavy duplication
+    ("uniform", 50, 33, 1),          # one chunk + 1, D = 1
+    ("zipf", 1, 777, 4),             # V = 1: a single segment over 25 chunks
+])
+def test_coalesce_parity_fp32(law, V, T, D):
+    ids = ids_for(law, V + T + D, T, V)
+    G = grads_for(V + T, T, D)
+    check_coalesce(ids, G, V)
+
+
+@pytest.mark.parametrize("V,T,D", [(262144, 16384, 1024), (1000, 3000, 12), (1000, 3000, 10)])
+def test_coalesce_parity_bf16(V, T, D):
+    ids = ids_for("zipf", V + T, T, V, 1.0)
+    G = grads_for(V + D, T, D, 0.01, bf16=True)
+    _, _, r = check_coalesce(ids, G, V, bf16=True)
+    assert r <= tolerance.RTOL_F32  # identical bf16 inputs: the fp32 bar holds too
+
+
+def test_coalesce_hot_row_spans_many_chunks():
+    # one id takes ~60% of 20000 tokens: ~375 chunk pieces in one segment
+    T, V, D = 20000, 5000, 256
+    ids = ids_for("zipf", 77, T, V, 2.5)
+    G = grads_for(78, T, D, 0.01)
+    check_coalesce(ids, G, V)
+
+
+def test_coalesce_all_one_id():
+    T, D = 5000, 64
+    check_coalesce(np.full(T, 7, np.int32), grads_for(3, T, D), 10)
+
+
+def test_coalesce_all_distinct_is_a_permutation():
+    V, T, D = 100000, 6000, 32
+    ids = np.random.default_rng(4).permutation(V)[:T].astype(np.int32)
+    G = grads_for(5, T, D)
+    gpu, orc, _ = check_coalesce(ids, G, V)
+    assert np.array_equal(gpu["uniq_grad"].view(np.uint32), G[np.argsort(ids)].view(np.uint32))
+
+
+def test_coalesce_out_of_range_ids_are_left_out():
+    V, T, D = 1000, 3000, 16
+    ids = ids_for("zipf", 9, T, V)
+    ids[::97] = -3
+    ids[5::101] = V + 5
+    check_coalesce(ids, grads_for(9, T, D), V)
+
+
+def test_coalesce_all_ids_invalid():
+    gpu = gpu_coalesce(np.full(100, -1, np.int32), grads_for(1, 100, 4), 50)
+    assert gpu["U"] == 0 and gpu["seg_offsets"].tolist() == [0]
+    assert gpu["status"] == emb.EMB_DEV_ID_OUT_OF_RANGE
+
+
+def test_coalesce_empty_batch():
+    gpu = gpu_coalesce(np.zeros(0, np.int32), np.zeros((0, 8), np.float32), 50)
+    assert gpu["U"] == 0 and gpu["seg_offsets"].tolist() == [0] and gpu["status"] == 0
+
+
+def test_coalesce_misaligned_gradient_rows_use_scalar_path():
+    V, T, D = 2000, 3000, 64
+    ids = ids_for("zipf", 11, T, V)
+    G = grads_for(11, T, D)
+    buf = torch.zeros(T * D + 1, dtype=torch.float32, device="cuda")
+    buf[1:] = to_dev(G.reshape(-1))
+    check_coalesce(ids, G, V, grad_dev=buf[1:].view(T, D))
+
+
+def test_coalesce_is_bitwise_deterministic():
+    V, T, D = 1 << 20, 65536, 256
+    ids = ids_for("zipf", 52, T, V, 1.3)
+    G = to_dev(grads_for(52, T, D, 0.01))
+    a = gpu_coalesce(ids, None, V, grad_dev=G)
+    b = gpu_coalesce(ids, None, V, grad_dev=G)
+    assert a["U"] == b["U"]
+    assert np.array_equal(a["uniq_grad"].view(np.uint32), b["uniq_grad"].view(np.uint32))
+
+
+# ------------------------------------------------------------------------ pack
+@pytest.mark.parametrize("P,rule", [(1, "mod"), (2, "mod"), (7, "range"), (16, "mod"), (1024, "mod"),
+                                    (1024, "range"), (5, "rand")])
+def test_pack_parity(P, rule):
+    V, T, D = 50000, 9000, 20
+    ids = ids_for("zipf", P, T, V, 1.05)
+    G = grads_for(P + 1, T, D)
+    gpu, _, _ = check_coalesce(ids, G, V)
+    if rule == "mod":
+        own = gen.owner_mod(V, P)
+    elif rule == "range":
+        own = gen.owner_range(V, P)
+    else:
+        own = np.random.default_rng(P).integers(0, P, V).astype(np.int32)
+    check_pack(gpu["dev"], gpu["U"], own, P)
+
+
+def test_pack_drops_rows_with_bad_owner():
+    V, T, D, P = 500, 2000, 4, 4
+    ids = ids_for("uniform", 3, T, V)
+    gpu, _, _ = check_coalesce(ids, grads_for(3, T, D), V)
+    own = gen.owner_mod(V, P)
+    own[10] = 9
+    own[11] = -2
+    uid, _, ug, nu = gpu["dev"]
+    st = emb.new_status()
+    send_ids, send_rows, counts, offs = emb.pack_by_owner(uid, ug, nu, to_dev(own), P, dev_status=st)
+    torch.cuda.synchronize()
+    orc = oracle.pack_by_owner(host(uid[:gpu["U"]]), host(ug[:gpu["U"]]), own, P)
+    n = int(offs[P].item())
+    assert np.array_equal(host(send_ids[:n]), orc["send_ids"])
+    assert np.array_equal(host(offs), orc["send_offsets"])
+    assert int(st.item()) == emb.EMB_DEV_OWNER_OUT_OF_RANGE
+
+
+def test_pack_empty():
+    uid = torch.zeros(0, dtype=torch.int32, device="cuda")
+    ug = torch.zeros((0, 4), dtype=torch.float32, device="cuda")
+    nu = torch.zeros(1, dtype=torch.int32, device="cuda")
+    own = to_dev(gen.owner_mod(10, 3))
+    _, _, counts, offs = emb.pack_by_owner(uid, ug, nu, own, 3)
+    torch.cuda.synchronize()
+    assert host(counts).tolist() == [0, 0, 0] and host(offs).tolist() == [0, 0, 0, 0]
+
+
+# ------------------------------------------------------------------------ adam
+@pytest.mark.parametrize("D", [3, 64, 256])
+def test_adam_parity_multi_step_by_shard(D):
+    V, T, P = 20000, 6000, 4
+    W0 = gen.normal_f32(gen.stream_key(D, 0, gen.PURPOSE_WEIGHTS), V * D).reshape(V, D)
+    state = [to_dev(W0), torch.zeros((V, D), device="cuda"), torch.zeros((V, D), device="cuda")]
+    own = gen.owner_range(V, P)
+    for step in range(1, 4):
+        ids = ids_for("zipf", 100 * D + step, T, V, 1.0)
+        gpu, _, _ = check_coalesce(ids, grads_for(step, T, D, 0.01), V)
+        pk = check_pack(gpu["dev"], gpu["U"], own, P)
+        for s in range(P):  # each simulated owner applies its own block
+            check_adam(state, pk["dev"], P, s, s + 1, HP, step)
+
+
+def test_adam_out_of_range_row_is_skipped_and_flagged():
+    V, D = 100, 4
+    W = to_dev(np.ones((V, D), np.float32))
+    M = torch.zeros((V, D), device="cuda")
+    S = torch.zeros((V, D), device="cuda")
+    row_ids = to_dev(np.array([3, 200, 5], np.int32))
+    rows = to_dev(np.full((3, D), 0.5, np.float32))
+    offs = to_dev(np.array([0, 3], np.int32))
+    st = emb.new_status()
+    emb.sparse_adam_apply(W, M, S, row_ids, rows, offs, 1, 0, 1, **HP, step=1, dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == emb.EMB_DEV_ID_OUT_OF_RANGE
+    Wh = host(W)
+    assert np.all(Wh[[0, 1, 2, 4, 6]] == 1.0) and np.all(Wh[[3, 5]] < 1.0)
+
+
+# ----------------------------------------------------------- the whole step
+def test_pipeline_on_streams_matches_default_stream():
+    """All four calls enqueued on a side stream give the same bits."""
+    V, T, D, P = 40000, 12000, 128, 8
+    ids = ids_for("zipf", 5, T, V, 1.05)
+    G = grads_for(5, T, D, 0.01)
+    W0 = gen.normal_f32(gen.stream_key(5, 0, 1), V * D).reshape(V, D)
+    own = to_dev(gen.owner_mod(V, P))
+
+    def run(stream):
+        with torch.cuda.stream(stream):
+            W = to_dev(W0)
+            M = torch.zeros_like(W)
+            S = torch.zeros_like(W)
+            out = emb.gather(W, to_dev(ids))
+            uid, seg, ug, nu = emb.grad_coalesce(to_dev(ids), to_dev(G), V)
+            send_ids, send_rows, counts, offs = emb.pack_by_owner(uid, ug, nu, own, P)
+            emb.sparse_adam_apply(W, M, S, send_ids, send_rows, offs, P, 0, P, **HP, step=1)
+        torch.cuda.synchronize()
+        return [host(x) for x in (out, W, M, S, send_rows)]
+
+    a = run(torch.cuda.current_stream())
+    b = run(torch.cuda.Stream())
+    for x, y in zip(a, b):
+        assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
