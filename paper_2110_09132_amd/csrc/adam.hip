@@ -52,29 +52,32 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
   const long long step = static_cast<long long>(rpw) * kRowsInFlight;
   bool bad = false;
   for (long long r0 = lo + wave * step; r0 < hi; r0 += nwaves * step) {
+    // All loads come from clamped, always-valid addresses and are issued
+    // together; only rows that exist and are valid are stored.
     int32_t rid[kRowsInFlight];
+    long long src[kRowsInFlight];
 #pragma unroll
     for (int u = 0; u < kRowsInFlight; ++u) {
       const long long i = r0 + u * rpw + sub;
-      rid[u] = -1;
-      if (i < hi) {
-        const int32_t r = row_ids[i];
-        if (r >= 0 && r < V) rid[u] = r;
-        else bad = true;
-      }
+      src[u] = i < hi ? i : hi - 1;
+      rid[u] = row_ids[src[u]];
+    }
+#pragma unroll
+    for (int u = 0; u < kRowsInFlight; ++u) {
+      const bool live = r0 + u * rpw + sub < hi;
+      const bool ok = rid[u] >= 0 && rid[u] < V;
+      bad |= live && !ok;
+      if (!live || !ok) rid[u] = -1;
     }
     for (int col = cl; col < Dv; col += L) {
       VecT g[kRowsInFlight], w[kRowsInFlight], m[kRowsInFlight], s[kRowsInFlight];
 #pragma unroll
       for (int u = 0; u < kRowsInFlight; ++u) {
-        if (rid[u] >= 0) {
-          const long long i = r0 + u * rpw + sub;
-          const size_t e = static_cast<size_t>(rid[u]) * Dv + col;
-          g[u] = rows[static_cast<size_t>(i) * Dv + col];
-          w[u] = W[e];
-          m[u] = M[e];
-          s[u] = S[e];
-        }
+        const size_t e = static_cast<size_t>(rid[u] < 0 ? 0 : rid[u]) * Dv + col;
+        g[u] = rows[static_cast<size_t>(src[u]) * Dv + col];
+        w[u] = W[e];
+        m[u] = M[e];
+        s[u] = S[e];
       }
 #pragma unroll
       for (int u = 0; u < kRowsInFlight; ++u) {

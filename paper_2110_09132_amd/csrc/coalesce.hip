@@ -47,17 +47,17 @@ __global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t* __
   __syncthreads();
   const int base = blockIdx.x * kTile;
   bool bad = false;
-  for (int i = threadIdx.x; i < kTile; i += kThreads) {
-    const int g = base + i;
-    if (g < T) {
-      uint32_t k;
-      if (raw_ids != nullptr) {
-        k = sanitize(raw_ids[g], V);
-        bad |= (k == V);
-      } else {
-        k = keys[g];
-      }
-      atomicAdd(&h[(k >> shift) & (bins - 1)], 1u);
+  uint32_t k[kItems];
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const int g = min(base + r * kThreads + static_cast<int>(threadIdx.x), T - 1);
+    k[r] = raw_ids != nullptr ? sanitize(raw_ids[g], V) : keys[g];
+  }
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    if (base + r * kThreads + static_cast<int>(threadIdx.x) < T) {
+      bad |= (k[r] == V);
+      atomicAdd(&h[(k[r] >> shift) & (bins - 1)], 1u);
     }
   }
   if (__any(bad) && lane_id() == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
@@ -70,7 +70,8 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     uint32_t V, int T, int shift, int bits, const uint32_t* __restrict__ tile_hist, int ntiles,
     uint32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out) {
   __shared__ uint32_t cnt[(kThreads / kWave) * kBinsMax];
-  __shared__ uint32_t dstart[kBinsMax], colall[kBinsMax], gbase[kBinsMax], before[kBinsMax];
+  __shared__ uint32_t dstart[kBinsMax], colall[kBinsMax], gbase[kBinsMax];
+  __shared__ uint32_t red_all[kThreads], red_bef[kThreads];
   __shared__ uint32_t wsum[kThreads / kWave];
   __shared__ uint32_t skeys[kTile];
   __shared__ int32_t svals[kTile];
@@ -85,16 +86,13 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const int g = base + w * kItems * kWave + r * kWave + static_cast<int>(lane_id());
+    const int gc = min(g, T - 1);  // clamped: every load is issued unconditionally
     valid[r] = g < T;
-    key[r] = 0;
-    val[r] = 0;
-    if (valid[r]) {
-      key[r] = raw_ids != nullptr ? sanitize(raw_ids[g], V) : keys_in[g];
-      val[r] = vals_in != nullptr ? vals_in[g] : g;
-    }
+    key[r] = raw_ids != nullptr ? sanitize(raw_ids[gc], V) : keys_in[gc];
+    val[r] = vals_in != nullptr ? vals_in[gc] : g;
     dig[r] = (key[r] >> shift) & (bins - 1);
   }
-  tile_global_bases<kThreads>(tile_hist, ntiles, tile, bins, colall, gbase, before, wsum);
+  tile_global_bases<kThreads>(tile_hist, ntiles, tile, bins, colall, gbase, red_all, red_bef, wsum);
   tile_stable_rank<kThreads, kItems>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
@@ -115,20 +113,29 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
 }
 
 // ------------------------------------------------------- segment discovery
-__device__ __forceinline__ bool is_head(const uint32_t* __restrict__ k, int i, uint32_t V) {
-  const uint32_t key = k[i];
-  return key < V && (i == 0 || k[i - 1] != key);
-}
+// Each thread owns kItems consecutive sorted keys; it loads them together with
+// the key before (head test) and the key after (last-valid test).
+struct KeyWindow {
+  uint32_t k[kItems + 2];  // k[j] = skeys[base - 1 + j], clamped to [0, T)
+  __device__ KeyWindow(const uint32_t* __restrict__ skeys, int base, int T) {
+#pragma unroll
+    for (int j = 0; j < kItems + 2; ++j) k[j] = skeys[min(max(base - 1 + j, 0), T - 1)];
+  }
+  // sorted element base + j is the first of its id (j < kItems)
+  __device__ bool head(int base, int j, int T, uint32_t V) const {
+    const int i = base + j;
+    return i < T && k[j + 1] < V && (i == 0 || k[j] != k[j + 1]);
+  }
+};
 
 __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t* __restrict__ skeys, uint32_t V, int T,
                                                              uint32_t* __restrict__ tile_heads) {
   __shared__ uint32_t wsum[kThreads / kWave];
   const int base = blockIdx.x * kTile + threadIdx.x * kItems;
+  const KeyWindow win(skeys, base, T);
   uint32_t c = 0;
-  for (int k = 0; k < kItems; ++k) {
-    const int i = base + k;
-    if (i < T) c += is_head(skeys, i, V) ? 1u : 0u;
-  }
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) c += win.head(base, j, T, V) ? 1u : 0u;
   c = wave_sum(c);
   if (lane_id() == 0) wsum[threadIdx.x / kWave] = c;
   __syncthreads();
@@ -148,9 +155,17 @@ __global__ __launch_bounds__(kThreads) void seg_emit_kernel(const uint32_t* __re
                                                             int32_t* __restrict__ span_count) {
   __shared__ uint32_t wsum[kThreads / kWave];
   __shared__ uint32_t tile_base;
-  // heads in earlier tiles
+  const int base = blockIdx.x * kTile + threadIdx.x * kItems;
+  const KeyWindow win(skeys, base, T);
+  // heads in earlier tiles (8 loads in flight per thread)
   uint32_t s = 0;
-  for (int t = threadIdx.x; t < static_cast<int>(blockIdx.x); t += kThreads) s += tile_heads[t];
+  for (int t0 = threadIdx.x; t0 < static_cast<int>(blockIdx.x); t0 += 8 * kThreads) {
+    uint32_t v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = tile_heads[min(t0 + k * kThreads, static_cast<int>(blockIdx.x) - 1)];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += (t0 + k * kThreads < static_cast<int>(blockIdx.x)) ? v[k] : 0u;
+  }
   s = wave_sum(s);
   if (lane_id() == 0) wsum[threadIdx.x / kWave] = s;
   __syncthreads();
@@ -161,39 +176,34 @@ __global__ __launch_bounds__(kThreads) void seg_emit_kernel(const uint32_t* __re
   }
   __syncthreads();
   // heads of this thread's items, exclusive scan over the block
-  const int base = blockIdx.x * kTile + threadIdx.x * kItems;
   uint32_t c = 0;
-  for (int k = 0; k < kItems; ++k) {
-    const int i = base + k;
-    if (i < T) c += is_head(skeys, i, V) ? 1u : 0u;
-  }
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) c += win.head(base, j, T, V) ? 1u : 0u;
   const uint32_t inc = wave_inclusive_scan(c);
   if (lane_id() == kWave - 1) wsum[threadIdx.x / kWave] = inc;
   __syncthreads();
   uint32_t wbase = 0;
   for (int i = 0; i < static_cast<int>(threadIdx.x / kWave); ++i) wbase += wsum[i];
-  // number of heads at positions <= the current item, over the whole array
+  // number of heads before the current item, over the whole sorted array
   uint32_t run = tile_base + wbase + inc - c;
-  for (int k = 0; k < kItems; ++k) {
-    const int i = base + k;
-    if (i >= T) break;
-    const uint32_t key = skeys[i];
-    if (key >= V) {
-      if (i == 0) {  // no valid token at all
-        seg_offsets[0] = 0;
-        num_unique[0] = 0;
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {
+    const int i = base + j;
+    const uint32_t key = win.k[j + 1];
+    if (i < T && key < V) {
+      if (win.head(base, j, T, V)) {
+        uniq_ids[run] = static_cast<int32_t>(key);
+        seg_offsets[run] = i;
+        ++run;
       }
-      break;
-    }
-    if (i == 0 || skeys[i - 1] != key) {
-      uniq_ids[run] = static_cast<int32_t>(key);
-      seg_offsets[run] = i;
-      ++run;
-    }
-    seg_of[i] = static_cast<int32_t>(run - 1);
-    if (i + 1 == T || skeys[i + 1] >= V) {  // last valid token
-      seg_offsets[run] = i + 1;
-      num_unique[0] = static_cast<int32_t>(run);
+      seg_of[i] = static_cast<int32_t>(run - 1);
+      if (i + 1 == T || win.k[j + 2] >= V) {  // last valid token
+        seg_offsets[run] = i + 1;
+        num_unique[0] = static_cast<int32_t>(run);
+      }
+    } else if (i == 0 && T > 0) {  // no valid token at all
+      seg_offsets[0] = 0;
+      num_unique[0] = 0;
     }
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) span_count[0] = 0;
@@ -255,6 +265,7 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   for (int cb = 0; cb < Dv; cb += kWave) {
     const int c = cb + static_cast<int>(lane_id());
     const bool colok = c < Dv;
+    const int cc = min(c, Dv - 1);  // clamped column: loads are unconditional
     Acc acc = Acc{};
     int cur = seg_of[a];
     int rs = a;
@@ -274,9 +285,9 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
       Acc g[kLoadsInFlight];
 #pragma unroll
       for (int k = 0; k < kLoadsInFlight; ++k) {
-        const int i = i0 + k;
-        u[k] = i < b ? seg_of[i] : -1;
-        g[k] = (i < b && colok) ? Row::load(grad, static_cast<size_t>(spos[i]), Dv, c) : Acc{};
+        const int ic = min(i0 + k, b - 1);
+        u[k] = seg_of[ic];
+        g[k] = Row::load(grad, static_cast<size_t>(spos[ic]), Dv, cc);
       }
 #pragma unroll
       for (int k = 0; k < kLoadsInFlight; ++k) {
@@ -321,14 +332,15 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
     for (int cb = 0; cb < Dv; cb += kWave) {
       const int c = cb + static_cast<int>(lane_id());
       const bool colok = c < Dv;
+      const int cc = min(c, Dv - 1);
       Acc acc = Acc{};
       for (int p0 = p_beg; p0 < p_end; p0 += kLoadsInFlight) {
         Acc g[kLoadsInFlight];
 #pragma unroll
         for (int k = 0; k < kLoadsInFlight; ++k) {
-          const int p = p0 + k;
+          const int p = min(p0 + k, p_end - 1);
           const int slot = (p == 0) ? first_slot : 0;
-          g[k] = (p < p_end && colok) ? part_rows[(static_cast<size_t>(c0 + p) * 2 + slot) * Dv + c] : Acc{};
+          g[k] = part_rows[(static_cast<size_t>(c0 + p) * 2 + slot) * Dv + cc];
         }
 #pragma unroll
         for (int k = 0; k < kLoadsInFlight; ++k)

@@ -132,24 +132,52 @@ __device__ uint32_t tile_stable_rank(const uint32_t (&dig)[ITEMS], const bool (&
 //   colall[d] = sum over all tiles of hist[t][d]
 //   gbase[d]  = sum over all tiles of digits d' < d  +  sum over tiles t < tile of hist[t][d]
 // i.e. where this tile's keys of digit d start in the stably sorted output.
-// before: LDS scratch [bins].  Returns the grand total.  Ends with a barrier.
+// When bins < NT, NT / bins threads share a digit, each summing every G-th
+// tile; loads are issued 8 at a time from clamped addresses so they overlap.
+// red_all, red_bef: LDS scratch of max(NT, bins) words each.
+// Returns the grand total.  Ends with a barrier.
 template <int NT>
 __device__ uint32_t tile_global_bases(const uint32_t* __restrict__ hist, int ntiles, int tile, int bins,
-                                      uint32_t* colall, uint32_t* gbase, uint32_t* before, uint32_t* wsum) {
+                                      uint32_t* colall, uint32_t* gbase, uint32_t* red_all, uint32_t* red_bef,
+                                      uint32_t* wsum) {
+  constexpr int kBatch = 8;
+  const int G = bins <= NT ? NT / bins : 1;
+  for (int item = threadIdx.x; item < G * bins; item += NT) {
+    const int d = item % bins;
+    const int g = item / bins;
+    uint32_t all = 0, bef = 0;
+    for (int t0 = g; t0 < ntiles; t0 += kBatch * G) {
+      uint32_t v[kBatch];
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const int t = min(t0 + k * G, ntiles - 1);
+        v[k] = hist[static_cast<size_t>(t) * bins + d];
+      }
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const int t = t0 + k * G;
+        const uint32_t x = t < ntiles ? v[k] : 0u;
+        all += x;
+        bef += t < tile ? x : 0u;
+      }
+    }
+    red_all[item] = all;
+    red_bef[item] = bef;
+  }
+  __syncthreads();
   for (int d = threadIdx.x; d < bins; d += NT) {
     uint32_t all = 0, bef = 0;
-    for (int t = 0; t < ntiles; ++t) {
-      const uint32_t v = hist[static_cast<size_t>(t) * bins + d];
-      all += v;
-      bef += (t < tile) ? v : 0u;
+    for (int g = 0; g < G; ++g) {
+      all += red_all[g * bins + d];
+      bef += red_bef[g * bins + d];
     }
     colall[d] = all;
     gbase[d] = all;
-    before[d] = bef;
+    red_bef[d] = bef;  // item d belongs to this thread: no other thread reads it now
   }
   __syncthreads();
   const uint32_t total = block_exclusive_scan<NT>(gbase, bins, wsum);
-  for (int d = threadIdx.x; d < bins; d += NT) gbase[d] += before[d];
+  for (int d = threadIdx.x; d < bins; d += NT) gbase[d] += red_bef[d];
   __syncthreads();
   return total;
 }

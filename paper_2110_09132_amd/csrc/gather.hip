@@ -26,25 +26,31 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const VecT* __restrict
   const long long rows_per_step = static_cast<long long>(rpw) * kRowsInFlight;
   bool bad = false;
   for (long long r0 = wave * rows_per_step; r0 < T; r0 += nwaves * rows_per_step) {
+    // Loads are issued unconditionally from clamped, always-valid addresses so
+    // that all of them are in flight together; only the stores are predicated.
     int32_t id[kRowsInFlight];
+    bool live[kRowsInFlight];
 #pragma unroll
     for (int u = 0; u < kRowsInFlight; ++u) {
       const long long row = r0 + u * rpw + sub;
-      id[u] = row < T ? ids[row] : 0;
-      if (row < T && (id[u] < 0 || id[u] >= V)) bad = true;
+      live[u] = row < T;
+      id[u] = ids[live[u] ? row : T - 1];
+    }
+#pragma unroll
+    for (int u = 0; u < kRowsInFlight; ++u) {
+      const bool ok = id[u] >= 0 && id[u] < V;
+      bad |= live[u] && !ok;
+      if (!ok) id[u] = -1;
     }
     for (int c = cl; c < Dv; c += L) {
       VecT v[kRowsInFlight];
 #pragma unroll
-      for (int u = 0; u < kRowsInFlight; ++u) {
-        const long long row = r0 + u * rpw + sub;
-        const bool ok = row < T && id[u] >= 0 && id[u] < V;
-        v[u] = ok ? table[static_cast<size_t>(id[u]) * Dv + c] : VecT{};
-      }
+      for (int u = 0; u < kRowsInFlight; ++u)
+        v[u] = table[static_cast<size_t>(id[u] < 0 ? 0 : id[u]) * Dv + c];
 #pragma unroll
       for (int u = 0; u < kRowsInFlight; ++u) {
         const long long row = r0 + u * rpw + sub;
-        if (row < T) out[static_cast<size_t>(row) * Dv + c] = v[u];
+        if (live[u]) out[static_cast<size_t>(row) * Dv + c] = id[u] < 0 ? VecT{} : v[u];
       }
     }
   }

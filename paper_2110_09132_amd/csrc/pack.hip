@@ -27,14 +27,16 @@ __device__ __forceinline__ int clamp_rows(const int32_t* num_unique, int cap) {
   return u < 0 ? 0 : (u > cap ? cap : u);
 }
 
-// Owner of a row, or P when the row is not sent.
+// Owner of a row, or P when the row is not sent.  The owner table is read
+// at a clamped index so the load never depends on a branch.
 __device__ __forceinline__ uint32_t owner_of(int32_t id, const int32_t* __restrict__ row_owner, int64_t V, int P,
                                              int& flags) {
-  if (id < 0 || id >= V) {
+  const bool id_ok = id >= 0 && id < V;
+  const int32_t o = row_owner[id_ok ? id : 0];
+  if (!id_ok) {
     flags |= EMB_DEV_ID_OUT_OF_RANGE;
     return static_cast<uint32_t>(P);
   }
-  const int32_t o = row_owner[id];
   if (o < 0 || o >= P) {
     flags |= EMB_DEV_OWNER_OUT_OF_RANGE;
     return static_cast<uint32_t>(P);
@@ -53,9 +55,16 @@ __global__ __launch_bounds__(kThreads) void pack_hist_kernel(const int32_t* __re
   const int U = clamp_rows(num_unique, cap);
   const int base = blockIdx.x * kTile;
   int flags = 0;
-  for (int i = threadIdx.x; i < kTile; i += kThreads) {
-    const int k = base + i;
-    if (k < U) atomicAdd(&h[owner_of(uniq_ids[k], row_owner, V, P, flags)], 1u);
+  if (base < U) {
+    int32_t id[kItems];
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) id[r] = uniq_ids[min(base + r * kThreads + static_cast<int>(threadIdx.x), U - 1)];
+    uint32_t d[kItems];
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) d[r] = owner_of(id[r], row_owner, V, P, flags);
+#pragma unroll
+    for (int r = 0; r < kItems; ++r)
+      if (base + r * kThreads + static_cast<int>(threadIdx.x) < U) atomicAdd(&h[d[r]], 1u);
   }
   if (flags != 0) raise_flag(status, flags);
   __syncthreads();
@@ -68,7 +77,8 @@ __global__ __launch_bounds__(kThreads) void pack_scatter_kernel(
     int ntiles, int32_t* __restrict__ send_ids, int32_t* __restrict__ slot_of, int32_t* __restrict__ send_counts,
     int32_t* __restrict__ send_offsets) {
   __shared__ uint32_t cnt[(kThreads / kWave) * kBinsMax];
-  __shared__ uint32_t dstart[kBinsMax], colall[kBinsMax], gbase[kBinsMax], before[kBinsMax];
+  __shared__ uint32_t dstart[kBinsMax], colall[kBinsMax], gbase[kBinsMax];
+  __shared__ uint32_t red_all[kBinsMax], red_bef[kBinsMax];
   __shared__ uint32_t wsum[kThreads / kWave];
   const int bins = P + 1;
   const int tile = blockIdx.x;
@@ -84,10 +94,15 @@ __global__ __launch_bounds__(kThreads) void pack_scatter_kernel(
   for (int r = 0; r < kItems; ++r) {
     const int k = base + w * kItems * kWave + r * kWave + static_cast<int>(lane_id());
     valid[r] = k < U;
-    id[r] = valid[r] ? uniq_ids[k] : 0;
-    dig[r] = valid[r] ? owner_of(id[r], row_owner, V, P, flags) : 0u;
+    id[r] = uniq_ids[max(min(k, U - 1), 0)];
   }
-  const uint32_t total = tile_global_bases<kThreads>(tile_hist, ntiles, tile, bins, colall, gbase, before, wsum);
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) {
+    const uint32_t d = owner_of(id[r], row_owner, V, P, flags);
+    dig[r] = valid[r] ? d : 0u;
+  }
+  const uint32_t total =
+      tile_global_bases<kThreads>(tile_hist, ntiles, tile, bins, colall, gbase, red_all, red_bef, wsum);
   tile_stable_rank<kThreads, kItems>(dig, valid, bins, owner_bits, cnt, dstart, wsum, lpos);
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
@@ -129,14 +144,15 @@ __global__ __launch_bounds__(kThreads) void pack_rows_kernel(const VecT* __restr
 #pragma unroll
     for (int u = 0; u < kRowsInFlight; ++u) {
       const long long k = r0 + u * rpw + sub;
-      dst[u] = k < U ? slot_of[k] : -1;
+      dst[u] = slot_of[k < U ? k : U - 1];
+      if (k >= U) dst[u] = -1;
     }
     for (int c = cl; c < Dv; c += L) {
       VecT v[kRowsInFlight];
 #pragma unroll
       for (int u = 0; u < kRowsInFlight; ++u) {
         const long long k = r0 + u * rpw + sub;
-        v[u] = dst[u] >= 0 ? uniq_grad[static_cast<size_t>(k) * Dv + c] : VecT{};
+        v[u] = uniq_grad[static_cast<size_t>(k < U ? k : U - 1) * Dv + c];
       }
 #pragma unroll
       for (int u = 0; u < kRowsInFlight; ++u)
