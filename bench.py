@@ -45,62 +45,6 @@ def byte_model(T, U, D, g, P):
     return dict(gather=gather, coalesce=coalesce, pack=pack, adam=adam)
 
 
-class Table:
-    """Device state, pre-generated batches and pre-allocated outputs of one table."""
-
-    def __init__(self, spec, nbatches, torch, emb, configs):
-        self.spec = spec
-        dev = "cuda"
-        V, D, T, P = spec.V, spec.D, spec.T, spec.P
-        self.W = torch.from_numpy(configs.make_weights(spec)).to(dev)
-        self.M = torch.zeros_like(self.W)
-        self.S = torch.zeros_like(self.W)
-        self.owner = torch.from_numpy(configs.row_owner(spec)).to(dev)
-        self.ids, self.grads = [], []
-        for b in range(nbatches):
-            ids, G = configs.make_batch(spec, 1000 + b)
-            self.ids.append(torch.from_numpy(ids).to(dev))
-            if spec.grad_dtype == "bf16":
-                self.grads.append(torch.from_numpy(G.view(np.int16)).to(dev).view(torch.bfloat16))
-            else:
-                self.grads.append(torch.from_numpy(G).to(dev))
-        i32, f32 = torch.int32, torch.float32
-        self.out = torch.empty((T, D), dtype=f32, device=dev)
-        self.coal = (torch.empty(T, dtype=i32, device=dev), torch.empty(T + 1, dtype=i32, device=dev),
-                     torch.empty((T, D), dtype=f32, device=dev), torch.empty(1, dtype=i32, device=dev))
-        self.pack = (torch.empty(T, dtype=i32, device=dev), torch.empty((T, D), dtype=f32, device=dev),
-                     torch.empty(P, dtype=i32, device=dev), torch.empty(P + 1, dtype=i32, device=dev))
-        code = emb.EMB_BF16 if spec.grad_dtype == "bf16" else emb.EMB_F32
-        self.ws_c = emb.new_workspace(emb.grad_coalesce_workspace_bytes(T, V, D, code), dev)
-        self.ws_p = emb.new_workspace(emb.pack_by_owner_workspace_bytes(T, P), dev)
-        self.U = [0] * nbatches
-
-
-def run_step(tables, b, step, wl, emb, ev=None):
-    for tb in tables:
-        sp = tb.spec
-        if ev is not None:
-            ev["gather"][0].record()
-        emb.gather(tb.W, tb.ids[b], out=tb.out)
-        if ev is not None:
-            ev["gather"][1].record()
-            ev["coalesce"][0].record()
-        emb.grad_coalesce(tb.ids[b], tb.grads[b], sp.V, out=tb.coal, workspace=tb.ws_c)
-        if ev is not None:
-            ev["coalesce"][1].record()
-            ev["pack"][0].record()
-        uid, _, ug, nu = tb.coal
-        emb.pack_by_owner(uid, ug, nu, tb.owner, sp.P, out=tb.pack, workspace=tb.ws_p)
-        if ev is not None:
-            ev["pack"][1].record()
-            ev["adam"][0].record()
-        send_ids, send_rows, _, offs = tb.pack
-        emb.sparse_adam_apply(tb.W, tb.M, tb.S, send_ids, send_rows, offs, sp.P, 0, sp.P, wl.lr, wl.beta1, wl.beta2,
-                              wl.eps, step)
-        if ev is not None:
-            ev["adam"][1].record()
-
-
 def cpu_baseline(wl, seconds):
     """The C oracle, single-threaded, on full steps of the same workload (same
     shapes, same generators) until about `seconds` of CPU time have passed."""
@@ -152,6 +96,7 @@ def main():
     ap.add_argument("--batches", type=int, default=8)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sequential", action="store_true", help="one stream, calls one after another")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -163,68 +108,95 @@ def main():
     import torch
 
     import paper_2110_09132_amd as emb
+    from paper_2110_09132_amd.step import EmbeddingTable, StepPipeline
     from workloads import configs
 
     wl = configs.WORKLOADS[args.workload]
     log(f"workload {wl.name}: {wl.description}")
-    tables = [Table(sp, args.batches, torch, emb, configs) for sp in wl.tables]
-    torch.cuda.synchronize()
+    dev = "cuda"
+    tables, batches = [], []
+    for sp in wl.tables:
+        gdt = torch.bfloat16 if sp.grad_dtype == "bf16" else torch.float32
+        W = torch.from_numpy(configs.make_weights(sp)).to(dev)
+        tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).to(dev), sp.P, sp.T, gdt))
+        tb_batches = []
+        for b in range(args.batches):
+            ids, G = configs.make_batch(sp, 1000 + b)
+            g = torch.from_numpy(G.view(np.int16)).to(dev).view(torch.bfloat16) if sp.grad_dtype == "bf16" \
+                else torch.from_numpy(G).to(dev)
+            tb_batches.append((torch.from_numpy(ids).to(dev), g))
+        batches.append(tb_batches)
+    step_batches = [[batches[k][b] for k in range(len(tables))] for b in range(args.batches)]
 
     # unique counts of each batch (outside any timed region)
+    U = [[0] * len(tables) for _ in range(args.batches)]
     for b in range(args.batches):
-        for tb in tables:
-            emb.grad_coalesce(tb.ids[b], tb.grads[b], tb.spec.V, out=tb.coal, workspace=tb.ws_c)
+        for k, tb in enumerate(tables):
+            ids, g = step_batches[b][k]
+            emb.grad_coalesce(ids, g, tb.V, out=tb.coal, workspace=tb.ws_coalesce)
             torch.cuda.synchronize()
-            tb.U[b] = int(tb.coal[3].item())
+            U[b][k] = int(tb.coal[3].item())
 
-    step = 0
+    pipe = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential)
+    t = 0
     for _ in range(args.warmup):
-        step += 1
-        run_step(tables, step % args.batches, step, wl, emb)
+        t += 1
+        pipe.step(step_batches[t % args.batches], t)
+    pipe.finish()
     torch.cuda.synchronize()
 
-    # timed region: exactly K steps
-    stream = torch.cuda.current_stream()
+    # timed region: exactly K steps; the update's duration is recorded on its own stream
+    main = torch.cuda.current_stream()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    rows = 0
+    adam_ev = [(emb.Event(timing=True), emb.Event(timing=True)) for _ in range(args.steps)]
+    rows, used = 0, []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    start.record(stream)
-    for _ in range(args.steps):
-        step += 1
-        b = step % args.batches
-        run_step(tables, b, step, wl, emb)
-        rows += sum(tb.U[b] for tb in tables)
-    end.record(stream)
+    start.record(main)
+    for s in range(args.steps):
+        t += 1
+        b = t % args.batches
+        pipe.step(step_batches[b], t, timing={"adam": adam_ev[s]})
+        rows += sum(U[b])
+        used.append(b)
+    pipe.finish()
+    end.record(main)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
+    adam_us = 1e3 * sum(a.elapsed_ms(z) for a, z in adam_ev) / args.steps
 
-    # per-stage timing in a second pass with events between the calls
+    # per-stage breakdown: the same steps run one call after another on one stream
+    seq = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=False)
     stage_ms = {k: 0.0 for k in ("gather", "coalesce", "pack", "adam")}
-    for _ in range(args.steps):
-        step += 1
-        b = step % args.batches
-        ev = {k: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for k in stage_ms}
-        run_step(tables, b, step, wl, emb, ev)
-        torch.cuda.synchronize()
-        for k in stage_ms:
-            stage_ms[k] += ev[k][0].elapsed_time(ev[k][1]) / args.steps
-
-    # byte model over the timed steps
-    bytes_step = {k: 0.0 for k in stage_ms}
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    seq_total = 0.0
     for s in range(args.steps):
-        b = (step - 2 * args.steps + 1 + s) % args.batches
-        for tb in tables:
-            g = 2 if tb.spec.grad_dtype == "bf16" else 4
-            bm = byte_model(tb.spec.T, tb.U[b], tb.spec.D, g, tb.spec.P)
-            for k in bytes_step:
-                bytes_step[k] += bm[k] / args.steps
+        t += 1
+        ev = {k: (emb.Event(timing=True), emb.Event(timing=True)) for k in stage_ms}
+        s0.record(main)
+        seq.step(step_batches[t % args.batches], t, timing=ev)
+        s1.record(main)
+        torch.cuda.synchronize()
+        seq_total += s0.elapsed_time(s1) / args.steps
+        for k in stage_ms:
+            stage_ms[k] += ev[k][0].elapsed_ms(ev[k][1]) / args.steps
+
+    # algorithmic bytes of the timed steps
+    bytes_step = {k: 0.0 for k in stage_ms}
+    for b in used:
+        for k, tb in enumerate(tables):
+            sp = wl.tables[k]
+            bm = byte_model(sp.T, U[b][k], sp.D, 2 if sp.grad_dtype == "bf16" else 4, sp.P)
+            for name in bytes_step:
+                bytes_step[name] += bm[name] / args.steps
     total_bytes = sum(bytes_step.values())
     step_gbps = total_bytes / (ms_step * 1e-3) / 1e9
-    adam_launches = len(tables)
-    adam_gbps = bytes_step["adam"] / (stage_ms["adam"] * 1e-3) / 1e9
+    # the roofline kernel: one adam launch of the first table per step
+    sp0 = wl.tables[0]
+    adam_bytes = sum(byte_model(sp0.T, U[b][0], sp0.D, 4, sp0.P)["adam"] for b in used) / args.steps
+    adam_gbps = adam_bytes / (adam_us * 1e-6) / 1e9
 
     result = {
         "metric": "unique grad rows/sec for coalesce+pack+update; achieved HBM GB/s vs peak",
@@ -237,22 +209,23 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16-in/f32" if any(tb.spec.grad_dtype == "bf16" for tb in tables) else "f32",
+        "dtype": "bf16-in/f32" if any(sp.grad_dtype == "bf16" for sp in wl.tables) else "f32",
         "data": "synthetic (seeded ids and N(0,sigma) gradients, random-init table)",
-        "config": {"workload": wl.name, "tables": [dict(V=t.spec.V, D=t.spec.D, T=t.spec.T, P=t.spec.P,
-                                                        ids=t.spec.id_law, owner=t.spec.owner_rule)
-                                                   for t in tables],
-                   "mean_unique_rows_per_step": rows / args.steps, "batches_rotated": args.batches},
+        "config": {"workload": wl.name,
+                   "tables": [dict(V=sp.V, D=sp.D, T=sp.T, P=sp.P, ids=sp.id_law, owner=sp.owner_rule)
+                              for sp in wl.tables],
+                   "mean_unique_rows_per_step": rows / args.steps, "batches_rotated": args.batches,
+                   "schedule": "sequential" if args.sequential else "two streams (coalesce+pack overlapped)"},
         "step_bytes_model": total_bytes,
         "step_hbm_GBps": step_gbps,
         "step_hbm_frac": step_gbps / HBM_PEAK_GBPS,
-        "stage_ms": stage_ms,
+        "sequential_ms_per_step": seq_total,
+        "stage_ms_sequential": stage_ms,
         "wall_s_timed": wall,
         "roofline": {"bound": "hbm", "kernel": "adam_kernel (emb_sparse_adam_apply)",
                      "achieved": adam_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": adam_gbps / HBM_PEAK_GBPS, "traffic": None,
-                     "bytes_per_launch": bytes_step["adam"] / adam_launches,
-                     "avg_launch_us": stage_ms["adam"] * 1e3 / adam_launches},
+                     "bytes_per_launch": adam_bytes, "avg_launch_us": adam_us},
         "host": host_info(),
     }
     if not args.no_cpu_baseline:

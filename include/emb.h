@@ -58,6 +58,8 @@ extern "C" {
 /* device status flags */
 #define EMB_DEV_ID_OUT_OF_RANGE 1    /* a token or row id was outside [0, V) */
 #define EMB_DEV_OWNER_OUT_OF_RANGE 2 /* row_owner[id] was outside [0, P) */
+#define EMB_DEV_STALLED 4            /* internal: a workgroup gave up waiting for the result \
+                                        of an earlier one; the outputs are invalid */
 
 int emb_abi_version(void);
 const char *emb_status_string(int status);
@@ -88,10 +90,13 @@ int emb_gather(const float *table, int64_t V, int32_t D, const int32_t *ids,
  * Sums are accumulated in fp32 in a fixed order that depends only on the ids
  * (sorted position order, in chunks of 32 tokens, then an ordered combine of
  * the chunk partials): results are bitwise reproducible run to run.
+ * Workgroups of one launch hand prefix sums to each other (decoupled
+ * look-back); every wait is bounded and a timeout sets EMB_DEV_STALLED.
  * workspace: device memory of at least
  * emb_grad_coalesce_workspace_bytes(T, V, D, grad_dtype) bytes, 256-byte
  * aligned; its contents on entry do not matter.
- * Requires 1 <= V < 2^31, D >= 1, T >= 0.  grad rows must be 4-byte aligned.
+ * Requires 1 <= V < 2^31, D >= 1, 0 <= T < 2^30.  grad must be 4-byte (fp32)
+ * or 2-byte (bf16) aligned.
  */
 size_t emb_grad_coalesce_workspace_bytes(int32_t T, int64_t V, int32_t D,
                                          int32_t grad_dtype);
@@ -157,6 +162,75 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
                           int32_t cap_rows, double lr, double beta1,
                           double beta2, double eps, int64_t step,
                           int32_t *dev_status, void *stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * Step executor.  Not a step of the path itself: it enqueues the four calls
+ * above for one training step of one table, in data order, on three streams,
+ * so that the latency-bound coalesce/pack work of a step overlaps the
+ * bandwidth-bound lookup and update of neighbouring steps (the sparse
+ * gradient work runs in GPU idle time, as in Vertical Sparse Scheduling,
+ * Sec. 4.2.2, here on one GPU).  One host call per step keeps the host ahead
+ * of the GPU.
+ *
+ * The caller alternates two buffer sets (uniq_* and send_* outputs) between
+ * consecutive steps and gives each set its own three events; `reuse` is
+ * nonzero when the set was used two steps earlier.  The executor then adds
+ * these waits, which keep every data dependency:
+ *   coalesce(s) after pack(s-2)             (same unique-row buffers)
+ *   pack(s)     after coalesce(s), update(s-2) (reads unique rows; same send buffers)
+ *   update(s)   after pack(s)               (reads the packed rows)
+ *   lookup(s+1) after update(s)              (same stream; reads the table)
+ * With all three streams equal the calls simply run one after another, and the
+ * results are bitwise the same either way.
+ * ---------------------------------------------------------------------------
+ */
+typedef struct {
+  void *lookup_update;          /* stream of emb_gather and emb_sparse_adam_apply */
+  void *coalesce;               /* stream of emb_grad_coalesce */
+  void *pack;                   /* stream of emb_pack_by_owner */
+  void *coalesced, *packed, *updated; /* events of this step's buffer set */
+  int32_t reuse;                /* the buffer set was used two steps ago */
+  void *timing[8];              /* optional timing events (NULL to skip): begin/end of
+                                   gather, coalesce, pack, adam, each recorded on the
+                                   stream its call runs on */
+} emb_step_schedule;
+
+typedef struct {
+  float *table, *exp_avg, *exp_avg_sq; /* [V][D] fp32, updated in place */
+  int64_t V;
+  int32_t D;
+  const int32_t *row_owner; /* [V] */
+  int32_t P;
+  const int32_t *ids;       /* [T] */
+  int32_t T;
+  const void *grad;         /* [T][D], grad_dtype */
+  int32_t grad_dtype;
+  int32_t cap_rows;         /* capacity of the uniq_* and send_* buffers (>= T) */
+  float *lookup;            /* [T][D] gather output */
+  int32_t *uniq_ids, *seg_offsets, *num_unique;
+  float *uniq_grad;
+  int32_t *send_ids, *send_counts, *send_offsets;
+  float *send_rows;
+  void *ws_coalesce;
+  size_t ws_coalesce_bytes;
+  void *ws_pack;
+  size_t ws_pack_bytes;
+  double lr, beta1, beta2, eps;
+  int64_t step;             /* Adam step (>= 1), one per iteration (Sec. 5.7) */
+  int32_t *dev_status;      /* optional */
+} emb_step_args;
+
+/* Events for the schedule (hipEventCreateWithFlags; timing: nonzero for
+ * timing events).  A host-side runtime object, not device memory. */
+int emb_event_create(void **event, int32_t timing);
+int emb_event_destroy(void *event);
+/* Milliseconds between two completed timing events. */
+int emb_event_elapsed_ms(void *start, void *end, float *ms);
+
+/* Enqueue one training step of one table (see above).  Returns the first
+ * failing call's status; nothing after it is enqueued. */
+int emb_train_step(const emb_step_args *args, const emb_step_schedule *sched);
 
 #ifdef __cplusplus
 }

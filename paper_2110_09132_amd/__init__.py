@@ -27,6 +27,7 @@ EMB_F32 = 0
 EMB_BF16 = 1
 EMB_DEV_ID_OUT_OF_RANGE = 1
 EMB_DEV_OWNER_OUT_OF_RANGE = 2
+EMB_DEV_STALLED = 4
 
 # (name, restype, argtypes) of every symbol include/emb.h declares.
 _P, _I32, _I64, _SZ, _D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_double
@@ -40,7 +41,27 @@ SIGNATURES = {
     "emb_pack_by_owner": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_sparse_adam_apply": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _P, _P, _P, _I32, _I32, _I32, _I32,
                                              _D, _D, _D, _D, _I64, _P, _P]),
+    "emb_event_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), _I32]),
+    "emb_event_destroy": (ctypes.c_int, [_P]),
+    "emb_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
+    "emb_train_step": (ctypes.c_int, [_P, _P]),
 }
+
+
+class StepSchedule(ctypes.Structure):
+    """emb_step_schedule of include/emb.h."""
+    _fields_ = [("lookup_update", _P), ("coalesce", _P), ("pack", _P), ("coalesced", _P), ("packed", _P),
+                ("updated", _P), ("reuse", _I32), ("timing", _P * 8)]
+
+
+class StepArgs(ctypes.Structure):
+    """emb_step_args of include/emb.h."""
+    _fields_ = [("table", _P), ("exp_avg", _P), ("exp_avg_sq", _P), ("V", _I64), ("D", _I32),
+                ("row_owner", _P), ("P", _I32), ("ids", _P), ("T", _I32), ("grad", _P), ("grad_dtype", _I32),
+                ("cap_rows", _I32), ("lookup", _P), ("uniq_ids", _P), ("seg_offsets", _P), ("num_unique", _P),
+                ("uniq_grad", _P), ("send_ids", _P), ("send_counts", _P), ("send_offsets", _P), ("send_rows", _P),
+                ("ws_coalesce", _P), ("ws_coalesce_bytes", _SZ), ("ws_pack", _P), ("ws_pack_bytes", _SZ),
+                ("lr", _D), ("beta1", _D), ("beta2", _D), ("eps", _D), ("step", _I64), ("dev_status", _P)]
 
 
 class EmbError(RuntimeError):
@@ -94,6 +115,26 @@ def _dtype_code(t):
 def _need(t, dtype, what):
     if t.dtype != dtype or not t.is_cuda or not t.is_contiguous():
         raise EmbError(f"{what} must be a contiguous {dtype} CUDA tensor (got {t.dtype}, {t.device})")
+
+
+class Event:
+    """A HIP event made by the library (emb_event_create); destroyed with the object."""
+
+    def __init__(self, timing: bool = False):
+        h = ctypes.c_void_p()
+        _check(lib.emb_event_create(ctypes.byref(h), 1 if timing else 0), "emb_event_create")
+        self.handle = h.value
+        self._lib = lib
+
+    def elapsed_ms(self, end: "Event") -> float:
+        ms = ctypes.c_float()
+        _check(lib.emb_event_elapsed_ms(self.handle, end.handle, ctypes.byref(ms)), "emb_event_elapsed_ms")
+        return float(ms.value)
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            self._lib.emb_event_destroy(self.handle)
+            self.handle = None
 
 
 def new_status(device=None):

@@ -1,22 +1,31 @@
 // COALESCE + UNIQUE of Algorithm 1 (Sec. 4.2.2): sum the gradient rows of
 // tokens with equal id, output the distinct ids in ascending order.
 //
-// Stages (all enqueued on one stream, no host synchronisation):
-//  1. LSD radix sort of (id, token position) pairs, stable, digits of <= 8 bits
-//     over bitwidth(V) key bits.  Ids outside [0, V) become the key V, which
-//     sorts after every valid id and is then ignored.  Each pass is two
-//     kernels: per-tile digit histograms, then a tile-local stable ranking in
-//     LDS (wave ballots) plus the tile's global digit bases, staged through LDS
-//     so that runs of one digit are written contiguously.
-//  2. Segment discovery over the sorted keys: per-tile head counts, then the
-//     unique index of every sorted element, uniq_ids, seg_offsets, num_unique.
-//  3. Deterministic segmented reduction: the sorted order is cut into chunks
-//     of kChunk tokens, one wave per chunk, summing rows in sorted order.
-//     Segments inside one chunk are written directly; the pieces of a segment
-//     that crosses chunk boundaries go to a partials buffer, and a combine
-//     kernel adds them in chunk order (4 waves per segment, each summing a
-//     contiguous range of pieces, then the 4 results in wave order).  The
-//     order of every addition depends only on the ids, never on scheduling.
+// Kernels (one stream, no host synchronisation):
+//  1. sort_upsweep: digit histograms of every radix pass at once (the digit
+//     totals do not depend on the order of the keys), one row per histogram
+//     tile; it also clears the look-back state used by the later kernels.
+//  2. sort_pass, once per digit of the bitwidth(V) key bits (<= 8 bits each):
+//     a stable LSD radix pass over (key, token position).  Each tile
+//     ranks its keys in LDS with wave ballots, publishes its per-digit counts
+//     and reads the counts of the tiles before it (decoupled look-back,
+//     Merrill & Garland 2016), so one launch per pass suffices.  Tiles take
+//     their index from a ticket counter, so a tile only waits for tiles that
+//     are already running.  Ids outside [0, V) become the key V, which sorts
+//     after every valid id.
+//  3. seg_count: the number of first tokens of an id (heads) in each run of
+//     128 sorted tokens.
+//  4. seg_reduce: each wave owns 32 consecutive sorted tokens.  It finds the
+//     heads with lane shuffles, adds up the head counts of the earlier
+//     workgroups, writes uniq_ids / seg_offsets / num_unique, and sums the
+//     gradient rows of its tokens in sorted order.  Sums of ids that lie
+//     inside the chunk are final; the pieces of an id that crosses chunk
+//     boundaries go to a partials buffer.
+//  5. seg_combine: adds the pieces of each crossing id in chunk order
+//     (4 waves per id, each summing a contiguous range of pieces, then the
+//     4 results in wave order).
+// The order of every floating-point addition depends only on the ids, never
+// on scheduling, so results are bitwise reproducible.
 #include "common.h"
 #include "launch.h"
 
@@ -24,76 +33,217 @@ namespace emb {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
 constexpr int kItems = 8;
-constexpr int kTile = kThreads * kItems;  // keys per sort / segment tile
-constexpr int kRadixBitsMax = 8;
-constexpr int kBinsMax = 1 << kRadixBitsMax;
-constexpr int kChunk = 32;       // sorted tokens per reduction wave
+constexpr int kMaxPasses = 4;  // up to 31 key bits
+
+// Radix configuration: passes of <= 8-bit digits, 256-thread tiles of 2048 keys.
+// (Two passes of 11-bit digits were measured slower than three of 8 bits: the
+// 2048-bin ranking is LDS-bound and runs on half as many tiles.)
+template <int NT, int BITS>
+struct SortCfg {
+  static constexpr int kNT = NT;
+  static constexpr int kBins = 1 << BITS;
+  static constexpr int kTile = NT * kItems;      // keys per sort tile
+  static constexpr int kUpTile = NT * 16;        // keys per histogram tile
+  static constexpr int kPasses = kMaxPasses;  // most passes this configuration runs
+};
+using Narrow = SortCfg<256, 8>;
+constexpr int kChunk = 32;                    // sorted tokens per reduction wave
+constexpr int kRedTile = kChunk * kWaves;     // sorted tokens per reduction workgroup
 constexpr int kLoadsInFlight = 8;
-constexpr int kCombineWaves = kThreads / kWave;
+constexpr uint32_t kSpinLimit = 1u << 22;
+
+// Look-back status word: value in the low 30 bits, state in the top 2 bits.
+constexpr uint32_t kAggregate = 1u << 30;  // the tile's own count
+constexpr uint32_t kInclusive = 2u << 30;  // the count of this and every earlier tile
+constexpr uint32_t kStateMask = 3u << 30;
+constexpr uint32_t kValueMask = ~kStateMask;
+
+__device__ __forceinline__ void publish(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t peek(uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 __device__ __forceinline__ uint32_t sanitize(int32_t id, uint32_t V) {
   return (id >= 0 && static_cast<uint32_t>(id) < V) ? static_cast<uint32_t>(id) : V;
 }
 
-// ---------------------------------------------------------------- radix sort
-__global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t* __restrict__ keys,
-                                                              const int32_t* __restrict__ raw_ids, uint32_t V,
-                                                              int T, int shift, int bits,
-                                                              uint32_t* __restrict__ tile_hist, int32_t* status) {
-  __shared__ uint32_t h[kBinsMax];
-  const int bins = 1 << bits;
-  for (int i = threadIdx.x; i < bins; i += kThreads) h[i] = 0;
-  __syncthreads();
-  const int base = blockIdx.x * kTile;
-  bool bad = false;
-  uint32_t k[kItems];
+// Exclusive prefix of one digit's counts over tiles 0 .. tile-1, read from
+// status words lb[t * stride] (nearest first, kWindow at a time) until a tile with
+// an inclusive count is found.  Every tile publishes its aggregate before it
+// waits, so the wait ends; it is bounded anyway and reports EMB_DEV_STALLED.
+__device__ uint32_t digit_look_back(uint32_t* lb, int tile, int stride, int32_t* status) {
+  constexpr int kWindow = 16;
+  uint32_t excl = 0;
+  int j = tile - 1;
+  uint32_t spins = 0;
+  while (j >= 0) {
+    uint32_t s[kWindow];
 #pragma unroll
-  for (int r = 0; r < kItems; ++r) {
-    const int g = min(base + r * kThreads + static_cast<int>(threadIdx.x), T - 1);
-    k[r] = raw_ids != nullptr ? sanitize(raw_ids[g], V) : keys[g];
+    for (int k = 0; k < kWindow; ++k) s[k] = peek(lb + static_cast<size_t>(max(j - k, 0)) * stride);
+    uint32_t acc = 0;
+    bool blocked = false, done = false;
+#pragma unroll
+    for (int k = 0; k < kWindow; ++k) {
+      if (done || blocked) continue;
+      if (j - k < 0) {
+        done = true;
+        continue;
+      }
+      const uint32_t st = s[k] & kStateMask;
+      if (st == 0) {
+        blocked = true;
+        continue;
+      }
+      acc += s[k] & kValueMask;
+      done = (st == kInclusive);
+    }
+    if (blocked) {
+      if (++spins > kSpinLimit) {
+        raise_flag(status, EMB_DEV_STALLED);
+        return excl;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    excl += acc;
+    if (done) return excl;
+    j -= kWindow;
   }
+  return excl;
+}
+
+struct RadixPlan {
+  int npass;  // number of passes
+  int per;    // bits per pass (<= 8)
+  int B;      // key bits
+  __host__ __device__ int shift(int p) const { return p * per; }
+  __host__ __device__ int bits(int p) const { return min(per, B - p * per); }
+};
+
+int key_bits(int64_t V) {  // keys 0 .. V (V is the key of invalid ids)
+  int B = 0;
+  while ((int64_t{1} << B) <= V) ++B;
+  return B;
+}
+
+RadixPlan plan_for(int64_t V) {
+  const int B = key_bits(V);
+  const int digit = 8;
+  const int npass = (B + digit - 1) / digit;
+  return RadixPlan{npass, (B + npass - 1) / npass, B};
+}
+
+// ---------------------------------------------------------------- radix sort
+template <class C>
+__global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const int32_t* __restrict__ ids, uint32_t V, int T,
+                                                              RadixPlan plan, uint32_t* __restrict__ up_hist,
+                                                              uint32_t* __restrict__ zero_begin, int zero_words,
+                                                              int32_t* status) {
+  constexpr int NT = C::kNT, kBins = C::kBins, kPer = C::kUpTile / NT;
+  __shared__ uint32_t h[C::kPasses * kBins];
+  for (int i = threadIdx.x; i < plan.npass * kBins; i += NT) h[i] = 0;
+  __syncthreads();
+  const int base = blockIdx.x * C::kUpTile;
+  uint32_t k[kPer];
 #pragma unroll
-  for (int r = 0; r < kItems; ++r) {
-    if (base + r * kThreads + static_cast<int>(threadIdx.x) < T) {
+  for (int r = 0; r < kPer; ++r) k[r] = sanitize(ids[min(base + r * NT + static_cast<int>(threadIdx.x), T - 1)], V);
+  bool bad = false;
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) {
+    if (base + r * NT + static_cast<int>(threadIdx.x) < T) {
       bad |= (k[r] == V);
-      atomicAdd(&h[(k[r] >> shift) & (bins - 1)], 1u);
+      for (int p = 0; p < plan.npass; ++p)
+        atomicAdd(&h[p * kBins + ((k[r] >> plan.shift(p)) & ((1u << plan.bits(p)) - 1u))], 1u);
     }
   }
   if (__any(bad) && lane_id() == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
   __syncthreads();
-  for (int i = threadIdx.x; i < bins; i += kThreads) tile_hist[static_cast<size_t>(blockIdx.x) * bins + i] = h[i];
+  for (int i = threadIdx.x; i < plan.npass * kBins; i += NT)
+    up_hist[static_cast<size_t>(blockIdx.x) * plan.npass * kBins + i] = h[i];
+  for (int i = blockIdx.x * NT + threadIdx.x; i < zero_words; i += gridDim.x * NT) zero_begin[i] = 0;
 }
 
-__global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
+template <class C>
+__global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ raw_ids, const int32_t* __restrict__ vals_in,
-    uint32_t V, int T, int shift, int bits, const uint32_t* __restrict__ tile_hist, int ntiles,
-    uint32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out) {
-  __shared__ uint32_t cnt[(kThreads / kWave) * kBinsMax];
-  __shared__ uint32_t dstart[kBinsMax], colall[kBinsMax], gbase[kBinsMax];
-  __shared__ uint32_t red_all[kThreads], red_bef[kThreads];
-  __shared__ uint32_t wsum[kThreads / kWave];
+    uint32_t V, int T, RadixPlan plan, int pass, const uint32_t* __restrict__ up_hist, int nup, uint32_t* lookback,
+    uint32_t* ticket, int ntiles, uint32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out, int32_t* status) {
+  constexpr int NT = C::kNT, kBins = C::kBins, kTile = C::kTile, NW = NT / kWave;
+  constexpr int kDigitsPerThread = (kBins + NT - 1) / NT;
+  __shared__ uint32_t cnt[NW * kBins];
+  __shared__ uint32_t dstart[kBins], gbase[kBins];
+  __shared__ uint32_t wsum[NW];
   __shared__ uint32_t skeys[kTile];
   __shared__ int32_t svals[kTile];
+  __shared__ int tile_s;
+  if (threadIdx.x == 0) tile_s = static_cast<int>(atomicAdd(ticket, 1u));
+  __syncthreads();
+  const int tile = tile_s;
+  if (tile < 0 || tile >= ntiles) {  // the ticket counter was not cleared: never index with it
+    if (threadIdx.x == 0) raise_flag(status, EMB_DEV_STALLED);
+    return;
+  }
+  const int shift = plan.shift(pass);
+  const int bits = plan.bits(pass);
   const int bins = 1 << bits;
-  const int tile = blockIdx.x;
   const int base = tile * kTile;
   const int w = threadIdx.x / kWave;
 
+  // keys of this tile, in (wave, round, lane) order = input order
   uint32_t key[kItems], dig[kItems], lpos[kItems];
   int32_t val[kItems];
   bool valid[kItems];
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const int g = base + w * kItems * kWave + r * kWave + static_cast<int>(lane_id());
-    const int gc = min(g, T - 1);  // clamped: every load is issued unconditionally
+    const int gc = min(g, T - 1);
     valid[r] = g < T;
     key[r] = raw_ids != nullptr ? sanitize(raw_ids[gc], V) : keys_in[gc];
     val[r] = vals_in != nullptr ? vals_in[gc] : g;
     dig[r] = (key[r] >> shift) & (bins - 1);
   }
-  tile_global_bases<kThreads>(tile_hist, ntiles, tile, bins, colall, gbase, red_all, red_bef, wsum);
-  tile_stable_rank<kThreads, kItems>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
+  // where each digit starts in the sorted output: exclusive scan of the digit totals
+#pragma unroll
+  for (int q = 0; q < kDigitsPerThread; ++q) {
+    const int d = static_cast<int>(threadIdx.x) + q * NT;
+    uint32_t tot = 0;
+    for (int u0 = 0; u0 < nup; u0 += 16) {
+      uint32_t v[16];
+#pragma unroll
+      for (int z = 0; z < 16; ++z)
+        v[z] = up_hist[(static_cast<size_t>(min(u0 + z, nup - 1)) * plan.npass + pass) * kBins + min(d, kBins - 1)];
+#pragma unroll
+      for (int z = 0; z < 16; ++z) tot += (u0 + z < nup) ? v[z] : 0u;
+    }
+    if (d < kBins) gbase[d] = d < bins ? tot : 0u;
+  }
+  __syncthreads();
+  block_exclusive_scan<NT>(gbase, bins, wsum);
+
+  const uint32_t nvalid = tile_stable_rank<NT, kItems>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
+#pragma unroll
+  for (int q = 0; q < kDigitsPerThread; ++q) {
+    const int d = static_cast<int>(threadIdx.x) + q * NT;
+    if (d < bins) {
+      const uint32_t mine = (d + 1 < bins ? dstart[d + 1] : nvalid) - dstart[d];
+      uint32_t* slot = lookback + static_cast<size_t>(tile) * kBins + d;
+      publish(slot, (tile == 0 ? kInclusive : kAggregate) | mine);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kDigitsPerThread; ++q) {
+    const int d = static_cast<int>(threadIdx.x) + q * NT;
+    if (d < bins && tile > 0) {
+      const uint32_t mine = (d + 1 < bins ? dstart[d + 1] : nvalid) - dstart[d];
+      const uint32_t excl = digit_look_back(lookback + d, tile, kBins, status);
+      publish(lookback + static_cast<size_t>(tile) * kBins + d, kInclusive | (excl + mine));
+      gbase[d] += excl;
+    }
+  }
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     if (valid[r]) {
@@ -102,114 +252,17 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     }
   }
   __syncthreads();
-  const int n = min(kTile, T - base);
-  for (int i = threadIdx.x; i < n; i += kThreads) {
+  const int n = static_cast<int>(nvalid);
+  for (int i = threadIdx.x; i < n; i += NT) {
     const uint32_t k = skeys[i];
-    const uint32_t d = (k >> shift) & (bins - 1);
-    const uint32_t dest = gbase[d] + (static_cast<uint32_t>(i) - dstart[d]);
+    const uint32_t dd = (k >> shift) & (bins - 1);
+    const uint32_t dest = gbase[dd] + (static_cast<uint32_t>(i) - dstart[dd]);
     keys_out[dest] = k;
     vals_out[dest] = svals[i];
   }
 }
 
-// ------------------------------------------------------- segment discovery
-// Each thread owns kItems consecutive sorted keys; it loads them together with
-// the key before (head test) and the key after (last-valid test).
-struct KeyWindow {
-  uint32_t k[kItems + 2];  // k[j] = skeys[base - 1 + j], clamped to [0, T)
-  __device__ KeyWindow(const uint32_t* __restrict__ skeys, int base, int T) {
-#pragma unroll
-    for (int j = 0; j < kItems + 2; ++j) k[j] = skeys[min(max(base - 1 + j, 0), T - 1)];
-  }
-  // sorted element base + j is the first of its id (j < kItems)
-  __device__ bool head(int base, int j, int T, uint32_t V) const {
-    const int i = base + j;
-    return i < T && k[j + 1] < V && (i == 0 || k[j] != k[j + 1]);
-  }
-};
-
-__global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t* __restrict__ skeys, uint32_t V, int T,
-                                                             uint32_t* __restrict__ tile_heads) {
-  __shared__ uint32_t wsum[kThreads / kWave];
-  const int base = blockIdx.x * kTile + threadIdx.x * kItems;
-  const KeyWindow win(skeys, base, T);
-  uint32_t c = 0;
-#pragma unroll
-  for (int j = 0; j < kItems; ++j) c += win.head(base, j, T, V) ? 1u : 0u;
-  c = wave_sum(c);
-  if (lane_id() == 0) wsum[threadIdx.x / kWave] = c;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t s = 0;
-    for (int i = 0; i < kThreads / kWave; ++i) s += wsum[i];
-    tile_heads[blockIdx.x] = s;
-  }
-}
-
-__global__ __launch_bounds__(kThreads) void seg_emit_kernel(const uint32_t* __restrict__ skeys, uint32_t V, int T,
-                                                            const uint32_t* __restrict__ tile_heads,
-                                                            int32_t* __restrict__ uniq_ids,
-                                                            int32_t* __restrict__ seg_offsets,
-                                                            int32_t* __restrict__ num_unique,
-                                                            int32_t* __restrict__ seg_of,
-                                                            int32_t* __restrict__ span_count) {
-  __shared__ uint32_t wsum[kThreads / kWave];
-  __shared__ uint32_t tile_base;
-  const int base = blockIdx.x * kTile + threadIdx.x * kItems;
-  const KeyWindow win(skeys, base, T);
-  // heads in earlier tiles (8 loads in flight per thread)
-  uint32_t s = 0;
-  for (int t0 = threadIdx.x; t0 < static_cast<int>(blockIdx.x); t0 += 8 * kThreads) {
-    uint32_t v[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = tile_heads[min(t0 + k * kThreads, static_cast<int>(blockIdx.x) - 1)];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) s += (t0 + k * kThreads < static_cast<int>(blockIdx.x)) ? v[k] : 0u;
-  }
-  s = wave_sum(s);
-  if (lane_id() == 0) wsum[threadIdx.x / kWave] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t b = 0;
-    for (int i = 0; i < kThreads / kWave; ++i) b += wsum[i];
-    tile_base = b;
-  }
-  __syncthreads();
-  // heads of this thread's items, exclusive scan over the block
-  uint32_t c = 0;
-#pragma unroll
-  for (int j = 0; j < kItems; ++j) c += win.head(base, j, T, V) ? 1u : 0u;
-  const uint32_t inc = wave_inclusive_scan(c);
-  if (lane_id() == kWave - 1) wsum[threadIdx.x / kWave] = inc;
-  __syncthreads();
-  uint32_t wbase = 0;
-  for (int i = 0; i < static_cast<int>(threadIdx.x / kWave); ++i) wbase += wsum[i];
-  // number of heads before the current item, over the whole sorted array
-  uint32_t run = tile_base + wbase + inc - c;
-#pragma unroll
-  for (int j = 0; j < kItems; ++j) {
-    const int i = base + j;
-    const uint32_t key = win.k[j + 1];
-    if (i < T && key < V) {
-      if (win.head(base, j, T, V)) {
-        uniq_ids[run] = static_cast<int32_t>(key);
-        seg_offsets[run] = i;
-        ++run;
-      }
-      seg_of[i] = static_cast<int32_t>(run - 1);
-      if (i + 1 == T || win.k[j + 2] >= V) {  // last valid token
-        seg_offsets[run] = i + 1;
-        num_unique[0] = static_cast<int32_t>(run);
-      }
-    } else if (i == 0 && T > 0) {  // no valid token at all
-      seg_offsets[0] = 0;
-      num_unique[0] = 0;
-    }
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) span_count[0] = 0;
-}
-
-// --------------------------------------------------------- segmented reduction
+// --------------------------------------------- segments + segmented reduction
 template <bool BF16, int VEC>
 struct GradRow;
 
@@ -244,66 +297,150 @@ struct GradRow<true, 1> {
   }
 };
 
+// Heads (first sorted token of an id) of element e, for the sorted keys: the
+// element is valid and its key differs from the previous one.
+__device__ __forceinline__ bool is_head(const uint32_t* __restrict__ skeys, int e, uint32_t V) {
+  const uint32_t k = skeys[e];
+  return k < V && (e == 0 || skeys[e - 1] != k);
+}
+
+// Number of heads among the kRedTile sorted tokens of each reduction workgroup.
+__global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t* __restrict__ skeys, uint32_t V, int T,
+                                                             uint32_t* __restrict__ tile_heads, int ntiles) {
+  const int tile = blockIdx.x * kWaves + threadIdx.x / kWave;  // one wave per reduction workgroup
+  if (tile >= ntiles) return;
+  uint32_t c = 0;
+  for (int k = static_cast<int>(lane_id()); k < kRedTile; k += kWave) {
+    const int e = tile * kRedTile + k;
+    c += (e < T && is_head(skeys, e, V)) ? 1u : 0u;
+  }
+  c = wave_sum(c);
+  if (lane_id() == 0) tile_heads[tile] = c;
+}
+
 template <bool BF16, int VEC>
 __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
-    const void* __restrict__ grad, int D, const int32_t* __restrict__ spos, const int32_t* __restrict__ seg_of,
-    const int32_t* __restrict__ seg_offsets, const int32_t* __restrict__ num_unique, int nchunks,
-    float* __restrict__ uniq_grad, float* __restrict__ partial, int32_t* __restrict__ span_list,
-    int32_t* __restrict__ span_count) {
+    const uint32_t* __restrict__ skeys, const int32_t* __restrict__ spos, uint32_t V, int T,
+    const void* __restrict__ grad, int D, const uint32_t* __restrict__ tile_heads,
+    int32_t* __restrict__ uniq_ids,
+    int32_t* __restrict__ seg_offsets, int32_t* __restrict__ num_unique, float* __restrict__ uniq_grad,
+    float* __restrict__ partial, int32_t* __restrict__ span_list, int32_t* __restrict__ span_count,
+    int32_t* status) {
+  __shared__ uint32_t wave_heads[kWaves];
+  __shared__ uint32_t red[kWaves];
+  const int tile = blockIdx.x;
+  const int w = threadIdx.x / kWave;
+  const int lane = static_cast<int>(lane_id());
+  const int chunk = tile * kWaves + w;
+  const int a = chunk * kChunk;
+
+  // lane L holds sorted element e = a - 1 + L, for L = 0 .. kChunk + 1
+  const int e = a - 1 + lane;
+  const int ec = min(max(e, 0), T - 1);
+  const uint32_t key = skeys[ec];
+  const int32_t pos = spos[ec];
+  const bool valid = e >= 0 && e < T && key < V && lane <= kChunk + 1;
+  const uint32_t key_prev = __shfl_up(key, 1, kWave);
+  // element e does not continue the id of element e - 1
+  const bool starts_new = !valid || e == 0 || key_prev != key;
+  const bool in_chunk = lane >= 1 && lane <= kChunk;
+  const bool head = in_chunk && valid && starts_new;
+  const uint64_t heads = __ballot(head);
+  const uint64_t brk = __ballot(starts_new);
+  const int nv = __popcll(__ballot(in_chunk && valid));  // valid tokens of the chunk (a prefix of it)
+  if (lane == 0) wave_heads[w] = static_cast<uint32_t>(__popcll(heads));
+  // heads before this workgroup: the sum of the earlier workgroups' counts
+  uint32_t before = 0;
+  for (int t0 = 0; t0 < tile; t0 += kThreads * 4) {
+    uint32_t v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = tile_heads[min(t0 + q * kThreads + static_cast<int>(threadIdx.x), tile - 1)];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) before += (t0 + q * kThreads + static_cast<int>(threadIdx.x) < tile) ? v[q] : 0u;
+  }
+  before = wave_sum(before);
+  if (lane == 0) red[w] = before;
+  // The first rows do not depend on the unique indices: their loads are issued
+  // before the workgroup combines its counts.
   using Row = GradRow<BF16, VEC>;
   using Acc = typename Row::Acc;
-  const int chunk = uniform(static_cast<int>(blockIdx.x) * (kThreads / kWave) + static_cast<int>(threadIdx.x / kWave));
-  if (chunk >= nchunks) return;
-  const int nvalid = seg_offsets[num_unique[0]];
-  const int a = chunk * kChunk;
-  const int b = min(a + kChunk, nvalid);
-  if (a >= b) return;
   const int Dv = D / VEC;
+  Acc g0[kLoadsInFlight];
+  if (nv > 0) {
+    const int cc = min(lane, Dv - 1);
+#pragma unroll
+    for (int k = 0; k < kLoadsInFlight; ++k)
+      g0[k] = Row::load(grad, static_cast<size_t>(__builtin_amdgcn_readlane(pos, min(k, nv - 1) + 1)), Dv, cc);
+  }
+  __syncthreads();
+  uint32_t ubase = 0;
+#pragma unroll
+  for (int q = 0; q < kWaves; ++q) ubase += red[q];
+  for (int q = 0; q < w; ++q) ubase += wave_heads[q];
+  const uint64_t upto = (lane == kWave - 1) ? ~0ull : ((2ull << lane) - 1ull);
+  const int u = static_cast<int>(ubase + __popcll(heads & upto)) - 1;  // unique index of element e
+  if (head) {
+    uniq_ids[u] = static_cast<int32_t>(key);
+    seg_offsets[u] = e;
+  }
+  const bool next_valid = __shfl_down(valid ? 1 : 0, 1, kWave) != 0;
+  if (in_chunk && valid && (e + 1 == T || !next_valid)) {
+    seg_offsets[u + 1] = e + 1;  // the last valid token of the whole batch
+    num_unique[0] = u + 1;
+  }
+  if (chunk == 0 && lane == 1 && !valid) {  // no valid token at all
+    seg_offsets[0] = 0;
+    num_unique[0] = 0;
+  }
+  if (nv == 0) return;
+
+  // sum the rows of the chunk's tokens in sorted order, one run of equal ids at a time
   Acc* out_rows = reinterpret_cast<Acc*>(uniq_grad);
   Acc* part_rows = reinterpret_cast<Acc*>(partial);
-
   for (int cb = 0; cb < Dv; cb += kWave) {
-    const int c = cb + static_cast<int>(lane_id());
+    const int c = cb + lane;
     const bool colok = c < Dv;
-    const int cc = min(c, Dv - 1);  // clamped column: loads are unconditional
+    const int cc = min(c, Dv - 1);
     Acc acc = Acc{};
-    int cur = seg_of[a];
-    int rs = a;
-    auto flush = [&](int u, int s, int e) {
-      const int S = seg_offsets[u];
-      const int E = seg_offsets[u + 1];
-      if (S == s && E == e) {
-        if (colok) out_rows[static_cast<size_t>(u) * Dv + c] = acc;
+    int rs = 0;
+    int cur = __builtin_amdgcn_readlane(u, 1);
+    auto flush = [&](int uu, int s, int t) {  // run of chunk tokens [s, t)
+      const bool whole = ((brk >> (s + 1)) & 1ull) && ((brk >> (t + 1)) & 1ull);
+      if (whole) {
+        if (colok) out_rows[static_cast<size_t>(uu) * Dv + c] = acc;
       } else {
-        const int slot = (s == a) ? 0 : 1;
+        const int slot = (s == 0) ? 0 : 1;
         if (colok) part_rows[(static_cast<size_t>(chunk) * 2 + slot) * Dv + c] = acc;
-        if (s == S && cb == 0 && lane_id() == 0) span_list[atomicAdd(span_count, 1)] = u;
+        if (((brk >> (s + 1)) & 1ull) && cb == 0 && lane == 0) span_list[atomicAdd(span_count, 1)] = uu;
       }
     };
-    for (int i0 = a; i0 < b; i0 += kLoadsInFlight) {
-      int u[kLoadsInFlight];
+    for (int j0 = 0; j0 < nv; j0 += kLoadsInFlight) {
       Acc g[kLoadsInFlight];
 #pragma unroll
       for (int k = 0; k < kLoadsInFlight; ++k) {
-        const int ic = min(i0 + k, b - 1);
-        u[k] = seg_of[ic];
-        g[k] = Row::load(grad, static_cast<size_t>(spos[ic]), Dv, cc);
+        if (cb == 0 && j0 == 0) {
+          g[k] = g0[k];  // already loaded
+        } else {
+          const int j = min(j0 + k, nv - 1);
+          const int p = __builtin_amdgcn_readlane(pos, j + 1);
+          g[k] = Row::load(grad, static_cast<size_t>(p), Dv, cc);
+        }
       }
 #pragma unroll
       for (int k = 0; k < kLoadsInFlight; ++k) {
-        const int i = i0 + k;
-        if (i < b) {
-          if (u[k] != cur) {
-            flush(cur, rs, i);
+        const int j = j0 + k;
+        if (j < nv) {
+          if (j > rs && ((brk >> (j + 1)) & 1ull)) {
+            flush(cur, rs, j);
             acc = Acc{};
-            cur = u[k];
-            rs = i;
+            rs = j;
+            cur = __builtin_amdgcn_readlane(u, j + 1);
           }
           acc += g[k];
         }
       }
     }
-    flush(cur, rs, b);
+    flush(cur, rs, nv);
   }
 }
 
@@ -314,7 +451,7 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
                                                                const int32_t* __restrict__ span_count,
                                                                float* __restrict__ uniq_grad) {
   using Acc = typename GradRow<false, VEC>::Acc;
-  __shared__ Acc red[kCombineWaves][kWave];
+  __shared__ Acc red[kWaves][kWave];
   const int n = span_count[0];
   const int Dv = D / VEC;
   const int w = threadIdx.x / kWave;
@@ -327,8 +464,8 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
     const int c0 = S / kChunk;
     const int np = (E - 1) / kChunk - c0 + 1;
     const int first_slot = (S == c0 * kChunk) ? 0 : 1;
-    const int p_beg = static_cast<int>((static_cast<long long>(w) * np) / kCombineWaves);
-    const int p_end = static_cast<int>((static_cast<long long>(w + 1) * np) / kCombineWaves);
+    const int p_beg = static_cast<int>((static_cast<long long>(w) * np) / kWaves);
+    const int p_end = static_cast<int>((static_cast<long long>(w + 1) * np) / kWaves);
     for (int cb = 0; cb < Dv; cb += kWave) {
       const int c = cb + static_cast<int>(lane_id());
       const bool colok = c < Dv;
@@ -351,7 +488,7 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
       if (w == 0 && colok) {
         Acc t = red[0][lane_id()];
 #pragma unroll
-        for (int q = 1; q < kCombineWaves; ++q) t += red[q][lane_id()];
+        for (int q = 1; q < kWaves; ++q) t += red[q][lane_id()];
         out_rows[static_cast<size_t>(u) * Dv + c] = t;
       }
       __syncthreads();
@@ -364,47 +501,78 @@ __global__ void empty_batch_kernel(int32_t* seg_offsets, int32_t* num_unique) {
   num_unique[0] = 0;
 }
 
-int key_bits(int64_t V) {  // bits needed for keys 0..V (V is the invalid-id key)
-  int b = 0;
-  while ((int64_t{1} << b) <= V) ++b;
-  return b;
-}
-
 struct CoalesceWs {
   uint32_t *keys_a, *keys_b;
   int32_t *vals_a, *vals_b;
-  uint32_t* tile_hist;
-  uint32_t* tile_heads;
-  int32_t* seg_of;
-  int32_t* span_list;
+  uint32_t* up_hist;
+  uint32_t* zero_begin;  // everything from here to zero_end starts at zero
+  uint32_t* sort_lb;     // [npass][ntiles][kBins]
+  uint32_t* tickets;     // [kMaxPasses]
   int32_t* span_count;
+  uint32_t* zero_end;
+  int32_t* span_list;
+  uint32_t* tile_heads;  // [nred]
   float* partial;
   size_t bytes;
 };
 
-CoalesceWs carve(void* base, int T, int D) {
+template <class C>
+CoalesceWs carve_with(void* base, int T, int64_t V, int D) {
   Carver cv{static_cast<char*>(base)};
+  const RadixPlan plan = plan_for(V);
   const size_t n = static_cast<size_t>(T);
-  const size_t ntiles = (n + kTile - 1) / kTile;
+  const size_t ntiles = (n + C::kTile - 1) / C::kTile;
+  const size_t nup = (n + C::kUpTile - 1) / C::kUpTile;
+  const size_t nred = (n + kRedTile - 1) / kRedTile;
   const size_t nchunks = (n + kChunk - 1) / kChunk;
   CoalesceWs w;
   w.keys_a = cv.take<uint32_t>(n);
   w.keys_b = cv.take<uint32_t>(n);
   w.vals_a = cv.take<int32_t>(n);
   w.vals_b = cv.take<int32_t>(n);
-  w.tile_hist = cv.take<uint32_t>(ntiles * kBinsMax);
-  w.tile_heads = cv.take<uint32_t>(ntiles);
-  w.seg_of = cv.take<int32_t>(n);
-  w.span_list = cv.take<int32_t>(nchunks);
+  w.up_hist = cv.take<uint32_t>(nup * plan.npass * C::kBins);
+  w.sort_lb = cv.take<uint32_t>(static_cast<size_t>(plan.npass) * ntiles * C::kBins);
+  w.zero_begin = w.sort_lb;
+  w.tickets = cv.take<uint32_t>(kMaxPasses);
   w.span_count = cv.take<int32_t>(1);
+  w.zero_end = cv.take<uint32_t>(0);
+  w.span_list = cv.take<int32_t>(nchunks);
+  w.tile_heads = cv.take<uint32_t>(nred);
   w.partial = cv.take<float>(nchunks * 2 * static_cast<size_t>(D));
   w.bytes = cv.size();
   return w;
 }
 
+CoalesceWs carve(void* base, int T, int64_t V, int D) { return carve_with<Narrow>(base, T, V, D); }
+
+template <class C>
+void launch_sort(const int32_t* ids, int T, uint32_t Vk, const RadixPlan& plan, const CoalesceWs& ws,
+                 int32_t* status, hipStream_t stream, const uint32_t** skeys, const int32_t** spos) {
+  const int ntiles = (T + C::kTile - 1) / C::kTile;
+  const int nup = (T + C::kUpTile - 1) / C::kUpTile;
+  const int zero_words = static_cast<int>(ws.zero_end - ws.zero_begin);
+  hipLaunchKernelGGL(sort_upsweep_kernel<C>, dim3(nup), dim3(C::kNT), 0, stream, ids, Vk, T, plan, ws.up_hist,
+                     ws.zero_begin, zero_words, status);
+  const uint32_t* kin = nullptr;
+  const int32_t* vin = nullptr;
+  uint32_t* kout = ws.keys_a;
+  int32_t* vout = ws.vals_a;
+  for (int p = 0; p < plan.npass; ++p) {
+    hipLaunchKernelGGL(sort_pass_kernel<C>, dim3(ntiles), dim3(C::kNT), 0, stream, kin, (p == 0) ? ids : nullptr,
+                       vin, Vk, T, plan, p, ws.up_hist, nup, ws.sort_lb + static_cast<size_t>(p) * ntiles * C::kBins,
+                       ws.tickets + p, ntiles, kout, vout, status);
+    kin = kout;
+    vin = vout;
+    kout = (kout == ws.keys_a) ? ws.keys_b : ws.keys_a;
+    vout = (vout == ws.vals_a) ? ws.vals_b : ws.vals_a;
+  }
+  *skeys = kin;
+  *spos = vin;
+}
+
 }  // namespace
 
-size_t coalesce_workspace_bytes(int T, int64_t /*V*/, int D) { return carve(nullptr, T, D).bytes; }
+size_t coalesce_workspace_bytes(int T, int64_t V, int D) { return carve(nullptr, T, V, D).bytes; }
 
 hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
                            int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad, int32_t* num_unique,
@@ -413,64 +581,42 @@ hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool gra
     hipLaunchKernelGGL(empty_batch_kernel, dim3(1), dim3(1), 0, stream, seg_offsets, num_unique);
     return hipGetLastError();
   }
-  CoalesceWs ws = carve(workspace, T, D);
+  CoalesceWs ws = carve(workspace, T, V, D);
+  const RadixPlan plan = plan_for(V);
   const uint32_t Vk = static_cast<uint32_t>(V);
-  const int ntiles = (T + kTile - 1) / kTile;
+  const int nred = (T + kRedTile - 1) / kRedTile;
   const int nchunks = (T + kChunk - 1) / kChunk;
 
-  // 1. radix sort of (key, position)
-  const int B = key_bits(V);
-  const int npass = (B + kRadixBitsMax - 1) / kRadixBitsMax;
-  const int per = (B + npass - 1) / npass;
+  // 1-2. digit histograms of all passes, then the radix passes over (key, position)
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
-  uint32_t* kout = ws.keys_a;
-  int32_t* vout = ws.vals_a;
-  for (int p = 0; p < npass; ++p) {
-    const int shift = p * per;
-    const int bits = min(per, B - shift);
-    const int32_t* raw = (p == 0) ? ids : nullptr;
-    hipLaunchKernelGGL(radix_hist_kernel, dim3(ntiles), dim3(kThreads), 0, stream, kin, raw, Vk, T, shift, bits,
-                       ws.tile_hist, status);
-    hipLaunchKernelGGL(radix_scatter_kernel, dim3(ntiles), dim3(kThreads), 0, stream, kin, raw, vin, Vk, T, shift,
-                       bits, ws.tile_hist, ntiles, kout, vout);
-    kin = kout;
-    vin = vout;
-    kout = (kout == ws.keys_a) ? ws.keys_b : ws.keys_a;
-    vout = (vout == ws.vals_a) ? ws.vals_b : ws.vals_a;
-  }
-  const uint32_t* skeys = kin;
-  const int32_t* spos = vin;
-
-  // 2. segments
-  hipLaunchKernelGGL(seg_count_kernel, dim3(ntiles), dim3(kThreads), 0, stream, skeys, Vk, T, ws.tile_heads);
-  hipLaunchKernelGGL(seg_emit_kernel, dim3(ntiles), dim3(kThreads), 0, stream, skeys, Vk, T, ws.tile_heads,
-                     uniq_ids, seg_offsets, num_unique, ws.seg_of, ws.span_count);
-
-  // 3. reduction
+  launch_sort<Narrow>(ids, T, Vk, plan, ws, status, stream, &kin, &vin);
+  // 3. heads per reduction workgroup; 4. segments and per-chunk sums; 5. pieces of ids that cross chunks
+  hipLaunchKernelGGL(seg_count_kernel, dim3((nred + kWaves - 1) / kWaves), dim3(kThreads), 0, stream, kin, Vk, T,
+                     ws.tile_heads, nred);
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(grad) % (grad_bf16 ? 8 : 16) == 0) &&
                     (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
-  const dim3 rgrid((nchunks + kThreads / kWave - 1) / (kThreads / kWave));
   const dim3 cgrid(grid_for(nchunks, 1024));
+#define EMB_REDUCE(BF, VC)                                                                                        \
+  hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred), dim3(kThreads), 0, stream, kin, vin, Vk, T, grad, D, \
+                     ws.tile_heads, uniq_ids, seg_offsets, num_unique, uniq_grad, ws.partial,  \
+                     ws.span_list, ws.span_count, status)
   if (vec4) {
     if (grad_bf16)
-      hipLaunchKernelGGL((seg_reduce_kernel<true, 4>), rgrid, dim3(kThreads), 0, stream, grad, D, spos, ws.seg_of,
-                         seg_offsets, num_unique, nchunks, uniq_grad, ws.partial, ws.span_list, ws.span_count);
+      EMB_REDUCE(true, 4);
     else
-      hipLaunchKernelGGL((seg_reduce_kernel<false, 4>), rgrid, dim3(kThreads), 0, stream, grad, D, spos, ws.seg_of,
-                         seg_offsets, num_unique, nchunks, uniq_grad, ws.partial, ws.span_list, ws.span_count);
+      EMB_REDUCE(false, 4);
     hipLaunchKernelGGL(seg_combine_kernel<4>, cgrid, dim3(kThreads), 0, stream, ws.partial, D, seg_offsets,
                        ws.span_list, ws.span_count, uniq_grad);
   } else {
     if (grad_bf16)
-      hipLaunchKernelGGL((seg_reduce_kernel<true, 1>), rgrid, dim3(kThreads), 0, stream, grad, D, spos, ws.seg_of,
-                         seg_offsets, num_unique, nchunks, uniq_grad, ws.partial, ws.span_list, ws.span_count);
+      EMB_REDUCE(true, 1);
     else
-      hipLaunchKernelGGL((seg_reduce_kernel<false, 1>), rgrid, dim3(kThreads), 0, stream, grad, D, spos, ws.seg_of,
-                         seg_offsets, num_unique, nchunks, uniq_grad, ws.partial, ws.span_list, ws.span_count);
+      EMB_REDUCE(false, 1);
     hipLaunchKernelGGL(seg_combine_kernel<1>, cgrid, dim3(kThreads), 0, stream, ws.partial, D, seg_offsets,
                        ws.span_list, ws.span_count, uniq_grad);
   }
+#undef EMB_REDUCE
   return hipGetLastError();
 }
 

@@ -1,0 +1,142 @@
+"""Training steps of the sparse-embedding path, scheduled on streams.
+
+A step of one table is the four C ABI calls in data order:
+    gather (forward lookup, Sec. 4.1.1)
+    grad_coalesce -> pack_by_owner (the exchange payload, Sec. 4.2.2 / 4.1.2)
+    sparse_adam_apply (the update of the owned rows)
+The library's step executor (emb_train_step) enqueues all four with one host
+call.  With overlap=True the coalesce of a step runs on one side stream and
+its pack on another, while the lookup and the update stay on the main
+stream; the executor adds the event waits that keep every data dependency
+(see emb_train_step in include/emb.h).  This module only allocates the
+buffers, alternates the two buffer sets and fills in the arguments.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import (EMB_BF16, EMB_F32, Event, StepArgs, StepSchedule, _check, grad_coalesce_workspace_bytes, lib,
+               new_workspace, pack_by_owner_workspace_bytes)
+
+STAGES = ("gather", "coalesce", "pack", "adam")
+
+
+class EmbeddingTable:
+    """Device state of one table (W, Adam moments, row owners) and the buffers of its steps."""
+
+    def __init__(self, W: torch.Tensor, row_owner: torch.Tensor, P: int, T_cap: int,
+                 grad_dtype: torch.dtype = torch.float32):
+        dev = W.device
+        self.V, self.D = W.shape
+        self.P, self.T_cap = P, T_cap
+        self.W = W
+        self.M = torch.zeros_like(W)
+        self.S = torch.zeros_like(W)
+        self.row_owner = row_owner
+        i32, f32 = torch.int32, torch.float32
+        self.lookup = torch.empty((T_cap, self.D), dtype=f32, device=dev)
+        # two buffer sets, alternated between consecutive steps
+        self.coals = [(torch.empty(T_cap, dtype=i32, device=dev), torch.empty(T_cap + 1, dtype=i32, device=dev),
+                       torch.empty((T_cap, self.D), dtype=f32, device=dev), torch.empty(1, dtype=i32, device=dev))
+                      for _ in range(2)]
+        self.send = [(torch.empty(T_cap, dtype=i32, device=dev), torch.empty((T_cap, self.D), dtype=f32, device=dev),
+                      torch.empty(P, dtype=i32, device=dev), torch.empty(P + 1, dtype=i32, device=dev))
+                     for _ in range(2)]
+        self.coal = self.coals[0]
+        self.grad_code = EMB_BF16 if grad_dtype == torch.bfloat16 else EMB_F32
+        self.ws_coalesce = new_workspace(grad_coalesce_workspace_bytes(T_cap, self.V, self.D, self.grad_code), dev)
+        self.ws_pack = new_workspace(pack_by_owner_workspace_bytes(T_cap, P), dev)
+
+
+def _stream_handle(s: torch.cuda.Stream) -> int:
+    return s.cuda_stream
+
+
+_SIDE_STREAMS: dict = {}
+
+
+def side_streams(device=None):
+    """The two side streams of a device, created once per process.  HIP maps
+    streams onto a few hardware queues in creation order; creating streams
+    once keeps the side streams on queues other than the main stream's."""
+    dev = torch.cuda.current_device() if device is None else torch.device(device).index
+    if dev not in _SIDE_STREAMS:
+        _SIDE_STREAMS[dev] = (torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev))
+    return _SIDE_STREAMS[dev]
+
+
+class StepPipeline:
+    """Enqueues training steps of the hot path for a list of tables."""
+
+    def __init__(self, tables, lr, beta1, beta2, eps, overlap: bool = True, dev_status: torch.Tensor | None = None,
+                 streams: int = 3):
+        """streams (with overlap=True): 2 puts coalesce and pack on one side stream, 3 gives
+        each its own (more concurrency, one more cross-stream wait per step)."""
+        self.tables = list(tables)
+        self.overlap = overlap
+        self.main = torch.cuda.current_stream()
+        s1, s2 = side_streams()
+        self.side = s1 if overlap else self.main  # coalesce
+        self.side2 = s2 if (overlap and streams >= 3) else self.side  # pack
+        self.count = 0
+        self.events = []  # keeps the library events alive
+        self.args, self.sched = [], []
+        st = 0 if dev_status is None else dev_status.data_ptr()
+        for tb in self.tables:
+            args, scheds = [], []
+            for i in range(2):
+                uid, seg, ug, nu = tb.coals[i]
+                sid, srows, cnt, offs = tb.send[i]
+                a = StepArgs(table=tb.W.data_ptr(), exp_avg=tb.M.data_ptr(), exp_avg_sq=tb.S.data_ptr(), V=tb.V,
+                             D=tb.D, row_owner=tb.row_owner.data_ptr(), P=tb.P, cap_rows=tb.T_cap,
+                             lookup=tb.lookup.data_ptr(), uniq_ids=uid.data_ptr(), seg_offsets=seg.data_ptr(),
+                             num_unique=nu.data_ptr(), uniq_grad=ug.data_ptr(), send_ids=sid.data_ptr(),
+                             send_counts=cnt.data_ptr(), send_offsets=offs.data_ptr(), send_rows=srows.data_ptr(),
+                             ws_coalesce=tb.ws_coalesce.data_ptr(), ws_coalesce_bytes=tb.ws_coalesce.numel(),
+                             ws_pack=tb.ws_pack.data_ptr(), ws_pack_bytes=tb.ws_pack.numel(), lr=lr, beta1=beta1,
+                             beta2=beta2, eps=eps, dev_status=st)
+                evs = [Event() for _ in range(3)]
+                self.events += evs
+                s = StepSchedule(lookup_update=_stream_handle(self.main), coalesce=_stream_handle(self.side),
+                                 pack=_stream_handle(self.side2), coalesced=evs[0].handle, packed=evs[1].handle,
+                                 updated=evs[2].handle)
+                args.append(a)
+                scheds.append(s)
+            self.args.append(args)
+            self.sched.append(scheds)
+
+    def step(self, batches, t: int, timing=None):
+        """Enqueue one step.  batches: [(ids int32 [T], grad [T, D]) per table]; t: Adam step (>= 1).
+        timing: optional dict stage -> (begin Event, end Event) of library timing events, recorded
+        around the calls of the first table on the streams they run on.
+        Inputs must be ready on the main stream when the pipeline's first step is enqueued."""
+        i = self.count % 2
+        if self.count == 0 and self.overlap:
+            self.side.wait_stream(self.main)
+            if self.side2 is not self.side:
+                self.side2.wait_stream(self.main)
+        for k, (ids, grad) in enumerate(batches):
+            a, s = self.args[k][i], self.sched[k][i]
+            a.ids = ids.data_ptr()
+            a.T = ids.numel()
+            a.grad = grad.data_ptr()
+            a.grad_dtype = EMB_BF16 if grad.dtype == torch.bfloat16 else EMB_F32
+            a.step = t
+            s.reuse = 1 if self.count >= 2 else 0
+            for n in range(8):
+                s.timing[n] = None
+            if timing is not None and k == 0:
+                for j, name in enumerate(STAGES):
+                    if name in timing:
+                        s.timing[2 * j] = timing[name][0].handle
+                        s.timing[2 * j + 1] = timing[name][1].handle
+            _check(lib.emb_train_step(ctypes.byref(a), ctypes.byref(s)), "emb_train_step")
+        self.count += 1
+
+    def finish(self):
+        """Make the main stream wait for everything enqueued on the side streams."""
+        self.main.wait_stream(self.side)
+        if self.side2 is not self.side:
+            self.main.wait_stream(self.side2)
