@@ -74,6 +74,119 @@ def cpu_baseline(wl, seconds):
                        f"single-threaded C oracle, {t_total:.1f} s of timed CPU work")
 
 
+ADAM_KERNEL = "adam_kernel"
+COPY_KERNEL = "bitwise_not"  # the reference stream: read N bytes, write N bytes
+COPY_MIB = 256
+PROFILES = os.path.join(ROOT, "profiles")
+TRAFFIC_FILE = os.path.join(PROFILES, "adam_kernel_traffic_lowdup_uniform.json")
+
+
+def source_hash(path):
+    import hashlib
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+ADAM_SOURCE = os.path.join(ROOT, "paper_2110_09132_amd", "csrc", "adam.hip")
+
+
+def copy_reference(torch, mib=COPY_MIB, reps=20):
+    """A plain device stream of known size (read mib MiB, write mib MiB), timed with events:
+    the bandwidth a streaming kernel reaches here, and the calibration dispatch for the
+    HBM byte counters."""
+    n = mib * (1 << 20) // 4
+    a = torch.randint(0, 1 << 30, (n,), dtype=torch.int32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        torch.bitwise_not(a, out=b)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        torch.bitwise_not(a, out=b)
+    e1.record()
+    torch.cuda.synchronize()
+    return 2 * n * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+
+def measured_traffic():
+    """HBM bytes per launch of the update kernel from the committed counter summary, or
+    None when there is none or the kernel source changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("adam_source_sha256_16") != source_hash(ADAM_SOURCE):
+        return None
+    return t.get("traffic_bytes_per_launch")
+
+
+def _read_csv(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _find(directory, suffix):
+    for root, _, files in os.walk(directory):
+        for fn in files:
+            if fn.endswith(suffix):
+                return os.path.join(root, fn)
+    raise FileNotFoundError(f"no *{suffix} under {directory}")
+
+
+def summarize_trace(directory, command, warmup=10, steps=50):
+    """Text summary of a rocprofv3 --kernel-trace --stats run (kernel_stats.csv), plus the
+    average duration of the update kernel over the timed steps of the bench run (its
+    dispatches warmup+1 .. warmup+steps in launch order, from kernel_trace.csv)."""
+    trace = [r for r in _read_csv(_find(directory, "kernel_trace.csv")) if ADAM_KERNEL in r["Kernel_Name"]]
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace[warmup:warmup + steps]]
+    rows = _read_csv(_find(directory, "kernel_stats.csv"))
+    out = [f"command: {command}", "", f"{'kernel':64s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} "
+           f"{'max_us':>9s} {'share':>6s}"]
+    for r in rows:
+        name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0][:64]
+        out.append(f"{name:64s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:9.2f} "
+                   f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):5.1f}%")
+    if durs:
+        out += ["", f"{ADAM_KERNEL} over the {len(durs)} timed steps (dispatches {warmup + 1}..{warmup + len(durs)}): "
+                    f"avg {sum(durs) / len(durs):.2f} us, min {min(durs):.2f} us, max {max(durs):.2f} us"]
+    return "\n".join(out) + "\n"
+
+
+def summarize_pmc(fetch_dir, write_dir, command_fetch, command_write):
+    """Scale FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the update kernel by what the same
+    counters read for the reference stream of known size."""
+    def per_kernel(directory, counter):
+        rows = _read_csv(_find(directory, "counter_collection.csv"))
+        vals = {}
+        for r in rows:
+            if r.get("Counter_Name") != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = ADAM_KERNEL if ADAM_KERNEL in name else (COPY_KERNEL if COPY_KERNEL in name else None)
+            if key:
+                vals.setdefault(key, []).append(float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in vals.items()}
+    f = per_kernel(fetch_dir, "FETCH_SIZE")
+    w = per_kernel(write_dir, "WRITE_SIZE")
+    copy_bytes = COPY_MIB * (1 << 20)
+    f_scale = copy_bytes / (f[COPY_KERNEL] * 1024.0)
+    w_scale = copy_bytes / (w[COPY_KERNEL] * 1024.0)
+    fetch_b = f[ADAM_KERNEL] * 1024.0 * f_scale
+    write_b = w[ADAM_KERNEL] * 1024.0 * w_scale
+    return {"kernel": ADAM_KERNEL, "workload": "lowdup_uniform",
+            "fetch_kib_per_dispatch": f[ADAM_KERNEL], "write_kib_per_dispatch": w[ADAM_KERNEL],
+            "copy_fetch_kib": f[COPY_KERNEL], "copy_write_kib": w[COPY_KERNEL], "copy_bytes_each_way": copy_bytes,
+            "fetch_scale": f_scale, "write_scale": w_scale,
+            "fetch_bytes_per_launch": fetch_b, "write_bytes_per_launch": write_b,
+            "traffic_bytes_per_launch": fetch_b + write_b,
+            "adam_source_sha256_16": source_hash(ADAM_SOURCE),
+            "command_fetch": command_fetch, "command_write": command_write}
+
+
 def host_info():
     model = platform.processor() or ""
     try:
@@ -97,7 +210,18 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one stream, calls one after another")
+    ap.add_argument("--summarize-trace", metavar="DIR", help="print a summary of a rocprofv3 kernel-stats run")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the scaled HBM traffic of the update kernel from two rocprofv3 --pmc runs")
+    ap.add_argument("--command", default="", help="the command recorded in a summary")
+    ap.add_argument("--command2", default="", help="the second command recorded in a summary")
     args = ap.parse_args()
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.command), end="")
+        return
+    if args.summarize_pmc:
+        print(json.dumps(summarize_pmc(*args.summarize_pmc, args.command, args.command2), indent=1))
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -183,6 +307,8 @@ def main():
         for k in stage_ms:
             stage_ms[k] += ev[k][0].elapsed_ms(ev[k][1]) / args.steps
 
+    copy_gbps = copy_reference(torch)
+
     # algorithmic bytes of the timed steps
     bytes_step = {k: 0.0 for k in stage_ms}
     for b in used:
@@ -215,7 +341,8 @@ def main():
                    "tables": [dict(V=sp.V, D=sp.D, T=sp.T, P=sp.P, ids=sp.id_law, owner=sp.owner_rule)
                               for sp in wl.tables],
                    "mean_unique_rows_per_step": rows / args.steps, "batches_rotated": args.batches,
-                   "schedule": "sequential" if args.sequential else "two streams (coalesce+pack overlapped)"},
+                   "schedule": "one stream" if args.sequential else
+                   "three streams (coalesce, pack overlapped with lookup+update)"},
         "step_bytes_model": total_bytes,
         "step_hbm_GBps": step_gbps,
         "step_hbm_frac": step_gbps / HBM_PEAK_GBPS,
@@ -224,8 +351,11 @@ def main():
         "wall_s_timed": wall,
         "roofline": {"bound": "hbm", "kernel": "adam_kernel (emb_sparse_adam_apply)",
                      "achieved": adam_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": adam_gbps / HBM_PEAK_GBPS, "traffic": None,
+                     "frac": adam_gbps / HBM_PEAK_GBPS,
+                     "traffic": measured_traffic() if args.workload == "lowdup_uniform" else None,
                      "bytes_per_launch": adam_bytes, "avg_launch_us": adam_us},
+        "copy_GBps": copy_gbps,
+        "step_frac_of_copy": step_gbps / copy_gbps,
         "host": host_info(),
     }
     if not args.no_cpu_baseline:
