@@ -35,13 +35,21 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def byte_model(T, U, D, g, P):
+def byte_model(T, U, D, g, P, by_owner=False):
     """Algorithmic bytes of each call: inputs read once, outputs written once,
-    repeated table rows counted once; sort scratch is not counted."""
+    repeated table rows counted once; sort scratch is not counted.  by_owner:
+    coalesce writes the send layout itself (emb_grad_coalesce_by_owner), so the
+    pack's read and write of the U rows (8 D U) and of the unique ids are gone:
+    it reads the ids, the owners of the U distinct ids and the gradient rows,
+    and writes the send ids and rows, the segment offsets and the owner counts
+    and offsets."""
     gather = 4 * T + 4 * D * U + 4 * D * T
+    adam = 4 * U + 4 * D * U + 24 * D * U
+    if by_owner:
+        coalesce = 4 * T + g * D * T + 8 * U + 4 * D * U + 4 * (U + 1) + 8 * P
+        return dict(gather=gather, coalesce=coalesce, pack=0, adam=adam)
     coalesce = 4 * T + g * D * T + 4 * U + 4 * D * U + 4 * (U + 1)
     pack = 12 * U + 8 * D * U + 8 * P
-    adam = 4 * U + 4 * D * U + 24 * D * U
     return dict(gather=gather, coalesce=coalesce, pack=pack, adam=adam)
 
 
@@ -210,6 +218,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one stream, calls one after another")
+    ap.add_argument("--unfused", action="store_true",
+                    help="emb_grad_coalesce then emb_pack_by_owner (three streams) instead of "
+                         "emb_grad_coalesce_by_owner")
     ap.add_argument("--summarize-trace", metavar="DIR", help="print a summary of a rocprofv3 kernel-stats run")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the scaled HBM traffic of the update kernel from two rocprofv3 --pmc runs")
@@ -261,7 +272,8 @@ def main():
             torch.cuda.synchronize()
             U[b][k] = int(tb.coal[3].item())
 
-    pipe = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential)
+    by_owner = not args.unfused
+    pipe = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential, by_owner=by_owner)
     t = 0
     for _ in range(args.warmup):
         t += 1
@@ -292,8 +304,8 @@ def main():
     adam_us = 1e3 * sum(a.elapsed_ms(z) for a, z in adam_ev) / args.steps
 
     # per-stage breakdown: the same steps run one call after another on one stream
-    seq = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=False)
-    stage_ms = {k: 0.0 for k in ("gather", "coalesce", "pack", "adam")}
+    seq = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=False, by_owner=by_owner)
+    stage_ms = {k: 0.0 for k in (("gather", "coalesce", "adam") if by_owner else ("gather", "coalesce", "pack", "adam"))}
     s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     seq_total = 0.0
     for s in range(args.steps):
@@ -314,7 +326,7 @@ def main():
     for b in used:
         for k, tb in enumerate(tables):
             sp = wl.tables[k]
-            bm = byte_model(sp.T, U[b][k], sp.D, 2 if sp.grad_dtype == "bf16" else 4, sp.P)
+            bm = byte_model(sp.T, U[b][k], sp.D, 2 if sp.grad_dtype == "bf16" else 4, sp.P, by_owner)
             for name in bytes_step:
                 bytes_step[name] += bm[name] / args.steps
     total_bytes = sum(bytes_step.values())
@@ -341,9 +353,13 @@ def main():
                    "tables": [dict(V=sp.V, D=sp.D, T=sp.T, P=sp.P, ids=sp.id_law, owner=sp.owner_rule)
                               for sp in wl.tables],
                    "mean_unique_rows_per_step": rows / args.steps, "batches_rotated": args.batches,
+                   "coalesce": "emb_grad_coalesce_by_owner (coalesce straight into the send layout)" if by_owner
+                   else "emb_grad_coalesce + emb_pack_by_owner",
                    "schedule": "one stream" if args.sequential else
-                   "three streams (coalesce, pack overlapped with lookup+update)"},
+                   ("sort on a side stream; lookup, reduction and update on the main stream" if by_owner else
+                    "three streams (coalesce, pack overlapped with lookup+update)")},
         "step_bytes_model": total_bytes,
+        "step_bytes_model_kind": "fused minimum (pack folded into coalesce)" if by_owner else "four calls",
         "step_hbm_GBps": step_gbps,
         "step_hbm_frac": step_gbps / HBM_PEAK_GBPS,
         "sequential_ms_per_step": seq_total,

@@ -137,6 +137,39 @@ int emb_pack_by_owner(const int32_t *uniq_ids, const float *uniq_grad,
                       int32_t *dev_status, void *stream);
 
 /*
+ * emb_grad_coalesce and emb_pack_by_owner in one call (Algorithm 1's COALESCE
+ * and UNIQUE, Sec. 4.2.2, with the per-owner send layout of Sec. 4.1.2): the
+ * tokens are sorted by (row_owner[id], id), so the distinct ids come out
+ * already grouped by owner, ascending inside each owner, and the summed rows
+ * are written straight into the send buffers.  The outputs equal those of
+ * emb_pack_by_owner applied to the output of emb_grad_coalesce:
+ *   send_ids  [T], send_rows [T][D]: owner p's rows at
+ *             [send_offsets[p], send_offsets[p + 1])
+ *   send_counts [P], send_offsets [P + 1]
+ *   num_unique [1]: rows sent (= send_offsets[P])
+ *   seg_offsets [T + 1]: seg_offsets[k + 1] - seg_offsets[k] tokens were summed
+ *             into send row k (offsets in the owner-major token order)
+ * except that the order of the fp32 additions inside a row may differ (same
+ * rule: position order in chunks of 32 sorted tokens, then an ordered combine;
+ * bitwise reproducible run to run).  A token whose id is outside [0, V) or
+ * whose owner is outside [0, P) is left out and sets EMB_DEV_ID_OUT_OF_RANGE /
+ * EMB_DEV_OWNER_OUT_OF_RANGE.
+ * workspace: emb_grad_coalesce_workspace_bytes(T, V, D, grad_dtype) bytes,
+ * 256-byte aligned.  Requires what emb_grad_coalesce requires, 1 <= P <= 1024,
+ * and bits(V) + bits(P) <= 32, where bits(n) is the number of bits of n - 1
+ * (EMB_ERR_UNSUPPORTED otherwise; use the two calls).
+ */
+int emb_grad_coalesce_by_owner(const int32_t *ids, int32_t T,
+                               const void *grad, int32_t grad_dtype,
+                               int32_t D, int64_t V,
+                               const int32_t *row_owner, int32_t P,
+                               int32_t *send_ids, int32_t *seg_offsets,
+                               float *send_rows, int32_t *send_counts,
+                               int32_t *send_offsets, int32_t *num_unique,
+                               void *workspace, size_t workspace_bytes,
+                               int32_t *dev_status, void *stream);
+
+/*
  * Row-wise (lazy) Adam on received rows (Sec. 4.1.1: each process updates its
  * embedding rows with the exchanged gradients; Sec. 5.7: Adam with a global
  * step counter that the caller owns and advances once per iteration).
@@ -173,27 +206,45 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  * Sec. 4.2.2, here on one GPU).  One host call per step keeps the host ahead
  * of the GPU.
  *
- * The caller alternates two buffer sets (uniq_* and send_* outputs) between
- * consecutive steps and gives each set its own three events; `reuse` is
- * nonzero when the set was used two steps earlier.  The executor then adds
- * these waits, which keep every data dependency:
- *   coalesce(s) after pack(s-2)             (same unique-row buffers)
+ * The caller alternates two buffer sets (coalesce workspace, uniq_* and send_*
+ * outputs) between consecutive steps and gives each set its own events;
+ * `reuse` is nonzero when the set was used two steps earlier.
+ *
+ * by_owner == 0: emb_grad_coalesce on the `coalesce` stream, emb_pack_by_owner
+ * on the `pack` stream, lookup and update on `lookup_update`, with the waits
+ *   coalesce(s) after pack(s-2)                (same unique-row buffers)
  *   pack(s)     after coalesce(s), update(s-2) (reads unique rows; same send buffers)
- *   update(s)   after pack(s)               (reads the packed rows)
- *   lookup(s+1) after update(s)              (same stream; reads the table)
- * With all three streams equal the calls simply run one after another, and the
+ *   update(s)   after pack(s)                  (reads the packed rows)
+ *   lookup(s+1) after update(s)                (same stream; reads the table)
+ * (events coalesced, packed, updated).
+ *
+ * by_owner != 0: emb_grad_coalesce_by_owner in its two halves.  The sort of
+ * the (owner, id) keys, which does not read the gradients, runs on the
+ * `coalesce` stream; the reduction, which writes the send buffers directly,
+ * runs on `lookup_update` after the lookup, followed there by the update;
+ * uniq_ids, uniq_grad, ws_pack and the `pack` stream are not used.  Waits:
+ *   sort(s)     after reduce(s-2)              (same coalesce workspace)
+ *   reduce(s)   after sort(s)                  (reads the sorted keys)
+ * (events sorted, coalesced); everything else is in stream order.  The sorts
+ * thus run up to a step ahead, beside the lookup, reduction and update.
+ *
+ * With all streams equal the calls simply run one after another, and the
  * results are bitwise the same either way.
  * ---------------------------------------------------------------------------
  */
 typedef struct {
   void *lookup_update;          /* stream of emb_gather and emb_sparse_adam_apply */
-  void *coalesce;               /* stream of emb_grad_coalesce */
+  void *coalesce;               /* stream of emb_grad_coalesce (by_owner: of its sort) */
   void *pack;                   /* stream of emb_pack_by_owner */
-  void *coalesced, *packed, *updated; /* events of this step's buffer set */
+  void *sorted, *coalesced, *packed, *updated; /* events of this step's buffer set
+                                   (sorted: by_owner only; packed, updated: by_owner == 0 only) */
   int32_t reuse;                /* the buffer set was used two steps ago */
+  int32_t by_owner;             /* use emb_grad_coalesce_by_owner instead of coalesce + pack */
   void *timing[8];              /* optional timing events (NULL to skip): begin/end of
                                    gather, coalesce, pack, adam, each recorded on the
-                                   stream its call runs on */
+                                   stream the (first / last) kernel runs on; the adam
+                                   pair takes the update kernel's own start and end
+                                   from its dispatch; by_owner records no pack pair */
 } emb_step_schedule;
 
 typedef struct {
@@ -206,7 +257,7 @@ typedef struct {
   int32_t T;
   const void *grad;         /* [T][D], grad_dtype */
   int32_t grad_dtype;
-  int32_t cap_rows;         /* capacity of the uniq_* and send_* buffers (>= T) */
+  int32_t cap_rows;         /* capacity of the uniq_*, seg_offsets and send_* buffers (>= T) */
   float *lookup;            /* [T][D] gather output */
   int32_t *uniq_ids, *seg_offsets, *num_unique;
   float *uniq_grad;

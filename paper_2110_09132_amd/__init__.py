@@ -37,6 +37,8 @@ SIGNATURES = {
     "emb_gather": (ctypes.c_int, [_P, _I64, _I32, _P, _I32, _P, _P, _P]),
     "emb_grad_coalesce_workspace_bytes": (_SZ, [_I32, _I64, _I32, _I32]),
     "emb_grad_coalesce": (ctypes.c_int, [_P, _I32, _P, _I32, _I32, _I64, _P, _P, _P, _P, _P, _SZ, _P, _P]),
+    "emb_grad_coalesce_by_owner": (ctypes.c_int, [_P, _I32, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P, _P,
+                                                  _P, _SZ, _P, _P]),
     "emb_pack_by_owner_workspace_bytes": (_SZ, [_I32, _I32]),
     "emb_pack_by_owner": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_sparse_adam_apply": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _P, _P, _P, _I32, _I32, _I32, _I32,
@@ -50,8 +52,8 @@ SIGNATURES = {
 
 class StepSchedule(ctypes.Structure):
     """emb_step_schedule of include/emb.h."""
-    _fields_ = [("lookup_update", _P), ("coalesce", _P), ("pack", _P), ("coalesced", _P), ("packed", _P),
-                ("updated", _P), ("reuse", _I32), ("timing", _P * 8)]
+    _fields_ = [("lookup_update", _P), ("coalesce", _P), ("pack", _P), ("sorted", _P), ("coalesced", _P),
+                ("packed", _P), ("updated", _P), ("reuse", _I32), ("by_owner", _I32), ("timing", _P * 8)]
 
 
 class StepArgs(ctypes.Structure):
@@ -186,6 +188,34 @@ def grad_coalesce(ids, grad, V, out=None, workspace=None, dev_status=None, strea
     _check(lib.emb_grad_coalesce(_ptr(ids), T, _ptr(grad), code, D, V, _ptr(uniq_ids), _ptr(seg_offsets),
                                  _ptr(uniq_grad), _ptr(num_unique), _ptr(workspace), workspace.numel(),
                                  _ptr(dev_status), _stream(stream)), "emb_grad_coalesce")
+    return out
+
+
+def grad_coalesce_by_owner(ids, grad, V, row_owner, P, out=None, workspace=None, dev_status=None, stream=None):
+    """Coalesce straight into the owner-major send layout (emb_grad_coalesce_by_owner).
+
+    Returns (send_ids [T], seg_offsets [T+1], send_rows [T, D], send_counts [P], send_offsets [P+1],
+    num_unique [1]); `out` may pass those six tensors in.
+    """
+    _need(ids, torch.int32, "ids")
+    _need(row_owner, torch.int32, "row_owner")
+    code = _dtype_code(grad)
+    if not grad.is_cuda or not grad.is_contiguous():
+        raise EmbError("grad must be a contiguous CUDA tensor")
+    T = ids.numel()
+    D = grad.shape[1]
+    dev = ids.device
+    if out is None:
+        out = (torch.empty(T, dtype=torch.int32, device=dev), torch.empty(T + 1, dtype=torch.int32, device=dev),
+               torch.empty((T, D), dtype=torch.float32, device=dev), torch.empty(P, dtype=torch.int32, device=dev),
+               torch.empty(P + 1, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
+    send_ids, seg_offsets, send_rows, send_counts, send_offsets, num_unique = out
+    if workspace is None:
+        workspace = new_workspace(grad_coalesce_workspace_bytes(T, V, D, code), dev)
+    _check(lib.emb_grad_coalesce_by_owner(_ptr(ids), T, _ptr(grad), code, D, V, _ptr(row_owner), P, _ptr(send_ids),
+                                          _ptr(seg_offsets), _ptr(send_rows), _ptr(send_counts), _ptr(send_offsets),
+                                          _ptr(num_unique), _ptr(workspace), workspace.numel(), _ptr(dev_status),
+                                          _stream(stream)), "emb_grad_coalesce_by_owner")
     return out
 
 

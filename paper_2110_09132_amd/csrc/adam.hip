@@ -1,10 +1,11 @@
 // Row-wise (lazy) Adam on the rows a shard owns (Sec. 4.1.1, Sec. 5.7;
 // Kingma & Ba, Algorithm 1).  One pass over the listed rows: for each element
 // read g, w, m, v once and write w, m, v once; rows not listed are not touched.
-// Rows are mapped to lanes as in the gather (L lanes per row, several rows in
-// flight per wave); table rows are random 4*D-byte blocks, gradient rows are
-// contiguous.
+// Rows are mapped to lanes as in the gather (L lanes per row); table rows are
+// random 4*D-byte blocks, gradient rows are contiguous.
 #include <cmath>
+
+#include <hip/hip_ext.h>
 
 #include "common.h"
 #include "launch.h"
@@ -33,6 +34,10 @@ __device__ __forceinline__ void adam_vec(const float& g, float& w, float& m, flo
   adam_elem(g, w, m, v, c);
 }
 
+// Each wave owns a contiguous range of the listed rows.  The row ids of 64
+// rows come in one coalesced load and reach their lanes by shuffle; rows are
+// processed in groups of kRowsInFlight steps, and the loads (g, w, m, v) of the
+// next group are issued before the current group is computed and stored.
 template <typename VecT>
 __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, VecT* __restrict__ M,
                                                         VecT* __restrict__ S, int64_t V, int Dv, int log2L,
@@ -45,49 +50,61 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
   hi = max(lo, min(hi, cap));
   const int L = 1 << log2L;
   const int rpw = kWave >> log2L;
-  const int sub = lane_id() >> log2L;
-  const int cl = lane_id() & (L - 1);
-  const long long wave = (static_cast<long long>(blockIdx.x) * kThreads + threadIdx.x) / kWave;
-  const long long nwaves = static_cast<long long>(gridDim.x) * (kThreads / kWave);
-  const long long step = static_cast<long long>(rpw) * kRowsInFlight;
+  const int lane = static_cast<int>(lane_id());
+  const int sub = lane >> log2L;
+  const int cl = lane & (L - 1);
+  const int wave = uniform(static_cast<int>(blockIdx.x) * (kThreads / kWave) + static_cast<int>(threadIdx.x / kWave));
+  const int nwaves = static_cast<int>(gridDim.x) * (kThreads / kWave);
+  const int step_rows = rpw * kRowsInFlight;
+  int per = (hi - lo + nwaves - 1) / nwaves;
+  per = (per + step_rows - 1) / step_rows * step_rows;
+  const long long r0 = lo + static_cast<long long>(wave) * per;
+  const long long r1 = min(static_cast<long long>(hi), r0 + per);
   bool bad = false;
-  for (long long r0 = lo + wave * step; r0 < hi; r0 += nwaves * step) {
-    // All loads come from clamped, always-valid addresses and are issued
-    // together; only rows that exist and are valid are stored.
-    int32_t rid[kRowsInFlight];
-    long long src[kRowsInFlight];
+  for (long long c0 = r0; c0 < r1; c0 += kWave) {  // 64 rows per id load
+    const int n = static_cast<int>(min(static_cast<long long>(kWave), r1 - c0));
+    const int32_t ridreg = row_ids[min(c0 + lane, static_cast<long long>(hi) - 1)];
+    bad |= lane < n && (ridreg < 0 || ridreg >= V);
+    const int ngroups = (n + step_rows - 1) / step_rows;
+    for (int cb = 0; cb < Dv; cb += L) {  // uniform column steps (the shuffles need every lane)
+      const int col = min(cb + cl, Dv - 1);
+      const bool cok = cb + cl < Dv;
+      // two register buffers used in turn; every index below is a compile-time constant
+      struct Buf {
+        VecT g[kRowsInFlight], w[kRowsInFlight], m[kRowsInFlight], s[kRowsInFlight];
+        int rid[kRowsInFlight];
+      } A, B;
+      auto load = [&](int grp, Buf& x) {
 #pragma unroll
-    for (int u = 0; u < kRowsInFlight; ++u) {
-      const long long i = r0 + u * rpw + sub;
-      src[u] = i < hi ? i : hi - 1;
-      rid[u] = row_ids[src[u]];
-    }
-#pragma unroll
-    for (int u = 0; u < kRowsInFlight; ++u) {
-      const bool live = r0 + u * rpw + sub < hi;
-      const bool ok = rid[u] >= 0 && rid[u] < V;
-      bad |= live && !ok;
-      if (!live || !ok) rid[u] = -1;
-    }
-    for (int col = cl; col < Dv; col += L) {
-      VecT g[kRowsInFlight], w[kRowsInFlight], m[kRowsInFlight], s[kRowsInFlight];
-#pragma unroll
-      for (int u = 0; u < kRowsInFlight; ++u) {
-        const size_t e = static_cast<size_t>(rid[u] < 0 ? 0 : rid[u]) * Dv + col;
-        g[u] = rows[static_cast<size_t>(src[u]) * Dv + col];
-        w[u] = W[e];
-        m[u] = M[e];
-        s[u] = S[e];
-      }
-#pragma unroll
-      for (int u = 0; u < kRowsInFlight; ++u) {
-        if (rid[u] >= 0) {
-          adam_vec(g[u], w[u], m[u], s[u], c);
-          const size_t e = static_cast<size_t>(rid[u]) * Dv + col;
-          W[e] = w[u];
-          M[e] = m[u];
-          S[e] = s[u];
+        for (int u = 0; u < kRowsInFlight; ++u) {
+          const int j = grp * step_rows + u * rpw + sub;
+          const int r = __shfl(ridreg, min(j, kWave - 1), kWave);
+          x.rid[u] = (j < n && r >= 0 && r < V) ? r : -1;
+          const size_t e = static_cast<size_t>(x.rid[u] < 0 ? 0 : x.rid[u]) * Dv + col;
+          x.g[u] = rows[static_cast<size_t>(c0 + min(j, n - 1)) * Dv + col];
+          x.w[u] = W[e];
+          x.m[u] = M[e];
+          x.s[u] = S[e];
         }
+      };
+      auto apply = [&](Buf& x) {
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+          if (x.rid[u] >= 0 && cok) {
+            adam_vec(x.g[u], x.w[u], x.m[u], x.s[u], c);
+            const size_t e = static_cast<size_t>(x.rid[u]) * Dv + col;
+            W[e] = x.w[u];
+            M[e] = x.m[u];
+            S[e] = x.s[u];
+          }
+        }
+      };
+      load(0, A);
+      for (int grp = 0; grp < ngroups; grp += 2) {
+        if (grp + 1 < ngroups) load(grp + 1, B);
+        apply(A);
+        if (grp + 2 < ngroups) load(grp + 2, A);
+        if (grp + 1 < ngroups) apply(B);
       }
     }
   }
@@ -98,22 +115,23 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
 
 hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int D, const int32_t* row_ids,
                        const float* rows, const int32_t* offsets, int shard_begin, int shard_end, int cap_rows,
-                       const AdamCoeffs& c, int32_t* status, hipStream_t stream) {
+                       const AdamCoeffs& c, int32_t* status, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
   if (cap_rows == 0 || shard_begin == shard_end) return hipSuccess;
   const auto al16 = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
   const bool vec4 = (D % 4 == 0) && al16(table) && al16(exp_avg) && al16(exp_avg_sq) && al16(rows);
   const int Dv = vec4 ? D / 4 : D;
   const RowLanes rl = row_lanes_for(Dv);
   const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * kRowsInFlight * (kThreads / kWave);
-  const unsigned grid = grid_for((cap_rows + rows_per_block - 1) / rows_per_block, 8192);
+  const unsigned grid = grid_for((cap_rows + rows_per_block - 1) / rows_per_block, kMaxBlocks);
   if (vec4)
-    hipLaunchKernelGGL(adam_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream, reinterpret_cast<float4*>(table),
-                       reinterpret_cast<float4*>(exp_avg), reinterpret_cast<float4*>(exp_avg_sq), V, Dv,
-                       rl.log2_lanes, row_ids, reinterpret_cast<const float4*>(rows), offsets, shard_begin, shard_end,
-                       cap_rows, c, status);
+    hipExtLaunchKernelGGL(adam_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream, start, stop, 0,
+                          reinterpret_cast<float4*>(table), reinterpret_cast<float4*>(exp_avg),
+                          reinterpret_cast<float4*>(exp_avg_sq), V, Dv, rl.log2_lanes, row_ids,
+                          reinterpret_cast<const float4*>(rows), offsets, shard_begin, shard_end, cap_rows, c, status);
   else
-    hipLaunchKernelGGL(adam_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, table, exp_avg, exp_avg_sq, V, Dv,
-                       rl.log2_lanes, row_ids, rows, offsets, shard_begin, shard_end, cap_rows, c, status);
+    hipExtLaunchKernelGGL(adam_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, start, stop, 0, table, exp_avg,
+                          exp_avg_sq, V, Dv, rl.log2_lanes, row_ids, rows, offsets, shard_begin, shard_end, cap_rows, c,
+                          status);
   return hipGetLastError();
 }
 

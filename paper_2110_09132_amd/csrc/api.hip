@@ -16,6 +16,67 @@ bool bad_table_dims(int64_t V, int32_t D) { return V < 1 || V > kMaxV || D < 1; 
 
 }  // namespace
 
+namespace emb {
+
+int coalesce_args_status(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D, int64_t V,
+                         const int32_t* uniq_ids, const int32_t* seg_offsets, const float* uniq_grad,
+                         const int32_t* num_unique, const void* workspace, size_t workspace_bytes) {
+  if (T < 0 || T >= (1 << 30) || bad_table_dims(V, D) || (grad_dtype != EMB_F32 && grad_dtype != EMB_BF16))
+    return EMB_ERR_INVALID_ARG;
+  if (!seg_offsets || !num_unique) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && (!ids || !grad || !uniq_ids || !uniq_grad || !workspace)) return EMB_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(grad) % (grad_dtype == EMB_BF16 ? 2 : 4) != 0) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && workspace_bytes < coalesce_workspace_bytes(T, D)) return EMB_ERR_WORKSPACE;
+  return EMB_OK;
+}
+
+int coalesce_by_owner_args_status(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D,
+                                  int64_t V, const int32_t* row_owner, int32_t P, const int32_t* send_ids,
+                                  const int32_t* seg_offsets, const float* send_rows, const int32_t* send_counts,
+                                  const int32_t* send_offsets, const int32_t* num_unique, const void* workspace,
+                                  size_t workspace_bytes) {
+  if (P < 1 || P > kMaxOwners || !send_counts || !send_offsets) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && !row_owner) return EMB_ERR_INVALID_ARG;
+  if (!bad_table_dims(V, D) && !coalesce_by_owner_supported(V, P)) return EMB_ERR_UNSUPPORTED;
+  return coalesce_args_status(ids, T, grad, grad_dtype, D, V, send_ids, seg_offsets, send_rows, num_unique, workspace,
+                              workspace_bytes);
+}
+
+
+int sparse_adam_call(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int32_t D, const int32_t* row_ids,
+                     const float* rows, const int32_t* offsets, int32_t P, int32_t shard_begin, int32_t shard_end,
+                     int32_t cap_rows, double lr, double beta1, double beta2, double eps, int64_t step,
+                     int32_t* dev_status, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
+  if (bad_table_dims(V, D) || P < 1 || P > kMaxOwners || cap_rows < 0) return EMB_ERR_INVALID_ARG;
+  if (shard_begin < 0 || shard_begin > shard_end || shard_end > P) return EMB_ERR_INVALID_ARG;
+  if (step < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0) ||
+      !std::isfinite(lr) || !std::isfinite(eps))
+    return EMB_ERR_INVALID_ARG;
+  if (cap_rows == 0 || shard_begin == shard_end) {  // nothing to launch: the timing pair still brackets this point
+    if (start && hipEventRecord(start, stream) != hipSuccess) return EMB_ERR_LAUNCH;
+    if (stop && hipEventRecord(stop, stream) != hipSuccess) return EMB_ERR_LAUNCH;
+    return EMB_OK;
+  }
+  if (!table || !exp_avg || !exp_avg_sq || !row_ids || !rows || !offsets) return EMB_ERR_INVALID_ARG;
+  // bias corrections in fp64 on the host, then the fp32 coefficients of the kernel
+  const double bc1 = 1.0 - std::pow(beta1, static_cast<double>(step));
+  const double bc2 = 1.0 - std::pow(beta2, static_cast<double>(step));
+  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return EMB_ERR_INVALID_ARG;  // beta == 0 edge cases stay valid: bc == 1
+  AdamCoeffs c;
+  c.beta1 = static_cast<float>(beta1);
+  c.one_minus_beta1 = static_cast<float>(1.0 - beta1);
+  c.beta2 = static_cast<float>(beta2);
+  c.one_minus_beta2 = static_cast<float>(1.0 - beta2);
+  c.step_size = static_cast<float>(lr / bc1);
+  c.inv_bc2 = static_cast<float>(1.0 / bc2);
+  c.eps = static_cast<float>(eps);
+  return launch_status(launch_adam(table, exp_avg, exp_avg_sq, V, D, row_ids, rows, offsets, shard_begin, shard_end,
+                                   cap_rows, c, dev_status, stream, start, stop));
+}
+
+}  // namespace emb
+
 extern "C" {
 
 int emb_abi_version(void) { return EMB_ABI_VERSION; }
@@ -41,21 +102,32 @@ int emb_gather(const float* table, int64_t V, int32_t D, const int32_t* ids, int
 
 size_t emb_grad_coalesce_workspace_bytes(int32_t T, int64_t V, int32_t D, int32_t grad_dtype) {
   if (T < 0 || bad_table_dims(V, D) || (grad_dtype != EMB_F32 && grad_dtype != EMB_BF16)) return 0;
-  return emb::coalesce_workspace_bytes(T, V, D);
+  return emb::coalesce_workspace_bytes(T, D);
 }
 
 int emb_grad_coalesce(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D, int64_t V,
                       int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad, int32_t* num_unique,
                       void* workspace, size_t workspace_bytes, int32_t* dev_status, void* stream) {
-  if (T < 0 || bad_table_dims(V, D) || (grad_dtype != EMB_F32 && grad_dtype != EMB_BF16)) return EMB_ERR_INVALID_ARG;
-  if (!seg_offsets || !num_unique) return EMB_ERR_INVALID_ARG;
-  if (T > 0 && (!ids || !grad || !uniq_ids || !uniq_grad || !workspace)) return EMB_ERR_INVALID_ARG;
-  if (reinterpret_cast<uintptr_t>(grad) % (grad_dtype == EMB_BF16 ? 2 : 4) != 0) return EMB_ERR_INVALID_ARG;
-  if (T > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return EMB_ERR_INVALID_ARG;
-  if (workspace_bytes < emb::coalesce_workspace_bytes(T, V, D) && T > 0) return EMB_ERR_WORKSPACE;
-  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, uniq_ids, seg_offsets,
-                                            uniq_grad, num_unique, workspace, dev_status,
-                                            static_cast<hipStream_t>(stream)));
+  const int st = emb::coalesce_args_status(ids, T, grad, grad_dtype, D, V, uniq_ids, seg_offsets, uniq_grad,
+                                           num_unique, workspace, workspace_bytes);
+  if (st != EMB_OK) return st;
+  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, nullptr, 1, uniq_ids,
+                                            seg_offsets, uniq_grad, num_unique, nullptr, nullptr, workspace,
+                                            dev_status, static_cast<hipStream_t>(stream)));
+}
+
+int emb_grad_coalesce_by_owner(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D,
+                               int64_t V, const int32_t* row_owner, int32_t P, int32_t* send_ids,
+                               int32_t* seg_offsets, float* send_rows, int32_t* send_counts, int32_t* send_offsets,
+                               int32_t* num_unique, void* workspace, size_t workspace_bytes, int32_t* dev_status,
+                               void* stream) {
+  const int st = emb::coalesce_by_owner_args_status(ids, T, grad, grad_dtype, D, V, row_owner, P, send_ids,
+                                                    seg_offsets, send_rows, send_counts, send_offsets, num_unique,
+                                                    workspace, workspace_bytes);
+  if (st != EMB_OK) return st;
+  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, row_owner, P, send_ids,
+                                            seg_offsets, send_rows, num_unique, send_counts, send_offsets,
+                                            workspace, dev_status, static_cast<hipStream_t>(stream)));
 }
 
 size_t emb_pack_by_owner_workspace_bytes(int32_t cap_rows, int32_t P) {
@@ -83,27 +155,9 @@ int emb_sparse_adam_apply(float* table, float* exp_avg, float* exp_avg_sq, int64
                           const int32_t* row_ids, const float* rows, const int32_t* offsets, int32_t P,
                           int32_t shard_begin, int32_t shard_end, int32_t cap_rows, double lr, double beta1,
                           double beta2, double eps, int64_t step, int32_t* dev_status, void* stream) {
-  if (bad_table_dims(V, D) || P < 1 || P > kMaxOwners || cap_rows < 0) return EMB_ERR_INVALID_ARG;
-  if (shard_begin < 0 || shard_begin > shard_end || shard_end > P) return EMB_ERR_INVALID_ARG;
-  if (step < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0) ||
-      !std::isfinite(lr) || !std::isfinite(eps))
-    return EMB_ERR_INVALID_ARG;
-  if (cap_rows == 0 || shard_begin == shard_end) return EMB_OK;
-  if (!table || !exp_avg || !exp_avg_sq || !row_ids || !rows || !offsets) return EMB_ERR_INVALID_ARG;
-  // bias corrections in fp64 on the host, then the fp32 coefficients of the kernel
-  const double bc1 = 1.0 - std::pow(beta1, static_cast<double>(step));
-  const double bc2 = 1.0 - std::pow(beta2, static_cast<double>(step));
-  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return EMB_ERR_INVALID_ARG;  // beta == 0 edge cases stay valid: bc == 1
-  emb::AdamCoeffs c;
-  c.beta1 = static_cast<float>(beta1);
-  c.one_minus_beta1 = static_cast<float>(1.0 - beta1);
-  c.beta2 = static_cast<float>(beta2);
-  c.one_minus_beta2 = static_cast<float>(1.0 - beta2);
-  c.step_size = static_cast<float>(lr / bc1);
-  c.inv_bc2 = static_cast<float>(1.0 / bc2);
-  c.eps = static_cast<float>(eps);
-  return launch_status(emb::launch_adam(table, exp_avg, exp_avg_sq, V, D, row_ids, rows, offsets, shard_begin,
-                                        shard_end, cap_rows, c, dev_status, static_cast<hipStream_t>(stream)));
+  return emb::sparse_adam_call(table, exp_avg, exp_avg_sq, V, D, row_ids, rows, offsets, P, shard_begin, shard_end,
+                               cap_rows, lr, beta1, beta2, eps, step, dev_status, static_cast<hipStream_t>(stream),
+                               nullptr, nullptr);
 }
 
 }  // extern "C"

@@ -1,29 +1,35 @@
 // COALESCE + UNIQUE of Algorithm 1 (Sec. 4.2.2): sum the gradient rows of
-// tokens with equal id, output the distinct ids in ascending order.
+// tokens with equal id, output the distinct ids in ascending order.  The
+// owner-major variant sorts by the key (owner, id) instead, which puts the
+// distinct ids straight into the per-owner send layout of Sec. 4.1.2 (owner
+// p's rows contiguous, ascending id inside): coalesce and pack in one pass
+// over the gradient rows.
 //
 // Kernels (one stream, no host synchronisation):
 //  1. sort_upsweep: digit histograms of every radix pass at once (the digit
 //     totals do not depend on the order of the keys), one row per histogram
 //     tile; it also clears the look-back state used by the later kernels.
-//  2. sort_pass, once per digit of the bitwidth(V) key bits (<= 8 bits each):
-//     a stable LSD radix pass over (key, token position).  Each tile
-//     ranks its keys in LDS with wave ballots, publishes its per-digit counts
-//     and reads the counts of the tiles before it (decoupled look-back,
-//     Merrill & Garland 2016), so one launch per pass suffices.  Tiles take
-//     their index from a ticket counter, so a tile only waits for tiles that
-//     are already running.  Ids outside [0, V) become the key V, which sorts
-//     after every valid id.
+//     Tokens whose id (or owner) is out of range take no part: they are left
+//     out of the histograms and so out of the sorted sequence.
+//  2. sort_pass, once per digit of the key bits (<= 8 bits each): a stable
+//     LSD radix pass over (key, token position).  Each tile ranks its keys in
+//     LDS with wave ballots, publishes its per-digit counts and reads the
+//     counts of the tiles before it (decoupled look-back, Merrill & Garland
+//     2016), so one launch per pass suffices.  Tiles take their index from a
+//     ticket counter, so a tile only waits for tiles that are already
+//     running.  The sorted sequence holds the n_valid tokens that take part.
 //  3. seg_count: the number of first tokens of an id (heads) in each run of
 //     128 sorted tokens.
 //  4. seg_reduce: each wave owns 32 consecutive sorted tokens.  It finds the
 //     heads with lane shuffles, adds up the head counts of the earlier
-//     workgroups, writes uniq_ids / seg_offsets / num_unique, and sums the
+//     workgroups, writes uniq_ids / seg_offsets / num_unique (and, by owner,
+//     where each owner's rows start), and sums the
 //     gradient rows of its tokens in sorted order.  Sums of ids that lie
 //     inside the chunk are final; the pieces of an id that crosses chunk
 //     boundaries go to a partials buffer.
 //  5. seg_combine: adds the pieces of each crossing id in chunk order
 //     (4 waves per id, each summing a contiguous range of pieces, then the
-//     4 results in wave order).
+//     4 results in wave order); by owner, it also forms the per-owner counts.
 // The order of every floating-point addition depends only on the ids, never
 // on scheduling, so results are bitwise reproducible.
 #include "common.h"
@@ -67,8 +73,50 @@ __device__ __forceinline__ uint32_t peek(uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ uint32_t sanitize(int32_t id, uint32_t V) {
-  return (id >= 0 && static_cast<uint32_t>(id) < V) ? static_cast<uint32_t>(id) : V;
+// How a token's id becomes its sort key: the id itself, or, with row owners,
+// owner << ib | id, which orders tokens by owner shard and by id inside it.
+struct KeySpec {
+  uint32_t V;                // ids in [0, V) take part
+  const int32_t* row_owner;  // nullptr: the key is the id
+  int32_t P;                 // owners in [0, P) take part
+  int ib;                    // id bits of a composite key
+  uint32_t id_mask;          // key -> id
+};
+
+// Keys of ITEMS tokens ids[idx[r]] (idx already clamped; inb[r]: the token
+// exists).  take[r] says whether the token takes part; with status != nullptr
+// the flags of the tokens that do not are raised.  Every load is issued
+// unconditionally, from a clamped address.
+template <int ITEMS>
+__device__ __forceinline__ void load_keys(const int32_t* __restrict__ ids, const int (&idx)[ITEMS],
+                                          const bool (&inb)[ITEMS], const KeySpec& ks, uint32_t (&key)[ITEMS],
+                                          bool (&take)[ITEMS], int32_t* status) {
+  int32_t id[ITEMS];
+  bool idok[ITEMS];
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) id[r] = ids[idx[r]];
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) idok[r] = id[r] >= 0 && static_cast<uint32_t>(id[r]) < ks.V;
+  uint32_t own[ITEMS];
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) own[r] = 0;
+  if (ks.row_owner != nullptr) {
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r) own[r] = static_cast<uint32_t>(ks.row_owner[idok[r] ? id[r] : 0]);
+  }
+  bool bad_id = false, bad_owner = false;
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) {
+    const bool ownok = own[r] < static_cast<uint32_t>(ks.P);
+    take[r] = inb[r] && idok[r] && ownok;
+    bad_id |= inb[r] && !idok[r];
+    bad_owner |= inb[r] && idok[r] && !ownok;
+    key[r] = (own[r] << ks.ib) | static_cast<uint32_t>(id[r]);
+  }
+  if (status != nullptr) {
+    if (__any(bad_id) && lane_id() == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
+    if (__any(bad_owner) && lane_id() == 0) raise_flag(status, EMB_DEV_OWNER_OUT_OF_RANGE);
+  }
 }
 
 // Exclusive prefix of one digit's counts over tiles 0 .. tile-1, read from
@@ -124,22 +172,35 @@ struct RadixPlan {
   __host__ __device__ int bits(int p) const { return min(per, B - p * per); }
 };
 
-int key_bits(int64_t V) {  // keys 0 .. V (V is the key of invalid ids)
+int bits_for(int64_t n) {  // bits of the values 0 .. n - 1
   int B = 0;
-  while ((int64_t{1} << B) <= V) ++B;
+  while ((int64_t{1} << B) < n) ++B;
   return B;
 }
 
-RadixPlan plan_for(int64_t V) {
-  const int B = key_bits(V);
+// Key bits: bits(V) for the id, plus bits(P) for the owner of a composite key.
+int key_bits(int64_t V, bool by_owner, int P) { return bits_for(V) + (by_owner ? bits_for(P) : 0); }
+
+RadixPlan plan_for(int B) {
+  B = max(B, 1);  // one pass even when every key is 0
   const int digit = 8;
   const int npass = (B + digit - 1) / digit;
   return RadixPlan{npass, (B + npass - 1) / npass, B};
 }
 
+KeySpec key_spec(int64_t V, const int32_t* row_owner, int P) {
+  KeySpec ks;
+  ks.V = static_cast<uint32_t>(V);
+  ks.row_owner = row_owner;
+  ks.P = row_owner != nullptr ? P : 1;
+  ks.ib = row_owner != nullptr ? bits_for(V) : 0;
+  ks.id_mask = row_owner != nullptr ? static_cast<uint32_t>((uint64_t{1} << ks.ib) - 1) : ~0u;
+  return ks;
+}
+
 // ---------------------------------------------------------------- radix sort
 template <class C>
-__global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const int32_t* __restrict__ ids, uint32_t V, int T,
+__global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const int32_t* __restrict__ ids, KeySpec ks, int T,
                                                               RadixPlan plan, uint32_t* __restrict__ up_hist,
                                                               uint32_t* __restrict__ zero_begin, int zero_words,
                                                               int32_t* status) {
@@ -148,19 +209,23 @@ __global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const int32_t* __r
   for (int i = threadIdx.x; i < plan.npass * kBins; i += NT) h[i] = 0;
   __syncthreads();
   const int base = blockIdx.x * C::kUpTile;
+  int idx[kPer];
+  bool inb[kPer], take[kPer];
   uint32_t k[kPer];
 #pragma unroll
-  for (int r = 0; r < kPer; ++r) k[r] = sanitize(ids[min(base + r * NT + static_cast<int>(threadIdx.x), T - 1)], V);
-  bool bad = false;
+  for (int r = 0; r < kPer; ++r) {
+    const int g = base + r * NT + static_cast<int>(threadIdx.x);
+    inb[r] = g < T;
+    idx[r] = min(g, T - 1);
+  }
+  load_keys<kPer>(ids, idx, inb, ks, k, take, status);
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
-    if (base + r * NT + static_cast<int>(threadIdx.x) < T) {
-      bad |= (k[r] == V);
+    if (take[r]) {
       for (int p = 0; p < plan.npass; ++p)
         atomicAdd(&h[p * kBins + ((k[r] >> plan.shift(p)) & ((1u << plan.bits(p)) - 1u))], 1u);
     }
   }
-  if (__any(bad) && lane_id() == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
   __syncthreads();
   for (int i = threadIdx.x; i < plan.npass * kBins; i += NT)
     up_hist[static_cast<size_t>(blockIdx.x) * plan.npass * kBins + i] = h[i];
@@ -170,8 +235,9 @@ __global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const int32_t* __r
 template <class C>
 __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ raw_ids, const int32_t* __restrict__ vals_in,
-    uint32_t V, int T, RadixPlan plan, int pass, const uint32_t* __restrict__ up_hist, int nup, uint32_t* lookback,
-    uint32_t* ticket, int ntiles, uint32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out, int32_t* status) {
+    KeySpec ks, int T, RadixPlan plan, int pass, const uint32_t* __restrict__ up_hist, int nup, uint32_t* lookback,
+    uint32_t* ticket, int ntiles, uint32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out,
+    uint32_t* __restrict__ n_valid, int32_t* status) {
   constexpr int NT = C::kNT, kBins = C::kBins, kTile = C::kTile, NW = NT / kWave;
   constexpr int kDigitsPerThread = (kBins + NT - 1) / NT;
   __shared__ uint32_t cnt[NW * kBins];
@@ -197,15 +263,23 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
   uint32_t key[kItems], dig[kItems], lpos[kItems];
   int32_t val[kItems];
   bool valid[kItems];
+  int idx[kItems];
+  bool inb[kItems];
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const int g = base + w * kItems * kWave + r * kWave + static_cast<int>(lane_id());
-    const int gc = min(g, T - 1);
-    valid[r] = g < T;
-    key[r] = raw_ids != nullptr ? sanitize(raw_ids[gc], V) : keys_in[gc];
-    val[r] = vals_in != nullptr ? vals_in[gc] : g;
-    dig[r] = (key[r] >> shift) & (bins - 1);
+    inb[r] = g < T;
+    idx[r] = min(g, T - 1);
+    val[r] = vals_in != nullptr ? vals_in[idx[r]] : g;
   }
+  if (raw_ids != nullptr) {
+    load_keys<kItems>(raw_ids, idx, inb, ks, key, valid, nullptr);
+  } else {
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) key[r] = keys_in[idx[r]];
+  }
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) dig[r] = (key[r] >> shift) & (bins - 1);
   // where each digit starts in the sorted output: exclusive scan of the digit totals
 #pragma unroll
   for (int q = 0; q < kDigitsPerThread; ++q) {
@@ -222,7 +296,13 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     if (d < kBins) gbase[d] = d < bins ? tot : 0u;
   }
   __syncthreads();
-  block_exclusive_scan<NT>(gbase, bins, wsum);
+  // the sorted sequence holds the tokens that take part: the sum of the totals
+  const uint32_t tv = block_exclusive_scan<NT>(gbase, bins, wsum);
+  if (raw_ids == nullptr) {
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) valid[r] = static_cast<uint32_t>(idx[r]) < tv && inb[r];
+  }
+  if (tile == 0 && threadIdx.x == 0) *n_valid = tv;
 
   const uint32_t nvalid = tile_stable_rank<NT, kItems>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
 #pragma unroll
@@ -297,22 +377,20 @@ struct GradRow<true, 1> {
   }
 };
 
-// Heads (first sorted token of an id) of element e, for the sorted keys: the
-// element is valid and its key differs from the previous one.
-__device__ __forceinline__ bool is_head(const uint32_t* __restrict__ skeys, int e, uint32_t V) {
-  const uint32_t k = skeys[e];
-  return k < V && (e == 0 || skeys[e - 1] != k);
-}
-
-// Number of heads among the kRedTile sorted tokens of each reduction workgroup.
-__global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t* __restrict__ skeys, uint32_t V, int T,
+// Number of heads (first sorted token of an id: its key differs from the
+// previous one) among the kRedTile sorted tokens of each reduction workgroup.
+__global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t* __restrict__ skeys,
+                                                             const uint32_t* __restrict__ n_valid,
                                                              uint32_t* __restrict__ tile_heads, int ntiles) {
   const int tile = blockIdx.x * kWaves + threadIdx.x / kWave;  // one wave per reduction workgroup
   if (tile >= ntiles) return;
+  const int tv = static_cast<int>(*n_valid);
   uint32_t c = 0;
   for (int k = static_cast<int>(lane_id()); k < kRedTile; k += kWave) {
     const int e = tile * kRedTile + k;
-    c += (e < T && is_head(skeys, e, V)) ? 1u : 0u;
+    const int ec = max(min(e, tv - 1), 0);  // loads stay inside the T sorted keys
+    const bool head = e < tv && (e == 0 || skeys[max(ec - 1, 0)] != skeys[ec]);
+    c += head ? 1u : 0u;
   }
   c = wave_sum(c);
   if (lane_id() == 0) tile_heads[tile] = c;
@@ -320,12 +398,11 @@ __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t* __r
 
 template <bool BF16, int VEC>
 __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
-    const uint32_t* __restrict__ skeys, const int32_t* __restrict__ spos, uint32_t V, int T,
-    const void* __restrict__ grad, int D, const uint32_t* __restrict__ tile_heads,
-    int32_t* __restrict__ uniq_ids,
-    int32_t* __restrict__ seg_offsets, int32_t* __restrict__ num_unique, float* __restrict__ uniq_grad,
-    float* __restrict__ partial, int32_t* __restrict__ span_list, int32_t* __restrict__ span_count,
-    int32_t* status) {
+    const uint32_t* __restrict__ skeys, const int32_t* __restrict__ spos, const uint32_t* __restrict__ n_valid, int T,
+    const void* __restrict__ grad, int D, const uint32_t* __restrict__ tile_heads, int ib, uint32_t id_mask,
+    int32_t* __restrict__ uniq_ids, int32_t* __restrict__ seg_offsets, int32_t* __restrict__ num_unique,
+    float* __restrict__ uniq_grad, int32_t* __restrict__ owner_offsets, int P, float* __restrict__ partial,
+    int32_t* __restrict__ span_list, int32_t* __restrict__ span_count) {
   __shared__ uint32_t wave_heads[kWaves];
   __shared__ uint32_t red[kWaves];
   const int tile = blockIdx.x;
@@ -335,11 +412,12 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const int a = chunk * kChunk;
 
   // lane L holds sorted element e = a - 1 + L, for L = 0 .. kChunk + 1
+  const int tv = static_cast<int>(*n_valid);
   const int e = a - 1 + lane;
   const int ec = min(max(e, 0), T - 1);
   const uint32_t key = skeys[ec];
   const int32_t pos = spos[ec];
-  const bool valid = e >= 0 && e < T && key < V && lane <= kChunk + 1;
+  const bool valid = e >= 0 && e < tv && lane <= kChunk + 1;
   const uint32_t key_prev = __shfl_up(key, 1, kWave);
   // element e does not continue the id of element e - 1
   const bool starts_new = !valid || e == 0 || key_prev != key;
@@ -380,17 +458,26 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const uint64_t upto = (lane == kWave - 1) ? ~0ull : ((2ull << lane) - 1ull);
   const int u = static_cast<int>(ubase + __popcll(heads & upto)) - 1;  // unique index of element e
   if (head) {
-    uniq_ids[u] = static_cast<int32_t>(key);
+    uniq_ids[u] = static_cast<int32_t>(key & id_mask);
     seg_offsets[u] = e;
+    if (owner_offsets != nullptr) {  // owners o' < p <= o start at this row
+      const int o = static_cast<int>(key >> ib);
+      const int o_prev = e == 0 ? -1 : static_cast<int>(key_prev >> ib);
+      for (int p = o_prev + 1; p <= o; ++p) owner_offsets[p] = u;
+    }
   }
   const bool next_valid = __shfl_down(valid ? 1 : 0, 1, kWave) != 0;
   if (in_chunk && valid && (e + 1 == T || !next_valid)) {
     seg_offsets[u + 1] = e + 1;  // the last valid token of the whole batch
     num_unique[0] = u + 1;
+    if (owner_offsets != nullptr)
+      for (int p = static_cast<int>(key >> ib) + 1; p <= P; ++p) owner_offsets[p] = u + 1;
   }
   if (chunk == 0 && lane == 1 && !valid) {  // no valid token at all
     seg_offsets[0] = 0;
     num_unique[0] = 0;
+    if (owner_offsets != nullptr)
+      for (int p = 0; p <= P; ++p) owner_offsets[p] = 0;
   }
   if (nv == 0) return;
 
@@ -449,9 +536,13 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
                                                                const int32_t* __restrict__ seg_offsets,
                                                                const int32_t* __restrict__ span_list,
                                                                const int32_t* __restrict__ span_count,
-                                                               float* __restrict__ uniq_grad) {
+                                                               float* __restrict__ uniq_grad,
+                                                               const int32_t* __restrict__ owner_offsets,
+                                                               int32_t* __restrict__ owner_counts, int P) {
   using Acc = typename GradRow<false, VEC>::Acc;
   __shared__ Acc red[kWaves][kWave];
+  if (owner_counts != nullptr && blockIdx.x == 0)
+    for (int p = threadIdx.x; p < P; p += kThreads) owner_counts[p] = owner_offsets[p + 1] - owner_offsets[p];
   const int n = span_count[0];
   const int Dv = D / VEC;
   const int w = threadIdx.x / kWave;
@@ -496,30 +587,39 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
   }
 }
 
-__global__ void empty_batch_kernel(int32_t* seg_offsets, int32_t* num_unique) {
-  seg_offsets[0] = 0;
-  num_unique[0] = 0;
+__global__ void empty_batch_kernel(int32_t* seg_offsets, int32_t* num_unique, int32_t* owner_counts,
+                                   int32_t* owner_offsets, int P) {
+  if (threadIdx.x == 0) {
+    seg_offsets[0] = 0;
+    num_unique[0] = 0;
+  }
+  if (owner_counts != nullptr) {
+    for (int p = threadIdx.x; p <= P; p += blockDim.x) {
+      owner_offsets[p] = 0;
+      if (p < P) owner_counts[p] = 0;
+    }
+  }
 }
 
 struct CoalesceWs {
   uint32_t *keys_a, *keys_b;
   int32_t *vals_a, *vals_b;
-  uint32_t* up_hist;
-  uint32_t* zero_begin;  // everything from here to zero_end starts at zero
-  uint32_t* sort_lb;     // [npass][ntiles][kBins]
-  uint32_t* tickets;     // [kMaxPasses]
+  uint32_t* up_hist;     // [nup][npass][kBins]
+  uint32_t* tickets;     // [kMaxPasses]; starts the region that starts at zero
   int32_t* span_count;
-  uint32_t* zero_end;
+  uint32_t* sort_lb;     // [npass][ntiles][kBins]; ends that region (npass of the call)
+  uint32_t* n_valid;     // tokens that take part (written by the radix passes)
   int32_t* span_list;
   uint32_t* tile_heads;  // [nred]
   float* partial;
   size_t bytes;
 };
 
+// The layout does not depend on the number of radix passes (sized for the
+// most), so one size serves both the plain and the owner-major call.
 template <class C>
-CoalesceWs carve_with(void* base, int T, int64_t V, int D) {
+CoalesceWs carve_with(void* base, int T, int D) {
   Carver cv{static_cast<char*>(base)};
-  const RadixPlan plan = plan_for(V);
   const size_t n = static_cast<size_t>(T);
   const size_t ntiles = (n + C::kTile - 1) / C::kTile;
   const size_t nup = (n + C::kUpTile - 1) / C::kUpTile;
@@ -530,12 +630,11 @@ CoalesceWs carve_with(void* base, int T, int64_t V, int D) {
   w.keys_b = cv.take<uint32_t>(n);
   w.vals_a = cv.take<int32_t>(n);
   w.vals_b = cv.take<int32_t>(n);
-  w.up_hist = cv.take<uint32_t>(nup * plan.npass * C::kBins);
-  w.sort_lb = cv.take<uint32_t>(static_cast<size_t>(plan.npass) * ntiles * C::kBins);
-  w.zero_begin = w.sort_lb;
+  w.up_hist = cv.take<uint32_t>(nup * kMaxPasses * C::kBins);
   w.tickets = cv.take<uint32_t>(kMaxPasses);
   w.span_count = cv.take<int32_t>(1);
-  w.zero_end = cv.take<uint32_t>(0);
+  w.sort_lb = cv.take<uint32_t>(static_cast<size_t>(kMaxPasses) * ntiles * C::kBins);
+  w.n_valid = cv.take<uint32_t>(1);
   w.span_list = cv.take<int32_t>(nchunks);
   w.tile_heads = cv.take<uint32_t>(nred);
   w.partial = cv.take<float>(nchunks * 2 * static_cast<size_t>(D));
@@ -543,24 +642,26 @@ CoalesceWs carve_with(void* base, int T, int64_t V, int D) {
   return w;
 }
 
-CoalesceWs carve(void* base, int T, int64_t V, int D) { return carve_with<Narrow>(base, T, V, D); }
+CoalesceWs carve(void* base, int T, int D) { return carve_with<Narrow>(base, T, D); }
 
 template <class C>
-void launch_sort(const int32_t* ids, int T, uint32_t Vk, const RadixPlan& plan, const CoalesceWs& ws,
+void launch_sort(const int32_t* ids, int T, const KeySpec& ks, const RadixPlan& plan, const CoalesceWs& ws,
                  int32_t* status, hipStream_t stream, const uint32_t** skeys, const int32_t** spos) {
   const int ntiles = (T + C::kTile - 1) / C::kTile;
   const int nup = (T + C::kUpTile - 1) / C::kUpTile;
-  const int zero_words = static_cast<int>(ws.zero_end - ws.zero_begin);
-  hipLaunchKernelGGL(sort_upsweep_kernel<C>, dim3(nup), dim3(C::kNT), 0, stream, ids, Vk, T, plan, ws.up_hist,
-                     ws.zero_begin, zero_words, status);
+  uint32_t* zero_begin = ws.tickets;
+  const int zero_words =
+      static_cast<int>((ws.sort_lb + static_cast<size_t>(plan.npass) * ntiles * C::kBins) - zero_begin);
+  hipLaunchKernelGGL(sort_upsweep_kernel<C>, dim3(nup), dim3(C::kNT), 0, stream, ids, ks, T, plan, ws.up_hist,
+                     zero_begin, zero_words, status);
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
   uint32_t* kout = ws.keys_a;
   int32_t* vout = ws.vals_a;
   for (int p = 0; p < plan.npass; ++p) {
     hipLaunchKernelGGL(sort_pass_kernel<C>, dim3(ntiles), dim3(C::kNT), 0, stream, kin, (p == 0) ? ids : nullptr,
-                       vin, Vk, T, plan, p, ws.up_hist, nup, ws.sort_lb + static_cast<size_t>(p) * ntiles * C::kBins,
-                       ws.tickets + p, ntiles, kout, vout, status);
+                       vin, ks, T, plan, p, ws.up_hist, nup, ws.sort_lb + static_cast<size_t>(p) * ntiles * C::kBins,
+                       ws.tickets + p, ntiles, kout, vout, ws.n_valid, status);
     kin = kout;
     vin = vout;
     kout = (kout == ws.keys_a) ? ws.keys_b : ws.keys_a;
@@ -570,54 +671,96 @@ void launch_sort(const int32_t* ids, int T, uint32_t Vk, const RadixPlan& plan, 
   *spos = vin;
 }
 
+RadixPlan plan_for_call(int64_t V, const int32_t* row_owner, int P) {
+  return plan_for(key_bits(V, row_owner != nullptr, P));
+}
+
+// The sorted keys and positions are in the ping-pong buffer the last pass wrote.
+void sorted_arrays(const CoalesceWs& ws, const RadixPlan& plan, const uint32_t** skeys, const int32_t** spos) {
+  const bool odd = plan.npass % 2 == 1;
+  *skeys = odd ? ws.keys_a : ws.keys_b;
+  *spos = odd ? ws.vals_a : ws.vals_b;
+}
+
 }  // namespace
 
-size_t coalesce_workspace_bytes(int T, int64_t V, int D) { return carve(nullptr, T, V, D).bytes; }
+size_t coalesce_workspace_bytes(int T, int D) { return carve(nullptr, T, D).bytes; }
 
-hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
-                           int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad, int32_t* num_unique,
-                           void* workspace, int32_t* status, hipStream_t stream) {
-  if (T == 0) {
-    hipLaunchKernelGGL(empty_batch_kernel, dim3(1), dim3(1), 0, stream, seg_offsets, num_unique);
-    return hipGetLastError();
-  }
-  CoalesceWs ws = carve(workspace, T, V, D);
-  const RadixPlan plan = plan_for(V);
-  const uint32_t Vk = static_cast<uint32_t>(V);
+bool coalesce_by_owner_supported(int64_t V, int P) { return key_bits(V, true, P) <= 8 * kMaxPasses; }
+
+hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const int32_t* row_owner, int P,
+                                void* workspace, int32_t* status, hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  CoalesceWs ws = carve(workspace, T, D);
+  const KeySpec ks = key_spec(V, row_owner, P);
+  const RadixPlan plan = plan_for_call(V, row_owner, P);
   const int nred = (T + kRedTile - 1) / kRedTile;
-  const int nchunks = (T + kChunk - 1) / kChunk;
-
   // 1-2. digit histograms of all passes, then the radix passes over (key, position)
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
-  launch_sort<Narrow>(ids, T, Vk, plan, ws, status, stream, &kin, &vin);
-  // 3. heads per reduction workgroup; 4. segments and per-chunk sums; 5. pieces of ids that cross chunks
-  hipLaunchKernelGGL(seg_count_kernel, dim3((nred + kWaves - 1) / kWaves), dim3(kThreads), 0, stream, kin, Vk, T,
+  launch_sort<Narrow>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
+  // 3. heads per reduction workgroup
+  hipLaunchKernelGGL(seg_count_kernel, dim3((nred + kWaves - 1) / kWaves), dim3(kThreads), 0, stream, kin, ws.n_valid,
                      ws.tile_heads, nred);
+  return hipGetLastError();
+}
+
+hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V, const int32_t* row_owner,
+                                  int P, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
+                                  int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
+                                  void* workspace, hipStream_t stream) {
+  // owner_offsets / owner_counts are given exactly for the owner-major variant
+  // (row_owner != nullptr whenever T > 0)
+  if (T == 0) {
+    hipLaunchKernelGGL(empty_batch_kernel, dim3(1), dim3(kThreads), 0, stream, seg_offsets, num_unique, owner_counts,
+                       owner_offsets, P);
+    return hipGetLastError();
+  }
+  CoalesceWs ws = carve(workspace, T, D);
+  const KeySpec ks = key_spec(V, row_owner, P);
+  const RadixPlan plan = plan_for_call(V, row_owner, P);
+  const int nred = (T + kRedTile - 1) / kRedTile;
+  const int nchunks = (T + kChunk - 1) / kChunk;
+  const uint32_t* kin = nullptr;
+  const int32_t* vin = nullptr;
+  sorted_arrays(ws, plan, &kin, &vin);
+  // 4. segments and per-chunk sums; 5. pieces of ids that cross chunks
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(grad) % (grad_bf16 ? 8 : 16) == 0) &&
                     (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
   const dim3 cgrid(grid_for(nchunks, 1024));
-#define EMB_REDUCE(BF, VC)                                                                                        \
-  hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred), dim3(kThreads), 0, stream, kin, vin, Vk, T, grad, D, \
-                     ws.tile_heads, uniq_ids, seg_offsets, num_unique, uniq_grad, ws.partial,  \
-                     ws.span_list, ws.span_count, status)
+#define EMB_REDUCE(BF, VC)                                                                                          \
+  hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred), dim3(kThreads), 0, stream, kin, vin, ws.n_valid, T, \
+                     grad, D, ws.tile_heads, ks.ib, ks.id_mask, uniq_ids, seg_offsets, num_unique, uniq_grad,        \
+                     owner_offsets, ks.P, ws.partial, ws.span_list, ws.span_count)
+#define EMB_COMBINE(VC)                                                                                             \
+  hipLaunchKernelGGL(seg_combine_kernel<VC>, cgrid, dim3(kThreads), 0, stream, ws.partial, D, seg_offsets,          \
+                     ws.span_list, ws.span_count, uniq_grad, owner_offsets, owner_counts, ks.P)
   if (vec4) {
     if (grad_bf16)
       EMB_REDUCE(true, 4);
     else
       EMB_REDUCE(false, 4);
-    hipLaunchKernelGGL(seg_combine_kernel<4>, cgrid, dim3(kThreads), 0, stream, ws.partial, D, seg_offsets,
-                       ws.span_list, ws.span_count, uniq_grad);
+    EMB_COMBINE(4);
   } else {
     if (grad_bf16)
       EMB_REDUCE(true, 1);
     else
       EMB_REDUCE(false, 1);
-    hipLaunchKernelGGL(seg_combine_kernel<1>, cgrid, dim3(kThreads), 0, stream, ws.partial, D, seg_offsets,
-                       ws.span_list, ws.span_count, uniq_grad);
+    EMB_COMBINE(1);
   }
 #undef EMB_REDUCE
+#undef EMB_COMBINE
   return hipGetLastError();
+}
+
+hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
+                           const int32_t* row_owner, int P, int32_t* uniq_ids, int32_t* seg_offsets,
+                           float* uniq_grad, int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
+                           void* workspace, int32_t* status, hipStream_t stream) {
+  const hipError_t e = launch_coalesce_sort(ids, T, V, D, row_owner, P, workspace, status, stream);
+  if (e != hipSuccess) return e;
+  return launch_coalesce_reduce(T, grad, grad_bf16, D, V, row_owner, P, uniq_ids, seg_offsets, uniq_grad, num_unique,
+                                owner_counts, owner_offsets, workspace, stream);
 }
 
 }  // namespace emb

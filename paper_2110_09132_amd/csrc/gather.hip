@@ -1,9 +1,12 @@
 // Forward lookup (Sec. 4.1.1): out[t][:] = table[ids[t]][:].
 //
-// A row is handled by L = min(64, 2^ceil(log2(D / VEC))) lanes; a wave covers
-// 64 / L rows per step and keeps kRowsInFlight steps of loads in flight before
-// storing, so every lane has several independent 16-byte loads outstanding.
-// Reads are whole table rows (contiguous), writes are contiguous output rows.
+// Each wave owns a contiguous range of output rows.  A row is handled by
+// L = min(64, 2^ceil(log2(D / VEC))) lanes, so a wave covers 64 / L rows per
+// step.  The ids of 64 rows come in one coalesced load (lane l holds the id of
+// row l) and reach their lanes by shuffle; rows are processed in groups of
+// kRowsInFlight steps, and the table loads of the next group are issued before
+// the current group is stored, so each lane keeps two groups of independent
+// 16-byte loads in flight.  Reads are whole table rows, writes contiguous rows.
 #include "common.h"
 #include "launch.h"
 
@@ -19,38 +22,61 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const VecT* __restrict
                                                           VecT* __restrict__ out, int32_t* status) {
   const int L = 1 << log2L;
   const int rpw = kWave >> log2L;
-  const int sub = lane_id() >> log2L;
-  const int cl = lane_id() & (L - 1);
-  const long long wave = (static_cast<long long>(blockIdx.x) * kThreads + threadIdx.x) / kWave;
-  const long long nwaves = static_cast<long long>(gridDim.x) * (kThreads / kWave);
-  const long long rows_per_step = static_cast<long long>(rpw) * kRowsInFlight;
+  const int lane = static_cast<int>(lane_id());
+  const int sub = lane >> log2L;
+  const int cl = lane & (L - 1);
+  const int wave = uniform(static_cast<int>(blockIdx.x) * (kThreads / kWave) + static_cast<int>(threadIdx.x / kWave));
+  const int nwaves = static_cast<int>(gridDim.x) * (kThreads / kWave);
+  // rows of this wave: [r0, r1), a multiple of the rows one step covers
+  const long long step_rows = static_cast<long long>(rpw) * kRowsInFlight;
+  long long per = (static_cast<long long>(T) + nwaves - 1) / nwaves;
+  per = (per + step_rows - 1) / step_rows * step_rows;
+  const long long r0 = static_cast<long long>(wave) * per;
+  const long long r1 = min(static_cast<long long>(T), r0 + per);
   bool bad = false;
-  for (long long r0 = wave * rows_per_step; r0 < T; r0 += nwaves * rows_per_step) {
-    // Loads are issued unconditionally from clamped, always-valid addresses so
-    // that all of them are in flight together; only the stores are predicated.
-    int32_t id[kRowsInFlight];
-    bool live[kRowsInFlight];
-#pragma unroll
-    for (int u = 0; u < kRowsInFlight; ++u) {
-      const long long row = r0 + u * rpw + sub;
-      live[u] = row < T;
-      id[u] = ids[live[u] ? row : T - 1];
-    }
-#pragma unroll
-    for (int u = 0; u < kRowsInFlight; ++u) {
-      const bool ok = id[u] >= 0 && id[u] < V;
-      bad |= live[u] && !ok;
-      if (!ok) id[u] = -1;
-    }
-    for (int c = cl; c < Dv; c += L) {
-      VecT v[kRowsInFlight];
-#pragma unroll
-      for (int u = 0; u < kRowsInFlight; ++u)
-        v[u] = table[static_cast<size_t>(id[u] < 0 ? 0 : id[u]) * Dv + c];
+  for (long long c0 = r0; c0 < r1; c0 += kWave) {  // 64 rows per id load
+    const int n = static_cast<int>(min(static_cast<long long>(kWave), r1 - c0));
+    const int32_t idreg = ids[min(c0 + lane, static_cast<long long>(T) - 1)];
+    bad |= lane < n && (idreg < 0 || idreg >= V);
+    // group g covers chunk rows [g * step_rows, (g + 1) * step_rows)
+    const int ngroups = static_cast<int>((n + step_rows - 1) / step_rows);
+    auto row_id = [&](int g, int u) {  // table row of this lane's row u of group g, -1 if none
+      const int j = g * static_cast<int>(step_rows) + u * rpw + sub;
+      const int id = __shfl(idreg, min(j, kWave - 1), kWave);
+      return (j < n && id >= 0 && id < V) ? id : -1;
+    };
+    // column steps are uniform across the wave (the shuffles need every lane)
+    for (int cb = 0; cb < Dv; cb += L) {
+      const int c = min(cb + cl, Dv - 1);
+      const bool cok = cb + cl < Dv;
+      VecT cur[kRowsInFlight], nxt[kRowsInFlight];
+      int cid[kRowsInFlight];
 #pragma unroll
       for (int u = 0; u < kRowsInFlight; ++u) {
-        const long long row = r0 + u * rpw + sub;
-        if (live[u]) out[static_cast<size_t>(row) * Dv + c] = id[u] < 0 ? VecT{} : v[u];
+        cid[u] = row_id(0, u);
+        cur[u] = table[static_cast<size_t>(cid[u] < 0 ? 0 : cid[u]) * Dv + c];
+      }
+      for (int g = 0; g < ngroups; ++g) {
+        int nid[kRowsInFlight];
+        if (g + 1 < ngroups) {
+#pragma unroll
+          for (int u = 0; u < kRowsInFlight; ++u) {
+            nid[u] = row_id(g + 1, u);
+            nxt[u] = table[static_cast<size_t>(nid[u] < 0 ? 0 : nid[u]) * Dv + c];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+          const int j = g * static_cast<int>(step_rows) + u * rpw + sub;
+          if (j < n && cok) out[static_cast<size_t>(c0 + j) * Dv + c] = cid[u] < 0 ? VecT{} : cur[u];
+        }
+        if (g + 1 < ngroups) {
+#pragma unroll
+          for (int u = 0; u < kRowsInFlight; ++u) {
+            cur[u] = nxt[u];
+            cid[u] = nid[u];
+          }
+        }
       }
     }
   }
@@ -67,7 +93,7 @@ hipError_t launch_gather(const float* table, int64_t V, int D, const int32_t* id
   const int Dv = vec4 ? D / 4 : D;
   const RowLanes rl = row_lanes_for(Dv);
   const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * kRowsInFlight * (kThreads / kWave);
-  const unsigned grid = grid_for((T + rows_per_block - 1) / rows_per_block, 4096);
+  const unsigned grid = grid_for((T + rows_per_block - 1) / rows_per_block, kMaxBlocks);
   if (vec4) {
     hipLaunchKernelGGL(gather_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream,
                        reinterpret_cast<const float4*>(table), V, Dv, rl.log2_lanes, ids, T,

@@ -11,10 +11,33 @@ namespace emb {
 hipError_t launch_gather(const float* table, int64_t V, int D, const int32_t* ids, int T, float* out,
                          int32_t* status, hipStream_t stream);
 
-size_t coalesce_workspace_bytes(int T, int64_t V, int D);
+// Coalesce of T tokens; with row_owner != nullptr the owner-major variant
+// (distinct ids grouped by owner in [0, P), counts and offsets per owner).
+// The workspace size does not depend on the variant.
+size_t coalesce_workspace_bytes(int T, int D);
+bool coalesce_by_owner_supported(int64_t V, int P);  // (owner, id) keys fit the radix passes
+// The two halves of launch_coalesce, for schedules that run them on different
+// streams (same workspace and variant; the reduce half must follow the sort half).
+hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const int32_t* row_owner, int P,
+                                void* workspace, int32_t* status, hipStream_t stream);
+hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V, const int32_t* row_owner,
+                                  int P, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
+                                  int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
+                                  void* workspace, hipStream_t stream);
 hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
-                           int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad, int32_t* num_unique,
+                           const int32_t* row_owner, int P, int32_t* uniq_ids, int32_t* seg_offsets,
+                           float* uniq_grad, int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
                            void* workspace, int32_t* status, hipStream_t stream);
+// Host-side argument checks of emb_grad_coalesce and emb_grad_coalesce_by_owner
+// (EMB_OK when the call is valid).
+int coalesce_args_status(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D, int64_t V,
+                         const int32_t* uniq_ids, const int32_t* seg_offsets, const float* uniq_grad,
+                         const int32_t* num_unique, const void* workspace, size_t workspace_bytes);
+int coalesce_by_owner_args_status(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D,
+                                  int64_t V, const int32_t* row_owner, int32_t P, const int32_t* send_ids,
+                                  const int32_t* seg_offsets, const float* send_rows, const int32_t* send_counts,
+                                  const int32_t* send_offsets, const int32_t* num_unique, const void* workspace,
+                                  size_t workspace_bytes);
 
 size_t pack_workspace_bytes(int cap_rows, int P);
 hipError_t launch_pack(const int32_t* uniq_ids, const float* uniq_grad, const int32_t* num_unique, int cap_rows,
@@ -29,9 +52,17 @@ struct AdamCoeffs {
   float eps;
 };
 
+// start / stop (may be null): events that take the kernel's own start and end
+// times from its dispatch (no separate marker packets on the stream).
 hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int D, const int32_t* row_ids,
                        const float* rows, const int32_t* offsets, int shard_begin, int shard_end, int cap_rows,
-                       const AdamCoeffs& c, int32_t* status, hipStream_t stream);
+                       const AdamCoeffs& c, int32_t* status, hipStream_t stream, hipEvent_t start = nullptr,
+                       hipEvent_t stop = nullptr);
+// emb_sparse_adam_apply with the optional start / stop events of launch_adam.
+int sparse_adam_call(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int32_t D, const int32_t* row_ids,
+                     const float* rows, const int32_t* offsets, int32_t P, int32_t shard_begin, int32_t shard_end,
+                     int32_t cap_rows, double lr, double beta1, double beta2, double eps, int64_t step,
+                     int32_t* dev_status, hipStream_t stream, hipEvent_t start, hipEvent_t stop);
 
 // Carves aligned regions out of a workspace; with base == nullptr it only measures.
 struct Carver {
@@ -46,6 +77,13 @@ struct Carver {
   }
   size_t size() const { return (off + 255) & ~static_cast<size_t>(255); }
 };
+
+// Grid cap of the bandwidth-bound row kernels (gather, row copy, update): two
+// 256-thread workgroups per CU keep enough bytes in flight to saturate HBM and
+// leave wave slots on every CU for the short latency-bound kernels that run
+// on the other streams of a step (measured: ~8 us per step less than filling
+// the chip).
+constexpr long long kMaxBlocks = 512;
 
 // Grid of at most `cap` blocks for `work` blocks of work (grid-stride kernels).
 inline unsigned grid_for(long long work, long long cap) {

@@ -3,7 +3,8 @@
 //
 // A stable partition by owner is one radix pass whose digit is the owner
 // (P <= 1024 owners plus one bin for rows that are not sent):
-//  1. per-tile owner histograms (LDS atomics),
+//  1. per-tile owner histograms (LDS atomics); the owner digit of every row
+//     is kept, so the owner table is read once,
 //  2. per tile: global base of each owner (sum of earlier tiles and owners) +
 //     stable rank inside the tile (wave ballots, as in the sort) -> the send
 //     slot of every row; ids are written there, the slot is kept for step 3;
@@ -16,8 +17,8 @@ namespace emb {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kItems = 8;
-constexpr int kTile = kThreads * kItems;
+constexpr int kItems = 4;
+constexpr int kTile = kThreads * kItems;  // rows per tile
 constexpr int kMaxOwners = 1024;
 constexpr int kBinsMax = kMaxOwners + 1;
 constexpr int kRowsInFlight = 8;
@@ -47,7 +48,8 @@ __device__ __forceinline__ uint32_t owner_of(int32_t id, const int32_t* __restri
 __global__ __launch_bounds__(kThreads) void pack_hist_kernel(const int32_t* __restrict__ uniq_ids,
                                                              const int32_t* __restrict__ num_unique, int cap,
                                                              const int32_t* __restrict__ row_owner, int64_t V, int P,
-                                                             uint32_t* __restrict__ tile_hist, int32_t* status) {
+                                                             uint32_t* __restrict__ tile_hist,
+                                                             uint16_t* __restrict__ digit_of, int32_t* status) {
   __shared__ uint32_t h[kBinsMax];
   const int bins = P + 1;
   for (int i = threadIdx.x; i < bins; i += kThreads) h[i] = 0;
@@ -63,8 +65,13 @@ __global__ __launch_bounds__(kThreads) void pack_hist_kernel(const int32_t* __re
 #pragma unroll
     for (int r = 0; r < kItems; ++r) d[r] = owner_of(id[r], row_owner, V, P, flags);
 #pragma unroll
-    for (int r = 0; r < kItems; ++r)
-      if (base + r * kThreads + static_cast<int>(threadIdx.x) < U) atomicAdd(&h[d[r]], 1u);
+    for (int r = 0; r < kItems; ++r) {
+      const int k = base + r * kThreads + static_cast<int>(threadIdx.x);
+      if (k < U) {
+        atomicAdd(&h[d[r]], 1u);
+        digit_of[k] = static_cast<uint16_t>(d[r]);
+      }
+    }
   }
   if (flags != 0) raise_flag(status, flags);
   __syncthreads();
@@ -73,7 +80,7 @@ __global__ __launch_bounds__(kThreads) void pack_hist_kernel(const int32_t* __re
 
 __global__ __launch_bounds__(kThreads) void pack_scatter_kernel(
     const int32_t* __restrict__ uniq_ids, const int32_t* __restrict__ num_unique, int cap,
-    const int32_t* __restrict__ row_owner, int64_t V, int P, int owner_bits, const uint32_t* __restrict__ tile_hist,
+    const uint16_t* __restrict__ digit_of, int P, int owner_bits, const uint32_t* __restrict__ tile_hist,
     int ntiles, int32_t* __restrict__ send_ids, int32_t* __restrict__ slot_of, int32_t* __restrict__ send_counts,
     int32_t* __restrict__ send_offsets) {
   __shared__ uint32_t cnt[(kThreads / kWave) * kBinsMax];
@@ -89,17 +96,14 @@ __global__ __launch_bounds__(kThreads) void pack_scatter_kernel(
   int32_t id[kItems];
   uint32_t dig[kItems], lpos[kItems];
   bool valid[kItems];
-  int flags = 0;
 #pragma unroll
   for (int r = 0; r < kItems; ++r) {
     const int k = base + w * kItems * kWave + r * kWave + static_cast<int>(lane_id());
+    const int kc = max(min(k, U - 1), 0);
     valid[r] = k < U;
-    id[r] = uniq_ids[max(min(k, U - 1), 0)];
-  }
-#pragma unroll
-  for (int r = 0; r < kItems; ++r) {
-    const uint32_t d = owner_of(id[r], row_owner, V, P, flags);
-    dig[r] = valid[r] ? d : 0u;
+    id[r] = uniq_ids[kc];
+    dig[r] = digit_of[kc];
+    if (!valid[r]) dig[r] = 0u;
   }
   const uint32_t total =
       tile_global_bases<kThreads>(tile_hist, ntiles, tile, bins, colall, gbase, red_all, red_bef, wsum);
@@ -164,6 +168,7 @@ __global__ __launch_bounds__(kThreads) void pack_rows_kernel(const VecT* __restr
 struct PackWs {
   uint32_t* tile_hist;
   int32_t* slot_of;
+  uint16_t* digit_of;
   size_t bytes;
 };
 
@@ -173,6 +178,7 @@ PackWs carve(void* base, int cap, int P) {
   PackWs w;
   w.tile_hist = cv.take<uint32_t>((ntiles > 0 ? ntiles : 1) * static_cast<size_t>(P + 1));
   w.slot_of = cv.take<int32_t>(static_cast<size_t>(cap > 0 ? cap : 1));
+  w.digit_of = cv.take<uint16_t>(static_cast<size_t>(cap > 0 ? cap : 1));
   w.bytes = cv.size();
   return w;
 }
@@ -201,16 +207,16 @@ hipError_t launch_pack(const int32_t* uniq_ids, const float* uniq_grad, const in
   int owner_bits = 0;
   while ((1 << owner_bits) <= P) ++owner_bits;  // digits 0..P
   hipLaunchKernelGGL(pack_hist_kernel, dim3(ntiles), dim3(kThreads), 0, stream, uniq_ids, num_unique, cap_rows,
-                     row_owner, V, P, ws.tile_hist, status);
+                     row_owner, V, P, ws.tile_hist, ws.digit_of, status);
   hipLaunchKernelGGL(pack_scatter_kernel, dim3(ntiles), dim3(kThreads), 0, stream, uniq_ids, num_unique, cap_rows,
-                     row_owner, V, P, owner_bits, ws.tile_hist, ntiles, send_ids, ws.slot_of, send_counts,
+                     ws.digit_of, P, owner_bits, ws.tile_hist, ntiles, send_ids, ws.slot_of, send_counts,
                      send_offsets);
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0) &&
                     (reinterpret_cast<uintptr_t>(send_rows) % 16 == 0);
   const int Dv = vec4 ? D / 4 : D;
   const RowLanes rl = row_lanes_for(Dv);
   const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * kRowsInFlight * (kThreads / kWave);
-  const unsigned grid = grid_for((cap_rows + rows_per_block - 1) / rows_per_block, 4096);
+  const unsigned grid = grid_for((cap_rows + rows_per_block - 1) / rows_per_block, kMaxBlocks);
   if (vec4)
     hipLaunchKernelGGL(pack_rows_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream,
                        reinterpret_cast<const float4*>(uniq_grad), num_unique, cap_rows, ws.slot_of, Dv,

@@ -1,6 +1,7 @@
 // Step executor: one host call enqueues a whole training step of one table
 // on three streams with the event waits of the schedule in include/emb.h.
 #include "common.h"
+#include "launch.h"
 
 namespace {
 
@@ -41,40 +42,70 @@ int emb_event_elapsed_ms(void* start, void* end, float* ms) {
 
 int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
   if (a == nullptr || s == nullptr) return EMB_ERR_INVALID_ARG;
-  if (s->coalesced == nullptr || s->packed == nullptr || s->updated == nullptr) return EMB_ERR_INVALID_ARG;
+  if (s->coalesced == nullptr) return EMB_ERR_INVALID_ARG;
+  if (s->by_owner ? s->sorted == nullptr : (s->packed == nullptr || s->updated == nullptr)) return EMB_ERR_INVALID_ARG;
   if (a->T < 0 || a->cap_rows < a->T) return EMB_ERR_INVALID_ARG;
+  const bool sep_c = s->coalesce != s->lookup_update;
   const bool sep_p = s->pack != s->lookup_update;
   int st = EMB_OK;
   // each step stops the sequence at the first failing call
   auto ok = [&st](int r) { return (st = r) == EMB_OK; };
-  // coalesce(s): after pack(s-2) has read this buffer set's unique rows
-  if (s->reuse && s->coalesce != s->pack && !ok(wait(s->coalesce, s->packed))) return st;
-  if (!ok(record(s->timing[2], s->coalesce))) return st;
-  if (!ok(emb_grad_coalesce(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->uniq_ids, a->seg_offsets,
-                            a->uniq_grad, a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes, a->dev_status,
-                            s->coalesce)))
-    return st;
-  if (!ok(record(s->timing[3], s->coalesce)) || !ok(record(s->coalesced, s->coalesce))) return st;
-  // pack(s): after coalesce(s), and after update(s-2) has read this set's send rows
-  if (s->pack != s->coalesce && !ok(wait(s->pack, s->coalesced))) return st;
-  if (s->reuse && sep_p && !ok(wait(s->pack, s->updated))) return st;
-  if (!ok(record(s->timing[4], s->pack))) return st;
-  if (!ok(emb_pack_by_owner(a->uniq_ids, a->uniq_grad, a->num_unique, a->cap_rows, a->D, a->row_owner, a->V, a->P,
-                            a->send_ids, a->send_rows, a->send_counts, a->send_offsets, a->ws_pack,
-                            a->ws_pack_bytes, a->dev_status, s->pack)))
-    return st;
-  if (!ok(record(s->timing[5], s->pack)) || !ok(record(s->packed, s->pack))) return st;
-  // lookup(s) on the main stream, then update(s) once the rows are packed
-  if (!ok(record(s->timing[0], s->lookup_update))) return st;
-  if (!ok(emb_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status, s->lookup_update))) return st;
-  if (!ok(record(s->timing[1], s->lookup_update))) return st;
-  if (sep_p && !ok(wait(s->lookup_update, s->packed))) return st;
-  if (!ok(record(s->timing[6], s->lookup_update))) return st;
-  if (!ok(emb_sparse_adam_apply(a->table, a->exp_avg, a->exp_avg_sq, a->V, a->D, a->send_ids, a->send_rows,
+  if (s->by_owner) {
+    // owner-major coalesce: the sort on the coalesce stream, the reduction
+    // (straight into the send buffers) and the rest on the main stream
+    if (!ok(emb::coalesce_by_owner_args_status(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->row_owner, a->P,
+                                               a->send_ids, a->seg_offsets, a->send_rows, a->send_counts,
+                                               a->send_offsets, a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes)))
+      return st;
+    auto launched = [](hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_ERR_LAUNCH; };
+    // sort(s): after reduce(s-2) has finished with this buffer set's workspace
+    // (the sorts run up to a step ahead, beside the bandwidth-bound kernels)
+    if (s->reuse && sep_c && !ok(wait(s->coalesce, s->coalesced))) return st;
+    if (!ok(record(s->timing[2], s->coalesce))) return st;
+    if (!ok(launched(emb::launch_coalesce_sort(a->ids, a->T, a->V, a->D, a->row_owner, a->P, a->ws_coalesce,
+                                               a->dev_status, S(s->coalesce)))))
+      return st;
+    if (!ok(record(s->sorted, s->coalesce))) return st;
+    if (!ok(record(s->timing[0], s->lookup_update))) return st;
+    if (!ok(emb_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status, s->lookup_update))) return st;
+    if (!ok(record(s->timing[1], s->lookup_update))) return st;
+    if (sep_c && !ok(wait(s->lookup_update, s->sorted))) return st;
+    if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, a->row_owner,
+                                                 a->P, a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
+                                                 a->send_counts, a->send_offsets, a->ws_coalesce,
+                                                 S(s->lookup_update)))))
+      return st;
+    if (!ok(record(s->timing[3], s->lookup_update)) || !ok(record(s->coalesced, s->lookup_update))) return st;
+  } else {
+    // coalesce(s): after pack(s-2) has read this buffer set's unique rows
+    if (s->reuse && s->coalesce != s->pack && !ok(wait(s->coalesce, s->packed))) return st;
+    if (!ok(record(s->timing[2], s->coalesce))) return st;
+    if (!ok(emb_grad_coalesce(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->uniq_ids, a->seg_offsets,
+                              a->uniq_grad, a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes, a->dev_status,
+                              s->coalesce)))
+      return st;
+    if (!ok(record(s->timing[3], s->coalesce)) || !ok(record(s->coalesced, s->coalesce))) return st;
+    // pack(s): after coalesce(s), and after update(s-2) has read this set's send rows
+    if (s->pack != s->coalesce && !ok(wait(s->pack, s->coalesced))) return st;
+    if (s->reuse && sep_p && !ok(wait(s->pack, s->updated))) return st;
+    if (!ok(record(s->timing[4], s->pack))) return st;
+    if (!ok(emb_pack_by_owner(a->uniq_ids, a->uniq_grad, a->num_unique, a->cap_rows, a->D, a->row_owner, a->V, a->P,
+                              a->send_ids, a->send_rows, a->send_counts, a->send_offsets, a->ws_pack,
+                              a->ws_pack_bytes, a->dev_status, s->pack)))
+      return st;
+    if (!ok(record(s->timing[5], s->pack)) || !ok(record(s->packed, s->pack))) return st;
+    // lookup(s) on the main stream, then update(s) once the rows are packed
+    if (!ok(record(s->timing[0], s->lookup_update))) return st;
+    if (!ok(emb_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status, s->lookup_update))) return st;
+    if (!ok(record(s->timing[1], s->lookup_update))) return st;
+    if (sep_p && !ok(wait(s->lookup_update, s->packed))) return st;
+  }
+  // the update's timing pair comes from its own dispatch (no marker packets)
+  if (!ok(emb::sparse_adam_call(a->table, a->exp_avg, a->exp_avg_sq, a->V, a->D, a->send_ids, a->send_rows,
                                 a->send_offsets, a->P, 0, a->P, a->cap_rows, a->lr, a->beta1, a->beta2, a->eps,
-                                a->step, a->dev_status, s->lookup_update)))
+                                a->step, a->dev_status, S(s->lookup_update), E(s->timing[6]), E(s->timing[7]))))
     return st;
-  if (!ok(record(s->timing[7], s->lookup_update)) || !ok(record(s->updated, s->lookup_update))) return st;
+  if (!s->by_owner && !ok(record(s->updated, s->lookup_update))) return st;
   return EMB_OK;
 }
 

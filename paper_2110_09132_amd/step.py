@@ -5,11 +5,14 @@ A step of one table is the four C ABI calls in data order:
     grad_coalesce -> pack_by_owner (the exchange payload, Sec. 4.2.2 / 4.1.2)
     sparse_adam_apply (the update of the owned rows)
 The library's step executor (emb_train_step) enqueues all four with one host
-call.  With overlap=True the coalesce of a step runs on one side stream and
-its pack on another, while the lookup and the update stay on the main
-stream; the executor adds the event waits that keep every data dependency
-(see emb_train_step in include/emb.h).  This module only allocates the
-buffers, alternates the two buffer sets and fills in the arguments.
+call.  With overlap=True the latency-bound work runs on side streams while
+the lookup and the update stay on the main stream:
+  by_owner=False: grad_coalesce on one side stream, pack_by_owner on another;
+  by_owner=True:  grad_coalesce_by_owner (coalesce and pack in one), its sort
+                  on a side stream and its reduction on the main stream.
+The executor adds the event waits that keep every data dependency (see
+emb_train_step in include/emb.h).  This module only allocates the buffers,
+alternates the two buffer sets and fills in the arguments.
 """
 from __future__ import annotations
 
@@ -46,7 +49,9 @@ class EmbeddingTable:
                      for _ in range(2)]
         self.coal = self.coals[0]
         self.grad_code = EMB_BF16 if grad_dtype == torch.bfloat16 else EMB_F32
-        self.ws_coalesce = new_workspace(grad_coalesce_workspace_bytes(T_cap, self.V, self.D, self.grad_code), dev)
+        nb = grad_coalesce_workspace_bytes(T_cap, self.V, self.D, self.grad_code)
+        self.ws_coalesces = [new_workspace(nb, dev) for _ in range(2)]
+        self.ws_coalesce = self.ws_coalesces[0]
         self.ws_pack = new_workspace(pack_by_owner_workspace_bytes(T_cap, P), dev)
 
 
@@ -71,15 +76,17 @@ class StepPipeline:
     """Enqueues training steps of the hot path for a list of tables."""
 
     def __init__(self, tables, lr, beta1, beta2, eps, overlap: bool = True, dev_status: torch.Tensor | None = None,
-                 streams: int = 3):
-        """streams (with overlap=True): 2 puts coalesce and pack on one side stream, 3 gives
-        each its own (more concurrency, one more cross-stream wait per step)."""
+                 streams: int = 3, by_owner: bool = True):
+        """streams (with overlap=True and by_owner=False): 2 puts coalesce and pack on one side
+        stream, 3 gives each its own (more concurrency, one more cross-stream wait per step).
+        by_owner: coalesce straight into the send layout (emb_grad_coalesce_by_owner)."""
         self.tables = list(tables)
         self.overlap = overlap
         self.main = torch.cuda.current_stream()
         s1, s2 = side_streams()
-        self.side = s1 if overlap else self.main  # coalesce
-        self.side2 = s2 if (overlap and streams >= 3) else self.side  # pack
+        self.by_owner = by_owner
+        self.side = s1 if overlap else self.main  # coalesce (by_owner: its sort)
+        self.side2 = s2 if (overlap and streams >= 3 and not by_owner) else self.side  # pack
         self.count = 0
         self.events = []  # keeps the library events alive
         self.args, self.sched = [], []
@@ -94,14 +101,15 @@ class StepPipeline:
                              lookup=tb.lookup.data_ptr(), uniq_ids=uid.data_ptr(), seg_offsets=seg.data_ptr(),
                              num_unique=nu.data_ptr(), uniq_grad=ug.data_ptr(), send_ids=sid.data_ptr(),
                              send_counts=cnt.data_ptr(), send_offsets=offs.data_ptr(), send_rows=srows.data_ptr(),
-                             ws_coalesce=tb.ws_coalesce.data_ptr(), ws_coalesce_bytes=tb.ws_coalesce.numel(),
+                             ws_coalesce=tb.ws_coalesces[i].data_ptr(),
+                             ws_coalesce_bytes=tb.ws_coalesces[i].numel(),
                              ws_pack=tb.ws_pack.data_ptr(), ws_pack_bytes=tb.ws_pack.numel(), lr=lr, beta1=beta1,
                              beta2=beta2, eps=eps, dev_status=st)
-                evs = [Event() for _ in range(3)]
+                evs = [Event() for _ in range(4)]
                 self.events += evs
                 s = StepSchedule(lookup_update=_stream_handle(self.main), coalesce=_stream_handle(self.side),
-                                 pack=_stream_handle(self.side2), coalesced=evs[0].handle, packed=evs[1].handle,
-                                 updated=evs[2].handle)
+                                 pack=_stream_handle(self.side2), sorted=evs[0].handle, coalesced=evs[1].handle,
+                                 packed=evs[2].handle, updated=evs[3].handle, by_owner=1 if by_owner else 0)
                 args.append(a)
                 scheds.append(s)
             self.args.append(args)

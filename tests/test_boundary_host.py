@@ -72,6 +72,28 @@ def test_coalesce_validation_and_workspace_query():
                                need, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
 
 
+def test_coalesce_by_owner_validation():
+    L = emb.lib
+    need = L.emb_grad_coalesce_workspace_bytes(1000, 5000, 64, emb.EMB_F32)
+    args = lambda T=1000, D=64, V=5000, own=FAKE, P=4, ids=FAKE, counts=FAKE, offs=FAKE, wsb=need: (
+        ids, T, FAKE, 0, D, V, own, P, FAKE, FAKE, FAKE, counts, offs, FAKE, FAKE, wsb, NULL, NULL)
+    assert L.emb_grad_coalesce_by_owner(*args(wsb=need - 1)) == emb.EMB_ERR_WORKSPACE
+    assert L.emb_grad_coalesce_by_owner(*args(P=0)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_by_owner(*args(P=1025)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_by_owner(*args(own=NULL)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_by_owner(*args(counts=NULL)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_by_owner(*args(offs=NULL)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_by_owner(*args(ids=NULL)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_by_owner(*args(D=0)) == emb.EMB_ERR_INVALID_ARG
+    # (owner, id) keys must fit 32 bits: bits(V) + bits(P).  The key check comes before the
+    # workspace check, so a short workspace tells the two apart without launching anything.
+    short = dict(wsb=need - 1)
+    assert L.emb_grad_coalesce_by_owner(*args(V=(1 << 31) - 1, P=2, **short)) == emb.EMB_ERR_WORKSPACE
+    assert L.emb_grad_coalesce_by_owner(*args(V=(1 << 31) - 1, P=3, **short)) == emb.EMB_ERR_UNSUPPORTED
+    assert L.emb_grad_coalesce_by_owner(*args(V=1 << 22, P=1024, **short)) == emb.EMB_ERR_WORKSPACE
+    assert L.emb_grad_coalesce_by_owner(*args(V=(1 << 22) + 1, P=1024, **short)) == emb.EMB_ERR_UNSUPPORTED
+
+
 def test_pack_validation_and_workspace_query():
     L = emb.lib
     need = L.emb_pack_by_owner_workspace_bytes(1000, 16)

@@ -1,0 +1,174 @@
+"""Parity of emb_grad_coalesce_by_owner (coalesce straight into the per-owner
+send layout) with the oracle's pack_by_owner applied to its coalesce: ids,
+counts and offsets bit-exact, rows within the summation bound, rows of one or
+two tokens bit-exact, token counts per row equal to the oracle's segment
+lengths.  Sizes span several sort tiles and reduction chunks with ragged
+tails; owner maps by id mod P, by range and at random; bad ids and owners;
+empty and degenerate batches; the key-width limit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2110_09132_amd as emb
+import tolerance
+from gpu_helpers import host, to_dev
+from workloads import gen
+
+pytestmark = pytest.mark.gpu
+
+
+def ids_for(law, seed, T, V, s=1.1):
+    key = gen.stream_key(seed, 0, gen.PURPOSE_IDS)
+    return gen.uniform_ids(key, T, V) if law == "uniform" else gen.zipf_ids(key, T, V, s)
+
+
+def grads_for(seed, T, D, sigma=1.0, bf16=False):
+    g = gen.normal_f32(gen.stream_key(seed, 0, gen.PURPOSE_GRADS), T * D, sigma).reshape(T, D)
+    return gen.bf16_round(g).reshape(T, D) if bf16 else g
+
+
+def owners(rule, V, P, seed=0):
+    if rule == "mod":
+        return gen.owner_mod(V, P)
+    if rule == "range":
+        return gen.owner_range(V, P)
+    return np.random.default_rng(seed).integers(0, P, V).astype(np.int32)
+
+
+def gpu_by_owner(ids_np, grad_np, V, own_np, P, grad_dev=None):
+    st = emb.new_status()
+    g = to_dev(grad_np) if grad_dev is None else grad_dev
+    out = emb.grad_coalesce_by_owner(to_dev(ids_np.astype(np.int32)), g, V, to_dev(own_np.astype(np.int32)), P,
+                                     dev_status=st)
+    torch.cuda.synchronize()
+    send_ids, seg, rows, counts, offs, nu = out
+    U = int(nu.item())
+    return dict(U=U, send_ids=host(send_ids[:U]), seg_offsets=host(seg[:U + 1]), send_rows=host(rows[:U]),
+                send_counts=host(counts), send_offsets=host(offs), status=int(st.item()), dev=out)
+
+
+def check_by_owner(ids_np, grad_np, V, own_np, P, bf16=False, grad_dev=None):
+    orc = oracle.coalesce(ids_np, grad_np, V, grad_is_bf16=bf16)
+    pk = oracle.pack_by_owner(orc["uniq_ids"], orc["uniq_grad"], own_np, P)
+    gpu = gpu_by_owner(ids_np, grad_np, V, own_np, P, grad_dev=grad_dev)
+    n = int(pk["send_offsets"][P])
+    assert gpu["U"] == n, (gpu["U"], n)
+    for k in ("send_ids", "send_counts", "send_offsets"):
+        assert np.array_equal(gpu[k], pk[k]), k
+    # each sent row against the oracle's exact sum of its id
+    idx = np.searchsorted(orc["uniq_ids"], pk["send_ids"])
+    assert np.array_equal(orc["uniq_ids"][idx], pk["send_ids"])
+    r = tolerance.assert_grad_close(gpu["send_rows"], orc["sum_f64"][idx], orc["absum"][idx], tolerance.RTOL_F32)
+    seglen = np.diff(orc["seg_offsets"])[idx]
+    assert gpu["seg_offsets"][0] == 0 and np.array_equal(np.diff(gpu["seg_offsets"]), seglen)
+    short = seglen <= 2
+    assert np.array_equal(gpu["send_rows"][short].view(np.uint32), orc["uniq_grad"][idx][short].view(np.uint32))
+    bad_owner = np.any((own_np[orc["uniq_ids"]] < 0) | (own_np[orc["uniq_ids"]] >= P)) if orc["U"] else False
+    expect = (emb.EMB_DEV_ID_OUT_OF_RANGE if orc["n_invalid"] else 0) | \
+             (emb.EMB_DEV_OWNER_OUT_OF_RANGE if bad_owner else 0)
+    assert gpu["status"] == expect, (gpu["status"], expect)
+    return gpu, r
+
+
+@pytest.mark.parametrize("law,V,T,D,P,rule", [
+    ("zipf", 1000, 512, 64, 2, "mod"),              # the tiny workload's shape
+    ("zipf", 32768, 25000, 64, 4, "range"),         # shared-vocab shape, narrower rows
+    ("zipf", 32000, 16384, 32, 8, "mod"),           # translation shape, narrower rows
+    ("uniform", 1 << 20, 20000, 16, 16, "mod"),     # 20 + 4 key bits: three 8-bit passes
+    ("zipf", 5000, 2049, 3, 7, "rand"),             # ragged tile, scalar width path
+    ("zipf", 300, 4001, 256, 5, "rand"),            # heavy duplication
+    ("uniform", 50, 33, 1, 3, "mod"),               # one chunk + 1, D = 1
+    ("zipf", 1, 777, 4, 1, "mod"),                  # V = 1, P = 1: every key 0
+    ("zipf", 1, 777, 4, 9, "rand"),                 # V = 1, one owner of nine
+    ("uniform", 50000, 9000, 20, 1024, "mod"),      # the most owners: 16 + 10 key bits
+    ("uniform", 50000, 9000, 20, 1024, "range"),
+    ("uniform", (1 << 22) - 1, 9000, 4, 1024, "rand"),  # 22 + 10 = 32 key bits: four passes
+    ("uniform", (1 << 24) + 3, 9000, 4, 128, "mod"),    # 25 + 7 = 32 key bits, the widest that fits
+])
+def test_by_owner_parity(law, V, T, D, P, rule):
+    ids = ids_for(law, V + T + P, T, V)
+    check_by_owner(ids, grads_for(V + D, T, D), V, owners(rule, V, P, seed=T), P)
+
+
+@pytest.mark.parametrize("V,T,D,P", [(262144, 16384, 1024, 8), (1000, 3000, 10, 3)])
+def test_by_owner_parity_bf16(V, T, D, P):
+    ids = ids_for("zipf", V + T, T, V, 1.0)
+    G = grads_for(V + D, T, D, 0.01, bf16=True)
+    check_by_owner(ids, G, V, gen.owner_range(V, P), P, bf16=True)
+
+
+def test_by_owner_hot_row_spans_many_chunks():
+    T, V, D, P = 20000, 5000, 256, 4
+    ids = ids_for("zipf", 77, T, V, 2.5)
+    check_by_owner(ids, grads_for(78, T, D, 0.01), V, gen.owner_mod(V, P), P)
+
+
+def test_by_owner_lowdup_full_size():
+    # the low-duplication stress shape: V = 2^20, D = 256, T = 65536 uniform ids, P = 16 by id mod P
+    V, T, D, P = 1 << 20, 65536, 256, 16
+    ids = ids_for("uniform", 51, T, V)
+    check_by_owner(ids, grads_for(51, T, D, 0.01), V, gen.owner_mod(V, P), P)
+
+
+def test_by_owner_bad_ids_and_owners_are_left_out():
+    V, T, D, P = 1000, 3000, 16, 4
+    ids = ids_for("zipf", 9, T, V)
+    ids[::97] = -3
+    ids[5::101] = V + 5
+    own = gen.owner_mod(V, P)
+    own[[0, 1, 7, 500]] = [P, -1, 1 << 20, P + 3]
+    gpu, _ = check_by_owner(ids, grads_for(9, T, D), V, own, P)
+    assert gpu["status"] == emb.EMB_DEV_ID_OUT_OF_RANGE | emb.EMB_DEV_OWNER_OUT_OF_RANGE
+
+
+def test_by_owner_every_owner_bad():
+    V, T, D, P = 100, 500, 4, 3
+    own = np.full(V, 5, np.int32)
+    gpu = gpu_by_owner(ids_for("uniform", 1, T, V), grads_for(1, T, D), V, own, P)
+    assert gpu["U"] == 0 and gpu["send_offsets"].tolist() == [0] * (P + 1)
+    assert gpu["send_counts"].tolist() == [0] * P and gpu["seg_offsets"].tolist() == [0]
+    assert gpu["status"] == emb.EMB_DEV_OWNER_OUT_OF_RANGE
+
+
+def test_by_owner_empty_batch():
+    P = 5
+    gpu = gpu_by_owner(np.zeros(0, np.int32), np.zeros((0, 8), np.float32), 50, gen.owner_mod(50, P), P)
+    assert gpu["U"] == 0 and gpu["send_offsets"].tolist() == [0] * (P + 1)
+    assert gpu["send_counts"].tolist() == [0] * P and gpu["status"] == 0
+
+
+def test_by_owner_empty_owners_between_full_ones():
+    # owners 0, 2 and 5 hold every row: 1, 3, 4 stay empty in the middle
+    V, T, D, P = 600, 4000, 8, 6
+    own = np.array([0, 2, 5], np.int32)[np.arange(V) % 3]
+    check_by_owner(ids_for("zipf", 3, T, V), grads_for(3, T, D), V, own, P)
+
+
+def test_by_owner_misaligned_gradient_rows_use_scalar_path():
+    V, T, D, P = 2000, 3000, 64, 4
+    ids = ids_for("zipf", 11, T, V)
+    G = grads_for(11, T, D)
+    buf = torch.zeros(T * D + 1, dtype=torch.float32, device="cuda")
+    buf[1:] = to_dev(G.reshape(-1))
+    check_by_owner(ids, G, V, gen.owner_mod(V, P), P, grad_dev=buf[1:].view(T, D))
+
+
+def test_by_owner_is_bitwise_deterministic():
+    V, T, D, P = 1 << 20, 65536, 256, 16
+    ids = ids_for("zipf", 52, T, V, 1.3)
+    G = to_dev(grads_for(52, T, D, 0.01))
+    own = gen.owner_mod(V, P)
+    a = gpu_by_owner(ids, None, V, own, P, grad_dev=G)
+    b = gpu_by_owner(ids, None, V, own, P, grad_dev=G)
+    assert a["U"] == b["U"] and np.array_equal(a["send_ids"], b["send_ids"])
+    assert np.array_equal(a["send_rows"].view(np.uint32), b["send_rows"].view(np.uint32))
+
+
+def test_by_owner_key_width_limit_is_unsupported():
+    # bits(V) + bits(P) = 31 + 2 > 32: the call refuses before launching anything
+    V, P, T, D = (1 << 31) - 1, 4, 16, 4
+    ids = to_dev(np.arange(T, dtype=np.int32))
+    own = torch.zeros(1, dtype=torch.int32, device="cuda")  # never read: the host check fails first
+    with pytest.raises(emb.EmbError, match="unsupported"):
+        emb.grad_coalesce_by_owner(ids, to_dev(grads_for(1, T, D)), V, own, P)

@@ -63,15 +63,15 @@ def test_gather_empty():
     ("zipf", 1000, 512, 64),         # the tiny workload's shape
     ("zipf", 5000, 2048, 8),         # exactly one sort tile
     ("zipf", 5000, 2049, 3),         # ragged second tile, scalar width path
-    ("uniform", 1 << 20, 10000, 16),  # 21 key bits: three passes of 7 bits
+    ("uniform", 1 << 20, 10000, 16),  # 20 key bits: three passes of 7 bits
     ("zipf", 32768, 25000, 65),      # odd width (scalar path), many chunks
     ("zipf", 300, 4001, 256),        # very heavy duplication
     ("uniform", 50, 33, 1),          # one chunk + 1, D = 1
-    ("zipf", 1, 777, 4),             # V = 1: a single segment over 25 chunks
+    ("zipf", 1, 777, 4),             # V = 1: every key 0 (one pass), one segment over 25 chunks
     ("uniform", 5_000_000, 9000, 8),  # 23 key bits: three 8-bit passes
     ("uniform", (1 << 31) - 1, 5000, 4),  # 31 key bits: four passes
     ("zipf", 65535, 12000, 16),      # 16 key bits: two 8-bit passes
-    ("zipf", 65536, 12000, 16),      # 17 key bits: three passes of 6 bits
+    ("zipf", 65537, 12000, 16),      # 17 key bits: three passes of 6 bits
     ("uniform", (1 << 22) - 1, 20000, 4),  # 22 key bits
 ])
 def test_coalesce_parity_fp32(law, V, T, D):

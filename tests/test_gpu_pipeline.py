@@ -1,16 +1,19 @@
-"""The two-stream step schedule gives bitwise the same table, moments and
-lookups as running the four calls one after another."""
+"""The overlapped step schedules give bitwise the same table, moments and
+lookups as running their calls one after another on one stream; the
+owner-major schedule (coalesce straight into the send layout) agrees with
+coalesce-then-pack to the fp32 tolerance (its sums add in another order)."""
 import numpy as np
 import pytest
 import torch
 
+import tolerance
 from paper_2110_09132_amd.step import EmbeddingTable, StepPipeline
 from workloads import configs, gen
 
 pytestmark = pytest.mark.gpu
 
 
-def run(overlap, steps=7):
+def run(overlap, by_owner, steps=7):
     torch.cuda.synchronize()
     specs = [configs.TableSpec(20000, 128, 6000, "zipf", 1.05, "f32", 0.01, 8, "mod", 61),
              configs.TableSpec(5000, 64, 3000, "uniform", 0.0, "bf16", 0.01, 3, "range", 62)]
@@ -28,7 +31,7 @@ def run(overlap, steps=7):
             per.append((torch.from_numpy(ids).cuda(), g))
         batches.append(per)
     torch.cuda.synchronize()
-    pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap)
+    pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner)
     lookups = []
     for t in range(1, steps + 1):
         pipe.step([batches[k][t % 3] for k in range(len(specs))], t)
@@ -40,12 +43,24 @@ def run(overlap, steps=7):
            [[x.cpu().numpy() for x in l] for l in lookups]
 
 
-def test_overlapped_schedule_equals_sequential():
-    a, la = run(True)
-    b, lb = run(False)
+@pytest.mark.parametrize("by_owner", [False, True])
+def test_overlapped_schedule_equals_sequential(by_owner):
+    a, la = run(True, by_owner)
+    b, lb = run(False, by_owner)
     for x, y in zip(a, b):
         for u, v in zip(x, y):
             assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
     for x, y in zip(la, lb):
         for u, v in zip(x, y):
             assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
+
+
+def test_owner_major_schedule_matches_coalesce_then_pack():
+    a, la = run(True, True)
+    b, lb = run(False, False)
+    for x, y in zip(a, b):
+        for u, v, name in zip(x, y, ("table", "exp_avg", "exp_avg_sq")):
+            tolerance.assert_rows_close(u, v, tolerance.RTOL_F32, name)
+    for x, y in zip(la, lb):
+        for u, v in zip(x, y):
+            tolerance.assert_rows_close(u, v, tolerance.RTOL_F32, "lookup")
