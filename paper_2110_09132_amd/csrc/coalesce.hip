@@ -32,6 +32,8 @@
 //     4 results in wave order); by owner, it also forms the per-owner counts.
 // The order of every floating-point addition depends only on the ids, never
 // on scheduling, so results are bitwise reproducible.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "launch.h"
 
@@ -337,8 +339,10 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     const uint32_t k = skeys[i];
     const uint32_t dd = (k >> shift) & (bins - 1);
     const uint32_t dest = gbase[dd] + (static_cast<uint32_t>(i) - dstart[dd]);
-    keys_out[dest] = k;
-    vals_out[dest] = svals[i];
+    if (dest < static_cast<uint32_t>(T)) {  // always, unless the histograms were overwritten meanwhile
+      keys_out[dest] = k;
+      vals_out[dest] = svals[i];
+    }
   }
 }
 
@@ -384,7 +388,7 @@ __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t* __r
                                                              uint32_t* __restrict__ tile_heads, int ntiles) {
   const int tile = blockIdx.x * kWaves + threadIdx.x / kWave;  // one wave per reduction workgroup
   if (tile >= ntiles) return;
-  const int tv = static_cast<int>(*n_valid);
+  const int tv = static_cast<int>(min(*n_valid, static_cast<uint32_t>(ntiles) * kRedTile));
   uint32_t c = 0;
   for (int k = static_cast<int>(lane_id()); k < kRedTile; k += kWave) {
     const int e = tile * kRedTile + k;
@@ -402,7 +406,7 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     const void* __restrict__ grad, int D, const uint32_t* __restrict__ tile_heads, int ib, uint32_t id_mask,
     int32_t* __restrict__ uniq_ids, int32_t* __restrict__ seg_offsets, int32_t* __restrict__ num_unique,
     float* __restrict__ uniq_grad, int32_t* __restrict__ owner_offsets, int P, float* __restrict__ partial,
-    int32_t* __restrict__ span_list, int32_t* __restrict__ span_count) {
+    int32_t* __restrict__ span_list, int32_t* __restrict__ span_count, int nchunks) {
   __shared__ uint32_t wave_heads[kWaves];
   __shared__ uint32_t red[kWaves];
   const int tile = blockIdx.x;
@@ -412,11 +416,12 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const int a = chunk * kChunk;
 
   // lane L holds sorted element e = a - 1 + L, for L = 0 .. kChunk + 1
-  const int tv = static_cast<int>(*n_valid);
+  // (workspace values are clamped so that no index can leave its array)
+  const int tv = static_cast<int>(min(*n_valid, static_cast<uint32_t>(T)));
   const int e = a - 1 + lane;
   const int ec = min(max(e, 0), T - 1);
   const uint32_t key = skeys[ec];
-  const int32_t pos = spos[ec];
+  const int32_t pos = min(max(spos[ec], 0), T - 1);
   const bool valid = e >= 0 && e < tv && lane <= kChunk + 1;
   const uint32_t key_prev = __shfl_up(key, 1, kWave);
   // element e does not continue the id of element e - 1
@@ -457,21 +462,23 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   for (int q = 0; q < w; ++q) ubase += wave_heads[q];
   const uint64_t upto = (lane == kWave - 1) ? ~0ull : ((2ull << lane) - 1ull);
   const int u = static_cast<int>(ubase + __popcll(heads & upto)) - 1;  // unique index of element e
-  if (head) {
+  const bool u_ok = u >= 0 && u < T;
+  if (head && u_ok) {
     uniq_ids[u] = static_cast<int32_t>(key & id_mask);
     seg_offsets[u] = e;
     if (owner_offsets != nullptr) {  // owners o' < p <= o start at this row
-      const int o = static_cast<int>(key >> ib);
+      const int o = min(static_cast<int>(key >> ib), P);
       const int o_prev = e == 0 ? -1 : static_cast<int>(key_prev >> ib);
       for (int p = o_prev + 1; p <= o; ++p) owner_offsets[p] = u;
     }
   }
   const bool next_valid = __shfl_down(valid ? 1 : 0, 1, kWave) != 0;
-  if (in_chunk && valid && (e + 1 == T || !next_valid)) {
+  if (in_chunk && valid && u_ok && (e + 1 == T || !next_valid)) {
     seg_offsets[u + 1] = e + 1;  // the last valid token of the whole batch
     num_unique[0] = u + 1;
     if (owner_offsets != nullptr)
-      for (int p = static_cast<int>(key >> ib) + 1; p <= P; ++p) owner_offsets[p] = u + 1;
+      for (int p = static_cast<int>(min(key >> ib, static_cast<uint32_t>(P))) + 1; p <= P; ++p)
+        owner_offsets[p] = u + 1;
   }
   if (chunk == 0 && lane == 1 && !valid) {  // no valid token at all
     seg_offsets[0] = 0;
@@ -494,11 +501,14 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     auto flush = [&](int uu, int s, int t) {  // run of chunk tokens [s, t)
       const bool whole = ((brk >> (s + 1)) & 1ull) && ((brk >> (t + 1)) & 1ull);
       if (whole) {
-        if (colok) out_rows[static_cast<size_t>(uu) * Dv + c] = acc;
+        if (colok && uu >= 0 && uu < T) out_rows[static_cast<size_t>(uu) * Dv + c] = acc;
       } else {
         const int slot = (s == 0) ? 0 : 1;
         if (colok) part_rows[(static_cast<size_t>(chunk) * 2 + slot) * Dv + c] = acc;
-        if (((brk >> (s + 1)) & 1ull) && cb == 0 && lane == 0) span_list[atomicAdd(span_count, 1)] = uu;
+        if (((brk >> (s + 1)) & 1ull) && cb == 0 && lane == 0) {
+          const int k = atomicAdd(span_count, 1);  // at most one per chunk
+          if (k < nchunks) span_list[k] = uu;
+        }
       }
     };
     for (int j0 = 0; j0 < nv; j0 += kLoadsInFlight) {
@@ -538,20 +548,22 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
                                                                const int32_t* __restrict__ span_count,
                                                                float* __restrict__ uniq_grad,
                                                                const int32_t* __restrict__ owner_offsets,
-                                                               int32_t* __restrict__ owner_counts, int P) {
+                                                               int32_t* __restrict__ owner_counts, int P, int T,
+                                                               int nchunks) {
   using Acc = typename GradRow<false, VEC>::Acc;
   __shared__ Acc red[kWaves][kWave];
   if (owner_counts != nullptr && blockIdx.x == 0)
     for (int p = threadIdx.x; p < P; p += kThreads) owner_counts[p] = owner_offsets[p + 1] - owner_offsets[p];
-  const int n = span_count[0];
+  const int n = min(span_count[0], nchunks);
   const int Dv = D / VEC;
   const int w = threadIdx.x / kWave;
   const Acc* part_rows = reinterpret_cast<const Acc*>(partial);
   Acc* out_rows = reinterpret_cast<Acc*>(uniq_grad);
   for (int j = blockIdx.x; j < n; j += gridDim.x) {
     const int u = span_list[j];
-    const int S = seg_offsets[u];
-    const int E = seg_offsets[u + 1];
+    if (u < 0 || u >= T) continue;
+    const int S = min(max(seg_offsets[u], 0), T);
+    const int E = min(max(seg_offsets[u + 1], S), T);
     const int c0 = S / kChunk;
     const int np = (E - 1) / kChunk - c0 + 1;
     const int first_slot = (S == c0 * kChunk) ? 0 : 1;
@@ -708,12 +720,12 @@ hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, con
 hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V, const int32_t* row_owner,
                                   int P, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
                                   int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
-                                  void* workspace, hipStream_t stream) {
+                                  void* workspace, hipStream_t stream, hipEvent_t done) {
   // owner_offsets / owner_counts are given exactly for the owner-major variant
   // (row_owner != nullptr whenever T > 0)
   if (T == 0) {
-    hipLaunchKernelGGL(empty_batch_kernel, dim3(1), dim3(kThreads), 0, stream, seg_offsets, num_unique, owner_counts,
-                       owner_offsets, P);
+    hipExtLaunchKernelGGL(empty_batch_kernel, dim3(1), dim3(kThreads), 0, stream, nullptr, done, 0, seg_offsets,
+                          num_unique, owner_counts, owner_offsets, P);
     return hipGetLastError();
   }
   CoalesceWs ws = carve(workspace, T, D);
@@ -731,10 +743,11 @@ hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D
 #define EMB_REDUCE(BF, VC)                                                                                          \
   hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred), dim3(kThreads), 0, stream, kin, vin, ws.n_valid, T, \
                      grad, D, ws.tile_heads, ks.ib, ks.id_mask, uniq_ids, seg_offsets, num_unique, uniq_grad,        \
-                     owner_offsets, ks.P, ws.partial, ws.span_list, ws.span_count)
+                     owner_offsets, ks.P, ws.partial, ws.span_list, ws.span_count, nchunks)
 #define EMB_COMBINE(VC)                                                                                             \
-  hipLaunchKernelGGL(seg_combine_kernel<VC>, cgrid, dim3(kThreads), 0, stream, ws.partial, D, seg_offsets,          \
-                     ws.span_list, ws.span_count, uniq_grad, owner_offsets, owner_counts, ks.P)
+  hipExtLaunchKernelGGL(seg_combine_kernel<VC>, cgrid, dim3(kThreads), 0, stream, nullptr, done, 0, ws.partial, D,  \
+                        seg_offsets, ws.span_list, ws.span_count, uniq_grad, owner_offsets, owner_counts, ks.P, T,  \
+                        nchunks)
   if (vec4) {
     if (grad_bf16)
       EMB_REDUCE(true, 4);
@@ -760,7 +773,7 @@ hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool gra
   const hipError_t e = launch_coalesce_sort(ids, T, V, D, row_owner, P, workspace, status, stream);
   if (e != hipSuccess) return e;
   return launch_coalesce_reduce(T, grad, grad_bf16, D, V, row_owner, P, uniq_ids, seg_offsets, uniq_grad, num_unique,
-                                owner_counts, owner_offsets, workspace, stream);
+                                owner_counts, owner_offsets, workspace, stream, nullptr);
 }
 
 }  // namespace emb

@@ -23,7 +23,7 @@ hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, con
 hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V, const int32_t* row_owner,
                                   int P, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
                                   int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
-                                  void* workspace, hipStream_t stream);
+                                  void* workspace, hipStream_t stream, hipEvent_t done);
 hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
                            const int32_t* row_owner, int P, int32_t* uniq_ids, int32_t* seg_offsets,
                            float* uniq_grad, int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
@@ -52,8 +52,9 @@ struct AdamCoeffs {
   float eps;
 };
 
-// start / stop (may be null): events that take the kernel's own start and end
-// times from its dispatch (no separate marker packets on the stream).
+// start / stop (may be null): timing events around the kernel; stop is
+// attached to the kernel's dispatch (no separate marker packet), start is
+// recorded just before it.
 hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int D, const int32_t* row_ids,
                        const float* rows, const int32_t* offsets, int shard_begin, int shard_end, int cap_rows,
                        const AdamCoeffs& c, int32_t* status, hipStream_t stream, hipEvent_t start = nullptr,

@@ -73,9 +73,9 @@ int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
     if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, a->row_owner,
                                                  a->P, a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
                                                  a->send_counts, a->send_offsets, a->ws_coalesce,
-                                                 S(s->lookup_update)))))
+                                                 S(s->lookup_update), E(s->coalesced)))))
       return st;
-    if (!ok(record(s->timing[3], s->lookup_update)) || !ok(record(s->coalesced, s->lookup_update))) return st;
+    if (!ok(record(s->timing[3], s->lookup_update))) return st;
   } else {
     // coalesce(s): after pack(s-2) has read this buffer set's unique rows
     if (s->reuse && s->coalesce != s->pack && !ok(wait(s->coalesce, s->packed))) return st;
@@ -100,12 +100,21 @@ int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
     if (!ok(record(s->timing[1], s->lookup_update))) return st;
     if (sep_p && !ok(wait(s->lookup_update, s->packed))) return st;
   }
-  // the update's timing pair comes from its own dispatch (no marker packets)
+  // Events after a kernel are attached to its dispatch where possible: that
+  // costs less idle time on the stream than a separate marker.
+  void* update_end = s->timing[7];
+  void* after_update = nullptr;
+  if (!s->by_owner) {
+    if (update_end == nullptr)
+      update_end = s->updated;
+    else
+      after_update = s->updated;
+  }
   if (!ok(emb::sparse_adam_call(a->table, a->exp_avg, a->exp_avg_sq, a->V, a->D, a->send_ids, a->send_rows,
                                 a->send_offsets, a->P, 0, a->P, a->cap_rows, a->lr, a->beta1, a->beta2, a->eps,
-                                a->step, a->dev_status, S(s->lookup_update), E(s->timing[6]), E(s->timing[7]))))
+                                a->step, a->dev_status, S(s->lookup_update), E(s->timing[6]), E(update_end))))
     return st;
-  if (!s->by_owner && !ok(record(s->updated, s->lookup_update))) return st;
+  if (!ok(record(after_update, s->lookup_update))) return st;
   return EMB_OK;
 }
 
