@@ -211,8 +211,8 @@ def host_info():
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="lowdup_uniform")
     ap.add_argument("--batches", type=int, default=8)
     ap.add_argument("--time-every", type=int, default=4, help="time the update kernel on every n-th timed step")

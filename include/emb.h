@@ -221,12 +221,15 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  * by_owner != 0: emb_grad_coalesce_by_owner in its two halves.  The sort of
  * the (owner, id) keys, which does not read the gradients, runs on the
  * `coalesce` stream; the reduction, which writes the send buffers directly,
- * runs on `lookup_update` after the lookup, followed there by the update;
- * uniq_ids, uniq_grad, ws_pack and the `pack` stream are not used.  Waits:
+ * on the `pack` stream; the lookup and the update on `lookup_update`;
+ * uniq_ids, uniq_grad and ws_pack are not used.  Waits:
  *   sort(s)     after reduce(s-2)              (same coalesce workspace)
- *   reduce(s)   after sort(s)                  (reads the sorted keys)
- * (events sorted, coalesced); everything else is in stream order.  The sorts
- * thus run up to a step ahead, beside the lookup, reduction and update.
+ *   reduce(s)   after sort(s), update(s-2)     (reads the sorted keys; same send buffers)
+ *   update(s)   after reduce(s)                (reads the send rows)
+ *   lookup(s+1) after update(s)                (same stream; reads the table)
+ * (events sorted, coalesced, updated).  The sorts thus run up to a step
+ * ahead, and a step's reduction runs beside the previous update and its own
+ * lookup.
  *
  * With all streams equal the calls simply run one after another, and the
  * results are bitwise the same either way.
@@ -237,7 +240,7 @@ typedef struct {
   void *coalesce;               /* stream of emb_grad_coalesce (by_owner: of its sort) */
   void *pack;                   /* stream of emb_pack_by_owner */
   void *sorted, *coalesced, *packed, *updated; /* events of this step's buffer set
-                                   (sorted: by_owner only; packed, updated: by_owner == 0 only) */
+                                   (sorted: by_owner only; packed: by_owner == 0 only) */
   int32_t reuse;                /* the buffer set was used two steps ago */
   int32_t by_owner;             /* use emb_grad_coalesce_by_owner instead of coalesce + pack */
   void *timing[8];              /* optional timing events (NULL to skip): begin/end of

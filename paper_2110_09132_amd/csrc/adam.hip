@@ -99,12 +99,15 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
           }
         }
       };
+      // Loads are unconditional (a group past the last one reads clamped
+      // addresses and stores nothing): with a branch around them the compiler
+      // could not count the loads in flight and would wait for all of them.
       load(0, A);
       for (int grp = 0; grp < ngroups; grp += 2) {
-        if (grp + 1 < ngroups) load(grp + 1, B);
+        load(grp + 1, B);
         apply(A);
-        if (grp + 2 < ngroups) load(grp + 2, A);
-        if (grp + 1 < ngroups) apply(B);
+        load(grp + 2, A);
+        apply(B);
       }
     }
   }

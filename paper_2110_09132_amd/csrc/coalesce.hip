@@ -422,6 +422,11 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const int ec = min(max(e, 0), T - 1);
   const uint32_t key = skeys[ec];
   const int32_t pos = min(max(spos[ec], 0), T - 1);
+  // head counts of the earlier workgroups: the first kThreads * 4 are loaded
+  // together with the keys (independent loads, one round trip for both)
+  uint32_t hv[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) hv[q] = tile_heads[min(q * kThreads + static_cast<int>(threadIdx.x), max(tile - 1, 0))];
   const bool valid = e >= 0 && e < tv && lane <= kChunk + 1;
   const uint32_t key_prev = __shfl_up(key, 1, kWave);
   // element e does not continue the id of element e - 1
@@ -432,9 +437,23 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const uint64_t brk = __ballot(starts_new);
   const int nv = __popcll(__ballot(in_chunk && valid));  // valid tokens of the chunk (a prefix of it)
   if (lane == 0) wave_heads[w] = static_cast<uint32_t>(__popcll(heads));
+  // The rows do not depend on the unique indices: the loads of the first
+  // column block of all kChunk rows are issued before the workgroup combines
+  // its counts.  Loads are unconditional, from clamped rows (a chunk with
+  // fewer valid tokens re-reads its last row), so they stay in flight together.
+  using Row = GradRow<BF16, VEC>;
+  using Acc = typename Row::Acc;
+  const int Dv = D / VEC;
+  const int last = max(nv, 1) - 1;
+  Acc g[kChunk];
+#pragma unroll
+  for (int k = 0; k < kChunk; ++k)
+    g[k] = Row::load(grad, static_cast<size_t>(__builtin_amdgcn_readlane(pos, min(k, last) + 1)), Dv, min(lane, Dv - 1));
   // heads before this workgroup: the sum of the earlier workgroups' counts
   uint32_t before = 0;
-  for (int t0 = 0; t0 < tile; t0 += kThreads * 4) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) before += (q * kThreads + static_cast<int>(threadIdx.x) < tile) ? hv[q] : 0u;
+  for (int t0 = kThreads * 4; t0 < tile; t0 += kThreads * 4) {  // more than 1024 earlier workgroups
     uint32_t v[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) v[q] = tile_heads[min(t0 + q * kThreads + static_cast<int>(threadIdx.x), tile - 1)];
@@ -443,18 +462,6 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   }
   before = wave_sum(before);
   if (lane == 0) red[w] = before;
-  // The first rows do not depend on the unique indices: their loads are issued
-  // before the workgroup combines its counts.
-  using Row = GradRow<BF16, VEC>;
-  using Acc = typename Row::Acc;
-  const int Dv = D / VEC;
-  Acc g0[kLoadsInFlight];
-  if (nv > 0) {
-    const int cc = min(lane, Dv - 1);
-#pragma unroll
-    for (int k = 0; k < kLoadsInFlight; ++k)
-      g0[k] = Row::load(grad, static_cast<size_t>(__builtin_amdgcn_readlane(pos, min(k, nv - 1) + 1)), Dv, cc);
-  }
   __syncthreads();
   uint32_t ubase = 0;
 #pragma unroll
@@ -495,6 +502,11 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     const int c = cb + lane;
     const bool colok = c < Dv;
     const int cc = min(c, Dv - 1);
+    if (cb > 0) {  // the next column block of the same rows
+#pragma unroll
+      for (int k = 0; k < kChunk; ++k)
+        g[k] = Row::load(grad, static_cast<size_t>(__builtin_amdgcn_readlane(pos, min(k, last) + 1)), Dv, cc);
+    }
     Acc acc = Acc{};
     int rs = 0;
     int cur = __builtin_amdgcn_readlane(u, 1);
@@ -511,30 +523,16 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
         }
       }
     };
-    for (int j0 = 0; j0 < nv; j0 += kLoadsInFlight) {
-      Acc g[kLoadsInFlight];
 #pragma unroll
-      for (int k = 0; k < kLoadsInFlight; ++k) {
-        if (cb == 0 && j0 == 0) {
-          g[k] = g0[k];  // already loaded
-        } else {
-          const int j = min(j0 + k, nv - 1);
-          const int p = __builtin_amdgcn_readlane(pos, j + 1);
-          g[k] = Row::load(grad, static_cast<size_t>(p), Dv, cc);
+    for (int j = 0; j < kChunk; ++j) {
+      if (j < nv) {
+        if (j > rs && ((brk >> (j + 1)) & 1ull)) {
+          flush(cur, rs, j);
+          acc = Acc{};
+          rs = j;
+          cur = __builtin_amdgcn_readlane(u, j + 1);
         }
-      }
-#pragma unroll
-      for (int k = 0; k < kLoadsInFlight; ++k) {
-        const int j = j0 + k;
-        if (j < nv) {
-          if (j > rs && ((brk >> (j + 1)) & 1ull)) {
-            flush(cur, rs, j);
-            acc = Acc{};
-            rs = j;
-            cur = __builtin_amdgcn_readlane(u, j + 1);
-          }
-          acc += g[k];
-        }
+        acc += g[j];
       }
     }
     flush(cur, rs, nv);

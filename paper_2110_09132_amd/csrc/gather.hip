@@ -5,8 +5,8 @@
 // step.  The ids of 64 rows come in one coalesced load (lane l holds the id of
 // row l) and reach their lanes by shuffle; rows are processed in groups of
 // kRowsInFlight steps, and the table loads of the next group are issued before
-// the current group is stored, so each lane keeps two groups of independent
-// 16-byte loads in flight.  Reads are whole table rows, writes contiguous rows.
+// the current group is stored (two register buffers used in turn), so each
+// lane keeps two groups of independent 16-byte loads in flight.  Reads are whole table rows, writes contiguous rows.
 #include "common.h"
 #include "launch.h"
 
@@ -49,34 +49,33 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const VecT* __restrict
     for (int cb = 0; cb < Dv; cb += L) {
       const int c = min(cb + cl, Dv - 1);
       const bool cok = cb + cl < Dv;
-      VecT cur[kRowsInFlight], nxt[kRowsInFlight];
-      int cid[kRowsInFlight];
+      // two register buffers used in turn (every index is a compile-time
+      // constant, and no loaded value is copied, so loads stay in flight)
+      struct Group {
+        VecT v[kRowsInFlight];
+        int id[kRowsInFlight];
+      } A, B;
+      // loads are unconditional: past the last group they read row 0 and are not stored
+      auto load = [&](int g, Group& x) {
 #pragma unroll
-      for (int u = 0; u < kRowsInFlight; ++u) {
-        cid[u] = row_id(0, u);
-        cur[u] = table[static_cast<size_t>(cid[u] < 0 ? 0 : cid[u]) * Dv + c];
-      }
-      for (int g = 0; g < ngroups; ++g) {
-        int nid[kRowsInFlight];
-        if (g + 1 < ngroups) {
-#pragma unroll
-          for (int u = 0; u < kRowsInFlight; ++u) {
-            nid[u] = row_id(g + 1, u);
-            nxt[u] = table[static_cast<size_t>(nid[u] < 0 ? 0 : nid[u]) * Dv + c];
-          }
+        for (int u = 0; u < kRowsInFlight; ++u) {
+          x.id[u] = row_id(g, u);
+          x.v[u] = table[static_cast<size_t>(x.id[u] < 0 ? 0 : x.id[u]) * Dv + c];
         }
+      };
+      auto store = [&](int g, const Group& x) {
 #pragma unroll
         for (int u = 0; u < kRowsInFlight; ++u) {
           const int j = g * static_cast<int>(step_rows) + u * rpw + sub;
-          if (j < n && cok) out[static_cast<size_t>(c0 + j) * Dv + c] = cid[u] < 0 ? VecT{} : cur[u];
+          if (j < n && cok) out[static_cast<size_t>(c0 + j) * Dv + c] = x.id[u] < 0 ? VecT{} : x.v[u];
         }
-        if (g + 1 < ngroups) {
-#pragma unroll
-          for (int u = 0; u < kRowsInFlight; ++u) {
-            cur[u] = nxt[u];
-            cid[u] = nid[u];
-          }
-        }
+      };
+      load(0, A);
+      for (int g = 0; g < ngroups; g += 2) {
+        load(g + 1, B);
+        store(g, A);
+        load(g + 2, A);
+        store(g + 1, B);
       }
     }
   }

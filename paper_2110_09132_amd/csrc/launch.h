@@ -79,12 +79,14 @@ struct Carver {
   size_t size() const { return (off + 255) & ~static_cast<size_t>(255); }
 };
 
-// Grid cap of the bandwidth-bound row kernels (gather, row copy, update): two
-// 256-thread workgroups per CU keep enough bytes in flight to saturate HBM and
-// leave wave slots on every CU for the short latency-bound kernels that run
-// on the other streams of a step (measured: ~8 us per step less than filling
-// the chip).
-constexpr long long kMaxBlocks = 512;
+// Grid of the bandwidth-bound row kernels (gather, row copy, update): one
+// workgroup per few dozen rows rather than a persistent grid.  Kernels of the
+// other streams of a step occupy CUs now and then; with small workgroups the
+// hardware hands the remaining work to whichever CU frees up, where a
+// persistent grid would wait for its late workgroups (measured: ~9 us per
+// step less than two persistent workgroups per CU).  The cap only bounds
+// huge launches.
+constexpr long long kMaxBlocks = 1 << 20;
 
 // Grid of at most `cap` blocks for `work` blocks of work (grid-stride kernels).
 inline unsigned grid_for(long long work, long long cap) {

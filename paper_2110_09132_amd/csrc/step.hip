@@ -42,8 +42,8 @@ int emb_event_elapsed_ms(void* start, void* end, float* ms) {
 
 int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
   if (a == nullptr || s == nullptr) return EMB_ERR_INVALID_ARG;
-  if (s->coalesced == nullptr) return EMB_ERR_INVALID_ARG;
-  if (s->by_owner ? s->sorted == nullptr : (s->packed == nullptr || s->updated == nullptr)) return EMB_ERR_INVALID_ARG;
+  if (s->coalesced == nullptr || s->updated == nullptr) return EMB_ERR_INVALID_ARG;
+  if ((s->by_owner ? s->sorted : s->packed) == nullptr) return EMB_ERR_INVALID_ARG;
   if (a->T < 0 || a->cap_rows < a->T) return EMB_ERR_INVALID_ARG;
   const bool sep_c = s->coalesce != s->lookup_update;
   const bool sep_p = s->pack != s->lookup_update;
@@ -51,31 +51,36 @@ int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
   // each step stops the sequence at the first failing call
   auto ok = [&st](int r) { return (st = r) == EMB_OK; };
   if (s->by_owner) {
-    // owner-major coalesce: the sort on the coalesce stream, the reduction
-    // (straight into the send buffers) and the rest on the main stream
+    // owner-major coalesce in its two halves: the sort on the coalesce stream,
+    // the reduction (straight into the send buffers) on the pack stream, the
+    // lookup and the update on the main stream
     if (!ok(emb::coalesce_by_owner_args_status(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->row_owner, a->P,
                                                a->send_ids, a->seg_offsets, a->send_rows, a->send_counts,
                                                a->send_offsets, a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes)))
       return st;
     auto launched = [](hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_ERR_LAUNCH; };
-    // sort(s): after reduce(s-2) has finished with this buffer set's workspace
-    // (the sorts run up to a step ahead, beside the bandwidth-bound kernels)
-    if (s->reuse && sep_c && !ok(wait(s->coalesce, s->coalesced))) return st;
+    const bool sep_sr = s->coalesce != s->pack;  // sort beside the reduction
+    // sort(s): after the reduction of step s-2 has finished with this set's workspace
+    if (s->reuse && sep_sr && !ok(wait(s->coalesce, s->coalesced))) return st;
     if (!ok(record(s->timing[2], s->coalesce))) return st;
     if (!ok(launched(emb::launch_coalesce_sort(a->ids, a->T, a->V, a->D, a->row_owner, a->P, a->ws_coalesce,
                                                a->dev_status, S(s->coalesce)))))
       return st;
-    if (!ok(record(s->sorted, s->coalesce))) return st;
+    if (sep_sr && !ok(record(s->sorted, s->coalesce))) return st;
+    // reduction(s): after the sort, and after update(s-2) has read this set's send buffers
+    if (sep_sr && !ok(wait(s->pack, s->sorted))) return st;
+    if (s->reuse && sep_p && !ok(wait(s->pack, s->updated))) return st;
+    if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, a->row_owner,
+                                                 a->P, a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
+                                                 a->send_counts, a->send_offsets, a->ws_coalesce, S(s->pack),
+                                                 (sep_sr || sep_p) ? E(s->coalesced) : nullptr))))
+      return st;
+    if (!ok(record(s->timing[3], s->pack))) return st;
+    // lookup(s), then update(s) once the rows are reduced
     if (!ok(record(s->timing[0], s->lookup_update))) return st;
     if (!ok(emb_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status, s->lookup_update))) return st;
     if (!ok(record(s->timing[1], s->lookup_update))) return st;
-    if (sep_c && !ok(wait(s->lookup_update, s->sorted))) return st;
-    if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, a->row_owner,
-                                                 a->P, a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
-                                                 a->send_counts, a->send_offsets, a->ws_coalesce,
-                                                 S(s->lookup_update), E(s->coalesced)))))
-      return st;
-    if (!ok(record(s->timing[3], s->lookup_update))) return st;
+    if (sep_p && !ok(wait(s->lookup_update, s->coalesced))) return st;
   } else {
     // coalesce(s): after pack(s-2) has read this buffer set's unique rows
     if (s->reuse && s->coalesce != s->pack && !ok(wait(s->coalesce, s->packed))) return st;
@@ -104,7 +109,7 @@ int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
   // costs less idle time on the stream than a separate marker.
   void* update_end = s->timing[7];
   void* after_update = nullptr;
-  if (!s->by_owner) {
+  if (sep_p) {  // the pack stream's next use of this set waits for it
     if (update_end == nullptr)
       update_end = s->updated;
     else

@@ -9,7 +9,7 @@ call.  With overlap=True the latency-bound work runs on side streams while
 the lookup and the update stay on the main stream:
   by_owner=False: grad_coalesce on one side stream, pack_by_owner on another;
   by_owner=True:  grad_coalesce_by_owner (coalesce and pack in one), its sort
-                  on a side stream and its reduction on the main stream.
+                  on one side stream and its reduction on another.
 The executor adds the event waits that keep every data dependency (see
 emb_train_step in include/emb.h).  This module only allocates the buffers,
 alternates the two buffer sets and fills in the arguments.
@@ -86,7 +86,7 @@ class StepPipeline:
         s1, s2 = side_streams()
         self.by_owner = by_owner
         self.side = s1 if overlap else self.main  # coalesce (by_owner: its sort)
-        self.side2 = s2 if (overlap and streams >= 3 and not by_owner) else self.side  # pack
+        self.side2 = s2 if (overlap and streams >= 3) else self.side  # pack (by_owner: the reduction)
         self.count = 0
         self.events = []  # keeps the library events alive
         self.args, self.sched = [], []
