@@ -67,6 +67,8 @@ def _bind(lib):
     lib.orc_coalesce.restype = I64
     lib.orc_pack_by_owner.argtypes = [P, P, I64, I64, P, I64, I32, P, P, P, P]
     lib.orc_pack_by_owner.restype = I64
+    lib.orc_vertical_split.argtypes = [P, I64, P, I64, P]
+    lib.orc_vertical_split.restype = I64
     lib.orc_sparse_adam.argtypes = [P, P, P, I64, I64, P, P, P, I32, I32, D, D, D, D, I64]
     lib.orc_sparse_adam.restype = I64
     return lib
@@ -132,6 +134,33 @@ def pack_by_owner(uniq_ids, uniq_grad, row_owner, P):
     n = int(offs[P])
     return dict(send_ids=send_ids[:n].copy(), send_rows=send_rows[:n, :D].copy(), send_counts=counts,
                 send_offsets=offs, n_dropped=int(bad))
+
+
+def vertical_split(uniq_ids, next_ids):
+    """Set split of Algorithm 1: is_prior[k] = uniq_ids[k] in next_ids.  Returns (is_prior bool [U], n_prior)."""
+    uniq_ids = _c(uniq_ids, np.int32)
+    next_ids = _c(next_ids, np.int32)
+    is_prior = np.empty(max(uniq_ids.size, 1), dtype=np.int32)
+    n = _load().orc_vertical_split(_ptr(uniq_ids), uniq_ids.size, _ptr(next_ids), next_ids.size, _ptr(is_prior))
+    return is_prior[:uniq_ids.size].astype(bool), int(n)
+
+
+def split_pack(uniq_ids, uniq_grad, next_ids, row_owner, P):
+    """Algorithm 1's INDEX_SELECT of the prior and delayed rows, each packed by owner (pack_by_owner),
+    laid out one after the other: groups g = 0 .. 2P-1, prior owner p is g = p, delayed owner p is
+    g = P + p.  Returns dict(send_ids, send_rows, send_counts [2P], send_offsets [2P+1], n_prior,
+    is_prior, n_dropped)."""
+    uniq_ids = _c(uniq_ids, np.int32)
+    uniq_grad = _c(uniq_grad, np.float32).reshape(uniq_ids.size, -1)
+    is_prior, n_prior = vertical_split(uniq_ids, next_ids)
+    pp = pack_by_owner(uniq_ids[is_prior], uniq_grad[is_prior], row_owner, P)
+    pd = pack_by_owner(uniq_ids[~is_prior], uniq_grad[~is_prior], row_owner, P)
+    np_ = int(pp["send_offsets"][P])
+    return dict(send_ids=np.concatenate([pp["send_ids"], pd["send_ids"]]),
+                send_rows=np.concatenate([pp["send_rows"], pd["send_rows"]]),
+                send_counts=np.concatenate([pp["send_counts"], pd["send_counts"]]),
+                send_offsets=np.concatenate([pp["send_offsets"], pd["send_offsets"][1:] + np_]).astype(np.int32),
+                n_prior=n_prior, is_prior=is_prior, n_dropped=pp["n_dropped"] + pd["n_dropped"])
 
 
 def sparse_adam(W, m, v, row_ids, rows, offsets, shard_begin, shard_end, lr, beta1, beta2, eps, step):

@@ -125,6 +125,30 @@ int64_t orc_pack_by_owner(const int32_t *uniq_ids, const float *uniq_grad,
     return bad;
 }
 
+static int orc_int32_cmp(const void *a, const void *b) {
+    const int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+/* Set split of Algorithm 1 (Vertical Sparse Scheduling, Sec. 4.2.2): a
+ * coalesced row is prior when its index is also in the next batch's data.
+ * Membership by binary search in a sorted copy of the next batch's ids. */
+int64_t orc_vertical_split(const int32_t *uniq_ids, int64_t U,
+                           const int32_t *next_ids, int64_t T_next,
+                           int32_t *is_prior) {
+    int32_t *nx = (int32_t *)malloc(sizeof(int32_t) * (size_t)(T_next > 0 ? T_next : 1));
+    for (int64_t t = 0; t < T_next; ++t) nx[t] = next_ids[t];
+    qsort(nx, (size_t)T_next, sizeof(int32_t), orc_int32_cmp);
+    int64_t n_prior = 0;
+    for (int64_t k = 0; k < U; ++k) {
+        const int32_t key = uniq_ids[k];
+        is_prior[k] = bsearch(&key, nx, (size_t)T_next, sizeof(int32_t), orc_int32_cmp) != NULL;
+        n_prior += is_prior[k];
+    }
+    free(nx);
+    return n_prior;
+}
+
 /* Row-wise Adam, Sec. 4.1.1 and Sec. 5.7; Kingma & Ba, Algorithm 1. */
 int64_t orc_sparse_adam(float *W, float *m, float *v, int64_t V, int64_t D,
                         const int32_t *row_ids, const float *rows,

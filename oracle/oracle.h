@@ -58,6 +58,18 @@ int64_t orc_pack_by_owner(const int32_t *uniq_ids, const float *uniq_grad,
                           float *send_rows, int32_t *send_counts,
                           int32_t *send_offsets);
 
+/* The set split of Vertical Sparse Scheduling (Algorithm 1; Sec. 4.2.2,
+ * "Minimum Dependency of Embedding"): with the next iteration's data known in
+ * advance, the coalesced rows whose index also occurs in the next batch are
+ * the prior rows (i_prior = D_u intersect D_next), the others the delayed rows
+ * (i_delayed = D_u minus i_prior).
+ *   is_prior[k] = 1 if uniq_ids[k] occurs among next_ids[0 .. T_next), else 0.
+ * Returns the number of prior rows.  INDEX_SELECT of the prior and delayed
+ * rows is then a plain selection by is_prior. */
+int64_t orc_vertical_split(const int32_t *uniq_ids, int64_t U,
+                           const int32_t *next_ids, int64_t T_next,
+                           int32_t *is_prior);
+
 /* Row-wise (lazy) Adam on the received rows (Sec. 4.1.1: each process updates
  * its embedding parameters with the new gradients; Sec. 5.7: Adam, with the
  * global step counter passed in by the caller).  Kingma & Ba, Algorithm 1:

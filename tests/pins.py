@@ -199,6 +199,92 @@ def pin_pack_invariants():
     assert 3 not in r2["send_ids"].tolist() and 7 not in r2["send_ids"].tolist()
 
 
+# --------------------------------------------------------- vertical split
+def pin_split_golden():
+    """Hand-worked set split of Algorithm 1 and the two owner-major packs."""
+    g = load_golden("vertical_split_worked.txt")
+    c = oracle.coalesce(np.array(g["ids"], np.int32), np.array(g["grad"], np.float32), g["V"])
+    assert c["uniq_ids"].tolist() == g["uniq_ids"]
+    r = oracle.split_pack(c["uniq_ids"], c["uniq_grad"], np.array(g["next_ids"], np.int32),
+                          np.array(g["owner"], np.int32), g["P"])
+    assert r["is_prior"].astype(int).tolist() == g["is_prior"] and r["n_prior"] == g["n_prior"]
+    assert r["send_ids"].tolist() == g["send_ids"]
+    assert r["send_rows"].tolist() == g["send_rows"]
+    assert r["send_counts"].tolist() == g["send_counts"]
+    assert r["send_offsets"].tolist() == g["send_offsets"]
+
+
+def check_split_result(r, uniq_ids, uniq_grad, next_ids, row_owner, P):
+    """What Algorithm 1 fixes about the split, checked with Python sets (shared by oracle pins and
+    GPU tests): prior = D_u & D_next, delayed = D_u - prior, each packed owner-major and stable."""
+    nxt = set(int(i) for i in next_ids)
+    prior = [int(i) for i in uniq_ids if int(i) in nxt]
+    delayed = [int(i) for i in uniq_ids if int(i) not in nxt]
+    offs = np.asarray(r["send_offsets"])
+    n_prior = int(offs[P])
+    assert n_prior == len(prior)
+    assert sorted(r["send_ids"][:n_prior].tolist()) == prior
+    assert sorted(r["send_ids"][n_prior:].tolist()) == delayed
+    assert set(r["send_ids"][:n_prior].tolist()).isdisjoint(r["send_ids"][n_prior:].tolist())
+    pos = {int(i): k for k, i in enumerate(uniq_ids)}
+    for part, (lo, hi) in enumerate(((0, P), (P, 2 * P))):
+        for p in range(P):
+            a, b = int(offs[lo + p]), int(offs[lo + p + 1])
+            blk = r["send_ids"][a:b]
+            assert np.all(row_owner[blk] == p) and np.all(np.diff(blk) > 0)
+        assert np.array_equal(np.asarray(r["send_counts"])[lo:hi], np.diff(offs[lo:hi + 1]))
+    src = np.array([pos[int(i)] for i in r["send_ids"]], dtype=np.int64)
+    assert np.array_equal(np.asarray(r["send_rows"]).view(np.uint32), uniq_grad[src].view(np.uint32))
+
+
+def pin_split_invariants():
+    for seed, (V, D, T, P, law) in enumerate([(1000, 3, 700, 4, "uniform"), (50, 2, 400, 3, "uniform"),
+                                             (20000, 4, 3000, 16, "zipf"), (7, 1, 30, 1, "uniform")]):
+        key = gen.stream_key(300 + seed, 0, gen.PURPOSE_IDS)
+        ids = gen.uniform_ids(key, T, V) if law == "uniform" else gen.zipf_ids(key, T, V, 1.1)
+        key2 = gen.stream_key(400 + seed, 0, gen.PURPOSE_IDS)
+        nxt = gen.uniform_ids(key2, T, V) if law == "uniform" else gen.zipf_ids(key2, T, V, 1.1)
+        c = oracle.coalesce(ids, _rng_normal(500 + seed, T * D).reshape(T, D), V)
+        own = gen.owner_mod(V, P)
+        r = oracle.split_pack(c["uniq_ids"], c["uniq_grad"], nxt, own, P)
+        check_split_result(r, c["uniq_ids"], c["uniq_grad"], nxt, own, P)
+    # special cases: the next batch repeats this one (all prior), shares nothing (all delayed),
+    # is empty, or holds only ids that are not rows
+    V, D, P = 300, 2, 5
+    ids = _rng_ids(9, 500, V)
+    c = oracle.coalesce(ids, _rng_normal(10, 500 * D).reshape(500, D), V)
+    own = gen.owner_mod(V, P)
+    for nxt, n_prior in ((ids[::-1].copy(), c["U"]), (ids + V, 0), (np.zeros(0, np.int32), 0),
+                         (np.array([-1, V, V + 7], np.int32), 0)):
+        is_prior, n = oracle.vertical_split(c["uniq_ids"], nxt)
+        assert n == n_prior and int(is_prior.sum()) == n_prior
+        r = oracle.split_pack(c["uniq_ids"], c["uniq_grad"], nxt, own, P)
+        check_split_result(r, c["uniq_ids"], c["uniq_grad"], nxt, own, P)
+
+
+def pin_split_two_applies():
+    """Applying Adam to the prior rows and then to the delayed rows with the same step t gives
+    exactly one apply on their union: the two row sets are disjoint and the update is per
+    element (the reading of the step counter rule of Sec. 5.7)."""
+    V, D, T, P, t = 400, 3, 600, 4, 3
+    ids, nxt = _rng_ids(21, T, V), _rng_ids(22, T, V)
+    c = oracle.coalesce(ids, _rng_normal(23, T * D, 0.1).reshape(T, D), V)
+    own = gen.owner_mod(V, P)
+    r = oracle.split_pack(c["uniq_ids"], c["uniq_grad"], nxt, own, P)
+    whole = oracle.pack_by_owner(c["uniq_ids"], c["uniq_grad"], own, P)
+    W0, M0, S0 = _adam_tables(V, D, 24)
+    M0 += _rng_normal(25, V * D, 0.01).reshape(V, D)
+    S0 += np.abs(_rng_normal(26, V * D, 0.01)).reshape(V, D)
+    A = [x.copy() for x in (W0, M0, S0)]
+    B = [x.copy() for x in (W0, M0, S0)]
+    offs = r["send_offsets"]
+    oracle.sparse_adam(*A, r["send_ids"], r["send_rows"], offs[:P + 1], 0, P, step=t, **ADAM)
+    oracle.sparse_adam(*A, r["send_ids"], r["send_rows"], offs[P:], 0, P, step=t, **ADAM)
+    oracle.sparse_adam(*B, whole["send_ids"], whole["send_rows"], whole["send_offsets"], 0, P, step=t, **ADAM)
+    for x, y in zip(A, B):
+        assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
+
+
 # ----------------------------------------------------------------------- adam
 def _adam_tables(V, D, seed):
     W = _rng_normal(seed, V * D, purpose=gen.PURPOSE_WEIGHTS).reshape(V, D)

@@ -28,6 +28,11 @@ MUTANTS = {
                                      ["pin_pack_golden", "pin_pack_invariants"]),
     "pack_owner_shifted": ("own[k] = row_owner[id];", "own[k] = (row_owner[id] + 1) % P;",
                            ["pin_pack_golden", "pin_pack_invariants"]),
+    "split_inverted": ("is_prior[k] = bsearch(&key, nx, (size_t)T_next, sizeof(int32_t), orc_int32_cmp) != NULL;",
+                       "is_prior[k] = bsearch(&key, nx, (size_t)T_next, sizeof(int32_t), orc_int32_cmp) == NULL;",
+                       ["pin_split_golden", "pin_split_invariants"]),
+    "split_drops_smallest_next_id": ("bsearch(&key, nx, (size_t)T_next,", "bsearch(&key, nx + 1, (size_t)(T_next > 0 ? T_next - 1 : 0),",
+                                     ["pin_split_golden", "pin_split_invariants"]),
     "adam_no_bias_correction": ("double mhat = mm / bc1;", "double mhat = mm;",
                                 ["pin_adam_golden", "pin_adam_closed_forms", "pin_adam_vs_torch_dense"]),
     "adam_eps_inside_sqrt": ("(sqrt(vhat) + eps)", "sqrt(vhat + eps)",
