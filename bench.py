@@ -35,18 +35,18 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def byte_model(T, U, D, g, P, by_owner=False):
+def byte_model(T, U, D, g, P, by_owner=False, T_next=0):
     """Algorithmic bytes of each call: inputs read once, outputs written once,
     repeated table rows counted once; sort scratch is not counted.  by_owner:
     coalesce writes the send layout itself (emb_grad_coalesce_by_owner), so the
     pack's read and write of the U rows (8 D U) and of the unique ids are gone:
     it reads the ids, the owners of the U distinct ids and the gradient rows,
     and writes the send ids and rows, the segment offsets and the owner counts
-    and offsets."""
+    and offsets.  The split (T_next > 0) also reads the next batch's ids."""
     gather = 4 * T + 4 * D * U + 4 * D * T
     adam = 4 * U + 4 * D * U + 24 * D * U
     if by_owner:
-        coalesce = 4 * T + g * D * T + 8 * U + 4 * D * U + 4 * (U + 1) + 8 * P
+        coalesce = 4 * T + 4 * T_next + g * D * T + 8 * U + 4 * D * U + 4 * (U + 1) + 8 * P
         return dict(gather=gather, coalesce=coalesce, pack=0, adam=adam)
     coalesce = 4 * T + g * D * T + 4 * U + 4 * D * U + 4 * (U + 1)
     pack = 12 * U + 8 * D * U + 8 * P
@@ -219,9 +219,11 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one stream, calls one after another")
-    ap.add_argument("--unfused", action="store_true",
-                    help="emb_grad_coalesce then emb_pack_by_owner (three streams) instead of "
-                         "emb_grad_coalesce_by_owner")
+    ap.add_argument("--schedule", choices=("by_owner", "split", "unfused"), default="by_owner",
+                    help="by_owner: emb_grad_coalesce_by_owner, one update; split: owner-major coalesce with "
+                         "the prior/delayed split of Vertical Sparse Scheduling (emb_grad_coalesce_split; the "
+                         "delayed update beside the next lookup); unfused: emb_grad_coalesce then "
+                         "emb_pack_by_owner")
     ap.add_argument("--summarize-trace", metavar="DIR", help="print a summary of a rocprofv3 kernel-stats run")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the scaled HBM traffic of the update kernel from two rocprofv3 --pmc runs")
@@ -264,21 +266,31 @@ def main():
         batches.append(tb_batches)
     step_batches = [[batches[k][b] for k in range(len(tables))] for b in range(args.batches)]
 
-    # unique counts of each batch (outside any timed region)
+    # unique and prior row counts of each batch (the next batch is the next one in rotation),
+    # outside any timed region
     U = [[0] * len(tables) for _ in range(args.batches)]
+    U_prior = [[0] * len(tables) for _ in range(args.batches)]
     for b in range(args.batches):
         for k, tb in enumerate(tables):
             ids, g = step_batches[b][k]
-            emb.grad_coalesce(ids, g, tb.V, out=tb.coal, workspace=tb.ws_coalesce)
+            nxt = step_batches[(b + 1) % args.batches][k][0]
+            out = emb.grad_coalesce_split(ids, nxt, g, tb.V, tb.row_owner, tb.P, workspace=tb.ws_coalesce)
             torch.cuda.synchronize()
-            U[b][k] = int(tb.coal[3].item())
+            U[b][k] = int(out[5].item())
+            U_prior[b][k] = int(out[4][tb.P].item())
 
-    by_owner = not args.unfused
-    pipe = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential, by_owner=by_owner)
+    split = args.schedule == "split"
+    by_owner = args.schedule != "unfused"
+    pipe = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential, by_owner=by_owner,
+                        split=split)
+
+    def next_ids(t):
+        return [x[0] for x in step_batches[(t + 1) % args.batches]] if split else None
+
     t = 0
     for _ in range(args.warmup):
         t += 1
-        pipe.step(step_batches[t % args.batches], t)
+        pipe.step(step_batches[t % args.batches], t, next_ids=next_ids(t))
     pipe.finish()
     torch.cuda.synchronize()
 
@@ -296,7 +308,7 @@ def main():
     for s in range(args.steps):
         t += 1
         b = t % args.batches
-        pipe.step(step_batches[b], t, timing={"adam": adam_ev[s]} if s in adam_ev else None)
+        pipe.step(step_batches[b], t, timing={"adam": adam_ev[s]} if s in adam_ev else None, next_ids=next_ids(t))
         rows += sum(U[b])
         used.append(b)
     pipe.finish()
@@ -307,38 +319,49 @@ def main():
     ms_step = ms_total / args.steps
     adam_us = 1e3 * sum(a.elapsed_ms(z) for a, z in adam_ev.values()) / len(adam_ev)
 
-    # per-stage breakdown: the same steps run one call after another on one stream
-    seq = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=False, by_owner=by_owner)
-    stage_ms = {k: 0.0 for k in (("gather", "coalesce", "adam") if by_owner else ("gather", "coalesce", "pack", "adam"))}
+    # per-stage breakdown: the same steps run one call after another on one stream (with the
+    # split, the "pack" pair of timing events times the prior update, "adam" the delayed one)
+    seq = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=False, by_owner=by_owner, split=split)
+    stage_ms = {k: 0.0 for k in (("gather", "coalesce", "pack", "adam") if split or not by_owner
+                                 else ("gather", "coalesce", "adam"))}
     s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     seq_total = 0.0
     for s in range(args.steps):
         t += 1
         ev = {k: (emb.Event(timing=True), emb.Event(timing=True)) for k in stage_ms}
         s0.record(main)
-        seq.step(step_batches[t % args.batches], t, timing=ev)
+        seq.step(step_batches[t % args.batches], t, timing=ev, next_ids=next_ids(t))
         s1.record(main)
         torch.cuda.synchronize()
         seq_total += s0.elapsed_time(s1) / args.steps
         for k in stage_ms:
             stage_ms[k] += ev[k][0].elapsed_ms(ev[k][1]) / args.steps
 
+    if split:  # name the timing pairs for what they time under the split
+        stage_ms = {"gather": stage_ms["gather"], "coalesce": stage_ms["coalesce"],
+                    "update_prior": stage_ms["pack"], "update_delayed": stage_ms["adam"]}
+
     copy_gbps = copy_reference(torch)
 
     # algorithmic bytes of the timed steps
-    bytes_step = {k: 0.0 for k in stage_ms}
+    bytes_step = {k: 0.0 for k in ("gather", "coalesce", "pack", "adam")}
     for b in used:
         for k, tb in enumerate(tables):
             sp = wl.tables[k]
-            bm = byte_model(sp.T, U[b][k], sp.D, 2 if sp.grad_dtype == "bf16" else 4, sp.P, by_owner)
+            bm = byte_model(sp.T, U[b][k], sp.D, 2 if sp.grad_dtype == "bf16" else 4, sp.P, by_owner,
+                            sp.T if split else 0)
             for name in bytes_step:
                 bytes_step[name] += bm[name] / args.steps
     total_bytes = sum(bytes_step.values())
     step_gbps = total_bytes / (ms_step * 1e-3) / 1e9
-    # the roofline kernel: one adam launch of the first table per step
+    # the roofline kernel: the update launch of the first table (with the split, its delayed part,
+    # the larger one), every time_every-th step
     sp0 = wl.tables[0]
-    adam_bytes = sum(byte_model(sp0.T, U[used[s]][0], sp0.D, 4, sp0.P)["adam"] for s in timed) / len(timed)
+    upd_rows = [U[used[s]][0] - (U_prior[used[s]][0] if split else 0) for s in timed]
+    adam_bytes = sum(byte_model(sp0.T, r, sp0.D, 4, sp0.P)["adam"] for r in upd_rows) / len(timed)
     adam_gbps = adam_bytes / (adam_us * 1e-6) / 1e9
+    prior_frac = sum(U_prior[b][k] for b in used for k in range(len(tables))) / max(1, sum(
+        U[b][k] for b in used for k in range(len(tables))))
 
     result = {
         "metric": "unique grad rows/sec for coalesce+pack+update; achieved HBM GB/s vs peak",
@@ -357,19 +380,26 @@ def main():
                    "tables": [dict(V=sp.V, D=sp.D, T=sp.T, P=sp.P, ids=sp.id_law, owner=sp.owner_rule)
                               for sp in wl.tables],
                    "mean_unique_rows_per_step": rows / args.steps, "batches_rotated": args.batches,
-                   "coalesce": "emb_grad_coalesce_by_owner (coalesce straight into the send layout)" if by_owner
-                   else "emb_grad_coalesce + emb_pack_by_owner",
+                   "coalesce": {"split": "emb_grad_coalesce_split (owner-major, prior/delayed split)",
+                                "by_owner": "emb_grad_coalesce_by_owner (coalesce straight into the send layout)",
+                                "unfused": "emb_grad_coalesce + emb_pack_by_owner"}[args.schedule],
                    "schedule": "one stream" if args.sequential else
-                   ("sort on a side stream; lookup, reduction and update on the main stream" if by_owner else
-                    "three streams (coalesce, pack overlapped with lookup+update)")},
+                   {"split": "sort, reduction and delayed update on three side streams; lookup and prior "
+                             "update on the main stream",
+                    "by_owner": "sort and reduction on two side streams; lookup and update on the main stream",
+                    "unfused": "coalesce and pack on two side streams; lookup and update on the main stream"}[
+                       args.schedule],
+                   "prior_rows_frac": prior_frac if split else None},
         "step_bytes_model": total_bytes,
         "step_bytes_model_kind": "fused minimum (pack folded into coalesce)" if by_owner else "four calls",
+        "stage_bytes_model": bytes_step,
         "step_hbm_GBps": step_gbps,
         "step_hbm_frac": step_gbps / HBM_PEAK_GBPS,
         "sequential_ms_per_step": seq_total,
         "stage_ms_sequential": stage_ms,
         "wall_s_timed": wall,
-        "roofline": {"bound": "hbm", "kernel": "adam_kernel (emb_sparse_adam_apply)",
+        "roofline": {"bound": "hbm",
+                     "kernel": "adam_kernel (emb_sparse_adam_apply)" + (", delayed rows" if split else ""),
                      "achieved": adam_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": adam_gbps / HBM_PEAK_GBPS,
                      "traffic": measured_traffic() if args.workload == "lowdup_uniform" else None,

@@ -170,6 +170,38 @@ int emb_grad_coalesce_by_owner(const int32_t *ids, int32_t T,
                                int32_t *dev_status, void *stream);
 
 /*
+ * emb_grad_coalesce_by_owner with the set split of Vertical Sparse Scheduling
+ * (Algorithm 1; Sec. 4.2.2, "Minimum Dependency of Embedding").  With the next
+ * batch's ids known in advance (next_ids [T_next]), a coalesced row is prior
+ * when its id occurs in the next batch (i_prior = D_u intersect D_next) and
+ * delayed otherwise.  The send layout holds 2P groups: the prior rows of
+ * owners 0 .. P-1, then the delayed rows of owners 0 .. P-1, each group in
+ * ascending id:
+ *   send_counts [2P], send_offsets [2P + 1]: group g is
+ *   [send_offsets[g], send_offsets[g + 1]); prior rows are
+ *   [send_offsets[0], send_offsets[P]), delayed [send_offsets[P], send_offsets[2P]).
+ * The other outputs and rules are those of emb_grad_coalesce_by_owner.  Ids
+ * of next_ids outside [0, V) match no row.  Adam is then applied to each part
+ * (emb_sparse_adam_apply with offsets send_offsets and send_offsets + P), both
+ * with the same step (Sec. 5.7).
+ * workspace: emb_grad_coalesce_split_workspace_bytes(T, T_next, V, D,
+ * grad_dtype) bytes, 256-byte aligned.  Requires 0 <= T_next < 2^30 and
+ * bits(V) + bits(P) + 1 <= 32 (EMB_ERR_UNSUPPORTED otherwise).
+ */
+size_t emb_grad_coalesce_split_workspace_bytes(int32_t T, int32_t T_next,
+                                               int64_t V, int32_t D,
+                                               int32_t grad_dtype);
+int emb_grad_coalesce_split(const int32_t *ids, int32_t T,
+                            const int32_t *next_ids, int32_t T_next,
+                            const void *grad, int32_t grad_dtype, int32_t D,
+                            int64_t V, const int32_t *row_owner, int32_t P,
+                            int32_t *send_ids, int32_t *seg_offsets,
+                            float *send_rows, int32_t *send_counts,
+                            int32_t *send_offsets, int32_t *num_unique,
+                            void *workspace, size_t workspace_bytes,
+                            int32_t *dev_status, void *stream);
+
+/*
  * Row-wise (lazy) Adam on received rows (Sec. 4.1.1: each process updates its
  * embedding rows with the exchanged gradients; Sec. 5.7: Adam with a global
  * step counter that the caller owns and advances once per iteration).
@@ -231,6 +263,21 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  * ahead, and a step's reduction runs beside the previous update and its own
  * lookup.
  *
+ * split != 0 (with by_owner): Vertical Sparse Scheduling (Sec. 4.2.2,
+ * Algorithm 1).  The coalesce is emb_grad_coalesce_split with the next
+ * batch's ids (args.next_ids, which must be the ids of the next call), and the
+ * update runs in two parts: the prior rows (needed by the next lookup) on
+ * `lookup_update` right after the lookup, the delayed rows on the `delayed`
+ * stream, beside the next lookup, which reads none of them.  Both parts use
+ * the same Adam step.  Waits, in addition to the above:
+ *   lookup(s)   after delayed update(s-2)      (its rows may be in this batch)
+ *   prior(s)    after reduce(s)
+ *   delayed(s)  after reduce(s), lookup(s)     (reads the send rows; lookup(s) reads its rows)
+ *   reduce(s)   after delayed update(s-2)      (same send buffers)
+ * (events gathered: the end of the lookup, delayed_done: the end of the
+ * delayed update).  The pair timing[4..5] times the prior update and
+ * timing[6..7] the delayed one.
+ *
  * With all streams equal the calls simply run one after another, and the
  * results are bitwise the same either way.
  * ---------------------------------------------------------------------------
@@ -239,10 +286,13 @@ typedef struct {
   void *lookup_update;          /* stream of emb_gather and emb_sparse_adam_apply */
   void *coalesce;               /* stream of emb_grad_coalesce (by_owner: of its sort) */
   void *pack;                   /* stream of emb_pack_by_owner */
+  void *delayed;                /* split: stream of the delayed update */
   void *sorted, *coalesced, *packed, *updated; /* events of this step's buffer set
                                    (sorted: by_owner only; packed: by_owner == 0 only) */
+  void *gathered, *delayed_done; /* split only: events of this step's buffer set */
   int32_t reuse;                /* the buffer set was used two steps ago */
   int32_t by_owner;             /* use emb_grad_coalesce_by_owner instead of coalesce + pack */
+  int32_t split;                /* by_owner with the prior / delayed split */
   void *timing[8];              /* optional timing events (NULL to skip): begin/end of
                                    gather, coalesce, pack, adam, each recorded on the
                                    stream the (first / last) kernel runs on; the adam
@@ -258,13 +308,15 @@ typedef struct {
   int32_t P;
   const int32_t *ids;       /* [T] */
   int32_t T;
+  const int32_t *next_ids;  /* split: [T_next] ids of the next call's batch */
+  int32_t T_next;
   const void *grad;         /* [T][D], grad_dtype */
   int32_t grad_dtype;
-  int32_t cap_rows;         /* capacity of the uniq_*, seg_offsets and send_* buffers (>= T) */
+  int32_t cap_rows;         /* capacity of the uniq_*, seg_offsets and send_* buffers (>= T, T_next) */
   float *lookup;            /* [T][D] gather output */
   int32_t *uniq_ids, *seg_offsets, *num_unique;
   float *uniq_grad;
-  int32_t *send_ids, *send_counts, *send_offsets;
+  int32_t *send_ids, *send_counts, *send_offsets; /* counts [P] and offsets [P + 1]; split: [2P], [2P + 1] */
   float *send_rows;
   void *ws_coalesce;
   size_t ws_coalesce_bytes;

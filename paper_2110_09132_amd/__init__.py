@@ -39,6 +39,9 @@ SIGNATURES = {
     "emb_grad_coalesce": (ctypes.c_int, [_P, _I32, _P, _I32, _I32, _I64, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_grad_coalesce_by_owner": (ctypes.c_int, [_P, _I32, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P, _P,
                                                   _P, _SZ, _P, _P]),
+    "emb_grad_coalesce_split_workspace_bytes": (_SZ, [_I32, _I32, _I64, _I32, _I32]),
+    "emb_grad_coalesce_split": (ctypes.c_int, [_P, _I32, _P, _I32, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P,
+                                               _P, _P, _SZ, _P, _P]),
     "emb_pack_by_owner_workspace_bytes": (_SZ, [_I32, _I32]),
     "emb_pack_by_owner": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_sparse_adam_apply": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _P, _P, _P, _I32, _I32, _I32, _I32,
@@ -52,14 +55,16 @@ SIGNATURES = {
 
 class StepSchedule(ctypes.Structure):
     """emb_step_schedule of include/emb.h."""
-    _fields_ = [("lookup_update", _P), ("coalesce", _P), ("pack", _P), ("sorted", _P), ("coalesced", _P),
-                ("packed", _P), ("updated", _P), ("reuse", _I32), ("by_owner", _I32), ("timing", _P * 8)]
+    _fields_ = [("lookup_update", _P), ("coalesce", _P), ("pack", _P), ("delayed", _P), ("sorted", _P),
+                ("coalesced", _P), ("packed", _P), ("updated", _P), ("gathered", _P), ("delayed_done", _P),
+                ("reuse", _I32), ("by_owner", _I32), ("split", _I32), ("timing", _P * 8)]
 
 
 class StepArgs(ctypes.Structure):
     """emb_step_args of include/emb.h."""
     _fields_ = [("table", _P), ("exp_avg", _P), ("exp_avg_sq", _P), ("V", _I64), ("D", _I32),
-                ("row_owner", _P), ("P", _I32), ("ids", _P), ("T", _I32), ("grad", _P), ("grad_dtype", _I32),
+                ("row_owner", _P), ("P", _I32), ("ids", _P), ("T", _I32), ("next_ids", _P), ("T_next", _I32),
+                ("grad", _P), ("grad_dtype", _I32),
                 ("cap_rows", _I32), ("lookup", _P), ("uniq_ids", _P), ("seg_offsets", _P), ("num_unique", _P),
                 ("uniq_grad", _P), ("send_ids", _P), ("send_counts", _P), ("send_offsets", _P), ("send_rows", _P),
                 ("ws_coalesce", _P), ("ws_coalesce_bytes", _SZ), ("ws_pack", _P), ("ws_pack_bytes", _SZ),
@@ -216,6 +221,42 @@ def grad_coalesce_by_owner(ids, grad, V, row_owner, P, out=None, workspace=None,
                                           _ptr(seg_offsets), _ptr(send_rows), _ptr(send_counts), _ptr(send_offsets),
                                           _ptr(num_unique), _ptr(workspace), workspace.numel(), _ptr(dev_status),
                                           _stream(stream)), "emb_grad_coalesce_by_owner")
+    return out
+
+
+def grad_coalesce_split_workspace_bytes(T, T_next, V, D, grad_dtype=EMB_F32) -> int:
+    return int(lib.emb_grad_coalesce_split_workspace_bytes(T, T_next, V, D, grad_dtype))
+
+
+def grad_coalesce_split(ids, next_ids, grad, V, row_owner, P, out=None, workspace=None, dev_status=None,
+                        stream=None):
+    """Coalesce into the send layout with the prior / delayed split (emb_grad_coalesce_split).
+
+    Returns (send_ids [T], seg_offsets [T+1], send_rows [T, D], send_counts [2P], send_offsets [2P+1],
+    num_unique [1]); groups 0 .. P-1 hold the prior rows, P .. 2P-1 the delayed rows.
+    """
+    _need(ids, torch.int32, "ids")
+    _need(next_ids, torch.int32, "next_ids")
+    _need(row_owner, torch.int32, "row_owner")
+    code = _dtype_code(grad)
+    if not grad.is_cuda or not grad.is_contiguous():
+        raise EmbError("grad must be a contiguous CUDA tensor")
+    T, T_next = ids.numel(), next_ids.numel()
+    D = grad.shape[1]
+    dev = ids.device
+    if out is None:
+        out = (torch.empty(T, dtype=torch.int32, device=dev), torch.empty(T + 1, dtype=torch.int32, device=dev),
+               torch.empty((T, D), dtype=torch.float32, device=dev),
+               torch.empty(2 * P, dtype=torch.int32, device=dev),
+               torch.empty(2 * P + 1, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
+    send_ids, seg_offsets, send_rows, send_counts, send_offsets, num_unique = out
+    if workspace is None:
+        workspace = new_workspace(grad_coalesce_split_workspace_bytes(T, T_next, V, D, code), dev)
+    _check(lib.emb_grad_coalesce_split(_ptr(ids), T, _ptr(next_ids), T_next, _ptr(grad), code, D, V,
+                                       _ptr(row_owner), P, _ptr(send_ids), _ptr(seg_offsets), _ptr(send_rows),
+                                       _ptr(send_counts), _ptr(send_offsets), _ptr(num_unique), _ptr(workspace),
+                                       workspace.numel(), _ptr(dev_status), _stream(stream)),
+           "emb_grad_coalesce_split")
     return out
 
 

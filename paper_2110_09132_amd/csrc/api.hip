@@ -27,20 +27,26 @@ int coalesce_args_status(const int32_t* ids, int32_t T, const void* grad, int32_
   if (T > 0 && (!ids || !grad || !uniq_ids || !uniq_grad || !workspace)) return EMB_ERR_INVALID_ARG;
   if (reinterpret_cast<uintptr_t>(grad) % (grad_dtype == EMB_BF16 ? 2 : 4) != 0) return EMB_ERR_INVALID_ARG;
   if (T > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return EMB_ERR_INVALID_ARG;
-  if (T > 0 && workspace_bytes < coalesce_workspace_bytes(T, D)) return EMB_ERR_WORKSPACE;
+  if (T > 0 && workspace_bytes < coalesce_workspace_bytes(T, D, -1, V)) return EMB_ERR_WORKSPACE;
   return EMB_OK;
 }
 
+// T_next < 0: the owner-major call without the split.
 int coalesce_by_owner_args_status(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D,
-                                  int64_t V, const int32_t* row_owner, int32_t P, const int32_t* send_ids,
-                                  const int32_t* seg_offsets, const float* send_rows, const int32_t* send_counts,
-                                  const int32_t* send_offsets, const int32_t* num_unique, const void* workspace,
-                                  size_t workspace_bytes) {
+                                  int64_t V, const int32_t* row_owner, int32_t P, const int32_t* next_ids,
+                                  int32_t T_next, const int32_t* send_ids, const int32_t* seg_offsets,
+                                  const float* send_rows, const int32_t* send_counts, const int32_t* send_offsets,
+                                  const int32_t* num_unique, const void* workspace, size_t workspace_bytes) {
+  const bool split = T_next >= 0;
   if (P < 1 || P > kMaxOwners || !send_counts || !send_offsets) return EMB_ERR_INVALID_ARG;
   if (T > 0 && !row_owner) return EMB_ERR_INVALID_ARG;
-  if (!bad_table_dims(V, D) && !coalesce_by_owner_supported(V, P)) return EMB_ERR_UNSUPPORTED;
-  return coalesce_args_status(ids, T, grad, grad_dtype, D, V, send_ids, seg_offsets, send_rows, num_unique, workspace,
-                              workspace_bytes);
+  if (split && (T_next >= (1 << 30) || (T_next > 0 && !next_ids))) return EMB_ERR_INVALID_ARG;
+  if (!bad_table_dims(V, D) && !coalesce_by_owner_supported(V, P, split)) return EMB_ERR_UNSUPPORTED;
+  const int st = coalesce_args_status(ids, T, grad, grad_dtype, D, V, send_ids, seg_offsets, send_rows, num_unique,
+                                      workspace, workspace_bytes);
+  if (st != EMB_OK) return st;
+  if (split && T > 0 && workspace_bytes < coalesce_workspace_bytes(T, D, T_next, V)) return EMB_ERR_WORKSPACE;
+  return EMB_OK;
 }
 
 
@@ -102,7 +108,12 @@ int emb_gather(const float* table, int64_t V, int32_t D, const int32_t* ids, int
 
 size_t emb_grad_coalesce_workspace_bytes(int32_t T, int64_t V, int32_t D, int32_t grad_dtype) {
   if (T < 0 || bad_table_dims(V, D) || (grad_dtype != EMB_F32 && grad_dtype != EMB_BF16)) return 0;
-  return emb::coalesce_workspace_bytes(T, D);
+  return emb::coalesce_workspace_bytes(T, D, -1, V);
+}
+
+size_t emb_grad_coalesce_split_workspace_bytes(int32_t T, int32_t T_next, int64_t V, int32_t D, int32_t grad_dtype) {
+  if (T < 0 || T_next < 0 || bad_table_dims(V, D) || (grad_dtype != EMB_F32 && grad_dtype != EMB_BF16)) return 0;
+  return emb::coalesce_workspace_bytes(T, D, T_next, V);
 }
 
 int emb_grad_coalesce(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D, int64_t V,
@@ -111,8 +122,8 @@ int emb_grad_coalesce(const int32_t* ids, int32_t T, const void* grad, int32_t g
   const int st = emb::coalesce_args_status(ids, T, grad, grad_dtype, D, V, uniq_ids, seg_offsets, uniq_grad,
                                            num_unique, workspace, workspace_bytes);
   if (st != EMB_OK) return st;
-  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, nullptr, 1, uniq_ids,
-                                            seg_offsets, uniq_grad, num_unique, nullptr, nullptr, workspace,
+  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, emb::CoalesceVariant{},
+                                            uniq_ids, seg_offsets, uniq_grad, num_unique, nullptr, nullptr, workspace,
                                             dev_status, static_cast<hipStream_t>(stream)));
 }
 
@@ -121,13 +132,36 @@ int emb_grad_coalesce_by_owner(const int32_t* ids, int32_t T, const void* grad, 
                                int32_t* seg_offsets, float* send_rows, int32_t* send_counts, int32_t* send_offsets,
                                int32_t* num_unique, void* workspace, size_t workspace_bytes, int32_t* dev_status,
                                void* stream) {
-  const int st = emb::coalesce_by_owner_args_status(ids, T, grad, grad_dtype, D, V, row_owner, P, send_ids,
-                                                    seg_offsets, send_rows, send_counts, send_offsets, num_unique,
-                                                    workspace, workspace_bytes);
+  const int st = emb::coalesce_by_owner_args_status(ids, T, grad, grad_dtype, D, V, row_owner, P, nullptr, -1,
+                                                    send_ids, seg_offsets, send_rows, send_counts, send_offsets,
+                                                    num_unique, workspace, workspace_bytes);
   if (st != EMB_OK) return st;
-  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, row_owner, P, send_ids,
-                                            seg_offsets, send_rows, num_unique, send_counts, send_offsets,
-                                            workspace, dev_status, static_cast<hipStream_t>(stream)));
+  emb::CoalesceVariant var;
+  var.row_owner = row_owner;
+  var.P = P;
+  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, var, send_ids, seg_offsets,
+                                            send_rows, num_unique, send_counts, send_offsets, workspace, dev_status,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+int emb_grad_coalesce_split(const int32_t* ids, int32_t T, const int32_t* next_ids, int32_t T_next, const void* grad,
+                            int32_t grad_dtype, int32_t D, int64_t V, const int32_t* row_owner, int32_t P,
+                            int32_t* send_ids, int32_t* seg_offsets, float* send_rows, int32_t* send_counts,
+                            int32_t* send_offsets, int32_t* num_unique, void* workspace, size_t workspace_bytes,
+                            int32_t* dev_status, void* stream) {
+  if (T_next < 0) return EMB_ERR_INVALID_ARG;
+  const int st = emb::coalesce_by_owner_args_status(ids, T, grad, grad_dtype, D, V, row_owner, P, next_ids, T_next,
+                                                    send_ids, seg_offsets, send_rows, send_counts, send_offsets,
+                                                    num_unique, workspace, workspace_bytes);
+  if (st != EMB_OK) return st;
+  emb::CoalesceVariant var;
+  var.row_owner = row_owner;
+  var.P = P;
+  var.next_ids = next_ids;
+  var.T_next = T_next;
+  return launch_status(emb::launch_coalesce(ids, T, grad, grad_dtype == EMB_BF16, D, V, var, send_ids, seg_offsets,
+                                            send_rows, num_unique, send_counts, send_offsets, workspace, dev_status,
+                                            static_cast<hipStream_t>(stream)));
 }
 
 size_t emb_pack_by_owner_workspace_bytes(int32_t cap_rows, int32_t P) {

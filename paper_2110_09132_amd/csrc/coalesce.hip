@@ -75,50 +75,114 @@ __device__ __forceinline__ uint32_t peek(uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// How a token's id becomes its sort key: the id itself, or, with row owners,
-// owner << ib | id, which orders tokens by owner shard and by id inside it.
+// How a token's id becomes its sort key: the id itself; with row owners,
+// owner << ib | id, which orders tokens by owner shard and by id inside it;
+// with the vertical split as well, class << (ib + ob) | owner << ib | id, where
+// class 0 marks the prior rows (the id occurs in the next batch) and 1 the
+// delayed ones, so that the prior rows of every owner come first.
 struct KeySpec {
   uint32_t V;                // ids in [0, V) take part
   const int32_t* row_owner;  // nullptr: the key is the id
   int32_t P;                 // owners in [0, P) take part
-  int ib;                    // id bits of a composite key
+  int ib, ob;                // id bits and owner bits of a composite key
   uint32_t id_mask;          // key -> id
+  uint32_t omask;            // (key >> ib) & omask -> owner
+  int cls_shift;             // key >> cls_shift -> class (32: no class bit)
+  const uint32_t* next_tab;  // set of the next batch's ids (nullptr: no split): a bitmap over
+                             // [0, V) (next_bitmap), else a hash set of 2^(32 - tab_shift) slots
+  bool next_bitmap;
+  int tab_shift;
+  int G;                     // groups of the output: owners, times 2 with the split
 };
 
-// Keys of ITEMS tokens ids[idx[r]] (idx already clamped; inb[r]: the token
-// exists).  take[r] says whether the token takes part; with status != nullptr
-// the flags of the tokens that do not are raised.  Every load is issued
-// unconditionally, from a clamped address.
-template <int ITEMS>
-__device__ __forceinline__ void load_keys(const int32_t* __restrict__ ids, const int (&idx)[ITEMS],
-                                          const bool (&inb)[ITEMS], const KeySpec& ks, uint32_t (&key)[ITEMS],
-                                          bool (&take)[ITEMS], int32_t* status) {
-  int32_t id[ITEMS];
-  bool idok[ITEMS];
+__device__ __forceinline__ int group_of(uint32_t key, const KeySpec& ks) {
+  const int cls = static_cast<int>(static_cast<uint64_t>(key) >> ks.cls_shift);
+  return cls * ks.P + static_cast<int>((key >> ks.ib) & ks.omask);
+}
+
+// Open-addressing hash set of ids (slot value id + 1, 0 = empty, linear probing).
+__device__ __forceinline__ uint32_t tab_slot(uint32_t id, int shift) { return (id * 0x9E3779B1u) >> shift; }
+
+__device__ __forceinline__ bool in_next(uint32_t id, const KeySpec& ks) {
+  if (ks.next_bitmap) return (ks.next_tab[id >> 5] >> (id & 31u)) & 1u;
+  const uint32_t mask = 0xFFFFFFFFu >> ks.tab_shift;
+  uint32_t slot = tab_slot(id, ks.tab_shift);
+  for (uint32_t probe = 0; probe <= mask; ++probe) {
+    const uint32_t v = ks.next_tab[slot];
+    if (v == id + 1) return true;
+    if (v == 0) return false;
+    slot = (slot + 1) & mask;
+  }
+  return false;
+}
+
+__global__ __launch_bounds__(kThreads) void tab_clear_kernel(uint32_t* __restrict__ tab, int n) {
+  for (int i = blockIdx.x * kThreads + threadIdx.x; i < n; i += gridDim.x * kThreads) tab[i] = 0;
+}
+
+// Inserts the in-range ids of the next batch: bits of a bitmap (atomics whose
+// result is not needed, so they do not wait), or slots of the hash set (at
+// most half full, so every insertion finds a free slot).
+__global__ __launch_bounds__(kThreads) void tab_insert_kernel(const int32_t* __restrict__ next_ids, int T_next,
+                                                              uint32_t V, uint32_t* __restrict__ tab, bool bitmap,
+                                                              int shift) {
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  if (t >= T_next) return;
+  const int32_t id = next_ids[t];
+  if (id < 0 || static_cast<uint32_t>(id) >= V) return;
+  if (bitmap) {
+    atomicOr(&tab[static_cast<uint32_t>(id) >> 5], 1u << (static_cast<uint32_t>(id) & 31u));
+    return;
+  }
+  const uint32_t mask = 0xFFFFFFFFu >> shift;
+  uint32_t slot = tab_slot(static_cast<uint32_t>(id), shift);
+  for (uint32_t probe = 0; probe <= mask; ++probe) {
+    const uint32_t old = atomicCAS(&tab[slot], 0u, static_cast<uint32_t>(id) + 1u);
+    if (old == 0u || old == static_cast<uint32_t>(id) + 1u) return;
+    slot = (slot + 1) & mask;
+  }
+}
+
+constexpr int kKeysPerThread = 4;
+
+// Sort key of every token, and vals[t] = t for a token that takes part, -1 for
+// one that does not (id outside [0, V), or owner outside [0, P)).  The owner
+// and next-batch lookups are done here once, so the sort reads plain keys.
+__global__ __launch_bounds__(kThreads) void make_keys_kernel(const int32_t* __restrict__ ids, int T, KeySpec ks,
+                                                             uint32_t* __restrict__ keys, int32_t* __restrict__ vals,
+                                                             int32_t* status) {
+  const int base = blockIdx.x * kThreads * kKeysPerThread + static_cast<int>(threadIdx.x);
+  int32_t id[kKeysPerThread];
+  bool idok[kKeysPerThread];
 #pragma unroll
-  for (int r = 0; r < ITEMS; ++r) id[r] = ids[idx[r]];
+  for (int r = 0; r < kKeysPerThread; ++r) id[r] = ids[min(base + r * kThreads, T - 1)];
 #pragma unroll
-  for (int r = 0; r < ITEMS; ++r) idok[r] = id[r] >= 0 && static_cast<uint32_t>(id[r]) < ks.V;
-  uint32_t own[ITEMS];
+  for (int r = 0; r < kKeysPerThread; ++r) idok[r] = id[r] >= 0 && static_cast<uint32_t>(id[r]) < ks.V;
+  uint32_t own[kKeysPerThread];
 #pragma unroll
-  for (int r = 0; r < ITEMS; ++r) own[r] = 0;
+  for (int r = 0; r < kKeysPerThread; ++r) own[r] = 0;
   if (ks.row_owner != nullptr) {
 #pragma unroll
-    for (int r = 0; r < ITEMS; ++r) own[r] = static_cast<uint32_t>(ks.row_owner[idok[r] ? id[r] : 0]);
+    for (int r = 0; r < kKeysPerThread; ++r) own[r] = static_cast<uint32_t>(ks.row_owner[idok[r] ? id[r] : 0]);
   }
   bool bad_id = false, bad_owner = false;
 #pragma unroll
-  for (int r = 0; r < ITEMS; ++r) {
+  for (int r = 0; r < kKeysPerThread; ++r) {
+    const int t = base + r * kThreads;
+    const bool inb = t < T;
     const bool ownok = own[r] < static_cast<uint32_t>(ks.P);
-    take[r] = inb[r] && idok[r] && ownok;
-    bad_id |= inb[r] && !idok[r];
-    bad_owner |= inb[r] && idok[r] && !ownok;
-    key[r] = (own[r] << ks.ib) | static_cast<uint32_t>(id[r]);
+    const bool take = inb && idok[r] && ownok;
+    bad_id |= inb && !idok[r];
+    bad_owner |= inb && idok[r] && !ownok;
+    uint32_t key = (own[r] << ks.ib) | static_cast<uint32_t>(id[r]);
+    if (ks.next_tab != nullptr && take && !in_next(static_cast<uint32_t>(id[r]), ks)) key |= 1u << ks.cls_shift;
+    if (inb) {
+      keys[t] = key;
+      vals[t] = take ? t : -1;
+    }
   }
-  if (status != nullptr) {
-    if (__any(bad_id) && lane_id() == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
-    if (__any(bad_owner) && lane_id() == 0) raise_flag(status, EMB_DEV_OWNER_OUT_OF_RANGE);
-  }
+  if (__any(bad_id) && lane_id() == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
+  if (__any(bad_owner) && lane_id() == 0) raise_flag(status, EMB_DEV_OWNER_OUT_OF_RANGE);
 }
 
 // Exclusive prefix of one digit's counts over tiles 0 .. tile-1, read from
@@ -180,8 +244,11 @@ int bits_for(int64_t n) {  // bits of the values 0 .. n - 1
   return B;
 }
 
-// Key bits: bits(V) for the id, plus bits(P) for the owner of a composite key.
-int key_bits(int64_t V, bool by_owner, int P) { return bits_for(V) + (by_owner ? bits_for(P) : 0); }
+// Key bits: bits(V) for the id, plus bits(P) for the owner of a composite key,
+// plus one for the class bit of the vertical split.
+int key_bits(int64_t V, bool by_owner, int P, bool split) {
+  return bits_for(V) + (by_owner ? bits_for(P) : 0) + (split ? 1 : 0);
+}
 
 RadixPlan plan_for(int B) {
   B = max(B, 1);  // one pass even when every key is 0
@@ -190,37 +257,46 @@ RadixPlan plan_for(int B) {
   return RadixPlan{npass, (B + npass - 1) / npass, B};
 }
 
-KeySpec key_spec(int64_t V, const int32_t* row_owner, int P) {
+KeySpec key_spec(int64_t V, const int32_t* row_owner, int P, bool split) {
   KeySpec ks;
   ks.V = static_cast<uint32_t>(V);
   ks.row_owner = row_owner;
-  ks.P = row_owner != nullptr ? P : 1;
-  ks.ib = row_owner != nullptr ? bits_for(V) : 0;
-  ks.id_mask = row_owner != nullptr ? static_cast<uint32_t>((uint64_t{1} << ks.ib) - 1) : ~0u;
+  const bool own = row_owner != nullptr;
+  ks.P = own ? P : 1;
+  ks.ib = own ? bits_for(V) : 0;
+  ks.ob = own ? bits_for(P) : 0;
+  ks.id_mask = own ? static_cast<uint32_t>((uint64_t{1} << ks.ib) - 1) : ~0u;
+  ks.omask = static_cast<uint32_t>((uint64_t{1} << ks.ob) - 1);
+  ks.cls_shift = (own && split) ? ks.ib + ks.ob : 32;
+  ks.next_tab = nullptr;
+  ks.next_bitmap = false;
+  ks.tab_shift = 32;
+  ks.G = (own && split) ? 2 * P : ks.P;
   return ks;
 }
 
 // ---------------------------------------------------------------- radix sort
 template <class C>
-__global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const int32_t* __restrict__ ids, KeySpec ks, int T,
+__global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const uint32_t* __restrict__ keys,
+                                                              const int32_t* __restrict__ vals, int T,
                                                               RadixPlan plan, uint32_t* __restrict__ up_hist,
-                                                              uint32_t* __restrict__ zero_begin, int zero_words,
-                                                              int32_t* status) {
+                                                              uint32_t* __restrict__ zero_begin, int zero_words) {
   constexpr int NT = C::kNT, kBins = C::kBins, kPer = C::kUpTile / NT;
   __shared__ uint32_t h[C::kPasses * kBins];
   for (int i = threadIdx.x; i < plan.npass * kBins; i += NT) h[i] = 0;
   __syncthreads();
   const int base = blockIdx.x * C::kUpTile;
-  int idx[kPer];
-  bool inb[kPer], take[kPer];
+  bool take[kPer];
   uint32_t k[kPer];
+  int32_t v[kPer];
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
-    const int g = base + r * NT + static_cast<int>(threadIdx.x);
-    inb[r] = g < T;
-    idx[r] = min(g, T - 1);
+    const int g = min(base + r * NT + static_cast<int>(threadIdx.x), T - 1);
+    k[r] = keys[g];
+    v[r] = vals[g];
   }
-  load_keys<kPer>(ids, idx, inb, ks, k, take, status);
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) take[r] = base + r * NT + static_cast<int>(threadIdx.x) < T && v[r] >= 0;
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
     if (take[r]) {
@@ -236,8 +312,8 @@ __global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const int32_t* __r
 
 template <class C>
 __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
-    const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ raw_ids, const int32_t* __restrict__ vals_in,
-    KeySpec ks, int T, RadixPlan plan, int pass, const uint32_t* __restrict__ up_hist, int nup, uint32_t* lookback,
+    const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int T, RadixPlan plan, int pass,
+    const uint32_t* __restrict__ up_hist, int nup, uint32_t* lookback,
     uint32_t* ticket, int ntiles, uint32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out,
     uint32_t* __restrict__ n_valid, int32_t* status) {
   constexpr int NT = C::kNT, kBins = C::kBins, kTile = C::kTile, NW = NT / kWave;
@@ -272,13 +348,8 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     const int g = base + w * kItems * kWave + r * kWave + static_cast<int>(lane_id());
     inb[r] = g < T;
     idx[r] = min(g, T - 1);
-    val[r] = vals_in != nullptr ? vals_in[idx[r]] : g;
-  }
-  if (raw_ids != nullptr) {
-    load_keys<kItems>(raw_ids, idx, inb, ks, key, valid, nullptr);
-  } else {
-#pragma unroll
-    for (int r = 0; r < kItems; ++r) key[r] = keys_in[idx[r]];
+    val[r] = vals_in[idx[r]];
+    key[r] = keys_in[idx[r]];
   }
 #pragma unroll
   for (int r = 0; r < kItems; ++r) dig[r] = (key[r] >> shift) & (bins - 1);
@@ -300,10 +371,11 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
   __syncthreads();
   // the sorted sequence holds the tokens that take part: the sum of the totals
   const uint32_t tv = block_exclusive_scan<NT>(gbase, bins, wsum);
-  if (raw_ids == nullptr) {
+  // the first pass reads every token (those that take part have a position);
+  // later passes read the tv sorted tokens
 #pragma unroll
-    for (int r = 0; r < kItems; ++r) valid[r] = static_cast<uint32_t>(idx[r]) < tv && inb[r];
-  }
+  for (int r = 0; r < kItems; ++r)
+    valid[r] = inb[r] && (pass == 0 ? val[r] >= 0 : static_cast<uint32_t>(idx[r]) < tv);
   if (tile == 0 && threadIdx.x == 0) *n_valid = tv;
 
   const uint32_t nvalid = tile_stable_rank<NT, kItems>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
@@ -403,9 +475,9 @@ __global__ __launch_bounds__(kThreads) void seg_count_kernel(const uint32_t* __r
 template <bool BF16, int VEC>
 __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     const uint32_t* __restrict__ skeys, const int32_t* __restrict__ spos, const uint32_t* __restrict__ n_valid, int T,
-    const void* __restrict__ grad, int D, const uint32_t* __restrict__ tile_heads, int ib, uint32_t id_mask,
+    const void* __restrict__ grad, int D, const uint32_t* __restrict__ tile_heads, KeySpec ks,
     int32_t* __restrict__ uniq_ids, int32_t* __restrict__ seg_offsets, int32_t* __restrict__ num_unique,
-    float* __restrict__ uniq_grad, int32_t* __restrict__ owner_offsets, int P, float* __restrict__ partial,
+    float* __restrict__ uniq_grad, int32_t* __restrict__ owner_offsets, float* __restrict__ partial,
     int32_t* __restrict__ span_list, int32_t* __restrict__ span_count, int nchunks) {
   __shared__ uint32_t wave_heads[kWaves];
   __shared__ uint32_t red[kWaves];
@@ -471,11 +543,11 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const int u = static_cast<int>(ubase + __popcll(heads & upto)) - 1;  // unique index of element e
   const bool u_ok = u >= 0 && u < T;
   if (head && u_ok) {
-    uniq_ids[u] = static_cast<int32_t>(key & id_mask);
+    uniq_ids[u] = static_cast<int32_t>(key & ks.id_mask);
     seg_offsets[u] = e;
-    if (owner_offsets != nullptr) {  // owners o' < p <= o start at this row
-      const int o = min(static_cast<int>(key >> ib), P);
-      const int o_prev = e == 0 ? -1 : static_cast<int>(key_prev >> ib);
+    if (owner_offsets != nullptr) {  // groups o' < p <= o start at this row
+      const int o = min(group_of(key, ks), ks.G);
+      const int o_prev = e == 0 ? -1 : group_of(key_prev, ks);
       for (int p = o_prev + 1; p <= o; ++p) owner_offsets[p] = u;
     }
   }
@@ -484,14 +556,13 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     seg_offsets[u + 1] = e + 1;  // the last valid token of the whole batch
     num_unique[0] = u + 1;
     if (owner_offsets != nullptr)
-      for (int p = static_cast<int>(min(key >> ib, static_cast<uint32_t>(P))) + 1; p <= P; ++p)
-        owner_offsets[p] = u + 1;
+      for (int p = min(group_of(key, ks), ks.G) + 1; p <= ks.G; ++p) owner_offsets[p] = u + 1;
   }
   if (chunk == 0 && lane == 1 && !valid) {  // no valid token at all
     seg_offsets[0] = 0;
     num_unique[0] = 0;
     if (owner_offsets != nullptr)
-      for (int p = 0; p <= P; ++p) owner_offsets[p] = 0;
+      for (int p = 0; p <= ks.G; ++p) owner_offsets[p] = 0;
   }
   if (nv == 0) return;
 
@@ -622,13 +693,29 @@ struct CoalesceWs {
   int32_t* span_list;
   uint32_t* tile_heads;  // [nred]
   float* partial;
+  uint32_t* next_tab;    // vertical split: set of the next batch's ids [tab_words]
+  int tab_words;
+  bool tab_bitmap;       // a bitmap over [0, V); else a hash set of 2^(32 - tab_shift) slots
+  int tab_shift;
   size_t bytes;
 };
 
+int tab_log2_slots(int T_next) {  // at least twice the ids, at least 64 slots
+  int lg = 6;
+  while ((int64_t{1} << lg) < 2 * static_cast<int64_t>(T_next)) ++lg;
+  return lg;
+}
+
+// The set of next ids is a bitmap over the rows (one load per lookup, inserts
+// that do not wait) unless the table is so large that clearing V bits per
+// call would cost more than it saves.
+constexpr int64_t kBitmapMaxRows = int64_t{1} << 27;
+
 // The layout does not depend on the number of radix passes (sized for the
-// most), so one size serves both the plain and the owner-major call.
+// most), so one size serves the plain and the owner-major call; the split
+// appends its hash set (T_next < 0: none).
 template <class C>
-CoalesceWs carve_with(void* base, int T, int D) {
+CoalesceWs carve_with(void* base, int T, int D, int T_next, int64_t V) {
   Carver cv{static_cast<char*>(base)};
   const size_t n = static_cast<size_t>(T);
   const size_t ntiles = (n + C::kTile - 1) / C::kTile;
@@ -648,30 +735,45 @@ CoalesceWs carve_with(void* base, int T, int D) {
   w.span_list = cv.take<int32_t>(nchunks);
   w.tile_heads = cv.take<uint32_t>(nred);
   w.partial = cv.take<float>(nchunks * 2 * static_cast<size_t>(D));
+  w.next_tab = nullptr;
+  w.tab_words = 0;
+  w.tab_bitmap = false;
+  w.tab_shift = 32;
+  if (T_next >= 0) {
+    w.tab_bitmap = V <= kBitmapMaxRows;
+    if (w.tab_bitmap) {
+      w.tab_words = static_cast<int>((V + 31) / 32);
+    } else {
+      const int lg = tab_log2_slots(T_next);
+      w.tab_words = 1 << lg;
+      w.tab_shift = 32 - lg;
+    }
+    w.next_tab = cv.take<uint32_t>(static_cast<size_t>(w.tab_words));
+  }
   w.bytes = cv.size();
   return w;
 }
 
-CoalesceWs carve(void* base, int T, int D) { return carve_with<Narrow>(base, T, D); }
+CoalesceWs carve(void* base, int T, int D, int T_next, int64_t V) { return carve_with<Narrow>(base, T, D, T_next, V); }
 
 template <class C>
-void launch_sort(const int32_t* ids, int T, const KeySpec& ks, const RadixPlan& plan, const CoalesceWs& ws,
+void launch_sort(const uint32_t* keys0, const int32_t* vals0, int T, const RadixPlan& plan, const CoalesceWs& ws,
                  int32_t* status, hipStream_t stream, const uint32_t** skeys, const int32_t** spos) {
   const int ntiles = (T + C::kTile - 1) / C::kTile;
   const int nup = (T + C::kUpTile - 1) / C::kUpTile;
   uint32_t* zero_begin = ws.tickets;
   const int zero_words =
       static_cast<int>((ws.sort_lb + static_cast<size_t>(plan.npass) * ntiles * C::kBins) - zero_begin);
-  hipLaunchKernelGGL(sort_upsweep_kernel<C>, dim3(nup), dim3(C::kNT), 0, stream, ids, ks, T, plan, ws.up_hist,
-                     zero_begin, zero_words, status);
-  const uint32_t* kin = nullptr;
-  const int32_t* vin = nullptr;
+  hipLaunchKernelGGL(sort_upsweep_kernel<C>, dim3(nup), dim3(C::kNT), 0, stream, keys0, vals0, T, plan, ws.up_hist,
+                     zero_begin, zero_words);
+  const uint32_t* kin = keys0;
+  const int32_t* vin = vals0;
   uint32_t* kout = ws.keys_a;
   int32_t* vout = ws.vals_a;
   for (int p = 0; p < plan.npass; ++p) {
-    hipLaunchKernelGGL(sort_pass_kernel<C>, dim3(ntiles), dim3(C::kNT), 0, stream, kin, (p == 0) ? ids : nullptr,
-                       vin, ks, T, plan, p, ws.up_hist, nup, ws.sort_lb + static_cast<size_t>(p) * ntiles * C::kBins,
-                       ws.tickets + p, ntiles, kout, vout, ws.n_valid, status);
+    hipLaunchKernelGGL(sort_pass_kernel<C>, dim3(ntiles), dim3(C::kNT), 0, stream, kin, vin, T, plan, p, ws.up_hist,
+                       nup, ws.sort_lb + static_cast<size_t>(p) * ntiles * C::kBins, ws.tickets + p, ntiles, kout,
+                       vout, ws.n_valid, status);
     kin = kout;
     vin = vout;
     kout = (kout == ws.keys_a) ? ws.keys_b : ws.keys_a;
@@ -681,11 +783,14 @@ void launch_sort(const int32_t* ids, int T, const KeySpec& ks, const RadixPlan& 
   *spos = vin;
 }
 
-RadixPlan plan_for_call(int64_t V, const int32_t* row_owner, int P) {
-  return plan_for(key_bits(V, row_owner != nullptr, P));
+bool is_split(const CoalesceVariant& var) { return var.row_owner != nullptr && var.T_next >= 0; }
+
+RadixPlan plan_for_call(int64_t V, const CoalesceVariant& var) {
+  return plan_for(key_bits(V, var.row_owner != nullptr, var.P, is_split(var)));
 }
 
-// The sorted keys and positions are in the ping-pong buffer the last pass wrote.
+// The keys start in keys_b / vals_b and the passes alternate from keys_a, so
+// the sorted keys and positions are in the buffer the last pass wrote.
 void sorted_arrays(const CoalesceWs& ws, const RadixPlan& plan, const uint32_t** skeys, const int32_t** spos) {
   const bool odd = plan.npass % 2 == 1;
   *skeys = odd ? ws.keys_a : ws.keys_b;
@@ -694,57 +799,73 @@ void sorted_arrays(const CoalesceWs& ws, const RadixPlan& plan, const uint32_t**
 
 }  // namespace
 
-size_t coalesce_workspace_bytes(int T, int D) { return carve(nullptr, T, D).bytes; }
+size_t coalesce_workspace_bytes(int T, int D, int T_next, int64_t V) { return carve(nullptr, T, D, T_next, V).bytes; }
 
-bool coalesce_by_owner_supported(int64_t V, int P) { return key_bits(V, true, P) <= 8 * kMaxPasses; }
+bool coalesce_by_owner_supported(int64_t V, int P, bool split) {
+  return key_bits(V, true, P, split) <= 8 * kMaxPasses;
+}
 
-hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const int32_t* row_owner, int P,
+hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const CoalesceVariant& var,
                                 void* workspace, int32_t* status, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  CoalesceWs ws = carve(workspace, T, D);
-  const KeySpec ks = key_spec(V, row_owner, P);
-  const RadixPlan plan = plan_for_call(V, row_owner, P);
+  CoalesceWs ws = carve(workspace, T, D, is_split(var) ? var.T_next : -1, V);
+  KeySpec ks = key_spec(V, var.row_owner, var.P, is_split(var));
+  const RadixPlan plan = plan_for_call(V, var);
   const int nred = (T + kRedTile - 1) / kRedTile;
-  // 1-2. digit histograms of all passes, then the radix passes over (key, position)
+  // 0. the next batch's ids into a hash set (vertical split)
+  if (is_split(var)) {
+    hipLaunchKernelGGL(tab_clear_kernel, dim3(grid_for((ws.tab_words + kThreads - 1) / kThreads, 1024)),
+                       dim3(kThreads), 0, stream, ws.next_tab, ws.tab_words);
+    if (var.T_next > 0)
+      hipLaunchKernelGGL(tab_insert_kernel, dim3((var.T_next + kThreads - 1) / kThreads), dim3(kThreads), 0, stream,
+                         var.next_ids, var.T_next, ks.V, ws.next_tab, ws.tab_bitmap, ws.tab_shift);
+    ks.next_tab = ws.next_tab;
+    ks.next_bitmap = ws.tab_bitmap;
+    ks.tab_shift = ws.tab_shift;
+  }
+  // 1. the key of every token (owner and next-batch lookups once)
+  const int per_block = kThreads * kKeysPerThread;
+  hipLaunchKernelGGL(make_keys_kernel, dim3((T + per_block - 1) / per_block), dim3(kThreads), 0, stream, ids, T, ks,
+                     ws.keys_b, ws.vals_b, status);
+  // 2-3. digit histograms of all passes, then the radix passes over (key, position)
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
-  launch_sort<Narrow>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
-  // 3. heads per reduction workgroup
+  launch_sort<Narrow>(ws.keys_b, ws.vals_b, T, plan, ws, status, stream, &kin, &vin);
+  // 4. heads per reduction workgroup
   hipLaunchKernelGGL(seg_count_kernel, dim3((nred + kWaves - 1) / kWaves), dim3(kThreads), 0, stream, kin, ws.n_valid,
                      ws.tile_heads, nred);
   return hipGetLastError();
 }
 
-hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V, const int32_t* row_owner,
-                                  int P, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
-                                  int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
-                                  void* workspace, hipStream_t stream, hipEvent_t done) {
-  // owner_offsets / owner_counts are given exactly for the owner-major variant
-  // (row_owner != nullptr whenever T > 0)
+hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V,
+                                  const CoalesceVariant& var, int32_t* uniq_ids, int32_t* seg_offsets,
+                                  float* uniq_grad, int32_t* num_unique, int32_t* group_counts,
+                                  int32_t* group_offsets, void* workspace, hipStream_t stream, hipEvent_t done) {
+  // group_offsets / group_counts are given exactly for the owner-major variants
+  const KeySpec ks = key_spec(V, var.row_owner, var.P, is_split(var));
   if (T == 0) {
     hipExtLaunchKernelGGL(empty_batch_kernel, dim3(1), dim3(kThreads), 0, stream, nullptr, done, 0, seg_offsets,
-                          num_unique, owner_counts, owner_offsets, P);
+                          num_unique, group_counts, group_offsets, ks.G);
     return hipGetLastError();
   }
-  CoalesceWs ws = carve(workspace, T, D);
-  const KeySpec ks = key_spec(V, row_owner, P);
-  const RadixPlan plan = plan_for_call(V, row_owner, P);
+  CoalesceWs ws = carve(workspace, T, D, -1, V);  // the next-id set, if any, lies past everything used here
+  const RadixPlan plan = plan_for_call(V, var);
   const int nred = (T + kRedTile - 1) / kRedTile;
   const int nchunks = (T + kChunk - 1) / kChunk;
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
   sorted_arrays(ws, plan, &kin, &vin);
-  // 4. segments and per-chunk sums; 5. pieces of ids that cross chunks
+  // 5. segments and per-chunk sums; 6. pieces of ids that cross chunks
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(grad) % (grad_bf16 ? 8 : 16) == 0) &&
                     (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
   const dim3 cgrid(grid_for(nchunks, 1024));
 #define EMB_REDUCE(BF, VC)                                                                                          \
   hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred), dim3(kThreads), 0, stream, kin, vin, ws.n_valid, T, \
-                     grad, D, ws.tile_heads, ks.ib, ks.id_mask, uniq_ids, seg_offsets, num_unique, uniq_grad,        \
-                     owner_offsets, ks.P, ws.partial, ws.span_list, ws.span_count, nchunks)
+                     grad, D, ws.tile_heads, ks, uniq_ids, seg_offsets, num_unique, uniq_grad, group_offsets,        \
+                     ws.partial, ws.span_list, ws.span_count, nchunks)
 #define EMB_COMBINE(VC)                                                                                             \
   hipExtLaunchKernelGGL(seg_combine_kernel<VC>, cgrid, dim3(kThreads), 0, stream, nullptr, done, 0, ws.partial, D,  \
-                        seg_offsets, ws.span_list, ws.span_count, uniq_grad, owner_offsets, owner_counts, ks.P, T,  \
+                        seg_offsets, ws.span_list, ws.span_count, uniq_grad, group_offsets, group_counts, ks.G, T,  \
                         nchunks)
   if (vec4) {
     if (grad_bf16)
@@ -765,13 +886,13 @@ hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D
 }
 
 hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
-                           const int32_t* row_owner, int P, int32_t* uniq_ids, int32_t* seg_offsets,
-                           float* uniq_grad, int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
-                           void* workspace, int32_t* status, hipStream_t stream) {
-  const hipError_t e = launch_coalesce_sort(ids, T, V, D, row_owner, P, workspace, status, stream);
+                           const CoalesceVariant& var, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
+                           int32_t* num_unique, int32_t* group_counts, int32_t* group_offsets, void* workspace,
+                           int32_t* status, hipStream_t stream) {
+  const hipError_t e = launch_coalesce_sort(ids, T, V, D, var, workspace, status, stream);
   if (e != hipSuccess) return e;
-  return launch_coalesce_reduce(T, grad, grad_bf16, D, V, row_owner, P, uniq_ids, seg_offsets, uniq_grad, num_unique,
-                                owner_counts, owner_offsets, workspace, stream, nullptr);
+  return launch_coalesce_reduce(T, grad, grad_bf16, D, V, var, uniq_ids, seg_offsets, uniq_grad, num_unique,
+                                group_counts, group_offsets, workspace, stream, nullptr);
 }
 
 }  // namespace emb

@@ -7,6 +7,8 @@
 // kRowsInFlight steps, and the table loads of the next group are issued before
 // the current group is stored (two register buffers used in turn), so each
 // lane keeps two groups of independent 16-byte loads in flight.  Reads are whole table rows, writes contiguous rows.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "launch.h"
 
@@ -85,8 +87,8 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const VecT* __restrict
 }  // namespace
 
 hipError_t launch_gather(const float* table, int64_t V, int D, const int32_t* ids, int T, float* out,
-                         int32_t* status, hipStream_t stream) {
-  if (T == 0) return hipSuccess;
+                         int32_t* status, hipStream_t stream, hipEvent_t done) {
+  if (T == 0) return done != nullptr ? hipEventRecord(done, stream) : hipSuccess;
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(table) % 16 == 0) &&
                     (reinterpret_cast<uintptr_t>(out) % 16 == 0);
   const int Dv = vec4 ? D / 4 : D;
@@ -94,12 +96,12 @@ hipError_t launch_gather(const float* table, int64_t V, int D, const int32_t* id
   const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * kRowsInFlight * (kThreads / kWave);
   const unsigned grid = grid_for((T + rows_per_block - 1) / rows_per_block, kMaxBlocks);
   if (vec4) {
-    hipLaunchKernelGGL(gather_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream,
-                       reinterpret_cast<const float4*>(table), V, Dv, rl.log2_lanes, ids, T,
-                       reinterpret_cast<float4*>(out), status);
+    hipExtLaunchKernelGGL(gather_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream, nullptr, done, 0,
+                          reinterpret_cast<const float4*>(table), V, Dv, rl.log2_lanes, ids, T,
+                          reinterpret_cast<float4*>(out), status);
   } else {
-    hipLaunchKernelGGL(gather_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, table, V, Dv, rl.log2_lanes,
-                       ids, T, out, status);
+    hipExtLaunchKernelGGL(gather_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, nullptr, done, 0, table, V,
+                          Dv, rl.log2_lanes, ids, T, out, status);
   }
   return hipGetLastError();
 }

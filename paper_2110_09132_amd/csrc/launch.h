@@ -8,36 +8,47 @@
 
 namespace emb {
 
+// done (may be null): an event attached to the kernel's dispatch.
 hipError_t launch_gather(const float* table, int64_t V, int D, const int32_t* ids, int T, float* out,
-                         int32_t* status, hipStream_t stream);
+                         int32_t* status, hipStream_t stream, hipEvent_t done = nullptr);
 
-// Coalesce of T tokens; with row_owner != nullptr the owner-major variant
-// (distinct ids grouped by owner in [0, P), counts and offsets per owner).
-// The workspace size does not depend on the variant.
-size_t coalesce_workspace_bytes(int T, int D);
-bool coalesce_by_owner_supported(int64_t V, int P);  // (owner, id) keys fit the radix passes
+// Which coalesce: plain (ids ascending), owner-major (row_owner given: the
+// distinct ids grouped by owner in [0, P)), or owner-major with the vertical
+// split (T_next >= 0 as well: the prior rows, whose ids occur in next_ids, in
+// groups 0 .. P-1, then the delayed rows in groups P .. 2P-1).
+struct CoalesceVariant {
+  const int32_t* row_owner = nullptr;
+  int P = 1;
+  const int32_t* next_ids = nullptr;
+  int T_next = -1;
+};
+
+// Workspace size (T_next < 0: no split); it does not depend on the other choices.
+size_t coalesce_workspace_bytes(int T, int D, int T_next, int64_t V);
+bool coalesce_by_owner_supported(int64_t V, int P, bool split);  // the composite keys fit the radix passes
 // The two halves of launch_coalesce, for schedules that run them on different
-// streams (same workspace and variant; the reduce half must follow the sort half).
-hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const int32_t* row_owner, int P,
+// streams (same workspace and variant; the reduce half must follow the sort
+// half).  done (may be null): an event attached to the reduce half's last kernel.
+hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const CoalesceVariant& var,
                                 void* workspace, int32_t* status, hipStream_t stream);
-hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V, const int32_t* row_owner,
-                                  int P, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
-                                  int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
-                                  void* workspace, hipStream_t stream, hipEvent_t done);
+hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V,
+                                  const CoalesceVariant& var, int32_t* uniq_ids, int32_t* seg_offsets,
+                                  float* uniq_grad, int32_t* num_unique, int32_t* group_counts,
+                                  int32_t* group_offsets, void* workspace, hipStream_t stream, hipEvent_t done);
 hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
-                           const int32_t* row_owner, int P, int32_t* uniq_ids, int32_t* seg_offsets,
-                           float* uniq_grad, int32_t* num_unique, int32_t* owner_counts, int32_t* owner_offsets,
-                           void* workspace, int32_t* status, hipStream_t stream);
-// Host-side argument checks of emb_grad_coalesce and emb_grad_coalesce_by_owner
-// (EMB_OK when the call is valid).
+                           const CoalesceVariant& var, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
+                           int32_t* num_unique, int32_t* group_counts, int32_t* group_offsets, void* workspace,
+                           int32_t* status, hipStream_t stream);
+// Host-side argument checks of emb_grad_coalesce, emb_grad_coalesce_by_owner and
+// emb_grad_coalesce_split (EMB_OK when the call is valid).
 int coalesce_args_status(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D, int64_t V,
                          const int32_t* uniq_ids, const int32_t* seg_offsets, const float* uniq_grad,
                          const int32_t* num_unique, const void* workspace, size_t workspace_bytes);
 int coalesce_by_owner_args_status(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D,
-                                  int64_t V, const int32_t* row_owner, int32_t P, const int32_t* send_ids,
-                                  const int32_t* seg_offsets, const float* send_rows, const int32_t* send_counts,
-                                  const int32_t* send_offsets, const int32_t* num_unique, const void* workspace,
-                                  size_t workspace_bytes);
+                                  int64_t V, const int32_t* row_owner, int32_t P, const int32_t* next_ids,
+                                  int32_t T_next, const int32_t* send_ids, const int32_t* seg_offsets,
+                                  const float* send_rows, const int32_t* send_counts, const int32_t* send_offsets,
+                                  const int32_t* num_unique, const void* workspace, size_t workspace_bytes);
 
 size_t pack_workspace_bytes(int cap_rows, int P);
 hipError_t launch_pack(const int32_t* uniq_ids, const float* uniq_grad, const int32_t* num_unique, int cap_rows,

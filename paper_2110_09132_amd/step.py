@@ -9,7 +9,12 @@ call.  With overlap=True the latency-bound work runs on side streams while
 the lookup and the update stay on the main stream:
   by_owner=False: grad_coalesce on one side stream, pack_by_owner on another;
   by_owner=True:  grad_coalesce_by_owner (coalesce and pack in one), its sort
-                  on one side stream and its reduction on another.
+                  on one side stream and its reduction on another;
+  split=True:     as by_owner, with the prior / delayed split of Vertical
+                  Sparse Scheduling (grad_coalesce_split, given the next
+                  batch's ids): the prior rows are updated right after the
+                  lookup, the delayed rows on a third side stream beside the
+                  next lookup.
 The executor adds the event waits that keep every data dependency (see
 emb_train_step in include/emb.h).  This module only allocates the buffers,
 alternates the two buffer sets and fills in the arguments.
@@ -20,9 +25,11 @@ import ctypes
 
 import torch
 
-from . import (EMB_BF16, EMB_F32, Event, StepArgs, StepSchedule, _check, grad_coalesce_workspace_bytes, lib,
+from . import (EMB_BF16, EMB_F32, Event, StepArgs, StepSchedule, _check, grad_coalesce_split_workspace_bytes, lib,
                new_workspace, pack_by_owner_workspace_bytes)
 
+# timing pairs of emb_step_schedule.timing; with the split, "pack" times the
+# prior update and "adam" the delayed one
 STAGES = ("gather", "coalesce", "pack", "adam")
 
 
@@ -44,12 +51,13 @@ class EmbeddingTable:
         self.coals = [(torch.empty(T_cap, dtype=i32, device=dev), torch.empty(T_cap + 1, dtype=i32, device=dev),
                        torch.empty((T_cap, self.D), dtype=f32, device=dev), torch.empty(1, dtype=i32, device=dev))
                       for _ in range(2)]
+        # send counts / offsets sized for the 2P groups of the split
         self.send = [(torch.empty(T_cap, dtype=i32, device=dev), torch.empty((T_cap, self.D), dtype=f32, device=dev),
-                      torch.empty(P, dtype=i32, device=dev), torch.empty(P + 1, dtype=i32, device=dev))
+                      torch.empty(2 * P, dtype=i32, device=dev), torch.empty(2 * P + 1, dtype=i32, device=dev))
                      for _ in range(2)]
         self.coal = self.coals[0]
         self.grad_code = EMB_BF16 if grad_dtype == torch.bfloat16 else EMB_F32
-        nb = grad_coalesce_workspace_bytes(T_cap, self.V, self.D, self.grad_code)
+        nb = grad_coalesce_split_workspace_bytes(T_cap, T_cap, self.V, self.D, self.grad_code)  # serves every variant
         self.ws_coalesces = [new_workspace(nb, dev) for _ in range(2)]
         self.ws_coalesce = self.ws_coalesces[0]
         self.ws_pack = new_workspace(pack_by_owner_workspace_bytes(T_cap, P), dev)
@@ -63,12 +71,12 @@ _SIDE_STREAMS: dict = {}
 
 
 def side_streams(device=None):
-    """The two side streams of a device, created once per process.  HIP maps
+    """The three side streams of a device, created once per process.  HIP maps
     streams onto a few hardware queues in creation order; creating streams
     once keeps the side streams on queues other than the main stream's."""
     dev = torch.cuda.current_device() if device is None else torch.device(device).index
     if dev not in _SIDE_STREAMS:
-        _SIDE_STREAMS[dev] = (torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev))
+        _SIDE_STREAMS[dev] = tuple(torch.cuda.Stream(device=dev) for _ in range(3))
     return _SIDE_STREAMS[dev]
 
 
@@ -76,17 +84,20 @@ class StepPipeline:
     """Enqueues training steps of the hot path for a list of tables."""
 
     def __init__(self, tables, lr, beta1, beta2, eps, overlap: bool = True, dev_status: torch.Tensor | None = None,
-                 streams: int = 3, by_owner: bool = True):
+                 streams: int = 3, by_owner: bool = True, split: bool = False):
         """streams (with overlap=True and by_owner=False): 2 puts coalesce and pack on one side
         stream, 3 gives each its own (more concurrency, one more cross-stream wait per step).
-        by_owner: coalesce straight into the send layout (emb_grad_coalesce_by_owner)."""
+        by_owner: coalesce straight into the send layout (emb_grad_coalesce_by_owner).
+        split: the prior / delayed split (implies by_owner); step() then needs the next ids."""
         self.tables = list(tables)
         self.overlap = overlap
         self.main = torch.cuda.current_stream()
-        s1, s2 = side_streams()
-        self.by_owner = by_owner
+        s1, s2, s3 = side_streams()
+        self.split = split
+        self.by_owner = by_owner or split
         self.side = s1 if overlap else self.main  # coalesce (by_owner: its sort)
         self.side2 = s2 if (overlap and streams >= 3) else self.side  # pack (by_owner: the reduction)
+        self.side3 = s3 if (overlap and split) else self.main  # the delayed update
         self.count = 0
         self.events = []  # keeps the library events alive
         self.args, self.sched = [], []
@@ -105,30 +116,37 @@ class StepPipeline:
                              ws_coalesce_bytes=tb.ws_coalesces[i].numel(),
                              ws_pack=tb.ws_pack.data_ptr(), ws_pack_bytes=tb.ws_pack.numel(), lr=lr, beta1=beta1,
                              beta2=beta2, eps=eps, dev_status=st)
-                evs = [Event() for _ in range(4)]
+                evs = [Event() for _ in range(6)]
                 self.events += evs
                 s = StepSchedule(lookup_update=_stream_handle(self.main), coalesce=_stream_handle(self.side),
-                                 pack=_stream_handle(self.side2), sorted=evs[0].handle, coalesced=evs[1].handle,
-                                 packed=evs[2].handle, updated=evs[3].handle, by_owner=1 if by_owner else 0)
+                                 pack=_stream_handle(self.side2), delayed=_stream_handle(self.side3),
+                                 sorted=evs[0].handle, coalesced=evs[1].handle, packed=evs[2].handle,
+                                 updated=evs[3].handle, gathered=evs[4].handle, delayed_done=evs[5].handle,
+                                 by_owner=1 if self.by_owner else 0, split=1 if split else 0)
                 args.append(a)
                 scheds.append(s)
             self.args.append(args)
             self.sched.append(scheds)
 
-    def step(self, batches, t: int, timing=None):
+    def step(self, batches, t: int, timing=None, next_ids=None):
         """Enqueue one step.  batches: [(ids int32 [T], grad [T, D]) per table]; t: Adam step (>= 1).
         timing: optional dict stage -> (begin Event, end Event) of library timing events, recorded
         around the calls of the first table on the streams they run on.
-        Inputs must be ready on the main stream when the pipeline's first step is enqueued."""
+        next_ids (split): [ids int32 per table] of the next step's batches (an empty tensor after
+        the last step).  Inputs must be ready on the main stream when the first step is enqueued."""
         i = self.count % 2
         if self.count == 0 and self.overlap:
-            self.side.wait_stream(self.main)
-            if self.side2 is not self.side:
-                self.side2.wait_stream(self.main)
+            for side in {self.side, self.side2, self.side3} - {self.main}:
+                side.wait_stream(self.main)
+        if self.split and (next_ids is None or len(next_ids) != len(batches)):
+            raise ValueError("the split schedule needs the next step's ids of every table")
         for k, (ids, grad) in enumerate(batches):
             a, s = self.args[k][i], self.sched[k][i]
             a.ids = ids.data_ptr()
             a.T = ids.numel()
+            if self.split:
+                a.next_ids = next_ids[k].data_ptr()
+                a.T_next = next_ids[k].numel()
             a.grad = grad.data_ptr()
             a.grad_dtype = EMB_BF16 if grad.dtype == torch.bfloat16 else EMB_F32
             a.step = t
@@ -145,6 +163,5 @@ class StepPipeline:
 
     def finish(self):
         """Make the main stream wait for everything enqueued on the side streams."""
-        self.main.wait_stream(self.side)
-        if self.side2 is not self.side:
-            self.main.wait_stream(self.side2)
+        for side in {self.side, self.side2, self.side3} - {self.main}:
+            self.main.wait_stream(side)

@@ -94,6 +94,24 @@ def test_coalesce_by_owner_validation():
     assert L.emb_grad_coalesce_by_owner(*args(V=(1 << 22) + 1, P=1024, **short)) == emb.EMB_ERR_UNSUPPORTED
 
 
+def test_coalesce_split_validation_and_workspace_query():
+    L = emb.lib
+    need = L.emb_grad_coalesce_split_workspace_bytes(1000, 3000, 5000, 64, emb.EMB_F32)
+    assert need > L.emb_grad_coalesce_workspace_bytes(1000, 5000, 64, emb.EMB_F32) and need % 256 == 0
+    assert L.emb_grad_coalesce_split_workspace_bytes(1000, -1, 5000, 64, emb.EMB_F32) == 0
+    args = lambda T=1000, nxt=FAKE, Tn=3000, V=5000, P=4, own=FAKE, wsb=need: (
+        FAKE, T, nxt, Tn, FAKE, 0, 64, V, own, P, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, wsb, NULL, NULL)
+    assert L.emb_grad_coalesce_split(*args(wsb=need - 1)) == emb.EMB_ERR_WORKSPACE
+    assert L.emb_grad_coalesce_split(*args(Tn=-1)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_split(*args(nxt=NULL)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_split(*args(own=NULL)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_grad_coalesce_split(*args(P=0)) == emb.EMB_ERR_INVALID_ARG
+    # bits(V) + bits(P) + 1 <= 32, checked before the workspace (so nothing launches here)
+    short = dict(wsb=need - 1)
+    assert L.emb_grad_coalesce_split(*args(V=1 << 21, P=1024, **short)) == emb.EMB_ERR_WORKSPACE
+    assert L.emb_grad_coalesce_split(*args(V=(1 << 21) + 1, P=1024, **short)) == emb.EMB_ERR_UNSUPPORTED
+
+
 def test_pack_validation_and_workspace_query():
     L = emb.lib
     need = L.emb_pack_by_owner_workspace_bytes(1000, 16)

@@ -172,3 +172,115 @@ def test_by_owner_key_width_limit_is_unsupported():
     own = torch.zeros(1, dtype=torch.int32, device="cuda")  # never read: the host check fails first
     with pytest.raises(emb.EmbError, match="unsupported"):
         emb.grad_coalesce_by_owner(ids, to_dev(grads_for(1, T, D)), V, own, P)
+
+
+# ------------------------------------------------------ vertical split (Algorithm 1)
+def gpu_split(ids_np, next_np, grad_np, V, own_np, P, grad_dev=None):
+    st = emb.new_status()
+    g = to_dev(grad_np) if grad_dev is None else grad_dev
+    out = emb.grad_coalesce_split(to_dev(ids_np.astype(np.int32)), to_dev(next_np.astype(np.int32)), g, V,
+                                  to_dev(own_np.astype(np.int32)), P, dev_status=st)
+    torch.cuda.synchronize()
+    send_ids, seg, rows, counts, offs, nu = out
+    U = int(nu.item())
+    return dict(U=U, send_ids=host(send_ids[:U]), seg_offsets=host(seg[:U + 1]), send_rows=host(rows[:U]),
+                send_counts=host(counts), send_offsets=host(offs), status=int(st.item()), dev=out)
+
+
+def check_split(ids_np, next_np, grad_np, V, own_np, P, bf16=False):
+    """GPU split vs the oracle's split_pack of its coalesce: ids, counts and offsets bit-exact, rows
+    within the summation bound (bit-exact for one or two tokens), token counts per row exact."""
+    orc = oracle.coalesce(ids_np, grad_np, V, grad_is_bf16=bf16)
+    sp = oracle.split_pack(orc["uniq_ids"], orc["uniq_grad"], next_np, own_np, P)
+    gpu = gpu_split(ids_np, next_np, grad_np, V, own_np, P)
+    n = int(sp["send_offsets"][2 * P])
+    assert gpu["U"] == n, (gpu["U"], n)
+    for k in ("send_ids", "send_counts", "send_offsets"):
+        assert np.array_equal(gpu[k], sp[k]), k
+    idx = np.searchsorted(orc["uniq_ids"], sp["send_ids"])
+    tolerance.assert_grad_close(gpu["send_rows"], orc["sum_f64"][idx], orc["absum"][idx], tolerance.RTOL_F32)
+    seglen = np.diff(orc["seg_offsets"])[idx]
+    assert gpu["seg_offsets"][0] == 0 and np.array_equal(np.diff(gpu["seg_offsets"]), seglen)
+    short = seglen <= 2
+    assert np.array_equal(gpu["send_rows"][short].view(np.uint32), orc["uniq_grad"][idx][short].view(np.uint32))
+    return gpu, sp
+
+
+@pytest.mark.parametrize("law,V,T,D,P,rule", [
+    ("zipf", 1000, 512, 64, 2, "mod"),            # the tiny workload's shape
+    ("zipf", 32768, 25000, 64, 4, "range"),       # shared-vocab shape, narrower rows
+    ("uniform", 1 << 20, 20000, 16, 16, "mod"),   # 20 + 4 + 1 key bits: four passes
+    ("zipf", 5000, 2049, 3, 7, "rand"),           # ragged tile, scalar width path
+    ("zipf", 1, 777, 4, 1, "mod"),                # V = 1, P = 1: keys 0 and 1 only
+    ("uniform", 50000, 9000, 20, 1024, "mod"),    # the most owners: 16 + 10 + 1 key bits
+    ("uniform", (1 << 21) - 1, 9000, 4, 1024, "rand"),  # 21 + 10 + 1 = 32 key bits
+])
+def test_split_parity(law, V, T, D, P, rule):
+    ids = ids_for(law, V + T + P, T, V)
+    nxt = ids_for(law, V + T + P + 1, T, V)
+    check_split(ids, nxt, grads_for(V + D, T, D), V, owners(rule, V, P, seed=T), P)
+
+
+def test_split_lowdup_full_size():
+    V, T, D, P = 1 << 20, 65536, 256, 16
+    ids, nxt = ids_for("uniform", 51, T, V), ids_for("uniform", 52, T, V)
+    gpu, sp = check_split(ids, nxt, grads_for(51, T, D, 0.01), V, gen.owner_mod(V, P), P)
+    assert 0 < sp["n_prior"] < gpu["U"]
+
+
+def test_split_bf16():
+    V, T, D, P = 262144, 16384, 1024, 8
+    ids, nxt = ids_for("zipf", 4, T, V, 1.0), ids_for("zipf", 5, T, V, 1.0)
+    check_split(ids, nxt, grads_for(4, T, D, 0.01, bf16=True), V, gen.owner_range(V, P), P, bf16=True)
+
+
+@pytest.mark.parametrize("case", ["same", "disjoint", "empty", "not_rows", "longer"])
+def test_split_degenerate_next_batches(case):
+    V, T, D, P = 3000, 4000, 8, 5
+    ids = ids_for("zipf", 8, T, V)
+    nxt = {"same": ids[::-1].copy(),
+           "disjoint": np.setdiff1d(np.arange(V, dtype=np.int32), ids).astype(np.int32),
+           "empty": np.zeros(0, np.int32), "not_rows": np.array([-5, V, V + 1, 1 << 30], np.int32),
+           "longer": ids_for("uniform", 9, 3 * T, V)}[case]
+    gpu, sp = check_split(ids, nxt, grads_for(8, T, D), V, gen.owner_mod(V, P), P)
+    if case == "same":
+        assert sp["n_prior"] == gpu["U"]
+    if case in ("disjoint", "empty", "not_rows"):
+        assert sp["n_prior"] == 0
+
+
+def test_split_bad_ids_and_owners_are_left_out():
+    V, T, D, P = 1000, 3000, 16, 4
+    ids = ids_for("zipf", 9, T, V)
+    ids[::97] = -3
+    nxt = ids_for("zipf", 10, T, V)
+    own = gen.owner_mod(V, P)
+    own[[0, 1, 500]] = [P, -1, P + 3]
+    gpu, _ = check_split(ids, nxt, grads_for(9, T, D), V, own, P)
+    assert gpu["status"] == emb.EMB_DEV_ID_OUT_OF_RANGE | emb.EMB_DEV_OWNER_OUT_OF_RANGE
+
+
+def test_split_empty_batch():
+    P = 3
+    gpu = gpu_split(np.zeros(0, np.int32), np.arange(5, dtype=np.int32), np.zeros((0, 4), np.float32), 50,
+                    gen.owner_mod(50, P), P)
+    assert gpu["U"] == 0 and gpu["send_offsets"].tolist() == [0] * (2 * P + 1)
+    assert gpu["send_counts"].tolist() == [0] * (2 * P) and gpu["status"] == 0
+
+
+def test_split_key_width_limit_is_unsupported():
+    # bits(V) + bits(P) + 1 = 22 + 10 + 1 > 32: refused on the host
+    V, P, T, D = (1 << 22) - 1, 1024, 16, 4
+    ids = to_dev(np.arange(T, dtype=np.int32))
+    own = torch.zeros(1, dtype=torch.int32, device="cuda")  # never read
+    with pytest.raises(emb.EmbError, match="unsupported"):
+        emb.grad_coalesce_split(ids, ids, to_dev(grads_for(1, T, D)), V, own, P)
+
+
+def test_split_hash_set_path_for_huge_tables():
+    # above 2^27 rows the next-batch set is a hash set instead of a bitmap over the rows
+    V, T, D, P = (1 << 27) + 5, 5000, 4, 4
+    ids = ids_for("uniform", 71, T, V)
+    nxt = np.concatenate([ids[: T // 3], ids_for("uniform", 72, T, V)]).astype(np.int32)
+    gpu, sp = check_split(ids, nxt, grads_for(71, T, D), V, gen.owner_mod(V, P), P)
+    assert 0 < sp["n_prior"] < gpu["U"]

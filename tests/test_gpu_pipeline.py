@@ -1,7 +1,8 @@
 """The overlapped step schedules give bitwise the same table, moments and
 lookups as running their calls one after another on one stream; the
 owner-major schedule (coalesce straight into the send layout) agrees with
-coalesce-then-pack to the fp32 tolerance (its sums add in another order)."""
+coalesce-then-pack, and the prior / delayed split with one update, to the
+fp32 tolerance (their sums add in another grouping)."""
 import numpy as np
 import pytest
 import torch
@@ -13,7 +14,7 @@ from workloads import configs, gen
 pytestmark = pytest.mark.gpu
 
 
-def run(overlap, by_owner, steps=7):
+def run(overlap, by_owner, steps=7, split=False):
     torch.cuda.synchronize()
     specs = [configs.TableSpec(20000, 128, 6000, "zipf", 1.05, "f32", 0.01, 8, "mod", 61),
              configs.TableSpec(5000, 64, 3000, "uniform", 0.0, "bf16", 0.01, 3, "range", 62)]
@@ -31,10 +32,12 @@ def run(overlap, by_owner, steps=7):
             per.append((torch.from_numpy(ids).cuda(), g))
         batches.append(per)
     torch.cuda.synchronize()
-    pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner)
+    pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner, split=split)
     lookups = []
+    empty = torch.zeros(0, dtype=torch.int32, device="cuda")
     for t in range(1, steps + 1):
-        pipe.step([batches[k][t % 3] for k in range(len(specs))], t)
+        nxt = [batches[k][(t + 1) % 3][0] if t < steps else empty for k in range(len(specs))]
+        pipe.step([batches[k][t % 3] for k in range(len(specs))], t, next_ids=nxt if split else None)
         # the lookup of step t is read on the main stream before step t+1's lookup overwrites it
         lookups.append([tb.lookup[: batches[k][t % 3][0].numel()].clone() for k, tb in enumerate(tables)])
     pipe.finish()
@@ -43,10 +46,10 @@ def run(overlap, by_owner, steps=7):
            [[x.cpu().numpy() for x in l] for l in lookups]
 
 
-@pytest.mark.parametrize("by_owner", [False, True])
-def test_overlapped_schedule_equals_sequential(by_owner):
-    a, la = run(True, by_owner)
-    b, lb = run(False, by_owner)
+@pytest.mark.parametrize("by_owner,split", [(False, False), (True, False), (True, True)])
+def test_overlapped_schedule_equals_sequential(by_owner, split):
+    a, la = run(True, by_owner, split=split)
+    b, lb = run(False, by_owner, split=split)
     for x, y in zip(a, b):
         for u, v in zip(x, y):
             assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
@@ -58,6 +61,20 @@ def test_overlapped_schedule_equals_sequential(by_owner):
 def test_owner_major_schedule_matches_coalesce_then_pack():
     a, la = run(True, True)
     b, lb = run(False, False)
+    for x, y in zip(a, b):
+        for u, v, name in zip(x, y, ("table", "exp_avg", "exp_avg_sq")):
+            tolerance.assert_rows_close(u, v, tolerance.RTOL_F32, name)
+    for x, y in zip(la, lb):
+        for u, v in zip(x, y):
+            tolerance.assert_rows_close(u, v, tolerance.RTOL_F32, "lookup")
+
+
+def test_split_schedule_matches_one_update():
+    """The prior and delayed updates of the split (same step t) give the table of one update on all
+    rows, to the fp32 tolerance: each row gets the same Adam arithmetic, and only the grouping of
+    the fp32 additions of a row's gradient sum follows the (split) sorted positions."""
+    a, la = run(True, True, split=True)
+    b, lb = run(False, True, split=False)
     for x, y in zip(a, b):
         for u, v, name in zip(x, y, ("table", "exp_avg", "exp_avg_sq")):
             tolerance.assert_rows_close(u, v, tolerance.RTOL_F32, name)
