@@ -144,7 +144,7 @@ def _find(directory, suffix):
     raise FileNotFoundError(f"no *{suffix} under {directory}")
 
 
-def summarize_trace(directory, command, warmup=10, steps=50):
+def summarize_trace(directory, command, warmup=20, steps=200):
     """Text summary of a rocprofv3 --kernel-trace --stats run (kernel_stats.csv), plus the
     average duration of the update kernel over the timed steps of the bench run (its
     dispatches warmup+1 .. warmup+steps in launch order, from kernel_trace.csv)."""
@@ -231,7 +231,7 @@ def main():
     ap.add_argument("--command2", default="", help="the second command recorded in a summary")
     args = ap.parse_args()
     if args.summarize_trace:
-        print(summarize_trace(args.summarize_trace, args.command), end="")
+        print(summarize_trace(args.summarize_trace, args.command, args.warmup, args.steps), end="")
         return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc, args.command, args.command2), indent=1))

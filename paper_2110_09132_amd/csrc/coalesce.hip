@@ -88,9 +88,9 @@ struct KeySpec {
   uint32_t id_mask;          // key -> id
   uint32_t omask;            // (key >> ib) & omask -> owner
   int cls_shift;             // key >> cls_shift -> class (32: no class bit)
-  const uint32_t* next_tab;  // set of the next batch's ids (nullptr: no split): a bitmap over
-                             // [0, V) (next_bitmap), else a hash set of 2^(32 - tab_shift) slots
-  bool next_bitmap;
+  const uint32_t* next_tab;  // set of the next batch's ids (nullptr: no split): one byte per
+                             // row of [0, V) (next_bytemap), else a hash set of 2^(32 - tab_shift) slots
+  bool next_bytemap;
   int tab_shift;
   int G;                     // groups of the output: owners, times 2 with the split
 };
@@ -104,7 +104,7 @@ __device__ __forceinline__ int group_of(uint32_t key, const KeySpec& ks) {
 __device__ __forceinline__ uint32_t tab_slot(uint32_t id, int shift) { return (id * 0x9E3779B1u) >> shift; }
 
 __device__ __forceinline__ bool in_next(uint32_t id, const KeySpec& ks) {
-  if (ks.next_bitmap) return (ks.next_tab[id >> 5] >> (id & 31u)) & 1u;
+  if (ks.next_bytemap) return reinterpret_cast<const uint8_t*>(ks.next_tab)[id] != 0;
   const uint32_t mask = 0xFFFFFFFFu >> ks.tab_shift;
   uint32_t slot = tab_slot(id, ks.tab_shift);
   for (uint32_t probe = 0; probe <= mask; ++probe) {
@@ -120,20 +120,42 @@ __global__ __launch_bounds__(kThreads) void tab_clear_kernel(uint32_t* __restric
   for (int i = blockIdx.x * kThreads + threadIdx.x; i < n; i += gridDim.x * kThreads) tab[i] = 0;
 }
 
-// Inserts the in-range ids of the next batch: bits of a bitmap (atomics whose
-// result is not needed, so they do not wait), or slots of the hash set (at
-// most half full, so every insertion finds a free slot).
+// Inserts the in-range ids of the next batch.  Byte map: a plain byte store
+// per id (setting a byte needs no read-modify-write, so repeated ids, the hot
+// rows of a skewed batch, do not queue on one atomic).  Hash set (at most half
+// full, so every insertion finds a free slot): each workgroup first drops the
+// repeats among its own ids with a small LDS set, so that hot ids do not pile
+// their atomics onto one slot.
+constexpr int kLdsSlots = 1024;  // a power of two, 4x the ids of a workgroup (slot = 10 hash bits)
+static_assert(kLdsSlots == 4 * kThreads, "the LDS set holds four slots per id");
+
 __global__ __launch_bounds__(kThreads) void tab_insert_kernel(const int32_t* __restrict__ next_ids, int T_next,
-                                                              uint32_t V, uint32_t* __restrict__ tab, bool bitmap,
+                                                              uint32_t V, uint32_t* __restrict__ tab, bool bytemap,
                                                               int shift) {
+  __shared__ uint32_t local[kLdsSlots];
   const int t = blockIdx.x * kThreads + threadIdx.x;
-  if (t >= T_next) return;
-  const int32_t id = next_ids[t];
-  if (id < 0 || static_cast<uint32_t>(id) >= V) return;
-  if (bitmap) {
-    atomicOr(&tab[static_cast<uint32_t>(id) >> 5], 1u << (static_cast<uint32_t>(id) & 31u));
+  const int32_t id = next_ids[min(t, T_next - 1)];
+  bool first = t < T_next && id >= 0 && static_cast<uint32_t>(id) < V;
+  if (bytemap) {
+    if (first) reinterpret_cast<uint8_t*>(tab)[id] = 1;
     return;
   }
+  for (int i = threadIdx.x; i < kLdsSlots; i += kThreads) local[i] = 0;
+  __syncthreads();
+  if (first) {  // the first thread of the workgroup to insert this id carries it on
+    const uint32_t key = static_cast<uint32_t>(id) + 1u;
+    uint32_t slot = tab_slot(static_cast<uint32_t>(id), 32 - 10) & (kLdsSlots - 1);
+    for (int probe = 0; probe < kLdsSlots; ++probe) {
+      const uint32_t old = atomicCAS(&local[slot], 0u, key);
+      if (old == 0u) break;
+      if (old == key) {
+        first = false;
+        break;
+      }
+      slot = (slot + 1) & (kLdsSlots - 1);
+    }
+  }
+  if (!first) return;
   const uint32_t mask = 0xFFFFFFFFu >> shift;
   uint32_t slot = tab_slot(static_cast<uint32_t>(id), shift);
   for (uint32_t probe = 0; probe <= mask; ++probe) {
@@ -269,7 +291,7 @@ KeySpec key_spec(int64_t V, const int32_t* row_owner, int P, bool split) {
   ks.omask = static_cast<uint32_t>((uint64_t{1} << ks.ob) - 1);
   ks.cls_shift = (own && split) ? ks.ib + ks.ob : 32;
   ks.next_tab = nullptr;
-  ks.next_bitmap = false;
+  ks.next_bytemap = false;
   ks.tab_shift = 32;
   ks.G = (own && split) ? 2 * P : ks.P;
   return ks;
@@ -695,7 +717,7 @@ struct CoalesceWs {
   float* partial;
   uint32_t* next_tab;    // vertical split: set of the next batch's ids [tab_words]
   int tab_words;
-  bool tab_bitmap;       // a bitmap over [0, V); else a hash set of 2^(32 - tab_shift) slots
+  bool tab_bytemap;      // a byte per row of [0, V); else a hash set of 2^(32 - tab_shift) slots
   int tab_shift;
   size_t bytes;
 };
@@ -706,10 +728,10 @@ int tab_log2_slots(int T_next) {  // at least twice the ids, at least 64 slots
   return lg;
 }
 
-// The set of next ids is a bitmap over the rows (one load per lookup, inserts
-// that do not wait) unless the table is so large that clearing V bits per
-// call would cost more than it saves.
-constexpr int64_t kBitmapMaxRows = int64_t{1} << 27;
+// The set of next ids is a byte per row (one load per lookup, one plain store
+// per insert) unless the table is so large that clearing V bytes per call
+// would cost more than the hash set.
+constexpr int64_t kBytemapMaxRows = int64_t{1} << 24;
 
 // The layout does not depend on the number of radix passes (sized for the
 // most), so one size serves the plain and the owner-major call; the split
@@ -737,12 +759,12 @@ CoalesceWs carve_with(void* base, int T, int D, int T_next, int64_t V) {
   w.partial = cv.take<float>(nchunks * 2 * static_cast<size_t>(D));
   w.next_tab = nullptr;
   w.tab_words = 0;
-  w.tab_bitmap = false;
+  w.tab_bytemap = false;
   w.tab_shift = 32;
   if (T_next >= 0) {
-    w.tab_bitmap = V <= kBitmapMaxRows;
-    if (w.tab_bitmap) {
-      w.tab_words = static_cast<int>((V + 31) / 32);
+    w.tab_bytemap = V <= kBytemapMaxRows;
+    if (w.tab_bytemap) {
+      w.tab_words = static_cast<int>((V + 3) / 4);
     } else {
       const int lg = tab_log2_slots(T_next);
       w.tab_words = 1 << lg;
@@ -818,9 +840,9 @@ hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, con
                        dim3(kThreads), 0, stream, ws.next_tab, ws.tab_words);
     if (var.T_next > 0)
       hipLaunchKernelGGL(tab_insert_kernel, dim3((var.T_next + kThreads - 1) / kThreads), dim3(kThreads), 0, stream,
-                         var.next_ids, var.T_next, ks.V, ws.next_tab, ws.tab_bitmap, ws.tab_shift);
+                         var.next_ids, var.T_next, ks.V, ws.next_tab, ws.tab_bytemap, ws.tab_shift);
     ks.next_tab = ws.next_tab;
-    ks.next_bitmap = ws.tab_bitmap;
+    ks.next_bytemap = ws.tab_bytemap;
     ks.tab_shift = ws.tab_shift;
   }
   // 1. the key of every token (owner and next-batch lookups once)

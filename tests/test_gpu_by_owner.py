@@ -278,9 +278,12 @@ def test_split_key_width_limit_is_unsupported():
 
 
 def test_split_hash_set_path_for_huge_tables():
-    # above 2^27 rows the next-batch set is a hash set instead of a bitmap over the rows
-    V, T, D, P = (1 << 27) + 5, 5000, 4, 4
+    # above 2^24 rows the next-batch set is a hash set instead of a byte per row
+    V, T, D, P = (1 << 24) + 5, 5000, 4, 4
     ids = ids_for("uniform", 71, T, V)
     nxt = np.concatenate([ids[: T // 3], ids_for("uniform", 72, T, V)]).astype(np.int32)
     gpu, sp = check_split(ids, nxt, grads_for(71, T, D), V, gen.owner_mod(V, P), P)
     assert 0 < sp["n_prior"] < gpu["U"]
+    # hot rows repeated across the whole next batch (the per-workgroup LDS set drops repeats)
+    nxt2 = np.concatenate([np.repeat(ids[:7], 3000), ids_for("zipf", 73, T, V, 1.3)]).astype(np.int32)
+    check_split(ids, nxt2, grads_for(72, T, D), V, gen.owner_mod(V, P), P)
