@@ -202,6 +202,44 @@ int emb_grad_coalesce_split(const int32_t *ids, int32_t T,
                             int32_t *dev_status, void *stream);
 
 /*
+ * The receiver side of the sparse-gradient AlltoAll (Sec. 4.1.1 / 4.1.2: every
+ * worker sends each owner the coalesced rows it owns; an owner then sums the
+ * rows it received for the same index), simulated on this device for P
+ * workers whose send layouts sit side by side:
+ *   send_ids [P][cap_rows], send_rows [P][cap_rows][D], send_offsets [P][P + 1]:
+ *   worker w's rows for owner p at [send_offsets[w][p], send_offsets[w][p + 1])
+ *   of its own block (the layout of emb_grad_coalesce_by_owner / emb_pack_by_owner).
+ * emb_exchange_simulated moves every block to its receiver (a P x P block
+ * transpose; rows are bit copies):
+ *   recv_offsets [P][P + 1]: owner p receives worker w's rows at
+ *   [recv_offsets[p][w], recv_offsets[p][w + 1]), and all its rows end at
+ *   recv_offsets[p][P]; receivers follow each other (owner-major).
+ *   recv_ids [P * cap_rows], recv_rows [P * cap_rows][D]; recv_total [1] = rows received.
+ * Offsets are clamped into [0, cap_rows]; rows outside a worker's blocks are
+ * not sent.  Requires 1 <= P <= 1024, P * cap_rows < 2^30.
+ *
+ * emb_receive_merge then coalesces the received rows of every owner (their
+ * ids can repeat across senders): emb_grad_coalesce_by_owner over the first
+ * *recv_total of the cap received rows (fp32), with the same outputs, rules
+ * and workspace (emb_grad_coalesce_workspace_bytes(cap, V, D, EMB_F32)).  Rows
+ * of one index are summed in sender order.  The result equals the owner-major
+ * coalesce of all workers' tokens together (to the fp32 summation bound).
+ */
+int emb_exchange_simulated(const int32_t *send_ids, const float *send_rows,
+                           const int32_t *send_offsets, int32_t P,
+                           int32_t cap_rows, int32_t D, int32_t *recv_ids,
+                           float *recv_rows, int32_t *recv_offsets,
+                           int32_t *recv_total, void *stream);
+int emb_receive_merge(const int32_t *recv_ids, const float *recv_rows,
+                      const int32_t *recv_total, int32_t cap, int32_t D,
+                      int64_t V, const int32_t *row_owner, int32_t P,
+                      int32_t *merged_ids, int32_t *seg_offsets,
+                      float *merged_rows, int32_t *merged_counts,
+                      int32_t *merged_offsets, int32_t *num_unique,
+                      void *workspace, size_t workspace_bytes,
+                      int32_t *dev_status, void *stream);
+
+/*
  * Row-wise (lazy) Adam on received rows (Sec. 4.1.1: each process updates its
  * embedding rows with the exchanged gradients; Sec. 5.7: Adam with a global
  * step counter that the caller owns and advances once per iteration).

@@ -42,6 +42,9 @@ SIGNATURES = {
     "emb_grad_coalesce_split_workspace_bytes": (_SZ, [_I32, _I32, _I64, _I32, _I32]),
     "emb_grad_coalesce_split": (ctypes.c_int, [_P, _I32, _P, _I32, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P,
                                                _P, _P, _SZ, _P, _P]),
+    "emb_exchange_simulated": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]),
+    "emb_receive_merge": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                                         _P, _P]),
     "emb_pack_by_owner_workspace_bytes": (_SZ, [_I32, _I32]),
     "emb_pack_by_owner": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_sparse_adam_apply": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _P, _P, _P, _I32, _I32, _I32, _I32,
@@ -257,6 +260,54 @@ def grad_coalesce_split(ids, next_ids, grad, V, row_owner, P, out=None, workspac
                                        _ptr(send_counts), _ptr(send_offsets), _ptr(num_unique), _ptr(workspace),
                                        workspace.numel(), _ptr(dev_status), _stream(stream)),
            "emb_grad_coalesce_split")
+    return out
+
+
+def exchange_simulated(send_ids, send_rows, send_offsets, out=None, stream=None):
+    """Simulated AlltoAll of P workers' send layouts (emb_exchange_simulated).
+
+    send_ids [P, cap], send_rows [P, cap, D], send_offsets [P, P+1].  Returns (recv_ids [P*cap],
+    recv_rows [P*cap, D], recv_offsets [P, P+1], recv_total [1])."""
+    _need(send_ids, torch.int32, "send_ids")
+    _need(send_rows, torch.float32, "send_rows")
+    _need(send_offsets, torch.int32, "send_offsets")
+    P, cap = send_ids.shape
+    D = send_rows.shape[-1]
+    dev = send_ids.device
+    if out is None:
+        out = (torch.empty(P * cap, dtype=torch.int32, device=dev),
+               torch.empty((P * cap, D), dtype=torch.float32, device=dev),
+               torch.empty((P, P + 1), dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
+    recv_ids, recv_rows, recv_offsets, recv_total = out
+    _check(lib.emb_exchange_simulated(_ptr(send_ids), _ptr(send_rows), _ptr(send_offsets), P, cap, D, _ptr(recv_ids),
+                                      _ptr(recv_rows), _ptr(recv_offsets), _ptr(recv_total), _stream(stream)),
+           "emb_exchange_simulated")
+    return out
+
+
+def receive_merge(recv_ids, recv_rows, recv_total, V, row_owner, P, out=None, workspace=None, dev_status=None,
+                  stream=None):
+    """Owner-major coalesce of the first recv_total received rows (emb_receive_merge).
+
+    Returns (merged_ids, seg_offsets, merged_rows, merged_counts [P], merged_offsets [P+1], num_unique)."""
+    _need(recv_ids, torch.int32, "recv_ids")
+    _need(recv_rows, torch.float32, "recv_rows")
+    _need(recv_total, torch.int32, "recv_total")
+    _need(row_owner, torch.int32, "row_owner")
+    cap = recv_ids.numel()
+    D = recv_rows.shape[1]
+    dev = recv_ids.device
+    if out is None:
+        out = (torch.empty(cap, dtype=torch.int32, device=dev), torch.empty(cap + 1, dtype=torch.int32, device=dev),
+               torch.empty((cap, D), dtype=torch.float32, device=dev), torch.empty(P, dtype=torch.int32, device=dev),
+               torch.empty(P + 1, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
+    merged_ids, seg, rows, counts, offs, nu = out
+    if workspace is None:
+        workspace = new_workspace(grad_coalesce_workspace_bytes(cap, V, D, EMB_F32), dev)
+    _check(lib.emb_receive_merge(_ptr(recv_ids), _ptr(recv_rows), _ptr(recv_total), cap, D, V, _ptr(row_owner), P,
+                                 _ptr(merged_ids), _ptr(seg), _ptr(rows), _ptr(counts), _ptr(offs), _ptr(nu),
+                                 _ptr(workspace), workspace.numel(), _ptr(dev_status), _stream(stream)),
+           "emb_receive_merge")
     return out
 
 

@@ -164,6 +164,36 @@ int emb_grad_coalesce_split(const int32_t* ids, int32_t T, const int32_t* next_i
                                             static_cast<hipStream_t>(stream)));
 }
 
+int emb_exchange_simulated(const int32_t* send_ids, const float* send_rows, const int32_t* send_offsets, int32_t P,
+                           int32_t cap_rows, int32_t D, int32_t* recv_ids, float* recv_rows, int32_t* recv_offsets,
+                           int32_t* recv_total, void* stream) {
+  if (P < 1 || P > kMaxOwners || cap_rows < 0 || D < 1) return EMB_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(P) * cap_rows >= (int64_t{1} << 30)) return EMB_ERR_INVALID_ARG;
+  if (!send_offsets || !recv_offsets || !recv_total) return EMB_ERR_INVALID_ARG;
+  if (cap_rows > 0 && (!send_ids || !send_rows || !recv_ids || !recv_rows)) return EMB_ERR_INVALID_ARG;
+  return launch_status(emb::launch_exchange(send_ids, send_rows, send_offsets, P, cap_rows, D, recv_ids, recv_rows,
+                                            recv_offsets, recv_total, static_cast<hipStream_t>(stream)));
+}
+
+int emb_receive_merge(const int32_t* recv_ids, const float* recv_rows, const int32_t* recv_total, int32_t cap,
+                      int32_t D, int64_t V, const int32_t* row_owner, int32_t P, int32_t* merged_ids,
+                      int32_t* seg_offsets, float* merged_rows, int32_t* merged_counts, int32_t* merged_offsets,
+                      int32_t* num_unique, void* workspace, size_t workspace_bytes, int32_t* dev_status,
+                      void* stream) {
+  if (!recv_total) return EMB_ERR_INVALID_ARG;
+  const int st = emb::coalesce_by_owner_args_status(recv_ids, cap, recv_rows, EMB_F32, D, V, row_owner, P, nullptr,
+                                                    -1, merged_ids, seg_offsets, merged_rows, merged_counts,
+                                                    merged_offsets, num_unique, workspace, workspace_bytes);
+  if (st != EMB_OK) return st;
+  emb::CoalesceVariant var;
+  var.row_owner = row_owner;
+  var.P = P;
+  var.count_dev = recv_total;
+  return launch_status(emb::launch_coalesce(recv_ids, cap, recv_rows, false, D, V, var, merged_ids, seg_offsets,
+                                            merged_rows, num_unique, merged_counts, merged_offsets, workspace,
+                                            dev_status, static_cast<hipStream_t>(stream)));
+}
+
 size_t emb_pack_by_owner_workspace_bytes(int32_t cap_rows, int32_t P) {
   if (cap_rows < 0 || P < 1 || P > kMaxOwners) return 0;
   return emb::pack_workspace_bytes(cap_rows, P);

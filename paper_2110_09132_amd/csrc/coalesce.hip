@@ -93,6 +93,7 @@ struct KeySpec {
   bool next_bytemap;
   int tab_shift;
   int G;                     // groups of the output: owners, times 2 with the split
+  const int32_t* count_dev;  // if given: only the first *count_dev tokens take part
 };
 
 __device__ __forceinline__ int group_of(uint32_t key, const KeySpec& ks) {
@@ -174,6 +175,7 @@ __global__ __launch_bounds__(kThreads) void make_keys_kernel(const int32_t* __re
                                                              uint32_t* __restrict__ keys, int32_t* __restrict__ vals,
                                                              int32_t* status) {
   const int base = blockIdx.x * kThreads * kKeysPerThread + static_cast<int>(threadIdx.x);
+  const int Tc = ks.count_dev != nullptr ? min(max(*ks.count_dev, 0), T) : T;  // tokens that exist
   int32_t id[kKeysPerThread];
   bool idok[kKeysPerThread];
 #pragma unroll
@@ -191,14 +193,14 @@ __global__ __launch_bounds__(kThreads) void make_keys_kernel(const int32_t* __re
 #pragma unroll
   for (int r = 0; r < kKeysPerThread; ++r) {
     const int t = base + r * kThreads;
-    const bool inb = t < T;
+    const bool inb = t < Tc;
     const bool ownok = own[r] < static_cast<uint32_t>(ks.P);
     const bool take = inb && idok[r] && ownok;
     bad_id |= inb && !idok[r];
     bad_owner |= inb && idok[r] && !ownok;
     uint32_t key = (own[r] << ks.ib) | static_cast<uint32_t>(id[r]);
     if (ks.next_tab != nullptr && take && !in_next(static_cast<uint32_t>(id[r]), ks)) key |= 1u << ks.cls_shift;
-    if (inb) {
+    if (t < T) {
       keys[t] = key;
       vals[t] = take ? t : -1;
     }
@@ -294,6 +296,7 @@ KeySpec key_spec(int64_t V, const int32_t* row_owner, int P, bool split) {
   ks.next_bytemap = false;
   ks.tab_shift = 32;
   ks.G = (own && split) ? 2 * P : ks.P;
+  ks.count_dev = nullptr;
   return ks;
 }
 
@@ -832,9 +835,10 @@ hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, con
   if (T == 0) return hipSuccess;
   CoalesceWs ws = carve(workspace, T, D, is_split(var) ? var.T_next : -1, V);
   KeySpec ks = key_spec(V, var.row_owner, var.P, is_split(var));
+  ks.count_dev = var.count_dev;
   const RadixPlan plan = plan_for_call(V, var);
   const int nred = (T + kRedTile - 1) / kRedTile;
-  // 0. the next batch's ids into a hash set (vertical split)
+  // 0. the next batch's ids into a set (vertical split)
   if (is_split(var)) {
     hipLaunchKernelGGL(tab_clear_kernel, dim3(grid_for((ws.tab_words + kThreads - 1) / kThreads, 1024)),
                        dim3(kThreads), 0, stream, ws.next_tab, ws.tab_words);

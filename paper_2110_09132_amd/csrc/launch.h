@@ -21,6 +21,7 @@ struct CoalesceVariant {
   int P = 1;
   const int32_t* next_ids = nullptr;
   int T_next = -1;
+  const int32_t* count_dev = nullptr;  // if given: only the first *count_dev of the T tokens take part
 };
 
 // Workspace size (T_next < 0: no split); it does not depend on the other choices.
@@ -49,6 +50,12 @@ int coalesce_by_owner_args_status(const int32_t* ids, int32_t T, const void* gra
                                   int32_t T_next, const int32_t* send_ids, const int32_t* seg_offsets,
                                   const float* send_rows, const int32_t* send_counts, const int32_t* send_offsets,
                                   const int32_t* num_unique, const void* workspace, size_t workspace_bytes);
+
+// The simulated AlltoAll of P workers' send layouts (send_* of worker w at
+// w * cap_rows): receiver-major blocks, senders in order inside a receiver.
+hipError_t launch_exchange(const int32_t* send_ids, const float* send_rows, const int32_t* send_offsets, int P,
+                           int cap, int D, int32_t* recv_ids, float* recv_rows, int32_t* recv_offsets,
+                           int32_t* recv_total, hipStream_t stream);
 
 size_t pack_workspace_bytes(int cap_rows, int P);
 hipError_t launch_pack(const int32_t* uniq_ids, const float* uniq_grad, const int32_t* num_unique, int cap_rows,

@@ -285,6 +285,29 @@ def pin_split_two_applies():
         assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
 
 
+# ------------------------------------------------ receiver side of the exchange
+def pin_concat_coalesce_is_sum_of_workers():
+    """The exchange delivers every worker's coalesced rows to their owner, who sums the rows of
+    one index (Sec. 4.1.1 / 4.1.2).  So the merged result is the coalesce of all workers' tokens
+    together: its ids are the union of the workers' ids, and each fp64 sum is the sum of the
+    workers' fp64 sums (checked here on the oracle; the GPU merge is compared with it)."""
+    V, D, T, P = 300, 3, 500, 4
+    ids = [_rng_ids(600 + w, T, V) for w in range(P)]
+    grads = [_rng_normal(700 + w, T * D).reshape(T, D) for w in range(P)]
+    parts = [oracle.coalesce(i, g, V) for i, g in zip(ids, grads)]
+    whole = oracle.coalesce(np.concatenate(ids), np.concatenate(grads), V)
+    union = sorted(set().union(*(set(c["uniq_ids"].tolist()) for c in parts)))
+    assert whole["uniq_ids"].tolist() == union
+    acc = {u: np.zeros(D) for u in union}
+    for c in parts:
+        for k, u in enumerate(c["uniq_ids"].tolist()):
+            acc[u] += c["sum_f64"][k]
+    ref = np.array([acc[u] for u in union])
+    assert np.allclose(whole["sum_f64"], ref, rtol=1e-12, atol=1e-12)
+    counts = np.bincount(np.concatenate(ids), minlength=V)
+    assert np.array_equal(np.diff(whole["seg_offsets"]), counts[whole["uniq_ids"]])
+
+
 # ----------------------------------------------------------------------- adam
 def _adam_tables(V, D, seed):
     W = _rng_normal(seed, V * D, purpose=gen.PURPOSE_WEIGHTS).reshape(V, D)
