@@ -13,6 +13,12 @@
  *   emb_sparse_adam_apply  row-wise Adam on the rows a shard owns   (Sec. 4.1.1,
  *                          Sec. 5.7)
  *
+ * with, around them: the owner-major coalesce that writes the send layout
+ * directly, and its prior/delayed split (Algorithm 1); the receiver side of
+ * the exchange (a simulated AlltoAll and the merge); the column-wise partition
+ * of Sec. 4.1.1 (gradient pack, every owner's lookup, the join of the lookup
+ * results); the Table 2 cost model; and a step executor.
+ *
  * Conventions for every call:
  *  - Array arguments are DEVICE pointers (memory of the current HIP device);
  *    scalars are passed by value.  The caller allocates and owns every buffer;
@@ -238,6 +244,85 @@ int emb_receive_merge(const int32_t *recv_ids, const float *recv_rows,
                       int32_t *merged_offsets, int32_t *num_unique,
                       void *workspace, size_t workspace_bytes,
                       int32_t *dev_status, void *stream);
+
+/*
+ * Column-wise partition (Sec. 4.1.1: the table is split by columns before
+ * training, so every process keeps the whole vocabulary for its slice of the
+ * embedding dimension and all owners receive the same number of rows; the
+ * lookup results are redistributed with one AlltoAll, the sparse gradients
+ * with another).  This is the paper's own partition; the owner-major calls
+ * above are the row-wise one.
+ *
+ * Owner p of P holds the float columns [off(p), off(p + 1)) of every row, with
+ * off(p) = floor(p * D / P) and width w(p) = off(p + 1) - off(p).
+ * The COLUMN-BLOCK LAYOUT of capacity C is C * D floats holding P blocks:
+ * block p is the [C][w(p)] row-major slice of owner p's columns, at float
+ * offset C * off(p); row r of block p is at C * off(p) + r * w(p).  With
+ * C = V it is the partitioned table (shard p = block p, all V rows); the
+ * shards of exp_avg and exp_avg_sq use the same layout.
+ * All three calls are bit copies.  Every call requires 1 <= P <= min(D, 1024)
+ * (each owner holds at least one column) and D * P < 2^31.
+ *
+ * emb_pack_by_column: the gradient payload of the column-wise AlltoAll.
+ *   rows [cap_rows][D] (the uniq_grad of emb_grad_coalesce); the first R rows
+ *   are packed, R = *num_rows (device int32, clamped into [0, cap_rows]) or
+ *   R = cap_rows when num_rows is NULL (this partitions a table: rows = the
+ *   [V][D] table, cap_rows = V).
+ *   blocks: column-block layout of capacity cap_rows; rows >= R not written.
+ *   send_counts [P] (device, may be NULL): R for every owner.  Each owner gets
+ *   the same R ids (the uniq_ids of the coalesce, not copied) with its w(p)
+ *   columns of each row.
+ *   Owner p then applies emb_sparse_adam_apply to its shard (table, exp_avg,
+ *   exp_avg_sq at float offset V * off(p), D = w(p)) with the rows of block p.
+ *
+ * emb_gather_by_column: the lookup of every owner (Sec. 4.1.1: each process
+ *   looks up the training data of all processes in its part of the table).
+ *   shards: the table in column-block layout of capacity V; ids [T].
+ *   blocks: column-block layout of capacity T; block p row t =
+ *   columns off(p) .. off(p + 1) - 1 of table row ids[t].  Worker q's tokens
+ *   at rows [t0, t1) of every block are what owner p sends q.  An id outside
+ *   [0, V) gives zeros and sets EMB_DEV_ID_OUT_OF_RANGE.  Requires
+ *   1 <= V < 2^31, T >= 0.
+ *
+ * emb_assemble_by_column: the receiving side of the lookup-result AlltoAll.
+ *   blocks: column-block layout of capacity C; rows [row0, row0 + R) of every
+ *   block are joined into rows [R][D].  With the blocks of
+ *   emb_gather_by_column and worker q's token range this yields exactly the
+ *   rows emb_gather would return for q's ids from the unpartitioned table.
+ *   Requires C >= 0, row0 >= 0, R >= 0, row0 + R <= C.
+ */
+int emb_pack_by_column(const float *rows, const int32_t *num_rows,
+                       int32_t cap_rows, int32_t D, int32_t P, float *blocks,
+                       int32_t *send_counts, void *stream);
+int emb_gather_by_column(const float *shards, int64_t V, int32_t D, int32_t P,
+                         const int32_t *ids, int32_t T, float *blocks,
+                         int32_t *dev_status, void *stream);
+int emb_assemble_by_column(const float *blocks, int64_t C, int64_t row0,
+                           int32_t R, int32_t D, int32_t P, float *rows,
+                           void *stream);
+
+/*
+ * Communication cost model of a sparse gradient (Sec. 4.1.2, Table 2): the
+ * time of one training step's exchange of an embedding table of M bytes whose
+ * gradient has density alpha (the fraction of rows with a nonzero gradient,
+ * U / V for one batch), for N workers, with bandwidth B between any two
+ * workers and start-up latency beta per message:
+ *   EMB_COMM_ALLTOALL   2 (N - 1) (alpha M / (N B) + beta)
+ *                       (lookup results and gradients, each alpha M / N per peer)
+ *   EMB_COMM_ALLREDUCE  2 (N - 1) (M / (N B) + beta)    (dense ring)
+ *   EMB_COMM_PS         2 N (alpha M / (S B) + beta)    (S servers; Table 2
+ *                       states the lower bound, S = n nodes)
+ *   EMB_COMM_ALLGATHER  (N - 1) (alpha M / B + beta)
+ * Host-only arithmetic in double.  *seconds receives the cost in the units of
+ * M / B and beta (host pointer).  S is read for EMB_COMM_PS only.
+ * Requires N >= 1, S >= 1, M >= 0, 0 <= alpha <= 1, B > 0, beta >= 0.
+ */
+#define EMB_COMM_ALLTOALL 0
+#define EMB_COMM_ALLREDUCE 1
+#define EMB_COMM_PS 2
+#define EMB_COMM_ALLGATHER 3
+int emb_comm_cost(int32_t scheme, int64_t N, int64_t S, double M,
+                  double alpha, double B, double beta, double *seconds);
 
 /*
  * Row-wise (lazy) Adam on received rows (Sec. 4.1.1: each process updates its

@@ -71,6 +71,14 @@ def _bind(lib):
     lib.orc_vertical_split.restype = I64
     lib.orc_sparse_adam.argtypes = [P, P, P, I64, I64, P, P, P, I32, I32, D, D, D, D, I64]
     lib.orc_sparse_adam.restype = I64
+    lib.orc_pack_by_column.argtypes = [P, I64, I64, I64, I32, P]
+    lib.orc_pack_by_column.restype = None
+    lib.orc_gather_by_column.argtypes = [P, I64, I64, I32, P, I64, P]
+    lib.orc_gather_by_column.restype = I64
+    lib.orc_assemble_by_column.argtypes = [P, I64, I64, I64, I64, I32, P]
+    lib.orc_assemble_by_column.restype = None
+    lib.orc_comm_cost.argtypes = [I32, I64, I64, D, D, D, D]
+    lib.orc_comm_cost.restype = D
     return lib
 
 
@@ -174,3 +182,40 @@ def sparse_adam(W, m, v, row_ids, rows, offsets, shard_begin, shard_end, lr, bet
     return int(_load().orc_sparse_adam(_ptr(W), _ptr(m), _ptr(v), V, D, _ptr(row_ids), _ptr(rows),
                                        _ptr(offsets), int(shard_begin), int(shard_end), float(lr),
                                        float(beta1), float(beta2), float(eps), int(step)))
+
+
+def pack_by_column(rows, P, C=None):
+    """Column-block layout of capacity C (default: the row count) of rows [R, D]; flat float32 [C * D].
+    Entries of rows >= R stay NaN."""
+    rows = _c(rows, np.float32)
+    R, D = rows.shape
+    C = R if C is None else C
+    blocks = np.full(C * D, np.nan, dtype=np.float32)
+    _load().orc_pack_by_column(_ptr(rows), R, C, D, P, _ptr(blocks))
+    return blocks
+
+
+def gather_by_column(shards, V, D, P, ids):
+    """Every owner's lookup of ids in its shard; returns (blocks flat [T * D], n_invalid)."""
+    shards = _c(shards, np.float32).reshape(-1)
+    ids = _c(ids, np.int32)
+    blocks = np.empty(ids.size * D, dtype=np.float32)
+    bad = _load().orc_gather_by_column(_ptr(shards), V, D, P, _ptr(ids), ids.size, _ptr(blocks))
+    return blocks, int(bad)
+
+
+def assemble_by_column(blocks, C, D, P, row0=0, R=None):
+    """Rows [row0, row0 + R) of a column-block layout of capacity C, joined into [R, D]."""
+    blocks = _c(blocks, np.float32).reshape(-1)
+    R = C - row0 if R is None else R
+    rows = np.empty((R, D), dtype=np.float32)
+    _load().orc_assemble_by_column(_ptr(blocks), C, row0, R, D, P, _ptr(rows))
+    return rows
+
+
+COMM_SCHEMES = {"alltoall": 0, "allreduce": 1, "ps": 2, "allgather": 3}
+
+
+def comm_cost(scheme, N, M, alpha, B, beta, S=1):
+    """Table 2 cost of one exchange by scheme name (alltoall, allreduce, ps, allgather)."""
+    return float(_load().orc_comm_cost(COMM_SCHEMES[scheme], N, S, float(M), float(alpha), float(B), float(beta)))

@@ -175,3 +175,60 @@ int64_t orc_sparse_adam(float *W, float *m, float *v, int64_t V, int64_t D,
     }
     return bad;
 }
+
+/* Column-wise partition, Sec. 4.1.1.  First column of owner p. */
+static int64_t orc_col_begin(int64_t p, int64_t D, int32_t P) { return p * D / P; }
+
+void orc_pack_by_column(const float *rows, int64_t R, int64_t C, int64_t D,
+                        int32_t P, float *blocks) {
+    for (int32_t p = 0; p < P; ++p) {
+        const int64_t a = orc_col_begin(p, D, P);
+        const int64_t w = orc_col_begin(p + 1, D, P) - a;
+        for (int64_t r = 0; r < R; ++r)
+            for (int64_t j = 0; j < w; ++j)
+                blocks[C * a + r * w + j] = rows[r * D + a + j];
+    }
+}
+
+int64_t orc_gather_by_column(const float *shards, int64_t V, int64_t D,
+                             int32_t P, const int32_t *ids, int64_t T,
+                             float *blocks) {
+    int64_t bad = 0;
+    for (int64_t t = 0; t < T; ++t) bad += ids[t] < 0 || ids[t] >= V;
+    for (int32_t p = 0; p < P; ++p) {
+        const int64_t a = orc_col_begin(p, D, P);
+        const int64_t w = orc_col_begin(p + 1, D, P) - a;
+        const float *shard = shards + V * a;
+        for (int64_t t = 0; t < T; ++t) {
+            const int64_t id = ids[t];
+            const int ok = id >= 0 && id < V;
+            for (int64_t j = 0; j < w; ++j)
+                blocks[T * a + t * w + j] = ok ? shard[id * w + j] : 0.0f;
+        }
+    }
+    return bad;
+}
+
+void orc_assemble_by_column(const float *blocks, int64_t C, int64_t row0,
+                            int64_t R, int64_t D, int32_t P, float *rows) {
+    for (int32_t p = 0; p < P; ++p) {
+        const int64_t a = orc_col_begin(p, D, P);
+        const int64_t w = orc_col_begin(p + 1, D, P) - a;
+        for (int64_t r = 0; r < R; ++r)
+            for (int64_t j = 0; j < w; ++j)
+                rows[r * D + a + j] = blocks[C * a + (row0 + r) * w + j];
+    }
+}
+
+/* Table 2 of Sec. 4.1.2. */
+double orc_comm_cost(int32_t scheme, int64_t N, int64_t S, double M,
+                     double alpha, double B, double beta) {
+    const double n = (double)N;
+    switch (scheme) {
+    case 0: return 2.0 * (n - 1.0) * (alpha * M / (n * B) + beta);
+    case 1: return 2.0 * (n - 1.0) * (M / (n * B) + beta);
+    case 2: return 2.0 * n * (alpha * M / ((double)S * B) + beta);
+    case 3: return (n - 1.0) * (alpha * M / B + beta);
+    default: return -1.0;
+    }
+}

@@ -84,6 +84,36 @@ int64_t orc_sparse_adam(float *W, float *m, float *v, int64_t V, int64_t D,
                         int32_t shard_end, double lr, double beta1,
                         double beta2, double eps, int64_t step);
 
+/* Column-wise partition (Sec. 4.1.1: the table is split along the embedding
+ * dimension, every part keeping the whole vocabulary).  The paper does not say
+ * how D columns split when P does not divide D; here owner p holds columns
+ * [floor(p D / P), floor((p + 1) D / P)), so widths differ by at most one.
+ * Block p of a column-block layout of capacity C is the [C][w(p)] row-major
+ * slice of owner p's columns at float offset C * floor(p D / P).
+ *   orc_pack_by_column:     rows[R][D]       -> blocks (rows r < R of each block)
+ *   orc_gather_by_column:   shards (C = V)   -> blocks of capacity T, row t of
+ *                           block p = owner p's columns of table row ids[t]
+ *                           (zeros for an id outside [0, V); returns their count)
+ *   orc_assemble_by_column: blocks (C), rows [row0, row0 + R) -> rows[R][D] */
+void orc_pack_by_column(const float *rows, int64_t R, int64_t C, int64_t D,
+                        int32_t P, float *blocks);
+int64_t orc_gather_by_column(const float *shards, int64_t V, int64_t D,
+                             int32_t P, const int32_t *ids, int64_t T,
+                             float *blocks);
+void orc_assemble_by_column(const float *blocks, int64_t C, int64_t row0,
+                            int64_t R, int64_t D, int32_t P, float *rows);
+
+/* Communication cost of a sparse tensor by approach (Sec. 4.1.2, Table 2):
+ * N workers, S parameter servers (PS only; the table's entry is S = n nodes),
+ * table of M bytes, gradient density alpha, bandwidth B, start latency beta.
+ *   scheme 0 AlltoAll  2(N-1)(alpha M / (N B) + beta)
+ *          1 AllReduce 2(N-1)(M / (N B) + beta)
+ *          2 PS        2N(alpha M / (S B) + beta)
+ *          3 AllGather (N-1)(alpha M / B + beta)
+ * Returns -1 for an unknown scheme. */
+double orc_comm_cost(int32_t scheme, int64_t N, int64_t S, double M,
+                     double alpha, double B, double beta);
+
 #ifdef __cplusplus
 }
 #endif

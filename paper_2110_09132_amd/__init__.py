@@ -28,6 +28,10 @@ EMB_BF16 = 1
 EMB_DEV_ID_OUT_OF_RANGE = 1
 EMB_DEV_OWNER_OUT_OF_RANGE = 2
 EMB_DEV_STALLED = 4
+EMB_COMM_ALLTOALL = 0
+EMB_COMM_ALLREDUCE = 1
+EMB_COMM_PS = 2
+EMB_COMM_ALLGATHER = 3
 
 # (name, restype, argtypes) of every symbol include/emb.h declares.
 _P, _I32, _I64, _SZ, _D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_double
@@ -49,6 +53,10 @@ SIGNATURES = {
     "emb_pack_by_owner": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_sparse_adam_apply": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _P, _P, _P, _I32, _I32, _I32, _I32,
                                              _D, _D, _D, _D, _I64, _P, _P]),
+    "emb_pack_by_column": (ctypes.c_int, [_P, _P, _I32, _I32, _I32, _P, _P, _P]),
+    "emb_gather_by_column": (ctypes.c_int, [_P, _I64, _I32, _I32, _P, _I32, _P, _P, _P]),
+    "emb_assemble_by_column": (ctypes.c_int, [_P, _I64, _I64, _I32, _I32, _I32, _P, _P]),
+    "emb_comm_cost": (ctypes.c_int, [_I32, _I64, _I64, _D, _D, _D, _D, ctypes.POINTER(ctypes.c_double)]),
     "emb_event_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), _I32]),
     "emb_event_destroy": (ctypes.c_int, [_P]),
     "emb_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
@@ -340,6 +348,68 @@ def pack_by_owner(uniq_ids, uniq_grad, num_unique, row_owner, P, out=None, works
                                  _ptr(workspace), workspace.numel(), _ptr(dev_status), _stream(stream)),
            "emb_pack_by_owner")
     return out
+
+
+def column_offsets(D, P):
+    """First float column of every owner of the column-wise partition, [P + 1]: floor(p * D / P)."""
+    return [(p * D) // P for p in range(P + 1)]
+
+
+def column_block(blocks, C, D, P, p):
+    """View of block p ([C, w(p)]) of a flat column-block layout of capacity C."""
+    off = column_offsets(D, P)
+    return blocks[C * off[p]:C * off[p + 1]].view(C, off[p + 1] - off[p])
+
+
+def pack_by_column(rows, P, num_rows=None, out=None, stream=None):
+    """Column-block layout of the rows (emb_pack_by_column).
+
+    rows [cap, D]; packs the first *num_rows rows (device int32 [1]) or all of them.
+    Returns (blocks [cap * D] flat, send_counts [P])."""
+    _need(rows, torch.float32, "rows")
+    if num_rows is not None:
+        _need(num_rows, torch.int32, "num_rows")
+    cap, D = rows.shape
+    dev = rows.device
+    if out is None:
+        out = (torch.empty(cap * D, dtype=torch.float32, device=dev), torch.empty(P, dtype=torch.int32, device=dev))
+    blocks, counts = out
+    _check(lib.emb_pack_by_column(_ptr(rows), _ptr(num_rows), cap, D, P, _ptr(blocks), _ptr(counts), _stream(stream)),
+           "emb_pack_by_column")
+    return out
+
+
+def gather_by_column(shards, V, D, P, ids, out=None, dev_status=None, stream=None):
+    """Every owner's lookup of ids in its shard (emb_gather_by_column).
+
+    shards: flat column-block layout of capacity V.  Returns blocks [T * D] flat (capacity T)."""
+    _need(shards, torch.float32, "shards")
+    _need(ids, torch.int32, "ids")
+    T = ids.numel()
+    if out is None:
+        out = torch.empty(T * D, dtype=torch.float32, device=ids.device)
+    _check(lib.emb_gather_by_column(_ptr(shards), V, D, P, _ptr(ids), T, _ptr(out), _ptr(dev_status),
+                                    _stream(stream)), "emb_gather_by_column")
+    return out
+
+
+def assemble_by_column(blocks, C, D, P, row0=0, R=None, out=None, stream=None):
+    """Rows [row0, row0 + R) of a column-block layout of capacity C, joined (emb_assemble_by_column)."""
+    _need(blocks, torch.float32, "blocks")
+    R = C - row0 if R is None else R
+    if out is None:
+        out = torch.empty((R, D), dtype=torch.float32, device=blocks.device)
+    _check(lib.emb_assemble_by_column(_ptr(blocks), C, row0, R, D, P, _ptr(out), _stream(stream)),
+           "emb_assemble_by_column")
+    return out
+
+
+def comm_cost(scheme, N, M, alpha, B, beta, S=1) -> float:
+    """Table 2 communication cost of one exchange (emb_comm_cost); host arithmetic."""
+    r = ctypes.c_double()
+    _check(lib.emb_comm_cost(scheme, N, S, float(M), float(alpha), float(B), float(beta), ctypes.byref(r)),
+           "emb_comm_cost")
+    return r.value
 
 
 def sparse_adam_apply(table, exp_avg, exp_avg_sq, row_ids, rows, offsets, P, shard_begin, shard_end, lr, beta1,

@@ -194,6 +194,61 @@ int emb_receive_merge(const int32_t* recv_ids, const float* recv_rows, const int
                                             dev_status, static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+bool bad_column_split(int32_t D, int32_t P) {
+  return D < 1 || P < 1 || P > D || P > kMaxOwners || static_cast<int64_t>(D) * P >= (int64_t{1} << 31);
+}
+}  // namespace
+
+int emb_pack_by_column(const float* rows, const int32_t* num_rows, int32_t cap_rows, int32_t D, int32_t P,
+                       float* blocks, int32_t* send_counts, void* stream) {
+  if (cap_rows < 0 || bad_column_split(D, P)) return EMB_ERR_INVALID_ARG;
+  if (cap_rows > 0 && (!rows || !blocks)) return EMB_ERR_INVALID_ARG;
+  return launch_status(
+      emb::launch_column_pack(rows, num_rows, cap_rows, D, P, blocks, send_counts, static_cast<hipStream_t>(stream)));
+}
+
+int emb_gather_by_column(const float* shards, int64_t V, int32_t D, int32_t P, const int32_t* ids, int32_t T,
+                         float* blocks, int32_t* dev_status, void* stream) {
+  if (bad_table_dims(V, D) || bad_column_split(D, P) || T < 0) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && (!shards || !ids || !blocks)) return EMB_ERR_INVALID_ARG;
+  return launch_status(
+      emb::launch_column_gather(shards, V, D, P, ids, T, blocks, dev_status, static_cast<hipStream_t>(stream)));
+}
+
+int emb_assemble_by_column(const float* blocks, int64_t C, int64_t row0, int32_t R, int32_t D, int32_t P,
+                           float* rows, void* stream) {
+  if (bad_column_split(D, P) || C < 0 || row0 < 0 || R < 0 || row0 > C - R) return EMB_ERR_INVALID_ARG;
+  if (R > 0 && (!blocks || !rows)) return EMB_ERR_INVALID_ARG;
+  return launch_status(
+      emb::launch_column_assemble(blocks, C, row0, R, D, P, rows, static_cast<hipStream_t>(stream)));
+}
+
+int emb_comm_cost(int32_t scheme, int64_t N, int64_t S, double M, double alpha, double B, double beta,
+                  double* seconds) {
+  if (!seconds || N < 1 || S < 1 || !(M >= 0) || !(alpha >= 0 && alpha <= 1) || !(B > 0) || !(beta >= 0) ||
+      !std::isfinite(M) || !std::isfinite(B) || !std::isfinite(beta))
+    return EMB_ERR_INVALID_ARG;
+  const double n = static_cast<double>(N);
+  const double sparse = alpha * M;  // bytes of the sparse gradient
+  switch (scheme) {
+    case EMB_COMM_ALLTOALL:  // N - 1 peers, 1/N of the sparse gradient each, twice
+      *seconds = 2.0 * (n - 1.0) * (sparse / (n * B) + beta);
+      return EMB_OK;
+    case EMB_COMM_ALLREDUCE:  // ring reduce-scatter then all-gather of dense 1/N chunks
+      *seconds = 2.0 * (n - 1.0) * (M / (n * B) + beta);
+      return EMB_OK;
+    case EMB_COMM_PS:  // pull and push of the sparse rows, 1/S per server, N workers
+      *seconds = 2.0 * n * (sparse / (static_cast<double>(S) * B) + beta);
+      return EMB_OK;
+    case EMB_COMM_ALLGATHER:  // every worker's whole sparse gradient to every other
+      *seconds = (n - 1.0) * (sparse / B + beta);
+      return EMB_OK;
+    default:
+      return EMB_ERR_INVALID_ARG;
+  }
+}
+
 size_t emb_pack_by_owner_workspace_bytes(int32_t cap_rows, int32_t P) {
   if (cap_rows < 0 || P < 1 || P > kMaxOwners) return 0;
   return emb::pack_workspace_bytes(cap_rows, P);

@@ -51,6 +51,15 @@ int coalesce_by_owner_args_status(const int32_t* ids, int32_t T, const void* gra
                                   const float* send_rows, const int32_t* send_counts, const int32_t* send_offsets,
                                   const int32_t* num_unique, const void* workspace, size_t workspace_bytes);
 
+// Column-block layout (block p = the [C][w(p)] slice of owner p's columns at
+// float offset C * off(p), off(p) = floor(p * D / P)); see column.hip.
+hipError_t launch_column_pack(const float* rows, const int32_t* num_rows, int cap, int D, int P, float* blocks,
+                              int32_t* send_counts, hipStream_t stream);
+hipError_t launch_column_gather(const float* shards, int64_t V, int D, int P, const int32_t* ids, int T,
+                                float* blocks, int32_t* status, hipStream_t stream);
+hipError_t launch_column_assemble(const float* blocks, int64_t C, int64_t row0, int R, int D, int P, float* rows,
+                                  hipStream_t stream);
+
 // The simulated AlltoAll of P workers' send layouts (send_* of worker w at
 // w * cap_rows): receiver-major blocks, senders in order inside a receiver.
 hipError_t launch_exchange(const int32_t* send_ids, const float* send_rows, const int32_t* send_offsets, int P,

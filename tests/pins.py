@@ -405,3 +405,170 @@ def pin_adam_shard_ranges():
                                ADAM["eps"], t)
     for a, b in ((Wa, Wb), (ma, mb), (va, vb)):
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+# ------------------------------------------------------- column-wise partition
+def _col_bounds(D, P):
+    return [(p * D) // P for p in range(P + 1)]
+
+
+def _blocks_equal(got, want_with_none):
+    want = np.array([np.nan if x is None else x for x in want_with_none], np.float32)
+    written = ~np.isnan(want)
+    assert got.shape == want.shape
+    assert np.array_equal(got[written], want[written])
+    assert np.all(np.isnan(got[~written]))  # the pack leaves rows >= R alone
+
+
+def pin_column_golden():
+    """Hand-worked column split, pack, lookup and join (Sec. 4.1.1)."""
+    g = load_golden("column_partition_worked.txt")
+    rows = np.array(g["rows"], np.float32)
+    _blocks_equal(oracle.pack_by_column(rows, g["P"], C=g["C"]), g["blocks"])
+    _blocks_equal(oracle.pack_by_column(rows, g["P3"]), g["blocks3"])
+    blocks, bad = oracle.gather_by_column(np.array(g["shards"], np.float32), g["V"], g["D"], g["P"],
+                                          np.array(g["ids"], np.int32))
+    assert bad == g["n_invalid"]
+    assert blocks.tolist() == g["lookup_blocks"]
+    out = oracle.assemble_by_column(blocks, len(g["ids"]), g["D"], g["P"], row0=g["row0"], R=g["R"])
+    assert out.tolist() == g["assembled"]
+
+
+def pin_column_layout():
+    """Special cases with known layouts, and a column-tagged brute force for ragged splits.
+      P = 1: the single block is the rows themselves.
+      P = D: block p is column p, so the blocks are the transpose of the rows.
+      P | D: the blocks are rows.reshape(R, P, D/P) with the first two axes swapped.
+      any P <= D: tag every float with (row, column); each block must hold, row by row, a
+      contiguous ascending run of columns, the runs of owners 0 .. P-1 following each other,
+      widths within one of each other, every column exactly once."""
+    R, C = 7, 9
+    for D in (1, 6, 12, 13):
+        rows = _rng_normal(60 + D, R * D).reshape(R, D)
+        b = oracle.pack_by_column(rows, 1, C=C)
+        assert np.array_equal(b[:R * D], rows.reshape(-1)) and np.all(np.isnan(b[R * D:]))
+        b = oracle.pack_by_column(rows, D)
+        assert np.array_equal(b.reshape(D, R), rows.T)
+        for P in (2, 3, 4, 6):
+            if D % P == 0:
+                b = oracle.pack_by_column(rows, P)
+                assert np.array_equal(b.reshape(P, R, D // P), rows.reshape(R, P, D // P).transpose(1, 0, 2))
+    for D, P in ((13, 4), (10, 3), (7, 7), (100, 16), (5, 2)):
+        tag = (np.arange(R)[:, None] * 1000 + np.arange(D)[None, :]).astype(np.float32)
+        b = oracle.pack_by_column(tag, P, C=C)
+        seen, start, widths = [], 0, []
+        for p in range(P):
+            w = None
+            for r in range(R):
+                blk = b[C * start + r * (w or 0):]
+                if w is None:  # width of block p: the run of row 0's columns that are consecutive
+                    w = 1
+                    while start + w < D and blk[w] == blk[0] + w:
+                        w += 1
+                    if p == P - 1:
+                        w = D - start
+                run = b[C * start + r * w: C * start + (r + 1) * w]
+                assert np.array_equal(run, r * 1000 + start + np.arange(w, dtype=np.float32))
+            seen.extend(range(start, start + w))
+            widths.append(w)
+            start += w
+        assert seen == list(range(D)) and max(widths) - min(widths) <= 1
+        assert [0] + np.cumsum(widths).tolist() == _col_bounds(D, P)
+
+
+def pin_column_roundtrip():
+    """Joining the blocks gives back the rows, for every row range (ragged splits included)."""
+    for seed, (R, C, D, P) in enumerate(((10, 12, 13, 4), (1, 1, 5, 5), (33, 40, 64, 16), (6, 6, 3, 1))):
+        rows = _rng_normal(70 + seed, R * D).reshape(R, D)
+        b = oracle.pack_by_column(rows, P, C=C)
+        assert np.array_equal(oracle.assemble_by_column(b, C, D, P, 0, R), rows)
+        for row0, n in ((1, R - 1), (R // 2, R - R // 2), (R - 1, 1), (R, 0)):
+            assert np.array_equal(oracle.assemble_by_column(b, C, D, P, row0, n), rows[row0:row0 + n])
+
+
+def pin_column_forward():
+    """The lookup-result exchange (Sec. 4.1.1): each owner looks up every worker's tokens in its
+    shard; joining a worker's rows from all owners gives numpy's table[ids] for that worker's ids
+    (zero rows for ids that are not rows), and equals the row-wise lookup."""
+    for seed, (V, D, P, sizes) in enumerate(((50, 13, 4, (7, 0, 11, 3)), (300, 64, 16, (40, 25)),
+                                             (9, 3, 3, (5,)))):
+        table = _rng_normal(80 + seed, V * D, purpose=gen.PURPOSE_WEIGHTS).reshape(V, D)
+        shards = oracle.pack_by_column(table, P)
+        ids = _rng_ids(90 + seed, sum(sizes), V + 3)  # a few ids >= V
+        blocks, bad = oracle.gather_by_column(shards, V, D, P, ids)
+        assert bad == int(np.sum(ids >= V))
+        t0 = 0
+        for n in sizes:
+            q = ids[t0:t0 + n]
+            want = np.where((q < V)[:, None], table[np.minimum(q, V - 1)], 0).astype(np.float32)
+            got = oracle.assemble_by_column(blocks, ids.size, D, P, t0, n)
+            assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+            assert np.array_equal(got, oracle.gather(table, q)[0])
+            t0 += n
+
+
+def pin_column_adam():
+    """Adam is elementwise, so each owner updating its shard with its column slice of the
+    coalesced rows (the column-wise exchange) gives bit for bit the row-wise update."""
+    V, D, P = 30, 13, 4
+    Wa, ma, va = _adam_tables(V, D, 95)
+    ids = np.array([0, 3, 4, 17, 29], np.int32)
+    sw, sm, sv = (oracle.pack_by_column(x, P) for x in (Wa, ma, va))
+    bnd = _col_bounds(D, P)
+    for t in (1, 2, 3):
+        rows = _rng_normal(96 + t, ids.size * D).reshape(ids.size, D)
+        oracle.sparse_adam(Wa, ma, va, ids, rows, np.array([0, ids.size], np.int32), 0, 1, ADAM["lr"],
+                           ADAM["beta1"], ADAM["beta2"], ADAM["eps"], t)
+        blocks = oracle.pack_by_column(rows, P)
+        for p in range(P):
+            a, w = bnd[p], bnd[p + 1] - bnd[p]
+            shard = [x[V * a: V * (a + w)].reshape(V, w) for x in (sw, sm, sv)]
+            oracle.sparse_adam(*shard, ids, blocks[ids.size * a: ids.size * (a + w)].reshape(ids.size, w),
+                               np.array([0, ids.size], np.int32), 0, 1, ADAM["lr"], ADAM["beta1"],
+                               ADAM["beta2"], ADAM["eps"], t)
+    for full, sh in ((Wa, sw), (ma, sm), (va, sv)):
+        assert np.array_equal(oracle.assemble_by_column(sh, V, D, P).view(np.uint32), full.view(np.uint32))
+
+
+# --------------------------------------------------------- communication cost
+_SCHEMES = ("alltoall", "allreduce", "ps", "allgather")
+
+
+def pin_comm_cost_golden():
+    """Table 2 evaluated by hand."""
+    g = load_golden("comm_cost_worked.txt")
+    for case in ("case_a", "case_b", "case_c"):
+        c = g[case]
+        got = [oracle.comm_cost(s, c["N"], c["M"], c["alpha"], c["B"], c["beta"], S=c["S"]) for s in _SCHEMES]
+        assert np.allclose(got, c["cost"], rtol=1e-15, atol=0), (case, got)
+
+
+def pin_comm_cost_claims():
+    """What Sec. 4.1.2 concludes from Table 2, over a grid of settings:
+      for N > 1 and N >= n (S = n servers) and alpha <= 1, AlltoAll is no slower than AllReduce
+      (equal at alpha = 1) and faster than PS;
+      with N = 2, AllGather undercuts AlltoAll by exactly one start latency;
+      without latency, AllGather's time grows linearly in N while AlltoAll's stays below
+      2 alpha M / B (AllGather / AlltoAll = N / 2);
+      with one worker nothing is exchanged except under PS."""
+    M, B = 1e9, 12.5e9
+    cost = {s: (lambda N, alpha, beta, S=1, s=s: oracle.comm_cost(s, N, M, alpha, B, beta, S=S)) for s in _SCHEMES}
+    for N in (2, 3, 4, 8, 16, 64):
+        for n in sorted({1, 2, N // 2 or 1, N}):
+            for alpha in (0.0, 0.003, 0.1, 0.4, 1.0):
+                for beta in (0.0, 1e-6, 1e-4, 1e-2):
+                    a2a = cost["alltoall"](N, alpha, beta)
+                    assert a2a <= cost["allreduce"](N, alpha, beta) * (1 + 1e-15)
+                    ps = cost["ps"](N, alpha, beta, S=n)
+                    assert a2a < ps if alpha > 0 or beta > 0 else a2a == ps == 0.0
+                    if alpha == 1.0:
+                        assert np.isclose(a2a, cost["allreduce"](N, alpha, beta), rtol=1e-15)
+        for alpha in (0.01, 0.5):
+            ag, a2a = cost["allgather"](N, alpha, 0.0), cost["alltoall"](N, alpha, 0.0)
+            assert np.isclose(ag, (N - 1) * alpha * M / B, rtol=1e-15)
+            assert np.isclose(ag / a2a, N / 2, rtol=1e-14) and a2a < 2 * alpha * M / B
+    for beta in (1e-6, 1e-3):
+        assert np.isclose(cost["alltoall"](2, 0.2, beta) - cost["allgather"](2, 0.2, beta), beta, rtol=1e-9)
+    for s in ("alltoall", "allreduce", "allgather"):
+        assert cost[s](1, 0.3, 1e-3) == 0.0
+    assert np.isclose(cost["ps"](1, 0.3, 1e-3, S=1), 2 * (0.3 * M / B + 1e-3), rtol=1e-15)

@@ -140,3 +140,57 @@ def test_adam_validation(bad):
 def test_adam_empty_range_is_noop():
     assert emb.lib.emb_sparse_adam_apply(FAKE, FAKE, FAKE, 5000, 8, FAKE, FAKE, FAKE, 4, 2, 2, 100, 1e-3, 0.9,
                                          0.999, 1e-8, 1, NULL, NULL) == emb.EMB_OK
+
+
+def test_column_calls_validation():
+    L = emb.lib
+    # pack: P must satisfy 1 <= P <= min(D, 1024); sizes >= 0; buffers present when rows > 0
+    assert L.emb_pack_by_column(FAKE, NULL, 10, 8, 0, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_pack_by_column(FAKE, NULL, 10, 8, 9, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG  # P > D
+    assert L.emb_pack_by_column(FAKE, NULL, 10, 4096, 1025, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_pack_by_column(FAKE, NULL, -1, 8, 2, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_pack_by_column(NULL, NULL, 10, 8, 2, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_pack_by_column(FAKE, NULL, 10, 8, 2, NULL, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_pack_by_column(FAKE, NULL, 10, 1 << 22, 1024, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_pack_by_column(NULL, NULL, 0, 8, 2, NULL, NULL, NULL) == emb.EMB_OK  # nothing to do
+    # lookup
+    assert L.emb_gather_by_column(FAKE, 0, 8, 2, FAKE, 5, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_gather_by_column(FAKE, 10, 8, 9, FAKE, 5, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_gather_by_column(FAKE, 10, 8, 2, FAKE, -1, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_gather_by_column(FAKE, 10, 8, 2, NULL, 5, FAKE, NULL, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_gather_by_column(NULL, 10, 8, 2, NULL, 0, NULL, NULL, NULL) == emb.EMB_OK
+    # join: row0 + R <= C
+    assert L.emb_assemble_by_column(FAKE, 10, 5, 6, 8, 2, FAKE, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_assemble_by_column(FAKE, 10, -1, 2, 8, 2, FAKE, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_assemble_by_column(FAKE, 10, 0, -1, 8, 2, FAKE, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_assemble_by_column(FAKE, 10, 0, 3, 8, 0, FAKE, NULL) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_assemble_by_column(NULL, 10, 10, 0, 8, 2, NULL, NULL) == emb.EMB_OK
+
+
+def test_comm_cost_validation():
+    L = emb.lib
+    out = ctypes.c_double()
+    ok = (emb.EMB_COMM_ALLTOALL, 8, 1, 1e9, 0.1, 1e10, 1e-5)
+    assert L.emb_comm_cost(*ok, ctypes.byref(out)) == emb.EMB_OK
+    assert L.emb_comm_cost(*ok, NULL) == emb.EMB_ERR_INVALID_ARG
+    for i, bad in ((0, 4), (0, -1), (1, 0), (2, 0), (3, -1.0), (4, 1.5), (4, -0.1), (5, 0.0), (6, -1e-6),
+                   (4, float("nan")), (5, float("inf"))):
+        args = list(ok)
+        args[i] = bad
+        assert L.emb_comm_cost(*args, ctypes.byref(out)) == emb.EMB_ERR_INVALID_ARG, (i, bad)
+
+
+def test_comm_cost_matches_oracle():
+    """The library's Table 2 arithmetic (host code) against the oracle's, which is pinned to
+    hand-worked values and the section's conclusions."""
+    import oracle
+    names = {emb.EMB_COMM_ALLTOALL: "alltoall", emb.EMB_COMM_ALLREDUCE: "allreduce", emb.EMB_COMM_PS: "ps",
+             emb.EMB_COMM_ALLGATHER: "allgather"}
+    for code, name in names.items():
+        for N, S in ((1, 1), (2, 1), (8, 1), (8, 2), (64, 8)):
+            for M in (0.0, 4e6, 1.2e9):
+                for alpha in (0.0, 0.0168, 0.5, 1.0):
+                    for B, beta in ((153e9, 0.0), (12.5e9, 5e-6)):
+                        got = emb.comm_cost(code, N, M, alpha, B, beta, S=S)
+                        want = oracle.comm_cost(name, N, M, alpha, B, beta, S=S)
+                        assert got == pytest.approx(want, rel=1e-15, abs=0.0)

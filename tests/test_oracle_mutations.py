@@ -33,6 +33,27 @@ MUTANTS = {
                        ["pin_split_golden", "pin_split_invariants"]),
     "split_drops_smallest_next_id": ("bsearch(&key, nx, (size_t)T_next,", "bsearch(&key, nx + 1, (size_t)(T_next > 0 ? T_next - 1 : 0),",
                                      ["pin_split_golden", "pin_split_invariants"]),
+    "column_split_rounds_up": ("return p * D / P;", "return (p * D + P - 1) / P;",
+                               ["pin_column_golden", "pin_column_layout"]),
+    "column_block_base_by_rows": ("blocks[C * a + r * w + j] = rows[r * D + a + j];",
+                                  "blocks[R * a + r * w + j] = rows[r * D + a + j];",
+                                  ["pin_column_golden", "pin_column_layout", "pin_column_roundtrip"]),
+    "column_block_column_major": ("blocks[C * a + r * w + j] = rows[r * D + a + j];",
+                                  "blocks[C * a + j * R + r] = rows[r * D + a + j];",
+                                  ["pin_column_golden", "pin_column_layout", "pin_column_roundtrip"]),
+    "column_join_ignores_row0": ("rows[r * D + a + j] = blocks[C * a + (row0 + r) * w + j];",
+                                 "rows[r * D + a + j] = blocks[C * a + r * w + j];",
+                                 ["pin_column_golden", "pin_column_roundtrip", "pin_column_forward"]),
+    "column_lookup_token_for_id": ("ok ? shard[id * w + j] : 0.0f;", "ok ? shard[(t % V) * w + j] : 0.0f;",
+                                   ["pin_column_golden", "pin_column_forward"]),
+    "comm_alltoall_once": ("case 0: return 2.0 * (n - 1.0)", "case 0: return (n - 1.0)",
+                           ["pin_comm_cost_golden", "pin_comm_cost_claims"]),
+    "comm_alltoall_whole_gradient": ("(alpha * M / (n * B) + beta);", "(alpha * M / B + beta);",
+                                     ["pin_comm_cost_golden", "pin_comm_cost_claims"]),
+    "comm_ps_n_minus_1": ("case 2: return 2.0 * n *", "case 2: return 2.0 * (n - 1.0) *",
+                          ["pin_comm_cost_golden", "pin_comm_cost_claims"]),
+    "comm_allgather_n": ("case 3: return (n - 1.0)", "case 3: return n",
+                         ["pin_comm_cost_golden", "pin_comm_cost_claims"]),
     "adam_no_bias_correction": ("double mhat = mm / bc1;", "double mhat = mm;",
                                 ["pin_adam_golden", "pin_adam_closed_forms", "pin_adam_vs_torch_dense"]),
     "adam_eps_inside_sqrt": ("(sqrt(vhat) + eps)", "sqrt(vhat + eps)",
