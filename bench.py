@@ -195,6 +195,83 @@ def summarize_pmc(fetch_dir, write_dir, command_fetch, command_write):
             "command_fetch": command_fetch, "command_write": command_write}
 
 
+XGMI_LINK_GBPS = 153.0  # one MI355X xGMI link, per direction (one link per peer in an 8-GPU node)
+
+
+def column_partition_report(torch, emb, sp, tb, batches, U, owner_rows, reps=20):
+    """The column-wise partition (Sec. 4.1.1) beside the row-wise one for the first table:
+    per-owner bytes of the gradient AlltoAll payload in each partition (ids as int32, rows fp32),
+    and the column kernels timed at the table's shape, each over `reps` back-to-back launches
+    (outside the timed steps).  Byte models: pack reads and writes U rows; the lookup reads each
+    distinct row once, the ids, and writes T rows; the join reads and writes T rows."""
+    V, D, P, T = sp.V, sp.D, sp.P, sp.T
+    off = emb.column_offsets(D, P)
+    widths = np.diff(off)
+    row_b, col_b = [], []
+    for b, (ids, g) in enumerate(batches):
+        rows_p = np.asarray(owner_rows[b], dtype=np.float64)
+        row_b.append(rows_p * (4 * D + 4))
+        col_b.append(U[b] * (4.0 * widths + 4))
+
+    def balance(per_owner):
+        a = np.array(per_owner)
+        return {"max_MB": float(a.max(axis=1).mean() / 1e6), "mean_MB": float(a.mean(axis=1).mean() / 1e6),
+                "max_over_mean": float((a.max(axis=1) / np.maximum(a.mean(axis=1), 1e-30)).mean())}
+
+    shards = emb.pack_by_column(tb.W, P)[0]
+    coalesced = []
+    for ids, g in batches:  # coalesced rows of each batch (any order serves the pack)
+        uid, seg, ug, nu = emb.grad_coalesce(ids, g, V)
+        coalesced.append((ug, nu))
+    blocks = torch.empty(T * D, dtype=torch.float32, device="cuda")
+    counts = torch.empty(P, dtype=torch.int32, device="cuda")
+    look = torch.empty(T * D, dtype=torch.float32, device="cuda")
+    joined = torch.empty((T, D), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        for i in range(3):
+            fn(i)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(reps):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    nb = len(batches)
+    Um = float(np.mean(U))
+    us_pack = timed(lambda i: emb.pack_by_column(coalesced[i % nb][0], P, num_rows=coalesced[i % nb][1],
+                                                 out=(blocks, counts)))
+    us_look = timed(lambda i: emb.gather_by_column(shards, V, D, P, batches[i % nb][0], out=look))
+    us_join = timed(lambda i: emb.assemble_by_column(look, T, D, P, out=joined))
+    kern = {}
+    for name, us, nbytes in (("pack_by_column", us_pack, 2 * Um * D * 4 + 4),
+                             ("gather_by_column", us_look, Um * D * 4 + T * 4 + T * D * 4),
+                             ("assemble_by_column", us_join, 2 * T * D * 4)):
+        kern[name] = {"avg_launch_us": us, "bytes_model": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9,
+                      "frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS}
+    del shards
+    return {"table": 0, "owner_rule_rowwise": sp.owner_rule, "column_widths": [int(widths.min()), int(widths.max())],
+            "payload_rowwise": balance(row_b), "payload_columnwise": balance(col_b), "kernels": kern}
+
+
+def cost_model_report(emb, sp, U, N=8):
+    """Table 2 (Sec. 4.1.2) fed with the measured density alpha = U / V of the first table's batches,
+    for N workers of one node with B = one xGMI link; the bandwidth terms (beta = 0) in microseconds
+    and, separately, how many start latencies each scheme pays."""
+    alpha = float(np.mean(U)) / sp.V
+    M = float(sp.V) * sp.D * 4
+    B = XGMI_LINK_GBPS * 1e9
+    names = (("alltoall", emb.EMB_COMM_ALLTOALL, 2 * (N - 1)), ("allreduce", emb.EMB_COMM_ALLREDUCE, 2 * (N - 1)),
+             ("ps_one_server_per_node", emb.EMB_COMM_PS, 2 * N), ("allgather", emb.EMB_COMM_ALLGATHER, N - 1))
+    return {"N": N, "alpha": alpha, "M_bytes": M, "B_GBps": XGMI_LINK_GBPS,
+            "bandwidth_term_us": {n: emb.comm_cost(c, N, M, alpha, B, 0.0, S=1) * 1e6 for n, c, _ in names},
+            "start_latencies": {n: k for n, _, k in names}}
+
+
 def host_info():
     model = platform.processor() or ""
     try:
@@ -270,6 +347,7 @@ def main():
     # outside any timed region
     U = [[0] * len(tables) for _ in range(args.batches)]
     U_prior = [[0] * len(tables) for _ in range(args.batches)]
+    owner_rows = [None] * args.batches  # rows per owner of the first table (prior + delayed)
     for b in range(args.batches):
         for k, tb in enumerate(tables):
             ids, g = step_batches[b][k]
@@ -278,6 +356,8 @@ def main():
             torch.cuda.synchronize()
             U[b][k] = int(out[5].item())
             U_prior[b][k] = int(out[4][tb.P].item())
+            if k == 0:
+                owner_rows[b] = out[3].view(2, tb.P).sum(0).cpu().numpy()
 
     split = args.schedule == "split"
     by_owner = args.schedule != "unfused"
@@ -342,6 +422,9 @@ def main():
                     "update_prior": stage_ms["pack"], "update_delayed": stage_ms["adam"]}
 
     copy_gbps = copy_reference(torch)
+    column = column_partition_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches],
+                                     [U[b][0] for b in range(args.batches)], owner_rows)
+    cost = cost_model_report(emb, wl.tables[0], [U[b][0] for b in range(args.batches)])
 
     # algorithmic bytes of the timed steps
     bytes_step = {k: 0.0 for k in ("gather", "coalesce", "pack", "adam")}
@@ -406,6 +489,8 @@ def main():
                      "bytes_per_launch": adam_bytes, "avg_launch_us": adam_us,
                      "launches_timed": len(adam_ev)},
         "copy_GBps": copy_gbps,
+        "column_partition": column,
+        "comm_cost_model": cost,
         "step_frac_of_copy": step_gbps / copy_gbps,
         "host": host_info(),
     }
