@@ -301,6 +301,9 @@ def main():
                          "the prior/delayed split of Vertical Sparse Scheduling (emb_grad_coalesce_split; the "
                          "delayed update beside the next lookup); unfused: emb_grad_coalesce then "
                          "emb_pack_by_owner")
+    ap.add_argument("--order", choices=("signals", "events"), default="events",
+                    help="cross-stream order of the overlapped schedule: step signals (stream memory operations) "
+                         "or events")
     ap.add_argument("--summarize-trace", metavar="DIR", help="print a summary of a rocprofv3 kernel-stats run")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the scaled HBM traffic of the update kernel from two rocprofv3 --pmc runs")
@@ -362,7 +365,7 @@ def main():
     split = args.schedule == "split"
     by_owner = args.schedule != "unfused"
     pipe = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential, by_owner=by_owner,
-                        split=split)
+                        split=split, signals=args.order == "signals")
 
     def next_ids(t):
         return [x[0] for x in step_batches[(t + 1) % args.batches]] if split else None
@@ -472,6 +475,9 @@ def main():
                     "by_owner": "sort and reduction on two side streams; lookup and update on the main stream",
                     "unfused": "coalesce and pack on two side streams; lookup and update on the main stream"}[
                        args.schedule],
+                   "cross_stream_order": None if args.sequential else
+                   {"signals": "step signals (hipStreamWriteValue32 / hipStreamWaitValue32)",
+                    "events": "events (hipEventRecord / hipStreamWaitEvent)"}[args.order],
                    "prior_rows_frac": prior_frac if split else None},
         "step_bytes_model": total_bytes,
         "step_bytes_model_kind": "fused minimum (pack folded into coalesce)" if by_owner else "four calls",

@@ -421,6 +421,10 @@ typedef struct {
                                    stream the (first / last) kernel runs on; the adam
                                    pair takes the update kernel's own start and end
                                    from its dispatch; by_owner records no pack pair */
+  void *signals;                /* optional step signals of the table
+                                   (emb_step_signals_create): when set, the waits above
+                                   go through them and the events sorted .. delayed_done
+                                   and `reuse` are not used (they may be NULL) */
 } emb_step_schedule;
 
 typedef struct {
@@ -456,6 +460,31 @@ int emb_event_create(void **event, int32_t timing);
 int emb_event_destroy(void *event);
 /* Milliseconds between two completed timing events. */
 int emb_event_elapsed_ms(void *start, void *end, float *ms);
+
+/* Step signals: the cross-stream order of emb_train_step kept through stream
+ * memory operations instead of events.  A handle holds one word of HIP signal
+ * memory per stage (sorted, coalesced, packed, updated, gathered,
+ * delayed_done) and a step counter.  Each emb_train_step call that names the
+ * handle takes the next step number n; the end of a stage writes n into its
+ * word (hipStreamWriteValue32) and a stream that must follow the stage of
+ * step n - k waits until the word reaches n - k (hipStreamWaitValue32, >=).
+ * The order is the one listed above for the events.  A wait never targets
+ * more than the value of the last write already enqueued for its word (a
+ * stage that did not run in the step waited for is waited for at its last
+ * run, or not at all), so every wait refers to an earlier enqueued write and
+ * the waits cannot deadlock, whatever modes the calls of a handle mix.
+ * On this runtime a wait on
+ * a pending event costs the host about four times as much as this write and
+ * wait, and with the host running ahead of the GPU nearly every wait is on a
+ * pending event; the GPU-side order is the same.
+ * Use one handle per table (both of its buffer sets), from one host thread.
+ * If a call fails part-way, every stage of its step is marked done so that no
+ * later wait blocks.  destroy: only once the work of every step enqueued with
+ * the handle has completed; the signal memory is kept for a later handle (it
+ * is never returned to the runtime).  create returns EMB_ERR_UNSUPPORTED if
+ * the device cannot wait on stream values. */
+int emb_step_signals_create(void **signals);
+int emb_step_signals_destroy(void *signals);
 
 /* Enqueue one training step of one table (see above).  Returns the first
  * failing call's status; nothing after it is enqueued. */

@@ -60,6 +60,8 @@ SIGNATURES = {
     "emb_event_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p), _I32]),
     "emb_event_destroy": (ctypes.c_int, [_P]),
     "emb_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
+    "emb_step_signals_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p)]),
+    "emb_step_signals_destroy": (ctypes.c_int, [_P]),
     "emb_train_step": (ctypes.c_int, [_P, _P]),
 }
 
@@ -68,7 +70,7 @@ class StepSchedule(ctypes.Structure):
     """emb_step_schedule of include/emb.h."""
     _fields_ = [("lookup_update", _P), ("coalesce", _P), ("pack", _P), ("delayed", _P), ("sorted", _P),
                 ("coalesced", _P), ("packed", _P), ("updated", _P), ("gathered", _P), ("delayed_done", _P),
-                ("reuse", _I32), ("by_owner", _I32), ("split", _I32), ("timing", _P * 8)]
+                ("reuse", _I32), ("by_owner", _I32), ("split", _I32), ("timing", _P * 8), ("signals", _P)]
 
 
 class StepArgs(ctypes.Structure):
@@ -152,6 +154,22 @@ class Event:
     def __del__(self):
         if getattr(self, "handle", None):
             self._lib.emb_event_destroy(self.handle)
+            self.handle = None
+
+
+class StepSignals:
+    """Step signals of one table (emb_step_signals_create); handed back to the library's pool when
+    the object goes away (only once the steps enqueued with it have completed)."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check(lib.emb_step_signals_create(ctypes.byref(h)), "emb_step_signals_create")
+        self.handle = h.value
+        self._lib = lib
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            self._lib.emb_step_signals_destroy(self.handle)
             self.handle = None
 
 

@@ -1,5 +1,18 @@
 // Step executor: one host call enqueues a whole training step of one table
-// on up to four streams with the event waits of the schedule in include/emb.h.
+// on up to four streams, with the cross-stream order of the schedule in
+// include/emb.h kept either by the caller's events or by step signals.
+//
+// Step signals are words of HIP signal memory, one per stage (sorted,
+// coalesced, packed, updated, gathered, delayed_done).  The end of a stage of
+// step n writes n into its word (hipStreamWriteValue32, after the stage's
+// kernels on that stream); a stream that must follow the stage of step n - k
+// waits for the word to reach n - k (hipStreamWaitValue32, ">=").  The step
+// numbers are kept by the handle, so the values only grow.  A wait on an event
+// that is still pending costs the host far more than these two operations,
+// and with the host running steps ahead of the GPU nearly every wait is.
+#include <mutex>
+#include <vector>
+
 #include "common.h"
 #include "launch.h"
 
@@ -8,13 +21,194 @@ namespace {
 hipStream_t S(void* p) { return static_cast<hipStream_t>(p); }
 hipEvent_t E(void* p) { return static_cast<hipEvent_t>(p); }
 
+int status_of(hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_ERR_LAUNCH; }
+
 int record(void* ev, void* stream) {
   if (ev == nullptr) return EMB_OK;
-  return hipEventRecord(E(ev), S(stream)) == hipSuccess ? EMB_OK : EMB_ERR_LAUNCH;
+  return status_of(hipEventRecord(E(ev), S(stream)));
 }
 
-int wait(void* stream, void* ev) {
-  return hipStreamWaitEvent(S(stream), E(ev), 0) == hipSuccess ? EMB_OK : EMB_ERR_LAUNCH;
+int wait(void* stream, void* ev) { return status_of(hipStreamWaitEvent(S(stream), E(ev), 0)); }
+
+enum Stage { kSorted = 0, kCoalesced, kPacked, kUpdated, kGathered, kDelayedDone, kStages };
+
+struct StepSignals {
+  int device;
+  void* word[kStages];       // hipMallocSignalMemory allocations
+  uint32_t seq;              // number of the last step enqueued with this handle
+  uint32_t written[kStages]; // the largest value a write already enqueued puts in each word
+  void* writer[kStages];     // the stream of that write
+};
+
+// Released handles are kept for reuse rather than freed, so that no signal
+// memory a queue may still poll is ever returned to the runtime.
+std::mutex g_pool_mu;
+std::vector<StepSignals*> g_pool;
+
+// The cross-stream order of one step.
+struct Order {
+  const emb_step_schedule* s;
+  StepSignals* sig;  // null: the schedule's events
+  uint32_t seq;      // this step's number (signals)
+
+  void* event(Stage k) const {
+    switch (k) {
+      case kSorted: return s->sorted;
+      case kCoalesced: return s->coalesced;
+      case kPacked: return s->packed;
+      case kUpdated: return s->updated;
+      case kGathered: return s->gathered;
+      default: return s->delayed_done;
+    }
+  }
+  // The event to attach to the last kernel of stage k (events only).
+  hipEvent_t attach(Stage k) const { return sig != nullptr ? nullptr : E(event(k)); }
+  // Stage k of this step ends here on `stream`; `attached`: its event was attached to the last kernel.
+  int done(Stage k, void* stream, bool attached = false) const {
+    if (sig != nullptr) return write(k, stream);
+    return attached ? EMB_OK : record(event(k), stream);
+  }
+  // Writes this step's number into word k on `stream`.  The values written to
+  // a word strictly increase (a second write of the same step is dropped), and
+  // the writes stay in enqueue order, so the value only grows: a write on
+  // another stream than the word's last one first waits for that write.
+  int write(Stage k, void* stream) const {
+    if (sig->written[k] >= seq) return EMB_OK;
+    if (sig->written[k] != 0 && sig->writer[k] != stream &&
+        hipStreamWaitValue32(S(stream), sig->word[k], sig->written[k], hipStreamWaitValueGte, 0xFFFFFFFFu) !=
+            hipSuccess)
+      return EMB_ERR_LAUNCH;
+    if (hipStreamWriteValue32(S(stream), sig->word[k], seq, 0) != hipSuccess) return EMB_ERR_LAUNCH;
+    sig->written[k] = seq;
+    sig->writer[k] = stream;
+    return EMB_OK;
+  }
+  // `stream` waits for stage k of the step `lag` steps back (lag 0: this step).
+  // With signals the target never exceeds what an enqueued write will put in
+  // the word: a stage that did not run in that step (another mode, a failed
+  // call) is waited for at its last run, or not at all if it never ran.  Every
+  // wait thus refers to a write enqueued before it, so the waits cannot form a
+  // cycle.
+  int after(void* stream, Stage k, uint32_t lag) const {
+    if (sig != nullptr) {
+      if (seq <= lag) return EMB_OK;  // no such step
+      const uint32_t target = seq - lag < sig->written[k] ? seq - lag : sig->written[k];
+      if (target == 0) return EMB_OK;  // the stage never ran
+      return status_of(hipStreamWaitValue32(S(stream), sig->word[k], target, hipStreamWaitValueGte, 0xFFFFFFFFu));
+    }
+    if (lag > 0 && !s->reuse) return EMB_OK;  // the buffer set was not used before
+    return wait(stream, event(k));
+  }
+  // After a failure part-way: mark every stage of this step done, so that no
+  // later wait is left without the write it needs.
+  void release_all() const {
+    if (sig == nullptr) return;
+    void* const streams[kStages] = {s->coalesce, s->pack, s->pack, s->lookup_update, s->lookup_update, s->delayed};
+    for (int k = 0; k < kStages; ++k) (void)write(static_cast<Stage>(k), streams[k]);
+  }
+};
+
+int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order& order) {
+  const bool sep_p = s->pack != s->lookup_update;
+  int st = EMB_OK;
+  // each step stops the sequence at the first failing call
+  auto ok = [&st](int r) { return (st = r) == EMB_OK; };
+  auto launched = [](hipError_t e) { return status_of(e); };
+  auto update = [&](int32_t groups_from, void* stream, void* t0, void* t1, Stage end_stage, bool announce) {
+    // Adam on the groups [groups_from, groups_from + P) of the send layout.  An
+    // event after the kernel is attached to its dispatch (less idle time on the
+    // stream than a separate marker): the timing event if any, else the end event.
+    const hipEvent_t end_ev = announce ? order.attach(end_stage) : nullptr;
+    const hipEvent_t first = t1 != nullptr ? E(t1) : end_ev;
+    return ok(emb::sparse_adam_call(a->table, a->exp_avg, a->exp_avg_sq, a->V, a->D, a->send_ids, a->send_rows,
+                                    a->send_offsets + groups_from, a->P, 0, a->P, a->cap_rows, a->lr, a->beta1,
+                                    a->beta2, a->eps, a->step, a->dev_status, S(stream), E(t0), first)) &&
+           (!announce || ok(order.done(end_stage, stream, t1 == nullptr && end_ev != nullptr)));
+  };
+  if (s->by_owner) {
+    // owner-major coalesce in its two halves: the sort on the coalesce stream,
+    // the reduction (straight into the send buffers) on the pack stream, the
+    // lookup and the update on the main stream; with the split, the delayed
+    // rows are updated on the delayed stream
+    emb::CoalesceVariant var;
+    var.row_owner = a->row_owner;
+    var.P = a->P;
+    if (s->split) {
+      var.next_ids = a->next_ids;
+      var.T_next = a->T_next;
+    }
+    const bool sep_sr = s->coalesce != s->pack;  // sort beside the reduction
+    // sort(s): after the reduction of step s-2 has finished with this set's workspace
+    if (sep_sr && !ok(order.after(s->coalesce, kCoalesced, 2))) return st;
+    if (!ok(record(s->timing[2], s->coalesce))) return st;
+    if (!ok(launched(emb::launch_coalesce_sort(a->ids, a->T, a->V, a->D, var, a->ws_coalesce, a->dev_status,
+                                               S(s->coalesce)))))
+      return st;
+    if (sep_sr && !ok(order.done(kSorted, s->coalesce))) return st;
+    // reduction(s): after the sort, and after the updates of step s-2 have read this set's send buffers
+    if (sep_sr && !ok(order.after(s->pack, kSorted, 0))) return st;
+    if (sep_p && !ok(order.after(s->pack, kUpdated, 2))) return st;
+    if (s->split && s->delayed != s->pack && !ok(order.after(s->pack, kDelayedDone, 2))) return st;
+    if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, var,
+                                                 a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
+                                                 a->send_counts, a->send_offsets, a->ws_coalesce, S(s->pack),
+                                                 order.attach(kCoalesced)))))
+      return st;
+    if (!ok(order.done(kCoalesced, s->pack, true))) return st;
+    if (!ok(record(s->timing[3], s->pack))) return st;
+    if (s->split) {
+      // lookup(s): after the delayed update of step s-2 (its rows may be in this
+      // batch; those of step s-1 are not, by construction)
+      const bool sep_d = s->delayed != s->lookup_update;
+      if (sep_d && !ok(order.after(s->lookup_update, kDelayedDone, 2))) return st;
+      if (!ok(record(s->timing[0], s->lookup_update))) return st;
+      if (!ok(launched(emb::launch_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status,
+                                          S(s->lookup_update), order.attach(kGathered)))))
+        return st;
+      if (!ok(order.done(kGathered, s->lookup_update, true))) return st;
+      if (!ok(record(s->timing[1], s->lookup_update))) return st;
+      // prior update(s): the rows the next lookup reads, right after this lookup
+      if (sep_p && !ok(order.after(s->lookup_update, kCoalesced, 0))) return st;
+      if (!update(0, s->lookup_update, s->timing[4], s->timing[5], kUpdated, true)) return st;
+      // delayed update(s): beside the next lookup (it reads none of these rows),
+      // after this step's lookup has read them and the reduction has written them
+      if (sep_d && !ok(order.after(s->delayed, kGathered, 0))) return st;
+      if (s->delayed != s->pack && !ok(order.after(s->delayed, kCoalesced, 0))) return st;
+      if (!update(a->P, s->delayed, s->timing[6], s->timing[7], kDelayedDone, true)) return st;
+      return EMB_OK;
+    }
+    // lookup(s), then update(s) once the rows are reduced
+    if (!ok(record(s->timing[0], s->lookup_update))) return st;
+    if (!ok(emb_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status, s->lookup_update))) return st;
+    if (!ok(record(s->timing[1], s->lookup_update))) return st;
+    if (sep_p && !ok(order.after(s->lookup_update, kCoalesced, 0))) return st;
+  } else {
+    // coalesce(s): after pack(s-2) has read this buffer set's unique rows
+    if (s->coalesce != s->pack && !ok(order.after(s->coalesce, kPacked, 2))) return st;
+    if (!ok(record(s->timing[2], s->coalesce))) return st;
+    if (!ok(emb_grad_coalesce(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->uniq_ids, a->seg_offsets,
+                              a->uniq_grad, a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes, a->dev_status,
+                              s->coalesce)))
+      return st;
+    if (!ok(record(s->timing[3], s->coalesce)) || !ok(order.done(kCoalesced, s->coalesce))) return st;
+    // pack(s): after coalesce(s), and after update(s-2) has read this set's send rows
+    if (s->pack != s->coalesce && !ok(order.after(s->pack, kCoalesced, 0))) return st;
+    if (sep_p && !ok(order.after(s->pack, kUpdated, 2))) return st;
+    if (!ok(record(s->timing[4], s->pack))) return st;
+    if (!ok(emb_pack_by_owner(a->uniq_ids, a->uniq_grad, a->num_unique, a->cap_rows, a->D, a->row_owner, a->V, a->P,
+                              a->send_ids, a->send_rows, a->send_counts, a->send_offsets, a->ws_pack,
+                              a->ws_pack_bytes, a->dev_status, s->pack)))
+      return st;
+    if (!ok(record(s->timing[5], s->pack)) || !ok(order.done(kPacked, s->pack))) return st;
+    // lookup(s) on the main stream, then update(s) once the rows are packed
+    if (!ok(record(s->timing[0], s->lookup_update))) return st;
+    if (!ok(emb_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status, s->lookup_update))) return st;
+    if (!ok(record(s->timing[1], s->lookup_update))) return st;
+    if (sep_p && !ok(order.after(s->lookup_update, kPacked, 0))) return st;
+  }
+  // the pack stream's next use of this set waits for `updated`
+  if (!update(0, s->lookup_update, s->timing[6], s->timing[7], kUpdated, sep_p)) return st;
+  return EMB_OK;
 }
 
 }  // namespace
@@ -40,117 +234,63 @@ int emb_event_elapsed_ms(void* start, void* end, float* ms) {
   return hipEventElapsedTime(ms, E(start), E(end)) == hipSuccess ? EMB_OK : EMB_ERR_LAUNCH;
 }
 
+int emb_step_signals_create(void** signals) {
+  if (signals == nullptr) return EMB_ERR_INVALID_ARG;
+  int dev = 0, can = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return EMB_ERR_LAUNCH;
+  if (hipDeviceGetAttribute(&can, hipDeviceAttributeCanUseStreamWaitValue, dev) != hipSuccess) return EMB_ERR_LAUNCH;
+  if (!can) return EMB_ERR_UNSUPPORTED;
+  {
+    std::lock_guard<std::mutex> lock(g_pool_mu);
+    for (size_t i = 0; i < g_pool.size(); ++i) {
+      if (g_pool[i]->device == dev) {  // values and step number carry on from the last user
+        *signals = g_pool[i];
+        g_pool.erase(g_pool.begin() + static_cast<std::ptrdiff_t>(i));
+        return EMB_OK;
+      }
+    }
+  }
+  auto* h = new StepSignals{};
+  h->device = dev;
+  for (int k = 0; k < kStages; ++k)  // on failure the partial handle is dropped, not freed
+    if (hipExtMallocWithFlags(&h->word[k], 8, hipMallocSignalMemory) != hipSuccess ||
+        hipStreamWriteValue32(nullptr, h->word[k], 0, 0) != hipSuccess)
+      return EMB_ERR_LAUNCH;
+  if (hipStreamSynchronize(nullptr) != hipSuccess) return EMB_ERR_LAUNCH;
+  *signals = h;
+  return EMB_OK;
+}
+
+int emb_step_signals_destroy(void* signals) {
+  if (signals == nullptr) return EMB_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lock(g_pool_mu);
+  g_pool.push_back(static_cast<StepSignals*>(signals));
+  return EMB_OK;
+}
+
 int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
   if (a == nullptr || s == nullptr) return EMB_ERR_INVALID_ARG;
   if (a->T < 0 || a->cap_rows < a->T) return EMB_ERR_INVALID_ARG;
-  if (s->coalesced == nullptr || s->updated == nullptr) return EMB_ERR_INVALID_ARG;
-  if (s->split && (!s->by_owner || s->sorted == nullptr || s->gathered == nullptr || s->delayed_done == nullptr ||
-                   a->T_next < 0 || a->T_next > a->cap_rows))  // streams may be NULL: the null stream
+  const bool events = s->signals == nullptr;
+  if (events && (s->coalesced == nullptr || s->updated == nullptr)) return EMB_ERR_INVALID_ARG;
+  if (s->split && (!s->by_owner || a->T_next < 0 || a->T_next > a->cap_rows))
+    return EMB_ERR_INVALID_ARG;  // streams may be NULL: the null stream
+  if (events && s->split && (s->sorted == nullptr || s->gathered == nullptr || s->delayed_done == nullptr))
     return EMB_ERR_INVALID_ARG;
-  if ((s->by_owner ? s->sorted : s->packed) == nullptr) return EMB_ERR_INVALID_ARG;
-  const bool sep_p = s->pack != s->lookup_update;
-  int st = EMB_OK;
-  // each step stops the sequence at the first failing call
-  auto ok = [&st](int r) { return (st = r) == EMB_OK; };
-  auto launched = [](hipError_t e) { return e == hipSuccess ? EMB_OK : EMB_ERR_LAUNCH; };
-  auto update = [&](int32_t groups_from, void* stream, void* t0, void* t1, void* end_event) {
-    // Adam on the groups [groups_from, groups_from + P) of the send layout; the
-    // event after the kernel is attached to its dispatch (less idle time on
-    // the stream than a separate marker), a second one is recorded after it
-    void* first = t1 != nullptr ? t1 : end_event;
-    void* second = t1 != nullptr ? end_event : nullptr;
-    return ok(emb::sparse_adam_call(a->table, a->exp_avg, a->exp_avg_sq, a->V, a->D, a->send_ids, a->send_rows,
-                                    a->send_offsets + groups_from, a->P, 0, a->P, a->cap_rows, a->lr, a->beta1,
-                                    a->beta2, a->eps, a->step, a->dev_status, S(stream), E(t0), E(first))) &&
-           ok(record(second, stream));
-  };
+  if (events && (s->by_owner ? s->sorted : s->packed) == nullptr) return EMB_ERR_INVALID_ARG;
+  // arguments of the calls that fail on the host, checked before anything is enqueued
   if (s->by_owner) {
-    // owner-major coalesce in its two halves: the sort on the coalesce stream,
-    // the reduction (straight into the send buffers) on the pack stream, the
-    // lookup and the update on the main stream; with the split, the delayed
-    // rows are updated on the delayed stream
-    emb::CoalesceVariant var;
-    var.row_owner = a->row_owner;
-    var.P = a->P;
-    if (s->split) {
-      var.next_ids = a->next_ids;
-      var.T_next = a->T_next;
-    }
-    if (!ok(emb::coalesce_by_owner_args_status(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->row_owner, a->P,
-                                               var.next_ids, var.T_next, a->send_ids, a->seg_offsets, a->send_rows,
-                                               a->send_counts, a->send_offsets, a->num_unique, a->ws_coalesce,
-                                               a->ws_coalesce_bytes)))
-      return st;
-    const bool sep_sr = s->coalesce != s->pack;  // sort beside the reduction
-    // sort(s): after the reduction of step s-2 has finished with this set's workspace
-    if (s->reuse && sep_sr && !ok(wait(s->coalesce, s->coalesced))) return st;
-    if (!ok(record(s->timing[2], s->coalesce))) return st;
-    if (!ok(launched(emb::launch_coalesce_sort(a->ids, a->T, a->V, a->D, var, a->ws_coalesce, a->dev_status,
-                                               S(s->coalesce)))))
-      return st;
-    if (sep_sr && !ok(record(s->sorted, s->coalesce))) return st;
-    // reduction(s): after the sort, and after the updates of step s-2 have read this set's send buffers
-    if (sep_sr && !ok(wait(s->pack, s->sorted))) return st;
-    if (s->reuse && sep_p && !ok(wait(s->pack, s->updated))) return st;
-    if (s->reuse && s->split && s->delayed != s->pack && !ok(wait(s->pack, s->delayed_done))) return st;
-    if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, var,
-                                                 a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
-                                                 a->send_counts, a->send_offsets, a->ws_coalesce, S(s->pack),
-                                                 E(s->coalesced)))))
-      return st;
-    if (!ok(record(s->timing[3], s->pack))) return st;
-    if (s->split) {
-      // lookup(s): after the delayed update of step s-2 (its rows may be in this
-      // batch; those of step s-1 are not, by construction)
-      const bool sep_d = s->delayed != s->lookup_update;
-      if (s->reuse && sep_d && !ok(wait(s->lookup_update, s->delayed_done))) return st;
-      if (!ok(record(s->timing[0], s->lookup_update))) return st;
-      if (!ok(launched(emb::launch_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status,
-                                          S(s->lookup_update), E(s->gathered)))))
-        return st;
-      if (!ok(record(s->timing[1], s->lookup_update))) return st;
-      // prior update(s): the rows the next lookup reads, right after this lookup
-      if (sep_p && !ok(wait(s->lookup_update, s->coalesced))) return st;
-      if (!update(0, s->lookup_update, s->timing[4], s->timing[5], s->updated)) return st;
-      // delayed update(s): beside the next lookup (it reads none of these rows),
-      // after this step's lookup has read them and the reduction has written them
-      if (sep_d && !ok(wait(s->delayed, s->gathered))) return st;
-      if (s->delayed != s->pack && !ok(wait(s->delayed, s->coalesced))) return st;
-      if (!update(a->P, s->delayed, s->timing[6], s->timing[7], s->delayed_done)) return st;
-      return EMB_OK;
-    }
-    // lookup(s), then update(s) once the rows are reduced
-    if (!ok(record(s->timing[0], s->lookup_update))) return st;
-    if (!ok(emb_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status, s->lookup_update))) return st;
-    if (!ok(record(s->timing[1], s->lookup_update))) return st;
-    if (sep_p && !ok(wait(s->lookup_update, s->coalesced))) return st;
-  } else {
-    // coalesce(s): after pack(s-2) has read this buffer set's unique rows
-    if (s->reuse && s->coalesce != s->pack && !ok(wait(s->coalesce, s->packed))) return st;
-    if (!ok(record(s->timing[2], s->coalesce))) return st;
-    if (!ok(emb_grad_coalesce(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->uniq_ids, a->seg_offsets,
-                              a->uniq_grad, a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes, a->dev_status,
-                              s->coalesce)))
-      return st;
-    if (!ok(record(s->timing[3], s->coalesce)) || !ok(record(s->coalesced, s->coalesce))) return st;
-    // pack(s): after coalesce(s), and after update(s-2) has read this set's send rows
-    if (s->pack != s->coalesce && !ok(wait(s->pack, s->coalesced))) return st;
-    if (s->reuse && sep_p && !ok(wait(s->pack, s->updated))) return st;
-    if (!ok(record(s->timing[4], s->pack))) return st;
-    if (!ok(emb_pack_by_owner(a->uniq_ids, a->uniq_grad, a->num_unique, a->cap_rows, a->D, a->row_owner, a->V, a->P,
-                              a->send_ids, a->send_rows, a->send_counts, a->send_offsets, a->ws_pack,
-                              a->ws_pack_bytes, a->dev_status, s->pack)))
-      return st;
-    if (!ok(record(s->timing[5], s->pack)) || !ok(record(s->packed, s->pack))) return st;
-    // lookup(s) on the main stream, then update(s) once the rows are packed
-    if (!ok(record(s->timing[0], s->lookup_update))) return st;
-    if (!ok(emb_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status, s->lookup_update))) return st;
-    if (!ok(record(s->timing[1], s->lookup_update))) return st;
-    if (sep_p && !ok(wait(s->lookup_update, s->packed))) return st;
+    const int st = emb::coalesce_by_owner_args_status(
+        a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->row_owner, a->P, s->split ? a->next_ids : nullptr,
+        s->split ? a->T_next : -1, a->send_ids, a->seg_offsets, a->send_rows, a->send_counts, a->send_offsets,
+        a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes);
+    if (st != EMB_OK) return st;
   }
-  // the pack stream's next use of this set waits for `updated`
-  if (!update(0, s->lookup_update, s->timing[6], s->timing[7], sep_p ? s->updated : nullptr)) return st;
-  return EMB_OK;
+  Order order{s, static_cast<StepSignals*>(s->signals), 0};
+  if (order.sig != nullptr) order.seq = ++order.sig->seq;
+  const int st = enqueue_step(a, s, order);
+  if (st != EMB_OK) order.release_all();
+  return st;
 }
 
 }  // extern "C"

@@ -1,5 +1,6 @@
 """The overlapped step schedules give bitwise the same table, moments and
-lookups as running their calls one after another on one stream; the
+lookups as running their calls one after another on one stream, with the
+cross-stream order kept by events or by step signals; the
 owner-major schedule (coalesce straight into the send layout) agrees with
 coalesce-then-pack, and the prior / delayed split with one update, to the
 fp32 tolerance (their sums add in another grouping)."""
@@ -14,7 +15,7 @@ from workloads import configs, gen
 pytestmark = pytest.mark.gpu
 
 
-def run(overlap, by_owner, steps=7, split=False):
+def run(overlap, by_owner, steps=7, split=False, signals=False):
     torch.cuda.synchronize()
     specs = [configs.TableSpec(20000, 128, 6000, "zipf", 1.05, "f32", 0.01, 8, "mod", 61),
              configs.TableSpec(5000, 64, 3000, "uniform", 0.0, "bf16", 0.01, 3, "range", 62)]
@@ -32,7 +33,8 @@ def run(overlap, by_owner, steps=7, split=False):
             per.append((torch.from_numpy(ids).cuda(), g))
         batches.append(per)
     torch.cuda.synchronize()
-    pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner, split=split)
+    pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner, split=split,
+                        signals=signals)
     lookups = []
     empty = torch.zeros(0, dtype=torch.int32, device="cuda")
     for t in range(1, steps + 1):
@@ -46,9 +48,11 @@ def run(overlap, by_owner, steps=7, split=False):
            [[x.cpu().numpy() for x in l] for l in lookups]
 
 
+@pytest.mark.parametrize("signals", [True, False], ids=["signals", "events"])
 @pytest.mark.parametrize("by_owner,split", [(False, False), (True, False), (True, True)])
-def test_overlapped_schedule_equals_sequential(by_owner, split):
-    a, la = run(True, by_owner, split=split)
+def test_overlapped_schedule_equals_sequential(by_owner, split, signals):
+    print(f"overlapped vs sequential by_owner={by_owner} split={split} signals={signals}", flush=True)
+    a, la = run(True, by_owner, split=split, signals=signals)
     b, lb = run(False, by_owner, split=split)
     for x, y in zip(a, b):
         for u, v in zip(x, y):
@@ -81,3 +85,44 @@ def test_split_schedule_matches_one_update():
     for x, y in zip(la, lb):
         for u, v in zip(x, y):
             tolerance.assert_rows_close(u, v, tolerance.RTOL_F32, "lookup")
+
+
+def test_failed_step_leaves_no_wait_blocked():
+    """A step that fails on the host part-way (here: the pack workspace of one call is declared
+    too small, after the coalesce was enqueued) marks its stages done, so the later steps of the
+    same step-signal handle run to the end and give the table of the sequential schedule when
+    the failed step is left out of both."""
+    import paper_2110_09132_amd as emb
+
+    def go(overlap):
+        torch.cuda.synchronize()
+        sp = configs.TableSpec(3000, 64, 2000, "zipf", 1.1, "f32", 0.01, 4, "mod", 63)
+        tb = EmbeddingTable(torch.from_numpy(configs.make_weights(sp)).cuda(),
+                            torch.from_numpy(configs.row_owner(sp)).cuda(), sp.P, sp.T)
+        pipe = StepPipeline([tb], 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=False, signals=True)
+        bs = []
+        for s in range(3):
+            ids, G = configs.make_batch(sp, s)
+            bs.append([(torch.from_numpy(ids).cuda(), torch.from_numpy(G).cuda())])
+        t = 0
+        for k in range(6):
+            if k == 2 and overlap:
+                i = pipe.count % 2
+                good = pipe.args[0][i].ws_pack_bytes
+                pipe.args[0][i].ws_pack_bytes = 1
+                with pytest.raises(emb.EmbError):
+                    pipe.step(bs[k % 3], t + 1)
+                pipe.args[0][i].ws_pack_bytes = good
+                pipe.count += 1  # the failed call's buffer set is skipped as if used
+                continue
+            if k == 2:
+                continue
+            t += 1
+            pipe.step(bs[k % 3], t)
+        pipe.finish()
+        torch.cuda.synchronize()
+        return tb.W.cpu().numpy()
+    print("failed step, then four more steps", flush=True)
+    a = go(True)
+    b = go(False)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
