@@ -301,9 +301,12 @@ def main():
                          "the prior/delayed split of Vertical Sparse Scheduling (emb_grad_coalesce_split; the "
                          "delayed update beside the next lookup); unfused: emb_grad_coalesce then "
                          "emb_pack_by_owner")
-    ap.add_argument("--order", choices=("signals", "events"), default="events",
-                    help="cross-stream order of the overlapped schedule: step signals (stream memory operations) "
-                         "or events")
+    ap.add_argument("--sort-streams", type=int, choices=(1, 2), default=2,
+                    help="by_owner: run the sorts of the two buffer sets on one or two side streams")
+    ap.add_argument("--order", choices=("auto", "signals", "events"), default="auto",
+                    help="cross-stream order of the overlapped schedule: step signals (stream memory operations), "
+                         "events, or auto: the faster of the two over --tune-steps untimed steps each")
+    ap.add_argument("--tune-steps", type=int, default=30)
     ap.add_argument("--summarize-trace", metavar="DIR", help="print a summary of a rocprofv3 kernel-stats run")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the scaled HBM traffic of the update kernel from two rocprofv3 --pmc runs")
@@ -364,13 +367,38 @@ def main():
 
     split = args.schedule == "split"
     by_owner = args.schedule != "unfused"
-    pipe = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential, by_owner=by_owner,
-                        split=split, signals=args.order == "signals")
+    def make_pipe(order):
+        return StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential,
+                            by_owner=by_owner, split=split, signals=order == "signals",
+                            sort_streams=args.sort_streams)
 
     def next_ids(t):
         return [x[0] for x in step_batches[(t + 1) % args.batches]] if split else None
 
     t = 0
+    # order "auto": time a few untimed steps with each cross-stream order and keep the faster
+    # (events cost the GPU nothing but the host ~85 us per overlapped step; step signals halve
+    # the host's cost but add small runtime kernels to the streams)
+    tune_ms = {}
+    order = args.order
+    if args.order == "auto" and not args.sequential:
+        for o in ("events", "signals"):
+            trial = make_pipe(o)
+            for k in range(5 + args.tune_steps):
+                if k == 5:
+                    trial.finish()
+                    torch.cuda.synchronize()
+                    t_start = time.perf_counter()
+                t += 1
+                trial.step(step_batches[t % args.batches], t, next_ids=next_ids(t))
+            trial.finish()
+            torch.cuda.synchronize()
+            tune_ms[o] = (time.perf_counter() - t_start) * 1e3 / args.tune_steps
+            del trial
+        order = min(tune_ms, key=tune_ms.get)
+    elif args.order == "auto":
+        order = "events"
+    pipe = make_pipe(order)
     for _ in range(args.warmup):
         t += 1
         pipe.step(step_batches[t % args.batches], t, next_ids=next_ids(t))
@@ -475,9 +503,11 @@ def main():
                     "by_owner": "sort and reduction on two side streams; lookup and update on the main stream",
                     "unfused": "coalesce and pack on two side streams; lookup and update on the main stream"}[
                        args.schedule],
+                   "sort_streams": None if (args.sequential or split or not by_owner) else args.sort_streams,
                    "cross_stream_order": None if args.sequential else
                    {"signals": "step signals (hipStreamWriteValue32 / hipStreamWaitValue32)",
-                    "events": "events (hipEventRecord / hipStreamWaitEvent)"}[args.order],
+                    "events": "events (hipEventRecord / hipStreamWaitEvent)"}[order],
+                   "order_tuning_ms_per_step": tune_ms or None,
                    "prior_rows_frac": prior_frac if split else None},
         "step_bytes_model": total_bytes,
         "step_bytes_model_kind": "fused minimum (pack folded into coalesce)" if by_owner else "four calls",

@@ -60,6 +60,11 @@ using Narrow = SortCfg<256, 8>;
 constexpr int kChunk = 32;                    // sorted tokens per reduction wave
 constexpr int kRedTile = kChunk * kWaves;     // sorted tokens per reduction workgroup
 constexpr int kLoadsInFlight = 8;
+// The combine of ids that cross chunks: one workgroup per such id, its waves
+// splitting the id's chunk pieces; wide, so that a hot id's hundreds of pieces
+// are summed by many waves at once.
+constexpr int kCombineThreads = 1024;
+constexpr int kCombineWaves = kCombineThreads / kWave;
 constexpr uint32_t kSpinLimit = 1u << 22;
 
 // Look-back status word: value in the low 30 bits, state in the top 2 bits.
@@ -636,7 +641,7 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
 }
 
 template <int VEC>
-__global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __restrict__ partial, int D,
+__global__ __launch_bounds__(kCombineThreads) void seg_combine_kernel(const float* __restrict__ partial, int D,
                                                                const int32_t* __restrict__ seg_offsets,
                                                                const int32_t* __restrict__ span_list,
                                                                const int32_t* __restrict__ span_count,
@@ -645,9 +650,9 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
                                                                int32_t* __restrict__ owner_counts, int P, int T,
                                                                int nchunks) {
   using Acc = typename GradRow<false, VEC>::Acc;
-  __shared__ Acc red[kWaves][kWave];
+  __shared__ Acc red[kCombineWaves][kWave];
   if (owner_counts != nullptr && blockIdx.x == 0)
-    for (int p = threadIdx.x; p < P; p += kThreads) owner_counts[p] = owner_offsets[p + 1] - owner_offsets[p];
+    for (int p = threadIdx.x; p < P; p += kCombineThreads) owner_counts[p] = owner_offsets[p + 1] - owner_offsets[p];
   const int n = min(span_count[0], nchunks);
   const int Dv = D / VEC;
   const int w = threadIdx.x / kWave;
@@ -661,8 +666,8 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
     const int c0 = S / kChunk;
     const int np = (E - 1) / kChunk - c0 + 1;
     const int first_slot = (S == c0 * kChunk) ? 0 : 1;
-    const int p_beg = static_cast<int>((static_cast<long long>(w) * np) / kWaves);
-    const int p_end = static_cast<int>((static_cast<long long>(w + 1) * np) / kWaves);
+    const int p_beg = static_cast<int>((static_cast<long long>(w) * np) / kCombineWaves);
+    const int p_end = static_cast<int>((static_cast<long long>(w + 1) * np) / kCombineWaves);
     for (int cb = 0; cb < Dv; cb += kWave) {
       const int c = cb + static_cast<int>(lane_id());
       const bool colok = c < Dv;
@@ -685,7 +690,7 @@ __global__ __launch_bounds__(kThreads) void seg_combine_kernel(const float* __re
       if (w == 0 && colok) {
         Acc t = red[0][lane_id()];
 #pragma unroll
-        for (int q = 1; q < kWaves; ++q) t += red[q][lane_id()];
+        for (int q = 1; q < kCombineWaves; ++q) t += red[q][lane_id()];
         out_rows[static_cast<size_t>(u) * Dv + c] = t;
       }
       __syncthreads();
@@ -884,13 +889,14 @@ hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D
   // 5. segments and per-chunk sums; 6. pieces of ids that cross chunks
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(grad) % (grad_bf16 ? 8 : 16) == 0) &&
                     (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
-  const dim3 cgrid(grid_for(nchunks, 1024));
+  const dim3 cgrid(grid_for(nchunks, 256));
 #define EMB_REDUCE(BF, VC)                                                                                          \
   hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred), dim3(kThreads), 0, stream, kin, vin, ws.n_valid, T, \
                      grad, D, ws.tile_heads, ks, uniq_ids, seg_offsets, num_unique, uniq_grad, group_offsets,        \
                      ws.partial, ws.span_list, ws.span_count, nchunks)
 #define EMB_COMBINE(VC)                                                                                             \
-  hipExtLaunchKernelGGL(seg_combine_kernel<VC>, cgrid, dim3(kThreads), 0, stream, nullptr, done, 0, ws.partial, D,  \
+  hipExtLaunchKernelGGL(seg_combine_kernel<VC>, cgrid, dim3(kCombineThreads), 0, stream, nullptr, done, 0,         \
+                        ws.partial, D,                                                                               \
                         seg_offsets, ws.span_list, ws.span_count, uniq_grad, group_offsets, group_counts, ks.G, T,  \
                         nchunks)
   if (vec4) {

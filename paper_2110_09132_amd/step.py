@@ -84,11 +84,15 @@ class StepPipeline:
     """Enqueues training steps of the hot path for a list of tables."""
 
     def __init__(self, tables, lr, beta1, beta2, eps, overlap: bool = True, dev_status: torch.Tensor | None = None,
-                 streams: int = 3, by_owner: bool = True, split: bool = False, signals: bool = False):
+                 streams: int = 3, by_owner: bool = True, split: bool = False, signals: bool = False,
+                 sort_streams: int = 1):
         """streams (with overlap=True and by_owner=False): 2 puts coalesce and pack on one side
         stream, 3 gives each its own (more concurrency, one more cross-stream wait per step).
         by_owner: coalesce straight into the send layout (emb_grad_coalesce_by_owner).
         split: the prior / delayed split (implies by_owner); step() then needs the next ids.
+        sort_streams (by_owner without the split, overlap=True): 2 runs the sorts of the two buffer
+        sets on two side streams, so that a step's sort can run beside the previous step's (they
+        share nothing; each waits only for the reduction of its own set two steps back).
         signals (with overlap=True): keep the cross-stream order with step signals (stream memory
         operations: about half the host time per step, for host-bound pipelines of small
         batches; with large batches events keep the GPU a few percent busier) instead of events."""
@@ -101,6 +105,8 @@ class StepPipeline:
         self.side = s1 if overlap else self.main  # coalesce (by_owner: its sort)
         self.side2 = s2 if (overlap and streams >= 3) else self.side  # pack (by_owner: the reduction)
         self.side3 = s3 if (overlap and split) else self.main  # the delayed update
+        # the sorts of buffer set 1 (by_owner without the split): the third side stream
+        self.side3_sort = s3 if (overlap and self.by_owner and not split and sort_streams >= 2) else None
         self.count = 0
         self.events = []  # keeps the library events alive
         self.signals = [StepSignals() for _ in self.tables] if (overlap and signals) else []
@@ -122,7 +128,8 @@ class StepPipeline:
                              beta2=beta2, eps=eps, dev_status=st)
                 evs = [Event() for _ in range(6)]
                 self.events += evs
-                s = StepSchedule(lookup_update=_stream_handle(self.main), coalesce=_stream_handle(self.side),
+                sort_side = self.side3_sort if (i == 1 and self.side3_sort is not None) else self.side
+                s = StepSchedule(lookup_update=_stream_handle(self.main), coalesce=_stream_handle(sort_side),
                                  pack=_stream_handle(self.side2), delayed=_stream_handle(self.side3),
                                  sorted=evs[0].handle, coalesced=evs[1].handle, packed=evs[2].handle,
                                  updated=evs[3].handle, gathered=evs[4].handle, delayed_done=evs[5].handle,
@@ -141,7 +148,7 @@ class StepPipeline:
         the last step).  Inputs must be ready on the main stream when the first step is enqueued."""
         i = self.count % 2
         if self.count == 0 and self.overlap:
-            for side in {self.side, self.side2, self.side3} - {self.main}:
+            for side in self._sides():
                 side.wait_stream(self.main)
         if self.split and (next_ids is None or len(next_ids) != len(batches)):
             raise ValueError("the split schedule needs the next step's ids of every table")
@@ -166,7 +173,10 @@ class StepPipeline:
             _check(lib.emb_train_step(ctypes.byref(a), ctypes.byref(s)), "emb_train_step")
         self.count += 1
 
+    def _sides(self):
+        return {x for x in (self.side, self.side2, self.side3, self.side3_sort) if x is not None} - {self.main}
+
     def finish(self):
         """Make the main stream wait for everything enqueued on the side streams."""
-        for side in {self.side, self.side2, self.side3} - {self.main}:
+        for side in self._sides():
             self.main.wait_stream(side)

@@ -15,7 +15,7 @@ from workloads import configs, gen
 pytestmark = pytest.mark.gpu
 
 
-def run(overlap, by_owner, steps=7, split=False, signals=False):
+def run(overlap, by_owner, steps=7, split=False, signals=False, sort_streams=1):
     torch.cuda.synchronize()
     specs = [configs.TableSpec(20000, 128, 6000, "zipf", 1.05, "f32", 0.01, 8, "mod", 61),
              configs.TableSpec(5000, 64, 3000, "uniform", 0.0, "bf16", 0.01, 3, "range", 62)]
@@ -34,7 +34,7 @@ def run(overlap, by_owner, steps=7, split=False, signals=False):
         batches.append(per)
     torch.cuda.synchronize()
     pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner, split=split,
-                        signals=signals)
+                        signals=signals, sort_streams=sort_streams)
     lookups = []
     empty = torch.zeros(0, dtype=torch.int32, device="cuda")
     for t in range(1, steps + 1):
@@ -54,6 +54,19 @@ def test_overlapped_schedule_equals_sequential(by_owner, split, signals):
     print(f"overlapped vs sequential by_owner={by_owner} split={split} signals={signals}", flush=True)
     a, la = run(True, by_owner, split=split, signals=signals)
     b, lb = run(False, by_owner, split=split)
+    for x, y in zip(a, b):
+        for u, v in zip(x, y):
+            assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
+    for x, y in zip(la, lb):
+        for u, v in zip(x, y):
+            assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
+
+
+@pytest.mark.parametrize("signals", [False, True], ids=["events", "signals"])
+def test_two_sort_streams_equal_sequential(signals):
+    print(f"two sort streams, signals={signals}", flush=True)
+    a, la = run(True, True, signals=signals, sort_streams=2)
+    b, lb = run(False, True)
     for x, y in zip(a, b):
         for u, v in zip(x, y):
             assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
