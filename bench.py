@@ -303,6 +303,8 @@ def main():
                          "emb_pack_by_owner")
     ap.add_argument("--sort-streams", type=int, choices=(1, 2), default=2,
                     help="by_owner: run the sorts of the two buffer sets on one or two side streams")
+    ap.add_argument("--sets", type=int, default=4,
+                    help="buffer sets rotated between steps (the split schedule uses 2)")
     ap.add_argument("--order", choices=("auto", "signals", "events"), default="auto",
                     help="cross-stream order of the overlapped schedule: step signals (stream memory operations), "
                          "events, or auto: the faster of the two over --tune-steps untimed steps each")
@@ -339,7 +341,8 @@ def main():
     for sp in wl.tables:
         gdt = torch.bfloat16 if sp.grad_dtype == "bf16" else torch.float32
         W = torch.from_numpy(configs.make_weights(sp)).to(dev)
-        tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).to(dev), sp.P, sp.T, gdt))
+        tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).to(dev), sp.P, sp.T, gdt,
+                                     sets=max(2, args.sets)))
         tb_batches = []
         for b in range(args.batches):
             ids, G = configs.make_batch(sp, 1000 + b)
@@ -370,7 +373,7 @@ def main():
     def make_pipe(order):
         return StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential,
                             by_owner=by_owner, split=split, signals=order == "signals",
-                            sort_streams=args.sort_streams)
+                            sort_streams=args.sort_streams, sets=2 if split else args.sets)
 
     def next_ids(t):
         return [x[0] for x in step_batches[(t + 1) % args.batches]] if split else None
@@ -504,6 +507,7 @@ def main():
                     "unfused": "coalesce and pack on two side streams; lookup and update on the main stream"}[
                        args.schedule],
                    "sort_streams": None if (args.sequential or split or not by_owner) else args.sort_streams,
+                   "buffer_sets": 2 if split else args.sets,
                    "cross_stream_order": None if args.sequential else
                    {"signals": "step signals (hipStreamWriteValue32 / hipStreamWaitValue32)",
                     "events": "events (hipEventRecord / hipStreamWaitEvent)"}[order],

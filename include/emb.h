@@ -361,9 +361,10 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  * Sec. 4.2.2, here on one GPU).  One host call per step keeps the host ahead
  * of the GPU.
  *
- * The caller alternates two buffer sets (coalesce workspace, uniq_* and send_*
- * outputs) between consecutive steps and gives each set its own events;
- * `reuse` is nonzero when the set was used two steps earlier.
+ * The caller rotates buffer sets (coalesce workspace, uniq_* and send_*
+ * outputs; two unless `sets` says more) between consecutive steps and gives
+ * each set its own events; `reuse` is nonzero when the set was used before.
+ * Below, "s-2" is the set's previous step, s - sets.
  *
  * by_owner == 0: emb_grad_coalesce on the `coalesce` stream, emb_pack_by_owner
  * on the `pack` stream, lookup and update on `lookup_update`, with the waits
@@ -393,7 +394,8 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  * `lookup_update` right after the lookup, the delayed rows on the `delayed`
  * stream, beside the next lookup, which reads none of them.  Both parts use
  * the same Adam step.  Waits, in addition to the above:
- *   lookup(s)   after delayed update(s-2)      (its rows may be in this batch)
+ *   lookup(s)   after delayed update of the step two back (its rows may be in
+ *               this batch; this one is two steps whatever `sets` is)
  *   prior(s)    after reduce(s)
  *   delayed(s)  after reduce(s), lookup(s)     (reads the send rows; lookup(s) reads its rows)
  *   reduce(s)   after delayed update(s-2)      (same send buffers)
@@ -425,6 +427,10 @@ typedef struct {
                                    (emb_step_signals_create): when set, the waits above
                                    go through them and the events sorted .. delayed_done
                                    and `reuse` are not used (they may be NULL) */
+  int32_t sets;                 /* buffer sets the caller rotates (0: 2; at most 64): the
+                                   waits for a set's earlier use ("s-2" above) reach back
+                                   this many steps; `reuse` means the set was used `sets`
+                                   steps ago.  With events the split needs 2 */
 } emb_step_schedule;
 
 typedef struct {

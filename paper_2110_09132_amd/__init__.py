@@ -70,7 +70,7 @@ class StepSchedule(ctypes.Structure):
     """emb_step_schedule of include/emb.h."""
     _fields_ = [("lookup_update", _P), ("coalesce", _P), ("pack", _P), ("delayed", _P), ("sorted", _P),
                 ("coalesced", _P), ("packed", _P), ("updated", _P), ("gathered", _P), ("delayed_done", _P),
-                ("reuse", _I32), ("by_owner", _I32), ("split", _I32), ("timing", _P * 8), ("signals", _P)]
+                ("reuse", _I32), ("by_owner", _I32), ("split", _I32), ("timing", _P * 8), ("signals", _P), ("sets", _I32)]
 
 
 class StepArgs(ctypes.Structure):

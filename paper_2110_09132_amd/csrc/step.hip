@@ -50,6 +50,7 @@ struct Order {
   const emb_step_schedule* s;
   StepSignals* sig;  // null: the schedule's events
   uint32_t seq;      // this step's number (signals)
+  uint32_t sets;     // buffer sets in rotation: a set's buffers come back after this many steps
 
   void* event(Stage k) const {
     switch (k) {
@@ -84,6 +85,8 @@ struct Order {
     return EMB_OK;
   }
   // `stream` waits for stage k of the step `lag` steps back (lag 0: this step).
+  // With events, a lag > 0 means the step that last used this buffer set (the
+  // set's own event), so it must equal `sets`.
   // With signals the target never exceeds what an enqueued write will put in
   // the word: a stage that did not run in that step (another mode, a failed
   // call) is waited for at its last run, or not at all if it never ran.  Every
@@ -138,17 +141,17 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
       var.T_next = a->T_next;
     }
     const bool sep_sr = s->coalesce != s->pack;  // sort beside the reduction
-    // sort(s): after the reduction of step s-2 has finished with this set's workspace
-    if (sep_sr && !ok(order.after(s->coalesce, kCoalesced, 2))) return st;
+    // sort(s): after the reduction of the set's last step (s - sets) has finished with its workspace
+    if (sep_sr && !ok(order.after(s->coalesce, kCoalesced, order.sets))) return st;
     if (!ok(record(s->timing[2], s->coalesce))) return st;
     if (!ok(launched(emb::launch_coalesce_sort(a->ids, a->T, a->V, a->D, var, a->ws_coalesce, a->dev_status,
                                                S(s->coalesce)))))
       return st;
     if (sep_sr && !ok(order.done(kSorted, s->coalesce))) return st;
-    // reduction(s): after the sort, and after the updates of step s-2 have read this set's send buffers
+    // reduction(s): after the sort, and after the updates of step s - sets have read this set's send buffers
     if (sep_sr && !ok(order.after(s->pack, kSorted, 0))) return st;
-    if (sep_p && !ok(order.after(s->pack, kUpdated, 2))) return st;
-    if (s->split && s->delayed != s->pack && !ok(order.after(s->pack, kDelayedDone, 2))) return st;
+    if (sep_p && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
+    if (s->split && s->delayed != s->pack && !ok(order.after(s->pack, kDelayedDone, order.sets))) return st;
     if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, var,
                                                  a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
                                                  a->send_counts, a->send_offsets, a->ws_coalesce, S(s->pack),
@@ -183,17 +186,17 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     if (!ok(record(s->timing[1], s->lookup_update))) return st;
     if (sep_p && !ok(order.after(s->lookup_update, kCoalesced, 0))) return st;
   } else {
-    // coalesce(s): after pack(s-2) has read this buffer set's unique rows
-    if (s->coalesce != s->pack && !ok(order.after(s->coalesce, kPacked, 2))) return st;
+    // coalesce(s): after pack(s - sets) has read this buffer set's unique rows
+    if (s->coalesce != s->pack && !ok(order.after(s->coalesce, kPacked, order.sets))) return st;
     if (!ok(record(s->timing[2], s->coalesce))) return st;
     if (!ok(emb_grad_coalesce(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->uniq_ids, a->seg_offsets,
                               a->uniq_grad, a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes, a->dev_status,
                               s->coalesce)))
       return st;
     if (!ok(record(s->timing[3], s->coalesce)) || !ok(order.done(kCoalesced, s->coalesce))) return st;
-    // pack(s): after coalesce(s), and after update(s-2) has read this set's send rows
+    // pack(s): after coalesce(s), and after update(s - sets) has read this set's send rows
     if (s->pack != s->coalesce && !ok(order.after(s->pack, kCoalesced, 0))) return st;
-    if (sep_p && !ok(order.after(s->pack, kUpdated, 2))) return st;
+    if (sep_p && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
     if (!ok(record(s->timing[4], s->pack))) return st;
     if (!ok(emb_pack_by_owner(a->uniq_ids, a->uniq_grad, a->num_unique, a->cap_rows, a->D, a->row_owner, a->V, a->P,
                               a->send_ids, a->send_rows, a->send_counts, a->send_offsets, a->ws_pack,
@@ -278,6 +281,10 @@ int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
   if (events && s->split && (s->sorted == nullptr || s->gathered == nullptr || s->delayed_done == nullptr))
     return EMB_ERR_INVALID_ARG;
   if (events && (s->by_owner ? s->sorted : s->packed) == nullptr) return EMB_ERR_INVALID_ARG;
+  const uint32_t sets = s->sets == 0 ? 2u : static_cast<uint32_t>(s->sets);
+  // the split's lookup waits for the delayed update two steps back, a data
+  // dependency that the set's own events express only with two sets
+  if (s->sets < 0 || s->sets > 64 || (events && s->split && sets != 2)) return EMB_ERR_INVALID_ARG;
   // arguments of the calls that fail on the host, checked before anything is enqueued
   if (s->by_owner) {
     const int st = emb::coalesce_by_owner_args_status(
@@ -286,7 +293,7 @@ int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
         a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes);
     if (st != EMB_OK) return st;
   }
-  Order order{s, static_cast<StepSignals*>(s->signals), 0};
+  Order order{s, static_cast<StepSignals*>(s->signals), 0, sets};
   if (order.sig != nullptr) order.seq = ++order.sig->seq;
   const int st = enqueue_step(a, s, order);
   if (st != EMB_OK) order.release_all();

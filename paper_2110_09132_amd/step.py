@@ -17,7 +17,7 @@ the lookup and the update stay on the main stream:
                   next lookup.
 The executor adds the cross-stream waits that keep every data dependency (see
 emb_train_step in include/emb.h), through events or step signals.  This module only allocates the buffers,
-alternates the two buffer sets and fills in the arguments.
+rotates the buffer sets and fills in the arguments.
 """
 from __future__ import annotations
 
@@ -37,7 +37,7 @@ class EmbeddingTable:
     """Device state of one table (W, Adam moments, row owners) and the buffers of its steps."""
 
     def __init__(self, W: torch.Tensor, row_owner: torch.Tensor, P: int, T_cap: int,
-                 grad_dtype: torch.dtype = torch.float32):
+                 grad_dtype: torch.dtype = torch.float32, sets: int = 2):
         dev = W.device
         self.V, self.D = W.shape
         self.P, self.T_cap = P, T_cap
@@ -47,18 +47,19 @@ class EmbeddingTable:
         self.row_owner = row_owner
         i32, f32 = torch.int32, torch.float32
         self.lookup = torch.empty((T_cap, self.D), dtype=f32, device=dev)
-        # two buffer sets, alternated between consecutive steps
+        # `sets` buffer sets, rotated between consecutive steps
+        self.sets = sets
         self.coals = [(torch.empty(T_cap, dtype=i32, device=dev), torch.empty(T_cap + 1, dtype=i32, device=dev),
                        torch.empty((T_cap, self.D), dtype=f32, device=dev), torch.empty(1, dtype=i32, device=dev))
-                      for _ in range(2)]
+                      for _ in range(sets)]
         # send counts / offsets sized for the 2P groups of the split
         self.send = [(torch.empty(T_cap, dtype=i32, device=dev), torch.empty((T_cap, self.D), dtype=f32, device=dev),
                       torch.empty(2 * P, dtype=i32, device=dev), torch.empty(2 * P + 1, dtype=i32, device=dev))
-                     for _ in range(2)]
+                     for _ in range(sets)]
         self.coal = self.coals[0]
         self.grad_code = EMB_BF16 if grad_dtype == torch.bfloat16 else EMB_F32
         nb = grad_coalesce_split_workspace_bytes(T_cap, T_cap, self.V, self.D, self.grad_code)  # serves every variant
-        self.ws_coalesces = [new_workspace(nb, dev) for _ in range(2)]
+        self.ws_coalesces = [new_workspace(nb, dev) for _ in range(sets)]
         self.ws_coalesce = self.ws_coalesces[0]
         self.ws_pack = new_workspace(pack_by_owner_workspace_bytes(T_cap, P), dev)
 
@@ -85,14 +86,17 @@ class StepPipeline:
 
     def __init__(self, tables, lr, beta1, beta2, eps, overlap: bool = True, dev_status: torch.Tensor | None = None,
                  streams: int = 3, by_owner: bool = True, split: bool = False, signals: bool = False,
-                 sort_streams: int = 1):
+                 sort_streams: int = 1, sets: int = 2):
         """streams (with overlap=True and by_owner=False): 2 puts coalesce and pack on one side
         stream, 3 gives each its own (more concurrency, one more cross-stream wait per step).
         by_owner: coalesce straight into the send layout (emb_grad_coalesce_by_owner).
         split: the prior / delayed split (implies by_owner); step() then needs the next ids.
-        sort_streams (by_owner without the split, overlap=True): 2 runs the sorts of the two buffer
-        sets on two side streams, so that a step's sort can run beside the previous step's (they
-        share nothing; each waits only for the reduction of its own set two steps back).
+        sort_streams (by_owner without the split, overlap=True): 2 runs the sorts of odd and even
+        buffer sets on two side streams, so that a step's sort can run beside the previous step's
+        (they share nothing; each waits only for the reduction of its own set's previous step).
+        sets: buffer sets rotated between steps (every table needs at least this many; the split
+        with events needs 2).  More sets let a step's sort start before the reduction of the step
+        two back has finished.
         signals (with overlap=True): keep the cross-stream order with step signals (stream memory
         operations: about half the host time per step, for host-bound pipelines of small
         batches; with large batches events keep the GPU a few percent busier) instead of events."""
@@ -107,6 +111,11 @@ class StepPipeline:
         self.side3 = s3 if (overlap and split) else self.main  # the delayed update
         # the sorts of buffer set 1 (by_owner without the split): the third side stream
         self.side3_sort = s3 if (overlap and self.by_owner and not split and sort_streams >= 2) else None
+        if sort_streams >= 2 and sets % 2:
+            raise ValueError("two sort streams need an even number of buffer sets")
+        if any(tb.sets < sets for tb in self.tables):
+            raise ValueError("a table has fewer buffer sets than the pipeline rotates")
+        self.sets = sets
         self.count = 0
         self.events = []  # keeps the library events alive
         self.signals = [StepSignals() for _ in self.tables] if (overlap and signals) else []
@@ -114,7 +123,7 @@ class StepPipeline:
         st = 0 if dev_status is None else dev_status.data_ptr()
         for tb in self.tables:
             args, scheds = [], []
-            for i in range(2):
+            for i in range(sets):
                 uid, seg, ug, nu = tb.coals[i]
                 sid, srows, cnt, offs = tb.send[i]
                 a = StepArgs(table=tb.W.data_ptr(), exp_avg=tb.M.data_ptr(), exp_avg_sq=tb.S.data_ptr(), V=tb.V,
@@ -128,13 +137,14 @@ class StepPipeline:
                              beta2=beta2, eps=eps, dev_status=st)
                 evs = [Event() for _ in range(6)]
                 self.events += evs
-                sort_side = self.side3_sort if (i == 1 and self.side3_sort is not None) else self.side
+                sort_side = self.side3_sort if (i % 2 == 1 and self.side3_sort is not None) else self.side
                 s = StepSchedule(lookup_update=_stream_handle(self.main), coalesce=_stream_handle(sort_side),
                                  pack=_stream_handle(self.side2), delayed=_stream_handle(self.side3),
                                  sorted=evs[0].handle, coalesced=evs[1].handle, packed=evs[2].handle,
                                  updated=evs[3].handle, gathered=evs[4].handle, delayed_done=evs[5].handle,
                                  by_owner=1 if self.by_owner else 0, split=1 if split else 0,
-                                 signals=self.signals[len(self.args)].handle if self.signals else None)
+                                 signals=self.signals[len(self.args)].handle if self.signals else None,
+                                 sets=sets)
                 args.append(a)
                 scheds.append(s)
             self.args.append(args)
@@ -146,7 +156,7 @@ class StepPipeline:
         around the calls of the first table on the streams they run on.
         next_ids (split): [ids int32 per table] of the next step's batches (an empty tensor after
         the last step).  Inputs must be ready on the main stream when the first step is enqueued."""
-        i = self.count % 2
+        i = self.count % self.sets
         if self.count == 0 and self.overlap:
             for side in self._sides():
                 side.wait_stream(self.main)
@@ -162,7 +172,7 @@ class StepPipeline:
             a.grad = grad.data_ptr()
             a.grad_dtype = EMB_BF16 if grad.dtype == torch.bfloat16 else EMB_F32
             a.step = t
-            s.reuse = 1 if self.count >= 2 else 0
+            s.reuse = 1 if self.count >= self.sets else 0
             for n in range(8):
                 s.timing[n] = None
             if timing is not None and k == 0:

@@ -250,6 +250,7 @@ int main() {
     const int mode = static_cast<int>(rnd(3));
     const bool fail_pack = mode == 0 && rnd(10) == 0;
     const bool one_stream = rnd(8) == 0;
+    t.sched.sets = static_cast<int32_t>(rnd(5));  // 0 (two), 1 .. 4
     if (one_stream) t.sched.coalesce = t.sched.pack = t.sched.delayed = fake_stream(1);
     const int st = step(t, mode, fail_pack);
     if ((st != EMB_OK) != fail_pack) fail("random step");

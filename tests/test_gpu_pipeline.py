@@ -15,7 +15,7 @@ from workloads import configs, gen
 pytestmark = pytest.mark.gpu
 
 
-def run(overlap, by_owner, steps=7, split=False, signals=False, sort_streams=1):
+def run(overlap, by_owner, steps=9, split=False, signals=False, sort_streams=1, sets=2):
     torch.cuda.synchronize()
     specs = [configs.TableSpec(20000, 128, 6000, "zipf", 1.05, "f32", 0.01, 8, "mod", 61),
              configs.TableSpec(5000, 64, 3000, "uniform", 0.0, "bf16", 0.01, 3, "range", 62)]
@@ -23,7 +23,7 @@ def run(overlap, by_owner, steps=7, split=False, signals=False, sort_streams=1):
     for sp in specs:
         W = torch.from_numpy(configs.make_weights(sp)).cuda()
         gdt = torch.bfloat16 if sp.grad_dtype == "bf16" else torch.float32
-        tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).cuda(), sp.P, sp.T, gdt))
+        tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).cuda(), sp.P, sp.T, gdt, sets=sets))
         per = []
         for s in range(3):  # three rotating batches of different sizes
             T = sp.T - 997 * s
@@ -34,7 +34,7 @@ def run(overlap, by_owner, steps=7, split=False, signals=False, sort_streams=1):
         batches.append(per)
     torch.cuda.synchronize()
     pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner, split=split,
-                        signals=signals, sort_streams=sort_streams)
+                        signals=signals, sort_streams=sort_streams, sets=sets)
     lookups = []
     empty = torch.zeros(0, dtype=torch.int32, device="cuda")
     for t in range(1, steps + 1):
@@ -62,10 +62,11 @@ def test_overlapped_schedule_equals_sequential(by_owner, split, signals):
             assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
 
 
+@pytest.mark.parametrize("sets", [2, 4])
 @pytest.mark.parametrize("signals", [False, True], ids=["events", "signals"])
-def test_two_sort_streams_equal_sequential(signals):
-    print(f"two sort streams, signals={signals}", flush=True)
-    a, la = run(True, True, signals=signals, sort_streams=2)
+def test_two_sort_streams_equal_sequential(signals, sets):
+    print(f"two sort streams, signals={signals}, sets={sets}", flush=True)
+    a, la = run(True, True, signals=signals, sort_streams=2, sets=sets)
     b, lb = run(False, True)
     for x, y in zip(a, b):
         for u, v in zip(x, y):
@@ -120,7 +121,7 @@ def test_failed_step_leaves_no_wait_blocked():
         t = 0
         for k in range(6):
             if k == 2 and overlap:
-                i = pipe.count % 2
+                i = pipe.count % pipe.sets
                 good = pipe.args[0][i].ws_pack_bytes
                 pipe.args[0][i].ws_pack_bytes = 1
                 with pytest.raises(emb.EmbError):
@@ -139,3 +140,18 @@ def test_failed_step_leaves_no_wait_blocked():
     a = go(True)
     b = go(False)
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+@pytest.mark.parametrize("by_owner,split", [(False, False), (True, True)])
+def test_three_sets_with_signals_equal_sequential(by_owner, split):
+    """An odd number of buffer sets (one sort stream), including the split, whose lookup waits for
+    the delayed update two steps back whatever the number of sets."""
+    print(f"three sets by_owner={by_owner} split={split}", flush=True)
+    a, la = run(True, by_owner, split=split, signals=True, sets=3)
+    b, lb = run(False, by_owner, split=split)
+    for x, y in zip(a, b):
+        for u, v in zip(x, y):
+            assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
+    for x, y in zip(la, lb):
+        for u, v in zip(x, y):
+            assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
