@@ -292,7 +292,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="lowdup_uniform")
     ap.add_argument("--batches", type=int, default=8)
-    ap.add_argument("--time-every", type=int, default=4, help="time the update kernel on every n-th timed step")
+    ap.add_argument("--time-every", type=int, default=10, help="time the update kernel on every n-th timed step")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one stream, calls one after another")

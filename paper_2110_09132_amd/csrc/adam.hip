@@ -2,7 +2,10 @@
 // Kingma & Ba, Algorithm 1).  One pass over the listed rows: for each element
 // read g, w, m, v once and write w, m, v once; rows not listed are not touched.
 // Rows are mapped to lanes as in the gather (L lanes per row); table rows are
-// random 4*D-byte blocks, gradient rows are contiguous.
+// random 4*D-byte blocks, gradient rows are contiguous.  W, m, v go back with
+// streaming stores (nothing in the step reads them again); the loads are plain
+// (the table rows were just read by the lookup, the gradient rows just written
+// by the reduction, and both are often still cached).
 #include <cmath>
 
 #include <hip/hip_ext.h>
@@ -93,9 +96,9 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
           if (x.rid[u] >= 0 && cok) {
             adam_vec(x.g[u], x.w[u], x.m[u], x.s[u], c);
             const size_t e = static_cast<size_t>(x.rid[u]) * Dv + col;
-            W[e] = x.w[u];
-            M[e] = x.m[u];
-            S[e] = x.s[u];
+            store_stream(&W[e], x.w[u]);
+            store_stream(&M[e], x.m[u]);
+            store_stream(&S[e], x.s[u]);
           }
         }
       };

@@ -456,21 +456,21 @@ template <>
 struct GradRow<false, 4> {
   using Acc = float4;
   __device__ static Acc load(const void* g, size_t row, int Dv, int c) {
-    return reinterpret_cast<const float4*>(g)[row * Dv + c];
+    return load_stream(reinterpret_cast<const float4*>(g) + row * Dv + c);
   }
 };
 template <>
 struct GradRow<false, 1> {
   using Acc = float;
   __device__ static Acc load(const void* g, size_t row, int Dv, int c) {
-    return reinterpret_cast<const float*>(g)[row * Dv + c];
+    return load_stream(reinterpret_cast<const float*>(g) + row * Dv + c);
   }
 };
 template <>
 struct GradRow<true, 4> {
   using Acc = float4;
   __device__ static Acc load(const void* g, size_t row, int Dv, int c) {
-    const uint2 h = reinterpret_cast<const uint2*>(g)[row * Dv + c];
+    const uint2 h = load_stream(reinterpret_cast<const uint2*>(g) + row * Dv + c);
     return make_float4(__uint_as_float(h.x << 16), __uint_as_float(h.x & 0xFFFF0000u), __uint_as_float(h.y << 16),
                        __uint_as_float(h.y & 0xFFFF0000u));
   }
@@ -479,7 +479,7 @@ template <>
 struct GradRow<true, 1> {
   using Acc = float;
   __device__ static Acc load(const void* g, size_t row, int Dv, int c) {
-    return __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(g)[row * Dv + c]) << 16);
+    return __uint_as_float(static_cast<uint32_t>(load_stream(reinterpret_cast<const uint16_t*>(g) + row * Dv + c)) << 16);
   }
 };
 

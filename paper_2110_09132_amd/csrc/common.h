@@ -21,6 +21,28 @@ __device__ __forceinline__ void raise_flag(int32_t* status, int32_t flag) {
   if (status != nullptr) atomicOr(status, flag);
 }
 
+// Streaming (non-temporal) accesses, for data a step touches once: the
+// lookup's output rows, the update's stores of W, m, v, the reduction's reads
+// of the per-token gradients.  Marking them keeps the caches for what a step
+// reads twice (the table rows that its lookup and its update both touch, and
+// the reduced rows that the update reads right after the reduction).
+typedef float stream_f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t stream_u2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void store_stream(float4* p, const float4& v) {
+  __builtin_nontemporal_store(*reinterpret_cast<const stream_f4*>(&v), reinterpret_cast<stream_f4*>(p));
+}
+__device__ __forceinline__ void store_stream(float* p, float v) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ float4 load_stream(const float4* p) {
+  const stream_f4 v = __builtin_nontemporal_load(reinterpret_cast<const stream_f4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float load_stream(const float* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ uint2 load_stream(const uint2* p) {
+  const stream_u2 v = __builtin_nontemporal_load(reinterpret_cast<const stream_u2*>(p));
+  return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ uint16_t load_stream(const uint16_t* p) { return __builtin_nontemporal_load(p); }
+
 // Wave-uniform value as an SGPR (lets the compiler use scalar loads).
 __device__ __forceinline__ int32_t uniform(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
 

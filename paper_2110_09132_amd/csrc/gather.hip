@@ -6,7 +6,8 @@
 // row l) and reach their lanes by shuffle; rows are processed in groups of
 // kRowsInFlight steps, and the table loads of the next group are issued before
 // the current group is stored (two register buffers used in turn), so each
-// lane keeps two groups of independent 16-byte loads in flight.  Reads are whole table rows, writes contiguous rows.
+// lane keeps two groups of independent 16-byte loads in flight.  Reads are whole table rows (cached: the
+// update of the same step reads most of them again), writes contiguous rows (streaming stores).
 #include <hip/hip_ext.h>
 
 #include "common.h"
@@ -69,7 +70,7 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const VecT* __restrict
 #pragma unroll
         for (int u = 0; u < kRowsInFlight; ++u) {
           const int j = g * static_cast<int>(step_rows) + u * rpw + sub;
-          if (j < n && cok) out[static_cast<size_t>(c0 + j) * Dv + c] = x.id[u] < 0 ? VecT{} : x.v[u];
+          if (j < n && cok) store_stream(&out[static_cast<size_t>(c0 + j) * Dv + c], x.id[u] < 0 ? VecT{} : x.v[u]);
         }
       };
       load(0, A);
