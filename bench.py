@@ -144,13 +144,14 @@ def _find(directory, suffix):
     raise FileNotFoundError(f"no *{suffix} under {directory}")
 
 
-def summarize_trace(directory, command, warmup=20, steps=200):
+def summarize_trace(directory, command, skip=20, steps=200):
     """Text summary of a rocprofv3 --kernel-trace --stats run (kernel_stats.csv), plus the
     average duration of the update kernel over the timed steps of the bench run (its
-    dispatches warmup+1 .. warmup+steps in launch order, from kernel_trace.csv)."""
+    dispatches skip+1 .. skip+steps in launch order, from kernel_trace.csv; skip counts the
+    untimed steps before them: the order tuning and the warm-up)."""
     trace = [r for r in _read_csv(_find(directory, "kernel_trace.csv")) if ADAM_KERNEL in r["Kernel_Name"]]
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
-    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace[warmup:warmup + steps]]
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace[skip:skip + steps]]
     rows = _read_csv(_find(directory, "kernel_stats.csv"))
     out = [f"command: {command}", "", f"{'kernel':64s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} "
            f"{'max_us':>9s} {'share':>6s}"]
@@ -159,7 +160,7 @@ def summarize_trace(directory, command, warmup=20, steps=200):
         out.append(f"{name:64s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:9.2f} "
                    f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):5.1f}%")
     if durs:
-        out += ["", f"{ADAM_KERNEL} over the {len(durs)} timed steps (dispatches {warmup + 1}..{warmup + len(durs)}): "
+        out += ["", f"{ADAM_KERNEL} over the {len(durs)} timed steps (dispatches {skip + 1}..{skip + len(durs)}): "
                     f"avg {sum(durs) / len(durs):.2f} us, min {min(durs):.2f} us, max {max(durs):.2f} us"]
     return "\n".join(out) + "\n"
 
@@ -316,7 +317,8 @@ def main():
     ap.add_argument("--command2", default="", help="the second command recorded in a summary")
     args = ap.parse_args()
     if args.summarize_trace:
-        print(summarize_trace(args.summarize_trace, args.command, args.warmup, args.steps), end="")
+        tuned = 2 * (5 + args.tune_steps) if (args.order == "auto" and not args.sequential) else 0
+        print(summarize_trace(args.summarize_trace, args.command, tuned + args.warmup, args.steps), end="")
         return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc, args.command, args.command2), indent=1))
@@ -401,6 +403,7 @@ def main():
         order = min(tune_ms, key=tune_ms.get)
     elif args.order == "auto":
         order = "events"
+    log(f"cross-stream order: {order} {tune_ms or ''}")
     pipe = make_pipe(order)
     for _ in range(args.warmup):
         t += 1
@@ -430,6 +433,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_total = start.elapsed_time(end)
+    log(f"timed {args.steps} steps: {ms_total / args.steps:.4f} ms/step")
     ms_step = ms_total / args.steps
     adam_us = 1e3 * sum(a.elapsed_ms(z) for a, z in adam_ev.values()) / len(adam_ev)
 
@@ -455,6 +459,7 @@ def main():
         stage_ms = {"gather": stage_ms["gather"], "coalesce": stage_ms["coalesce"],
                     "update_prior": stage_ms["pack"], "update_delayed": stage_ms["adam"]}
 
+    log("per-stage breakdown done; copy reference, column partition, cost model ...")
     copy_gbps = copy_reference(torch)
     column = column_partition_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches],
                                      [U[b][0] for b in range(args.batches)], owner_rows)

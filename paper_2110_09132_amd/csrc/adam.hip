@@ -129,18 +129,16 @@ hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t 
   const RowLanes rl = row_lanes_for(Dv);
   const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * kRowsInFlight * (kThreads / kWave);
   const unsigned grid = grid_for((cap_rows + rows_per_block - 1) / rows_per_block, kMaxBlocks);
-  // an event attached as the dispatch's start costs more than a marker just before it
-  if (start != nullptr) {
-    const hipError_t e = hipEventRecord(start, stream);
-    if (e != hipSuccess) return e;
-  }
+  // Both events are attached to the dispatch, so they time the kernel itself
+  // (an attached start event idles the stream a few microseconds longer than a
+  // marker before the launch, which would also count the dispatch latency).
   if (vec4)
-    hipExtLaunchKernelGGL(adam_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream, nullptr, stop, 0,
+    hipExtLaunchKernelGGL(adam_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream, start, stop, 0,
                           reinterpret_cast<float4*>(table), reinterpret_cast<float4*>(exp_avg),
                           reinterpret_cast<float4*>(exp_avg_sq), V, Dv, rl.log2_lanes, row_ids,
                           reinterpret_cast<const float4*>(rows), offsets, shard_begin, shard_end, cap_rows, c, status);
   else
-    hipExtLaunchKernelGGL(adam_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, nullptr, stop, 0, table, exp_avg,
+    hipExtLaunchKernelGGL(adam_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, start, stop, 0, table, exp_avg,
                           exp_avg_sq, V, Dv, rl.log2_lanes, row_ids, rows, offsets, shard_begin, shard_end, cap_rows, c,
                           status);
   return hipGetLastError();
