@@ -273,6 +273,15 @@ def cost_model_report(emb, sp, U, N=8):
             "start_latencies": {n: k for n, _, k in names}}
 
 
+def schedule_candidates(args):
+    """(cross-stream order, buffer sets) pairs the bench chooses among: those the options leave open."""
+    if args.sequential:
+        return [("events", 2)]
+    orders = ("events", "signals") if args.order == "auto" else (args.order,)
+    sets = (2,) if args.schedule == "split" else ((2, 4) if args.sets == 0 else (args.sets,))
+    return [(o, n) for o in orders for n in sets]
+
+
 def host_info():
     model = platform.processor() or ""
     try:
@@ -293,7 +302,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="lowdup_uniform")
     ap.add_argument("--batches", type=int, default=8)
-    ap.add_argument("--time-every", type=int, default=10, help="time the update kernel on every n-th timed step")
+    ap.add_argument("--time-every", type=int, default=20, help="time the update kernel on every n-th timed step")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one stream, calls one after another")
@@ -302,13 +311,12 @@ def main():
                          "the prior/delayed split of Vertical Sparse Scheduling (emb_grad_coalesce_split; the "
                          "delayed update beside the next lookup); unfused: emb_grad_coalesce then "
                          "emb_pack_by_owner")
-    ap.add_argument("--sort-streams", type=int, choices=(1, 2), default=2,
-                    help="by_owner: run the sorts of the two buffer sets on one or two side streams")
-    ap.add_argument("--sets", type=int, default=4,
-                    help="buffer sets rotated between steps (the split schedule uses 2)")
+    ap.add_argument("--sets", type=int, choices=(0, 2, 4), default=0,
+                    help="buffer sets rotated between steps, with the sorts of odd and even sets on two side "
+                         "streams when 4 (0: tuned; the split schedule uses 2)")
     ap.add_argument("--order", choices=("auto", "signals", "events"), default="auto",
                     help="cross-stream order of the overlapped schedule: step signals (stream memory operations), "
-                         "events, or auto: the faster of the two over --tune-steps untimed steps each")
+                         "events, or auto (tuned)")
     ap.add_argument("--tune-steps", type=int, default=30)
     ap.add_argument("--summarize-trace", metavar="DIR", help="print a summary of a rocprofv3 kernel-stats run")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -317,7 +325,8 @@ def main():
     ap.add_argument("--command2", default="", help="the second command recorded in a summary")
     args = ap.parse_args()
     if args.summarize_trace:
-        tuned = 2 * (5 + args.tune_steps) if (args.order == "auto" and not args.sequential) else 0
+        tuned = len(schedule_candidates(args)) * (5 + args.tune_steps) if not args.sequential else 0
+        tuned = tuned if tuned > 5 + args.tune_steps else 0
         print(summarize_trace(args.summarize_trace, args.command, tuned + args.warmup, args.steps), end="")
         return
     if args.summarize_pmc:
@@ -344,7 +353,7 @@ def main():
         gdt = torch.bfloat16 if sp.grad_dtype == "bf16" else torch.float32
         W = torch.from_numpy(configs.make_weights(sp)).to(dev)
         tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).to(dev), sp.P, sp.T, gdt,
-                                     sets=max(2, args.sets)))
+                                     sets=4))
         tb_batches = []
         for b in range(args.batches):
             ids, G = configs.make_batch(sp, 1000 + b)
@@ -372,23 +381,27 @@ def main():
 
     split = args.schedule == "split"
     by_owner = args.schedule != "unfused"
-    def make_pipe(order):
+    def make_pipe(cand):
+        order, sets = cand
         return StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential,
                             by_owner=by_owner, split=split, signals=order == "signals",
-                            sort_streams=args.sort_streams, sets=2 if split else args.sets)
+                            sort_streams=2 if (sets == 4 and by_owner and not split) else 1, sets=sets)
 
     def next_ids(t):
         return [x[0] for x in step_batches[(t + 1) % args.batches]] if split else None
 
     t = 0
-    # order "auto": time a few untimed steps with each cross-stream order and keep the faster
-    # (events cost the GPU nothing but the host ~85 us per overlapped step; step signals halve
-    # the host's cost but add small runtime kernels to the streams)
+    # the schedule: time a few untimed steps of each candidate (cross-stream order x buffer sets)
+    # and keep the fastest.  Events cost the GPU nothing but the host ~85 us per overlapped step;
+    # step signals halve the host's cost but add small runtime kernels to the streams.  Four sets
+    # (sorts on two streams) free the sorts of latency-bound steps; two interfere less with the
+    # bandwidth-bound ones.
     tune_ms = {}
-    order = args.order
-    if args.order == "auto" and not args.sequential:
-        for o in ("events", "signals"):
-            trial = make_pipe(o)
+    cands = schedule_candidates(args)
+    cand = cands[0]
+    if len(cands) > 1:
+        for c in cands:
+            trial = make_pipe(c)
             for k in range(5 + args.tune_steps):
                 if k == 5:
                     trial.finish()
@@ -398,13 +411,12 @@ def main():
                 trial.step(step_batches[t % args.batches], t, next_ids=next_ids(t))
             trial.finish()
             torch.cuda.synchronize()
-            tune_ms[o] = (time.perf_counter() - t_start) * 1e3 / args.tune_steps
+            tune_ms[f"{c[0]}/{c[1]} sets"] = (time.perf_counter() - t_start) * 1e3 / args.tune_steps
             del trial
-        order = min(tune_ms, key=tune_ms.get)
-    elif args.order == "auto":
-        order = "events"
-    log(f"cross-stream order: {order} {tune_ms or ''}")
-    pipe = make_pipe(order)
+        cand = cands[min(range(len(cands)), key=lambda i: list(tune_ms.values())[i])]
+    order, nsets = cand
+    log(f"schedule: {order}, {nsets} buffer sets {tune_ms or ''}")
+    pipe = make_pipe(cand)
     for _ in range(args.warmup):
         t += 1
         pipe.step(step_batches[t % args.batches], t, next_ids=next_ids(t))
@@ -482,6 +494,18 @@ def main():
     upd_rows = [U[used[s]][0] - (U_prior[used[s]][0] if split else 0) for s in timed]
     adam_bytes = sum(byte_model(sp0.T, r, sp0.D, 4, sp0.P)["adam"] for r in upd_rows) / len(timed)
     adam_gbps = adam_bytes / (adam_us * 1e-6) / 1e9
+    # sizes of the sparse gradient as Table 3 reports them (per step, all tables): the per-token
+    # COO gradient (original), after COALESCE (coalesced), and the prior part of the vertical split
+    # (prioritized: rows whose id is in the next batch, the part that must arrive before the next
+    # forward pass); ids int32, rows in the gradient's element type
+    def mb(rows, sp):
+        return rows * (4 + sp.D * (2 if sp.grad_dtype == "bf16" else 4)) / 1e6
+    orig = sum(mb(sp.T, sp) for sp in wl.tables)
+    coal = sum(mb(U[b][k], wl.tables[k]) for b in range(args.batches) for k in range(len(tables))) / args.batches
+    prio = sum(mb(U_prior[b][k], wl.tables[k]) for b in range(args.batches) for k in range(len(tables))) / args.batches
+    table3 = {"original_MB": orig, "coalesced_MB": coal, "prioritized_MB": prio,
+              "reduction_by_coalescing": 1 - coal / orig, "further_reduction_by_prioritizing": 1 - prio / coal,
+              "next_batch": "the next batch of the rotation"}
     prior_frac = sum(U_prior[b][k] for b in used for k in range(len(tables))) / max(1, sum(
         U[b][k] for b in used for k in range(len(tables))))
 
@@ -511,12 +535,12 @@ def main():
                     "by_owner": "sort and reduction on two side streams; lookup and update on the main stream",
                     "unfused": "coalesce and pack on two side streams; lookup and update on the main stream"}[
                        args.schedule],
-                   "sort_streams": None if (args.sequential or split or not by_owner) else args.sort_streams,
-                   "buffer_sets": 2 if split else args.sets,
+                   "sort_streams": None if (args.sequential or split or not by_owner) else (2 if nsets == 4 else 1),
+                   "buffer_sets": nsets,
                    "cross_stream_order": None if args.sequential else
                    {"signals": "step signals (hipStreamWriteValue32 / hipStreamWaitValue32)",
                     "events": "events (hipEventRecord / hipStreamWaitEvent)"}[order],
-                   "order_tuning_ms_per_step": tune_ms or None,
+                   "schedule_tuning_ms_per_step": tune_ms or None,
                    "prior_rows_frac": prior_frac if split else None},
         "step_bytes_model": total_bytes,
         "step_bytes_model_kind": "fused minimum (pack folded into coalesce)" if by_owner else "four calls",
@@ -534,6 +558,7 @@ def main():
                      "bytes_per_launch": adam_bytes, "avg_launch_us": adam_us,
                      "launches_timed": len(adam_ev)},
         "copy_GBps": copy_gbps,
+        "gradient_sizes_table3": table3,
         "column_partition": column,
         "comm_cost_model": cost,
         "step_frac_of_copy": step_gbps / copy_gbps,

@@ -3,9 +3,10 @@
 // read g, w, m, v once and write w, m, v once; rows not listed are not touched.
 // Rows are mapped to lanes as in the gather (L lanes per row); table rows are
 // random 4*D-byte blocks, gradient rows are contiguous.  W, m, v go back with
-// streaming stores (nothing in the step reads them again); the loads are plain
-// (the table rows were just read by the lookup, the gradient rows just written
-// by the reduction, and both are often still cached).
+// streaming stores and m, v come in with streaming loads (nothing else in the
+// step touches them); the loads of W and of the gradient rows are plain (the
+// table rows were just read by the lookup, the gradient rows just written by
+// the reduction, and both are often still cached).
 #include <cmath>
 
 #include <hip/hip_ext.h>
@@ -86,8 +87,8 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
           const size_t e = static_cast<size_t>(x.rid[u] < 0 ? 0 : x.rid[u]) * Dv + col;
           x.g[u] = rows[static_cast<size_t>(c0 + min(j, n - 1)) * Dv + col];
           x.w[u] = W[e];
-          x.m[u] = M[e];
-          x.s[u] = S[e];
+          x.m[u] = load_stream(&M[e]);
+          x.s[u] = load_stream(&S[e]);
         }
       };
       auto apply = [&](Buf& x) {
