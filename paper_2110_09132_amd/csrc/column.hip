@@ -15,10 +15,12 @@
 //                   lookup of the tokens of every worker)
 //  column_assemble: blocks, rows [row0, row0 + R) -> rows [R][D]  (what a
 //                   worker holds after the lookup-result AlltoAll)
-// All are bit copies.  A row is handled by L lanes; lane l moves the vectors
-// c = l, l + L, ... of its row, so the reads and writes of one owner's slice
-// are contiguous.  A wave moves kRowsInFlight steps of 64 / L rows, all loads
-// before any store; the grid is one wave per such group of rows.
+// All are bit copies.  The default kernels work on tiles of rows staged
+// through LDS (column_tile_kernel, below), so that both sides move long
+// contiguous runs.  Rows too wide for a tile take column_kernel: a row is
+// handled by L lanes; lane l moves the vectors c = l, l + L, ... of its row, so
+// the reads and writes of one owner's slice are contiguous; a wave moves
+// kRowsInFlight steps of 64 / L rows, all loads before any store.
 // When D is a multiple of 4P, every slice is a whole number of float4 and the
 // kernels move float4; otherwise single floats.
 #include "common.h"
@@ -32,14 +34,15 @@ constexpr int kRowsInFlight = 8;
 
 enum ColumnMode { kPack = 0, kGather = 1, kAssemble = 2 };
 
-// First vector column of owner p (Dv vectors per row).
+// First vector column of owner p (Dv vectors per row).  32-bit: the boundary
+// requires D * P < 2^31, so p * Dv and c * P fit.
 __device__ __forceinline__ int col_begin(int p, int Dv, int P) {
-  return static_cast<int>((static_cast<int64_t>(p) * Dv) / P);
+  return static_cast<int>(static_cast<uint32_t>(p * Dv) / static_cast<uint32_t>(P));
 }
 
 // Owner of vector column c: the p with col_begin(p) <= c < col_begin(p + 1).
 __device__ __forceinline__ int col_owner(int c, int Dv, int P) {
-  int p = static_cast<int>((static_cast<int64_t>(c) * P) / Dv);
+  int p = static_cast<int>(static_cast<uint32_t>(c * P) / static_cast<uint32_t>(Dv));
   p = min(max(p, 0), P - 1);
   while (p + 1 < P && col_begin(p + 1, Dv, P) <= c) ++p;
   while (p > 0 && col_begin(p, Dv, P) > c) --p;
@@ -111,6 +114,115 @@ __global__ __launch_bounds__(kThreads) void column_kernel(const VecT* __restrict
   if (kMode == kGather && __any(bad) && lane == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
 }
 
+// Tiled form (the default): a workgroup takes a tile of n <= TR consecutive
+// rows.  Each owner's part of the tile is one contiguous run of n * w(p) units
+// in block p (rows r0 .. r0 + n - 1 of the block), and each row one contiguous
+// run of Dv units on the row-major side:
+// pack:   rows -> LDS in row order (whole tile rows), LDS -> blocks in owner order;
+// join:   blocks -> LDS in owner order, LDS -> rows in row order;
+// lookup: owner order on both sides, no LDS (the shard rows are random anyway;
+//         the block runs are written contiguously).
+// In owner order wave v takes owners v, v + 4, ...; its lanes walk the owner's
+// run (unit k is row k / w, column k % w of the owner's slice), so the owner's
+// start and width are wave-uniform.  LDS rows are padded by one unit so that
+// the rows of a tile start in different banks.  Threads issue kUnroll loads
+// before they store.
+constexpr int kTileUnits = 1024;  // units per tile (16 KB of float4)
+constexpr int kUnroll = 4;
+constexpr int kLdsPad = 1;
+
+template <typename VecT, int kMode>
+__global__ __launch_bounds__(kThreads) void column_tile_kernel(const VecT* __restrict__ src, VecT* __restrict__ dst,
+                                                               const int32_t* __restrict__ ids,
+                                                               const int32_t* __restrict__ count, int cap,
+                                                               int64_t src_cap, int64_t dst_cap, int64_t row0,
+                                                               int Dv, int P, int TR, int32_t* status) {
+  extern __shared__ __align__(16) unsigned char column_lds[];
+  VecT* tile = reinterpret_cast<VecT*>(column_lds);
+  const int ld = Dv + kLdsPad;
+  const int R = (kMode == kPack && count != nullptr) ? min(max(*count, 0), cap) : cap;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * TR;
+  if (r0 >= R) return;
+  const int n = static_cast<int>(min(static_cast<int64_t>(TR), R - r0));
+  const int units = n * Dv;
+  const int wv = static_cast<int>(threadIdx.x) / kWave;
+  const int lane = static_cast<int>(lane_id());
+  bool bad = false;
+  if (kMode != kPack) {
+    // owner order from the source: blocks (join) or shard rows (lookup)
+    for (int p = wv; p < P; p += kThreads / kWave) {
+      const int a = uniform(col_begin(p, Dv, P));
+      const int w = uniform(col_begin(p + 1, Dv, P) - a);
+      const int run = n * w;
+      for (int k0 = lane; k0 < run; k0 += kWave * kUnroll) {
+        VecT v[kUnroll];
+        int rr[kUnroll], jj[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const int k = min(k0 + u * kWave, run - 1);  // clamped: past the run re-reads its last unit
+          rr[u] = k / w;
+          jj[u] = k - rr[u] * w;
+          if (kMode == kGather) {
+            const int32_t id = ids[r0 + rr[u]];
+            const bool ok = id >= 0 && id < src_cap;
+            bad |= !ok && k0 + u * kWave < run;
+            v[u] = src[static_cast<size_t>(src_cap * a + static_cast<int64_t>(ok ? id : 0) * w + jj[u])];
+            if (!ok) v[u] = VecT{};
+          } else {
+            v[u] = src[static_cast<size_t>(src_cap * a + (row0 + r0 + rr[u]) * w + jj[u])];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          if (k0 + u * kWave >= run) continue;
+          if (kMode == kGather) dst[static_cast<size_t>(dst_cap * a + (r0 + rr[u]) * w + jj[u])] = v[u];
+          else tile[rr[u] * ld + a + jj[u]] = v[u];
+        }
+      }
+    }
+    if (kMode == kGather) {
+      if (__any(bad) && lane == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
+      return;
+    }
+  } else {
+    // row order from the rows
+    for (int i0 = threadIdx.x; i0 < units; i0 += kThreads * kUnroll) {
+      VecT v[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u)
+        v[u] = src[static_cast<size_t>(r0) * Dv + min(i0 + u * kThreads, units - 1)];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = i0 + u * kThreads;
+        if (i < units) {
+          const int r = i / Dv;
+          tile[r * ld + (i - r * Dv)] = v[u];
+        }
+      }
+    }
+  }
+  __syncthreads();
+  if (kMode == kPack) {
+    // owner order to the blocks
+    for (int p = wv; p < P; p += kThreads / kWave) {
+      const int a = uniform(col_begin(p, Dv, P));
+      const int w = uniform(col_begin(p + 1, Dv, P) - a);
+      const int run = n * w;
+      for (int k = lane; k < run; k += kWave) {
+        const int r = k / w;
+        const int j = k - r * w;
+        dst[static_cast<size_t>(dst_cap * a + (r0 + r) * w + j)] = tile[r * ld + a + j];
+      }
+    }
+  } else {
+    // row order to the rows
+    for (int i = threadIdx.x; i < units; i += kThreads) {
+      const int r = i / Dv;
+      dst[static_cast<size_t>(r0) * Dv + i] = tile[r * ld + (i - r * Dv)];
+    }
+  }
+}
+
 __global__ void column_counts_kernel(const int32_t* __restrict__ count, int cap, int P,
                                      int32_t* __restrict__ send_counts) {
   const int R = count != nullptr ? min(max(*count, 0), cap) : cap;
@@ -128,6 +240,23 @@ hipError_t launch_column(const float* src, float* dst, const int32_t* ids, const
   const RowLanes rl = row_lanes_for(Dv);
   const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * kRowsInFlight * (kThreads / kWave);
   const unsigned grid = grid_for((cap + rows_per_block - 1) / rows_per_block, kMaxBlocks);
+  // tiles of up to kTileUnits units (at least one row); rows too wide for a
+  // 32 KB tile take the row-per-lanes kernel
+  const size_t unit = vec4 ? sizeof(float4) : sizeof(float);
+  const int TR = max(1, kTileUnits / Dv);
+  const size_t lds = static_cast<size_t>(TR) * (Dv + kLdsPad) * unit;
+  if (lds <= 32768) {
+    const unsigned tiles = static_cast<unsigned>((static_cast<long long>(cap) + TR - 1) / TR);
+    const size_t shm = kMode == kGather ? 0 : lds;
+    if (vec4)
+      hipLaunchKernelGGL((column_tile_kernel<float4, kMode>), dim3(tiles), dim3(kThreads), shm, stream,
+                         reinterpret_cast<const float4*>(src), reinterpret_cast<float4*>(dst), ids, count, cap,
+                         src_cap, dst_cap, row0, Dv, P, TR, status);
+    else
+      hipLaunchKernelGGL((column_tile_kernel<float, kMode>), dim3(tiles), dim3(kThreads), shm, stream, src, dst, ids,
+                         count, cap, src_cap, dst_cap, row0, Dv, P, TR, status);
+    return hipGetLastError();
+  }
   if (vec4)
     hipLaunchKernelGGL((column_kernel<float4, kMode>), dim3(grid), dim3(kThreads), 0, stream,
                        reinterpret_cast<const float4*>(src), reinterpret_cast<float4*>(dst), ids, count, cap,

@@ -33,7 +33,8 @@ def bits(a):
 # (cap, R, D, P): float4 path (D % 4P == 0) and float path (ragged widths), P = D, P = 1,
 # R = 0, R clamped from above, several tiles with a ragged tail
 PACK_CASES = [(5000, 4321, 256, 16), (3000, 2999, 100, 7), (777, 777, 13, 13), (1000, 1000, 64, 1),
-              (1000, 0, 64, 4), (300, 299, 32, 8), (1, 1, 1, 1), (2049, 2049, 48, 5)]
+              (1000, 0, 64, 4), (300, 299, 32, 8), (1, 1, 1, 1), (2049, 2049, 48, 5),
+              (64, 50, 4096, 16), (40, 37, 9001, 3), (30, 30, 8192, 8)]  # one-row tiles; rows too wide for a tile
 
 
 @pytest.mark.parametrize("cap,R,D,P", PACK_CASES)
@@ -81,7 +82,8 @@ def test_partition_table_without_count():
 
 # (V, D, P, worker token counts)
 FORWARD_CASES = [(10007, 256, 16, (3000, 0, 2500, 1)), (5000, 100, 7, (1200, 800)), (300, 13, 13, (77,)),
-                 (1 << 16, 64, 4, (4096, 4096, 4096, 4096)), (50, 3, 1, (9, 9))]
+                 (1 << 16, 64, 4, (4096, 4096, 4096, 4096)), (50, 3, 1, (9, 9)), (900, 9001, 3, (40, 33)),
+                 (700, 4096, 16, (50, 0, 21))]
 
 
 @pytest.mark.parametrize("V,D,P,sizes", FORWARD_CASES)
