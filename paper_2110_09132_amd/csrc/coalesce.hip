@@ -171,49 +171,6 @@ __global__ __launch_bounds__(kThreads) void tab_insert_kernel(const int32_t* __r
   }
 }
 
-constexpr int kKeysPerThread = 4;
-
-// Sort key of every token, and vals[t] = t for a token that takes part, -1 for
-// one that does not (id outside [0, V), or owner outside [0, P)).  The owner
-// and next-batch lookups are done here once, so the sort reads plain keys.
-__global__ __launch_bounds__(kThreads) void make_keys_kernel(const int32_t* __restrict__ ids, int T, KeySpec ks,
-                                                             uint32_t* __restrict__ keys, int32_t* __restrict__ vals,
-                                                             int32_t* status) {
-  const int base = blockIdx.x * kThreads * kKeysPerThread + static_cast<int>(threadIdx.x);
-  const int Tc = ks.count_dev != nullptr ? min(max(*ks.count_dev, 0), T) : T;  // tokens that exist
-  int32_t id[kKeysPerThread];
-  bool idok[kKeysPerThread];
-#pragma unroll
-  for (int r = 0; r < kKeysPerThread; ++r) id[r] = ids[min(base + r * kThreads, T - 1)];
-#pragma unroll
-  for (int r = 0; r < kKeysPerThread; ++r) idok[r] = id[r] >= 0 && static_cast<uint32_t>(id[r]) < ks.V;
-  uint32_t own[kKeysPerThread];
-#pragma unroll
-  for (int r = 0; r < kKeysPerThread; ++r) own[r] = 0;
-  if (ks.row_owner != nullptr) {
-#pragma unroll
-    for (int r = 0; r < kKeysPerThread; ++r) own[r] = static_cast<uint32_t>(ks.row_owner[idok[r] ? id[r] : 0]);
-  }
-  bool bad_id = false, bad_owner = false;
-#pragma unroll
-  for (int r = 0; r < kKeysPerThread; ++r) {
-    const int t = base + r * kThreads;
-    const bool inb = t < Tc;
-    const bool ownok = own[r] < static_cast<uint32_t>(ks.P);
-    const bool take = inb && idok[r] && ownok;
-    bad_id |= inb && !idok[r];
-    bad_owner |= inb && idok[r] && !ownok;
-    uint32_t key = (own[r] << ks.ib) | static_cast<uint32_t>(id[r]);
-    if (ks.next_tab != nullptr && take && !in_next(static_cast<uint32_t>(id[r]), ks)) key |= 1u << ks.cls_shift;
-    if (t < T) {
-      keys[t] = key;
-      vals[t] = take ? t : -1;
-    }
-  }
-  if (__any(bad_id) && lane_id() == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
-  if (__any(bad_owner) && lane_id() == 0) raise_flag(status, EMB_DEV_OWNER_OUT_OF_RANGE);
-}
-
 // Exclusive prefix of one digit's counts over tiles 0 .. tile-1, read from
 // status words lb[t * stride] (nearest first, kWindow at a time) until a tile with
 // an inclusive count is found.  Every tile publishes its aggregate before it
@@ -306,34 +263,60 @@ KeySpec key_spec(int64_t V, const int32_t* row_owner, int P, bool split) {
 }
 
 // ---------------------------------------------------------------- radix sort
+// The sort key of every token and the digit histograms of every pass, in one
+// kernel per tile of kUpTile tokens: keys[t], and vals[t] = t for a token that
+// takes part, -1 for one that does not (id outside [0, V), owner outside
+// [0, P), or t beyond the device-side token count).  The owner and next-batch
+// lookups are done here once, so the passes read plain keys.  The workgroups
+// also clear the look-back words and tickets of the passes.
 template <class C>
-__global__ __launch_bounds__(C::kNT) void sort_upsweep_kernel(const uint32_t* __restrict__ keys,
-                                                              const int32_t* __restrict__ vals, int T,
-                                                              RadixPlan plan, uint32_t* __restrict__ up_hist,
-                                                              uint32_t* __restrict__ zero_begin, int zero_words) {
+__global__ __launch_bounds__(C::kNT) void sort_keys_upsweep_kernel(const int32_t* __restrict__ ids, int T, KeySpec ks,
+                                                                   RadixPlan plan, uint32_t* __restrict__ keys,
+                                                                   int32_t* __restrict__ vals,
+                                                                   uint32_t* __restrict__ up_hist,
+                                                                   uint32_t* __restrict__ zero_begin, int zero_words,
+                                                                   int32_t* status) {
   constexpr int NT = C::kNT, kBins = C::kBins, kPer = C::kUpTile / NT;
   __shared__ uint32_t h[C::kPasses * kBins];
   for (int i = threadIdx.x; i < plan.npass * kBins; i += NT) h[i] = 0;
-  __syncthreads();
   const int base = blockIdx.x * C::kUpTile;
-  bool take[kPer];
-  uint32_t k[kPer];
-  int32_t v[kPer];
+  const int Tc = ks.count_dev != nullptr ? min(max(*ks.count_dev, 0), T) : T;  // tokens that exist
+  int32_t id[kPer];
+  bool idok[kPer];
+  uint32_t own[kPer];
+#pragma unroll
+  for (int r = 0; r < kPer; ++r) id[r] = ids[min(base + r * NT + static_cast<int>(threadIdx.x), T - 1)];
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
-    const int g = min(base + r * NT + static_cast<int>(threadIdx.x), T - 1);
-    k[r] = keys[g];
-    v[r] = vals[g];
+    idok[r] = id[r] >= 0 && static_cast<uint32_t>(id[r]) < ks.V;
+    own[r] = 0;
   }
+  if (ks.row_owner != nullptr) {
 #pragma unroll
-  for (int r = 0; r < kPer; ++r) take[r] = base + r * NT + static_cast<int>(threadIdx.x) < T && v[r] >= 0;
+    for (int r = 0; r < kPer; ++r) own[r] = static_cast<uint32_t>(ks.row_owner[idok[r] ? id[r] : 0]);
+  }
+  __syncthreads();  // the histograms are cleared
+  bool bad_id = false, bad_owner = false;
 #pragma unroll
   for (int r = 0; r < kPer; ++r) {
-    if (take[r]) {
-      for (int p = 0; p < plan.npass; ++p)
-        atomicAdd(&h[p * kBins + ((k[r] >> plan.shift(p)) & ((1u << plan.bits(p)) - 1u))], 1u);
+    const int t = base + r * NT + static_cast<int>(threadIdx.x);
+    const bool inb = t < Tc;
+    const bool ownok = own[r] < static_cast<uint32_t>(ks.P);
+    const bool take = inb && idok[r] && ownok;
+    bad_id |= inb && !idok[r];
+    bad_owner |= inb && idok[r] && !ownok;
+    uint32_t key = (own[r] << ks.ib) | static_cast<uint32_t>(id[r]);
+    if (ks.next_tab != nullptr && take && !in_next(static_cast<uint32_t>(id[r]), ks)) key |= 1u << ks.cls_shift;
+    if (t < T) {
+      keys[t] = key;
+      vals[t] = take ? t : -1;
     }
+    if (take)
+      for (int p = 0; p < plan.npass; ++p)
+        atomicAdd(&h[p * kBins + ((key >> plan.shift(p)) & ((1u << plan.bits(p)) - 1u))], 1u);
   }
+  if (__any(bad_id) && lane_id() == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
+  if (__any(bad_owner) && lane_id() == 0) raise_flag(status, EMB_DEV_OWNER_OUT_OF_RANGE);
   __syncthreads();
   for (int i = threadIdx.x; i < plan.npass * kBins; i += NT)
     up_hist[static_cast<size_t>(blockIdx.x) * plan.npass * kBins + i] = h[i];
@@ -786,18 +769,19 @@ CoalesceWs carve_with(void* base, int T, int D, int T_next, int64_t V) {
 
 CoalesceWs carve(void* base, int T, int D, int T_next, int64_t V) { return carve_with<Narrow>(base, T, D, T_next, V); }
 
+// The key build with the histograms, then the radix passes over (key, position).
 template <class C>
-void launch_sort(const uint32_t* keys0, const int32_t* vals0, int T, const RadixPlan& plan, const CoalesceWs& ws,
+void launch_sort(const int32_t* ids, int T, const KeySpec& ks, const RadixPlan& plan, const CoalesceWs& ws,
                  int32_t* status, hipStream_t stream, const uint32_t** skeys, const int32_t** spos) {
   const int ntiles = (T + C::kTile - 1) / C::kTile;
   const int nup = (T + C::kUpTile - 1) / C::kUpTile;
   uint32_t* zero_begin = ws.tickets;
   const int zero_words =
       static_cast<int>((ws.sort_lb + static_cast<size_t>(plan.npass) * ntiles * C::kBins) - zero_begin);
-  hipLaunchKernelGGL(sort_upsweep_kernel<C>, dim3(nup), dim3(C::kNT), 0, stream, keys0, vals0, T, plan, ws.up_hist,
-                     zero_begin, zero_words);
-  const uint32_t* kin = keys0;
-  const int32_t* vin = vals0;
+  hipLaunchKernelGGL(sort_keys_upsweep_kernel<C>, dim3(nup), dim3(C::kNT), 0, stream, ids, T, ks, plan, ws.keys_b,
+                     ws.vals_b, ws.up_hist, zero_begin, zero_words, status);
+  const uint32_t* kin = ws.keys_b;
+  const int32_t* vin = ws.vals_b;
   uint32_t* kout = ws.keys_a;
   int32_t* vout = ws.vals_a;
   for (int p = 0; p < plan.npass; ++p) {
@@ -854,14 +838,11 @@ hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, con
     ks.next_bytemap = ws.tab_bytemap;
     ks.tab_shift = ws.tab_shift;
   }
-  // 1. the key of every token (owner and next-batch lookups once)
-  const int per_block = kThreads * kKeysPerThread;
-  hipLaunchKernelGGL(make_keys_kernel, dim3((T + per_block - 1) / per_block), dim3(kThreads), 0, stream, ids, T, ks,
-                     ws.keys_b, ws.vals_b, status);
-  // 2-3. digit histograms of all passes, then the radix passes over (key, position)
+  // 1-3. the key of every token (owner and next-batch lookups once) with the digit
+  // histograms of all passes, then the radix passes over (key, position)
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
-  launch_sort<Narrow>(ws.keys_b, ws.vals_b, T, plan, ws, status, stream, &kin, &vin);
+  launch_sort<Narrow>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
   // 4. heads per reduction workgroup
   hipLaunchKernelGGL(seg_count_kernel, dim3((nred + kWaves - 1) / kWaves), dim3(kThreads), 0, stream, kin, ws.n_valid,
                      ws.tile_heads, nred);
