@@ -144,7 +144,7 @@ def _find(directory, suffix):
     raise FileNotFoundError(f"no *{suffix} under {directory}")
 
 
-def summarize_trace(directory, command, skip=20, steps=200):
+def summarize_trace(directory, command, skip=20, steps=200, every=20):
     """Text summary of a rocprofv3 --kernel-trace --stats run (kernel_stats.csv), plus the
     average duration of the update kernel over the timed steps of the bench run (its
     dispatches skip+1 .. skip+steps in launch order, from kernel_trace.csv; skip counts the
@@ -152,6 +152,7 @@ def summarize_trace(directory, command, skip=20, steps=200):
     trace = [r for r in _read_csv(_find(directory, "kernel_trace.csv")) if ADAM_KERNEL in r["Kernel_Name"]]
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
     durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace[skip:skip + steps]]
+    sampled = durs[::every]  # the launches the bench times with events (every `every`-th timed step)
     rows = _read_csv(_find(directory, "kernel_stats.csv"))
     out = [f"command: {command}", "", f"{'kernel':64s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} "
            f"{'max_us':>9s} {'share':>6s}"]
@@ -160,7 +161,9 @@ def summarize_trace(directory, command, skip=20, steps=200):
         out.append(f"{name:64s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e3:9.2f} "
                    f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):5.1f}%")
     if durs:
-        out += ["", f"{ADAM_KERNEL} over the {len(durs)} timed steps (dispatches {skip + 1}..{skip + len(durs)}): "
+        out += ["", f"{ADAM_KERNEL} over the {len(sampled)} launches the bench times with events (every "
+                    f"{every}th timed step): avg {sum(sampled) / len(sampled):.2f} us",
+                f"{ADAM_KERNEL} over the {len(durs)} timed steps (dispatches {skip + 1}..{skip + len(durs)}): "
                     f"avg {sum(durs) / len(durs):.2f} us, min {min(durs):.2f} us, max {max(durs):.2f} us"]
     return "\n".join(out) + "\n"
 
@@ -327,7 +330,8 @@ def main():
     if args.summarize_trace:
         tuned = len(schedule_candidates(args)) * (5 + args.tune_steps) if not args.sequential else 0
         tuned = tuned if tuned > 5 + args.tune_steps else 0
-        print(summarize_trace(args.summarize_trace, args.command, tuned + args.warmup, args.steps), end="")
+        print(summarize_trace(args.summarize_trace, args.command, tuned + args.warmup, args.steps, args.time_every),
+              end="")
         return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc, args.command, args.command2), indent=1))
