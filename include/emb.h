@@ -381,6 +381,8 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  * uniq_ids, uniq_grad and ws_pack are not used.  Waits:
  *   sort(s)     after reduce(s-2)              (same coalesce workspace)
  *   reduce(s)   after sort(s), update(s-2)     (reads the sorted keys; same send buffers)
+ * (with sets >= 4 and no split: sort(s) after update(s-sets), which followed
+ * reduce(s-sets), and reduce(s) after sort(s) only: one wait fewer per step)
  *   update(s)   after reduce(s)                (reads the send rows)
  *   lookup(s+1) after update(s)                (same stream; reads the table)
  * (events sorted, coalesced, updated).  The sorts thus run up to a step

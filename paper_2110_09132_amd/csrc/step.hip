@@ -141,8 +141,14 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
       var.T_next = a->T_next;
     }
     const bool sep_sr = s->coalesce != s->pack;  // sort beside the reduction
+    // With four or more sets the sort waits for the update of the set's last
+    // step (s - sets), which came after that step's reduction: the workspace and
+    // the send buffers are then both free once the sort has run, and the
+    // reduction needs to wait for the sort alone (one cross-stream wait fewer;
+    // with two sets it would hold the sort back by a whole update).
+    const bool chained = order.sets >= 4 && !s->split && sep_sr && sep_p;
     // sort(s): after the reduction of the set's last step (s - sets) has finished with its workspace
-    if (sep_sr && !ok(order.after(s->coalesce, kCoalesced, order.sets))) return st;
+    if (sep_sr && !ok(order.after(s->coalesce, chained ? kUpdated : kCoalesced, order.sets))) return st;
     if (!ok(record(s->timing[2], s->coalesce))) return st;
     if (!ok(launched(emb::launch_coalesce_sort(a->ids, a->T, a->V, a->D, var, a->ws_coalesce, a->dev_status,
                                                S(s->coalesce)))))
@@ -150,7 +156,7 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     if (sep_sr && !ok(order.done(kSorted, s->coalesce))) return st;
     // reduction(s): after the sort, and after the updates of step s - sets have read this set's send buffers
     if (sep_sr && !ok(order.after(s->pack, kSorted, 0))) return st;
-    if (sep_p && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
+    if (sep_p && !chained && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
     if (s->split && s->delayed != s->pack && !ok(order.after(s->pack, kDelayedDone, order.sets))) return st;
     if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, var,
                                                  a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
