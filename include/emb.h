@@ -354,7 +354,7 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
 /*
  * ---------------------------------------------------------------------------
  * Step executor.  Not a step of the path itself: it enqueues the four calls
- * above for one training step of one table, in data order, on three streams,
+ * above for one training step of one table, in data order, on up to four streams,
  * so that the latency-bound coalesce/pack work of a step overlaps the
  * bandwidth-bound lookup and update of neighbouring steps (the sparse
  * gradient work runs in GPU idle time, as in Vertical Sparse Scheduling,
@@ -364,7 +364,9 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  * The caller rotates buffer sets (coalesce workspace, uniq_* and send_*
  * outputs; two unless `sets` says more) between consecutive steps and gives
  * each set its own events; `reuse` is nonzero when the set was used before.
- * Below, "s-2" is the set's previous step, s - sets.
+ * Below, "s-2" is the set's previous step, s - sets.  The streams may differ
+ * between sets: with the `coalesce` stream alternating between two streams,
+ * the sorts of consecutive steps run side by side.
  *
  * by_owner == 0: emb_grad_coalesce on the `coalesce` stream, emb_pack_by_owner
  * on the `pack` stream, lookup and update on `lookup_update`, with the waits
