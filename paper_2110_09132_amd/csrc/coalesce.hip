@@ -45,9 +45,10 @@ constexpr int kWaves = kThreads / kWave;
 constexpr int kItems = 8;
 constexpr int kMaxPasses = 4;  // up to 31 key bits
 
-// Radix configuration: passes of <= 8-bit digits, 256-thread tiles of 2048 keys.
-// (Two passes of 11-bit digits were measured slower than three of 8 bits: the
-// 2048-bin ranking is LDS-bound and runs on half as many tiles.)
+// Radix configuration: 256-thread tiles of 2048 keys, digits of at most 8 bits,
+// or 9 bits for keys of 17 or 18 bits (two passes instead of three).  (Two
+// passes of 11-bit digits were measured slower than three of 8 bits for 24-bit
+// keys: the 2048-bin ranking is LDS-bound and runs on half as many tiles.)
 template <int NT, int BITS>
 struct SortCfg {
   static constexpr int kNT = NT;
@@ -57,6 +58,7 @@ struct SortCfg {
   static constexpr int kPasses = kMaxPasses;  // most passes this configuration runs
 };
 using Narrow = SortCfg<256, 8>;
+using Wide9 = SortCfg<256, 9>;  // same workspace sizes as Narrow for its two passes
 constexpr int kChunk = 32;                    // sorted tokens per reduction wave
 constexpr int kRedTile = kChunk * kWaves;     // sorted tokens per reduction workgroup
 constexpr int kLoadsInFlight = 8;
@@ -218,8 +220,9 @@ __device__ uint32_t digit_look_back(uint32_t* lb, int tile, int stride, int32_t*
 
 struct RadixPlan {
   int npass;  // number of passes
-  int per;    // bits per pass (<= 8)
+  int per;    // bits per pass (<= the digit width)
   int B;      // key bits
+  int digit;  // digit width of the configuration: 8 (Narrow) or 9 (Wide9)
   __host__ __device__ int shift(int p) const { return p * per; }
   __host__ __device__ int bits(int p) const { return min(per, B - p * per); }
 };
@@ -238,9 +241,9 @@ int key_bits(int64_t V, bool by_owner, int P, bool split) {
 
 RadixPlan plan_for(int B) {
   B = max(B, 1);  // one pass even when every key is 0
-  const int digit = 8;
+  const int digit = (B == 17 || B == 18) ? 9 : 8;
   const int npass = (B + digit - 1) / digit;
-  return RadixPlan{npass, (B + npass - 1) / npass, B};
+  return RadixPlan{npass, (B + npass - 1) / npass, B, digit};
 }
 
 KeySpec key_spec(int64_t V, const int32_t* row_owner, int P, bool split) {
@@ -842,7 +845,10 @@ hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, con
   // histograms of all passes, then the radix passes over (key, position)
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
-  launch_sort<Narrow>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
+  if (plan.digit == 9)
+    launch_sort<Wide9>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
+  else
+    launch_sort<Narrow>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
   // 4. heads per reduction workgroup
   hipLaunchKernelGGL(seg_count_kernel, dim3((nred + kWaves - 1) / kWaves), dim3(kThreads), 0, stream, kin, ws.n_valid,
                      ws.tile_heads, nred);
