@@ -1,8 +1,9 @@
 // Host-only check of the step executor's cross-stream order with step signals.
 //
 // The executor (step.hip) is linked against stand-ins for the HIP stream
-// operations and for the kernel launchers: every launch, signal write and
-// signal wait is appended to a trace, per stream, instead of reaching a GPU.
+// operations and for the kernel launchers: every launch, event record or
+// wait, and signal write or wait is appended to a trace, per stream, instead
+// of reaching a GPU.
 // The trace is then executed by a model of the device (each stream runs its
 // operations in order; a wait proceeds once its word holds at least its
 // value; a write stores its value).  The program fails if a wait ever targets
@@ -26,7 +27,7 @@ namespace {
 enum Kind { kLaunch, kWrite, kWait, kRecord, kWaitEvent };
 struct Op {
   Kind kind;
-  long word;        // signal word index
+  long word;        // signal word index; for events: the record's number (a wait: the record it waits for, or -1)
   uint32_t value;   // written / waited-for value
   std::string what;
 };
@@ -35,6 +36,8 @@ std::map<long, std::deque<Op>> g_streams;  // stream id -> operations in enqueue
 std::map<void*, long> g_word_of;           // signal memory -> word index
 std::vector<uint32_t> g_enqueued_max;      // per word: largest value of a write enqueued so far
 std::vector<uint32_t> g_mem;               // per word: the model's current value
+std::map<void*, long> g_last_record;       // event -> number of its latest record enqueued
+std::vector<bool> g_record_done;           // record number -> executed
 long g_words = 0;
 int g_failures = 0;
 long g_ops = 0;
@@ -60,6 +63,8 @@ void drain() {
       while (!q.empty()) {
         Op& op = q.front();
         if (op.kind == kWait && g_mem[op.word] < op.value) break;
+        if (op.kind == kWaitEvent && op.word >= 0 && !g_record_done[op.word]) break;
+        if (op.kind == kRecord) g_record_done[op.word] = true;
         if (op.kind == kWrite) {
           if (op.value < g_mem[op.word]) {
             std::printf("stream %ld word %ld: %u -> %u\n", kv.first, op.word, g_mem[op.word], op.value);
@@ -100,11 +105,19 @@ hipError_t hipStreamWaitValue32(hipStream_t stream, void* ptr, uint32_t value, u
   push(stream, Op{kWait, w, value, "wait"});
   return hipSuccess;
 }
-hipError_t hipEventRecord(hipEvent_t, hipStream_t stream) {
-  push(stream, Op{kRecord, 0, 0, "record"});
+hipError_t hipEventRecord(hipEvent_t event, hipStream_t stream) {
+  const long n = static_cast<long>(g_record_done.size());
+  g_record_done.push_back(false);
+  g_last_record[event] = n;
+  push(stream, Op{kRecord, n, 0, "record"});
   return hipSuccess;
 }
-hipError_t hipStreamWaitEvent(hipStream_t, hipEvent_t, unsigned int) { fail("an event wait with signals"); return hipSuccess; }
+hipError_t hipStreamWaitEvent(hipStream_t stream, hipEvent_t event, unsigned int) {
+  // HIP semantics: wait for the event's latest record at the time of the call (none: no wait)
+  auto it = g_last_record.find(event);
+  push(stream, Op{kWaitEvent, it == g_last_record.end() ? -1 : it->second, 0, "wait event"});
+  return hipSuccess;
+}
 hipError_t hipExtMallocWithFlags(void** ptr, size_t, unsigned int flags) {
   if (flags != hipMallocSignalMemory) fail("unexpected allocation");
   *ptr = std::malloc(8);
@@ -155,7 +168,7 @@ int sparse_adam_call(float*, float*, float*, int64_t, int32_t, const int32_t*, c
                      int32_t, int32_t, int32_t, double, double, double, double, int64_t, int32_t*, hipStream_t stream,
                      hipEvent_t, hipEvent_t stop) {
   push(stream, Op{kLaunch, 0, 0, "adam"});
-  if (stop) fail("an attached event with signals");
+  if (stop) hipEventRecord(stop, stream);  // an event attached to the dispatch completes with it
   return EMB_OK;
 }
 }  // namespace emb
@@ -223,6 +236,7 @@ int main() {
     t.sched.coalesce = fake_stream(2);
     t.sched.pack = fake_stream(3);
     t.sched.delayed = fake_stream(4);
+    t.sched.updated = reinterpret_cast<void*>(&t);  // the update's end goes through this event
     new_handle(t);
   }
   // handles taken back from the pool by pipelines of other modes
@@ -252,6 +266,8 @@ int main() {
     const bool one_stream = rnd(8) == 0;
     t.sched.sets = static_cast<int32_t>(rnd(5));  // 0 (two), 1 .. 4
     if (one_stream) t.sched.coalesce = t.sched.pack = t.sched.delayed = fake_stream(1);
+    t.sched.reuse = rnd(2);
+    t.sched.updated = rnd(4) == 0 ? nullptr : reinterpret_cast<void*>(&t);  // sometimes no event: a signal
     const int st = step(t, mode, fail_pack);
     if ((st != EMB_OK) != fail_pack) fail("random step");
     t.sched.coalesce = fake_stream(2);

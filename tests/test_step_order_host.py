@@ -1,5 +1,5 @@
 """The step executor's cross-stream order with step signals, checked on the host: step.hip is
-linked against stand-ins that record every launch, signal write and signal wait per stream, and a
+linked against stand-ins that record every launch, signal write and wait, and event record and wait per stream, and a
 model of the device runs the recorded work (tests/host_order/order_sim.cpp).  It must never wait
 for a value that no write enqueued before it supplies, never let a signal word decrease, and never
 deadlock: across handles reused between modes, a call that fails part-way, and a long random mix
