@@ -281,8 +281,9 @@ def schedule_candidates(args):
     if args.sequential:
         return [("events", 2)]
     orders = ("events", "signals") if args.order == "auto" else (args.order,)
-    sets = (2,) if args.schedule == "split" else ((2, 4) if args.sets == 0 else (args.sets,))
-    return [(o, n) for o in orders for n in sets]
+    sets = (2, 4) if args.sets == 0 else (args.sets,)
+    # with events the split needs two sets (its lookup waits for the delayed update two steps back)
+    return [(o, n) for o in orders for n in sets if not (args.schedule == "split" and o == "events" and n != 2)]
 
 
 def host_info():
@@ -316,7 +317,7 @@ def main():
                          "emb_pack_by_owner")
     ap.add_argument("--sets", type=int, choices=(0, 2, 4), default=0,
                     help="buffer sets rotated between steps, with the sorts of odd and even sets on two side "
-                         "streams when 4 (0: tuned; the split schedule uses 2)")
+                         "streams when 4 and not split (0: tuned; the split with events uses 2)")
     ap.add_argument("--order", choices=("auto", "signals", "events"), default="auto",
                     help="cross-stream order of the overlapped schedule: step signals (stream memory operations), "
                          "events, or auto (tuned)")
