@@ -279,11 +279,16 @@ def cost_model_report(emb, sp, U, N=8):
 def schedule_candidates(args):
     """(cross-stream order, buffer sets) pairs the bench chooses among: those the options leave open."""
     if args.sequential:
-        return [("events", 2)]
+        return [("events", 2, False)]
     orders = ("events", "signals") if args.order == "auto" else (args.order,)
     sets = (2, 4) if args.sets == 0 else (args.sets,)
     # with events the split needs two sets (its lookup waits for the delayed update two steps back)
-    return [(o, n) for o in orders for n in sets if not (args.schedule == "split" and o == "events" and n != 2)]
+    cands = [(o, n, False) for o in orders for n in sets
+             if not (args.schedule == "split" and o == "events" and n != 2)]
+    # owner-major with four sets: also with each sort stream running its steps' reductions
+    if args.schedule == "by_owner":
+        cands += [(o, 4, True) for o in orders if 4 in sets]
+    return cands
 
 
 def host_info():
@@ -387,10 +392,11 @@ def main():
     split = args.schedule == "split"
     by_owner = args.schedule != "unfused"
     def make_pipe(cand):
-        order, sets = cand
+        order, sets, paired = cand
         return StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential,
                             by_owner=by_owner, split=split, signals=order == "signals",
-                            sort_streams=2 if (sets == 4 and by_owner and not split) else 1, sets=sets)
+                            sort_streams=2 if (sets == 4 and by_owner and not split) else 1, sets=sets,
+                            paired=paired)
 
     def next_ids(t):
         return [x[0] for x in step_batches[(t + 1) % args.batches]] if split else None
@@ -416,11 +422,12 @@ def main():
                 trial.step(step_batches[t % args.batches], t, next_ids=next_ids(t))
             trial.finish()
             torch.cuda.synchronize()
-            tune_ms[f"{c[0]}/{c[1]} sets"] = (time.perf_counter() - t_start) * 1e3 / args.tune_steps
+            tune_ms[f"{c[0]}/{c[1]} sets{'/paired' if c[2] else ''}"] = \
+                (time.perf_counter() - t_start) * 1e3 / args.tune_steps
             del trial
         cand = cands[min(range(len(cands)), key=lambda i: list(tune_ms.values())[i])]
-    order, nsets = cand
-    log(f"schedule: {order}, {nsets} buffer sets {tune_ms or ''}")
+    order, nsets, paired = cand
+    log(f"schedule: {order}, {nsets} buffer sets{', paired' if paired else ''} {tune_ms or ''}")
     pipe = make_pipe(cand)
     for _ in range(args.warmup):
         t += 1
@@ -542,6 +549,7 @@ def main():
                        args.schedule],
                    "sort_streams": None if (args.sequential or split or not by_owner) else (2 if nsets == 4 else 1),
                    "buffer_sets": nsets,
+                   "sort_and_reduce_paired": paired,
                    "cross_stream_order": None if args.sequential else
                    {"signals": "step signals (hipStreamWriteValue32 / hipStreamWaitValue32)",
                     "events": "events (hipEventRecord / hipStreamWaitEvent)"}[order],

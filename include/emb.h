@@ -472,12 +472,16 @@ int emb_event_destroy(void *event);
 int emb_event_elapsed_ms(void *start, void *end, float *ms);
 
 /* Step signals: the cross-stream order of emb_train_step kept through stream
- * memory operations instead of events.  A handle holds one word of HIP signal
- * memory per stage (sorted, coalesced, packed, updated, gathered,
- * delayed_done) and a step counter.  Each emb_train_step call that names the
- * handle takes the next step number n; the end of a stage writes n into its
- * word (hipStreamWriteValue32) and a stream that must follow the stage of
- * step n - k waits until the word reaches n - k (hipStreamWaitValue32, >=).
+ * memory operations instead of events.  A handle holds two words of HIP
+ * signal memory per stage (sorted, coalesced, packed, updated, gathered,
+ * delayed_done), for steps of even and of odd number, and a step counter.
+ * Each emb_train_step call that names the handle takes the next step number n;
+ * the end of a stage writes n into its word of n's parity
+ * (hipStreamWriteValue32) and a stream that must follow the stage of step
+ * n - k waits until the word of (n - k)'s parity reaches n - k
+ * (hipStreamWaitValue32, >=).  (With the two parities on two streams, as when
+ * the odd and even steps' coalesce runs on two streams, each word has a single
+ * writer.)
  * The order is the one listed above for the events.  A wait never targets
  * more than the value of the last write already enqueued for its word (a
  * stage that did not run in the step waited for is waited for at its last

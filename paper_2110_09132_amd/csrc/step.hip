@@ -32,12 +32,14 @@ int wait(void* stream, void* ev) { return status_of(hipStreamWaitEvent(S(stream)
 
 enum Stage { kSorted = 0, kCoalesced, kPacked, kUpdated, kGathered, kDelayedDone, kStages };
 
+// Two words per stage, for the steps of even and of odd number: in a schedule
+// whose odd and even steps run on two streams, each word then has one writer.
 struct StepSignals {
   int device;
-  void* word[kStages];       // hipMallocSignalMemory allocations
-  uint32_t seq;              // number of the last step enqueued with this handle
-  uint32_t written[kStages]; // the largest value a write already enqueued puts in each word
-  void* writer[kStages];     // the stream of that write
+  void* word[kStages][2];       // hipMallocSignalMemory allocations
+  uint32_t seq;                 // number of the last step enqueued with this handle
+  uint32_t written[kStages][2]; // the largest value a write already enqueued puts in each word
+  void* writer[kStages][2];     // the stream of that write
 };
 
 // Released handles are kept for reuse rather than freed, so that no signal
@@ -74,30 +76,34 @@ struct Order {
   // the writes stay in enqueue order, so the value only grows: a write on
   // another stream than the word's last one first waits for that write.
   int write(Stage k, void* stream) const {
-    if (sig->written[k] >= seq) return EMB_OK;
-    if (sig->written[k] != 0 && sig->writer[k] != stream &&
-        hipStreamWaitValue32(S(stream), sig->word[k], sig->written[k], hipStreamWaitValueGte, 0xFFFFFFFFu) !=
-            hipSuccess)
+    const int q = seq & 1;
+    if (sig->written[k][q] >= seq) return EMB_OK;
+    if (sig->written[k][q] != 0 && sig->writer[k][q] != stream &&
+        hipStreamWaitValue32(S(stream), sig->word[k][q], sig->written[k][q], hipStreamWaitValueGte,
+                             0xFFFFFFFFu) != hipSuccess)
       return EMB_ERR_LAUNCH;
-    if (hipStreamWriteValue32(S(stream), sig->word[k], seq, 0) != hipSuccess) return EMB_ERR_LAUNCH;
-    sig->written[k] = seq;
-    sig->writer[k] = stream;
+    if (hipStreamWriteValue32(S(stream), sig->word[k][q], seq, 0) != hipSuccess) return EMB_ERR_LAUNCH;
+    sig->written[k][q] = seq;
+    sig->writer[k][q] = stream;
     return EMB_OK;
   }
   // `stream` waits for stage k of the step `lag` steps back (lag 0: this step).
   // With events, a lag > 0 means the step that last used this buffer set (the
   // set's own event), so it must equal `sets`.
-  // With signals the target never exceeds what an enqueued write will put in
-  // the word: a stage that did not run in that step (another mode, a failed
-  // call) is waited for at its last run, or not at all if it never ran.  Every
+  // With signals the wait uses the word of that step's parity, and the target
+  // never exceeds what an enqueued write will put in the word: a stage that did
+  // not run in that step (another mode, a failed call) is waited for at its
+  // last run in a step of that parity, or not at all.  Every
   // wait thus refers to a write enqueued before it, so the waits cannot form a
   // cycle.
   int after(void* stream, Stage k, uint32_t lag) const {
     if (sig != nullptr) {
       if (seq <= lag) return EMB_OK;  // no such step
-      const uint32_t target = seq - lag < sig->written[k] ? seq - lag : sig->written[k];
-      if (target == 0) return EMB_OK;  // the stage never ran
-      return status_of(hipStreamWaitValue32(S(stream), sig->word[k], target, hipStreamWaitValueGte, 0xFFFFFFFFu));
+      const uint32_t n = seq - lag;
+      const int q = n & 1;
+      const uint32_t target = n < sig->written[k][q] ? n : sig->written[k][q];
+      if (target == 0) return EMB_OK;  // the stage never ran in a step of that parity
+      return status_of(hipStreamWaitValue32(S(stream), sig->word[k][q], target, hipStreamWaitValueGte, 0xFFFFFFFFu));
     }
     if (lag > 0 && !s->reuse) return EMB_OK;  // the buffer set was not used before
     return wait(stream, event(k));
@@ -262,9 +268,10 @@ int emb_step_signals_create(void** signals) {
   auto* h = new StepSignals{};
   h->device = dev;
   for (int k = 0; k < kStages; ++k)  // on failure the partial handle is dropped, not freed
-    if (hipExtMallocWithFlags(&h->word[k], 8, hipMallocSignalMemory) != hipSuccess ||
-        hipStreamWriteValue32(nullptr, h->word[k], 0, 0) != hipSuccess)
-      return EMB_ERR_LAUNCH;
+    for (int q = 0; q < 2; ++q)
+      if (hipExtMallocWithFlags(&h->word[k][q], 8, hipMallocSignalMemory) != hipSuccess ||
+          hipStreamWriteValue32(nullptr, h->word[k][q], 0, 0) != hipSuccess)
+        return EMB_ERR_LAUNCH;
   if (hipStreamSynchronize(nullptr) != hipSuccess) return EMB_ERR_LAUNCH;
   *signals = h;
   return EMB_OK;

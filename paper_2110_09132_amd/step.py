@@ -86,7 +86,7 @@ class StepPipeline:
 
     def __init__(self, tables, lr, beta1, beta2, eps, overlap: bool = True, dev_status: torch.Tensor | None = None,
                  streams: int = 3, by_owner: bool = True, split: bool = False, signals: bool = False,
-                 sort_streams: int = 1, sets: int = 2):
+                 sort_streams: int = 1, sets: int = 2, paired: bool = False):
         """streams (with overlap=True and by_owner=False): 2 puts coalesce and pack on one side
         stream, 3 gives each its own (more concurrency, one more cross-stream wait per step).
         by_owner: coalesce straight into the send layout (emb_grad_coalesce_by_owner).
@@ -97,6 +97,8 @@ class StepPipeline:
         sets: buffer sets rotated between steps (every table needs at least this many; the split
         with events needs 2).  More sets let a step's sort start before the reduction of the step
         two back has finished.
+        paired (with sort_streams=2): each of the two sort streams also runs the reductions of its
+        steps, right after their sorts (no cross-stream wait between the two halves).
         signals (with overlap=True): keep the cross-stream order with step signals (stream memory
         operations: about half the host time per step, for host-bound pipelines of small
         batches; with large batches events keep the GPU a few percent busier) instead of events."""
@@ -111,6 +113,7 @@ class StepPipeline:
         self.side3 = s3 if (overlap and split) else self.main  # the delayed update
         # the sorts of buffer set 1 (by_owner without the split): the third side stream
         self.side3_sort = s3 if (overlap and self.by_owner and not split and sort_streams >= 2) else None
+        self.paired = paired and self.side3_sort is not None
         if sort_streams >= 2 and sets % 2:
             raise ValueError("two sort streams need an even number of buffer sets")
         if any(tb.sets < sets for tb in self.tables):
@@ -138,8 +141,9 @@ class StepPipeline:
                 evs = [Event() for _ in range(6)]
                 self.events += evs
                 sort_side = self.side3_sort if (i % 2 == 1 and self.side3_sort is not None) else self.side
+                red_side = sort_side if self.paired else self.side2
                 s = StepSchedule(lookup_update=_stream_handle(self.main), coalesce=_stream_handle(sort_side),
-                                 pack=_stream_handle(self.side2), delayed=_stream_handle(self.side3),
+                                 pack=_stream_handle(red_side), delayed=_stream_handle(self.side3),
                                  sorted=evs[0].handle, coalesced=evs[1].handle, packed=evs[2].handle,
                                  updated=evs[3].handle, gathered=evs[4].handle, delayed_done=evs[5].handle,
                                  by_owner=1 if self.by_owner else 0, split=1 if split else 0,

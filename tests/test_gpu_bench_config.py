@@ -23,12 +23,13 @@ from workloads import configs
 
 pytestmark = pytest.mark.gpu
 
-SCHEDULES = [("events", 2, 1), ("signals", 4, 2), ("events", 4, 2)]
+SCHEDULES = [("events", 2, 1, False), ("signals", 4, 2, False), ("events", 4, 2, False), ("signals", 4, 2, True)]
 
 
-@pytest.mark.parametrize("order,sets,sort_streams", SCHEDULES, ids=[f"{o}-{s}sets" for o, s, _ in SCHEDULES])
+@pytest.mark.parametrize("order,sets,sort_streams,paired", SCHEDULES,
+                         ids=[f"{o}-{s}sets{'-paired' if p else ''}" for o, s, _, p in SCHEDULES])
 @pytest.mark.parametrize("name", ["lowdup_uniform", "lowdup_zipf13"])
-def test_bench_schedule_full_size(name, order, sets, sort_streams):
+def test_bench_schedule_full_size(name, order, sets, sort_streams, paired):
     wl = configs.WORKLOADS[name]
     sp = wl.tables[0]
     steps = sets  # every step's send buffers survive until the end
@@ -37,7 +38,7 @@ def test_bench_schedule_full_size(name, order, sets, sort_streams):
     own = configs.row_owner(sp)
     tb = EmbeddingTable(to_dev(W0), to_dev(own), sp.P, sp.T, sets=sets)
     pipe = StepPipeline([tb], wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=True, signals=order == "signals",
-                        sets=sets, sort_streams=sort_streams)
+                        sets=sets, sort_streams=sort_streams, paired=paired)
     batches = [configs.make_batch(sp, 500 + k) for k in range(steps)]
     dev_batches = [(to_dev(ids), to_dev(G)) for ids, G in batches]
     rng = np.random.default_rng(7)

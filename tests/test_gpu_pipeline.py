@@ -15,7 +15,7 @@ from workloads import configs, gen
 pytestmark = pytest.mark.gpu
 
 
-def run(overlap, by_owner, steps=9, split=False, signals=False, sort_streams=1, sets=2):
+def run(overlap, by_owner, steps=9, split=False, signals=False, sort_streams=1, sets=2, paired=False):
     torch.cuda.synchronize()
     specs = [configs.TableSpec(20000, 128, 6000, "zipf", 1.05, "f32", 0.01, 8, "mod", 61),
              configs.TableSpec(5000, 64, 3000, "uniform", 0.0, "bf16", 0.01, 3, "range", 62)]
@@ -34,7 +34,7 @@ def run(overlap, by_owner, steps=9, split=False, signals=False, sort_streams=1, 
         batches.append(per)
     torch.cuda.synchronize()
     pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner, split=split,
-                        signals=signals, sort_streams=sort_streams, sets=sets)
+                        signals=signals, sort_streams=sort_streams, sets=sets, paired=paired)
     lookups = []
     empty = torch.zeros(0, dtype=torch.int32, device="cuda")
     for t in range(1, steps + 1):
@@ -62,11 +62,11 @@ def test_overlapped_schedule_equals_sequential(by_owner, split, signals):
             assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
 
 
-@pytest.mark.parametrize("sets", [2, 4])
+@pytest.mark.parametrize("sets,paired", [(2, False), (4, False), (4, True)])
 @pytest.mark.parametrize("signals", [False, True], ids=["events", "signals"])
-def test_two_sort_streams_equal_sequential(signals, sets):
-    print(f"two sort streams, signals={signals}, sets={sets}", flush=True)
-    a, la = run(True, True, signals=signals, sort_streams=2, sets=sets)
+def test_two_sort_streams_equal_sequential(signals, sets, paired):
+    print(f"two sort streams, signals={signals}, sets={sets}, paired={paired}", flush=True)
+    a, la = run(True, True, signals=signals, sort_streams=2, sets=sets, paired=paired)
     b, lb = run(False, True)
     for x, y in zip(a, b):
         for u, v in zip(x, y):
