@@ -265,6 +265,9 @@ int main() {
     const bool fail_pack = mode == 0 && rnd(10) == 0;
     const bool one_stream = rnd(8) == 0;
     t.sched.sets = static_cast<int32_t>(rnd(5));  // 0 (two), 1 .. 4
+    // sorts of odd steps on another stream, sometimes with their reductions (paired)
+    if (rnd(2)) t.sched.coalesce = fake_stream(s % 2 ? 5 : 2);
+    if (rnd(3) == 0) t.sched.pack = t.sched.coalesce;
     if (one_stream) t.sched.coalesce = t.sched.pack = t.sched.delayed = fake_stream(1);
     t.sched.reuse = rnd(2);
     t.sched.updated = rnd(4) == 0 ? nullptr : reinterpret_cast<void*>(&t);  // sometimes no event: a signal
