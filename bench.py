@@ -346,7 +346,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU's share of the path; runs on more than one GPU are not "
-              "supported by this build (use --gpus 1)", file=sys.stderr)
+              "supported (use --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
     import torch

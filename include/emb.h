@@ -55,7 +55,7 @@ extern "C" {
 #define EMB_ERR_INVALID_ARG 1 /* null pointer, size or range out of bounds */
 #define EMB_ERR_WORKSPACE 2   /* workspace smaller than the size query */
 #define EMB_ERR_LAUNCH 3      /* the HIP runtime refused a launch */
-#define EMB_ERR_UNSUPPORTED 4 /* valid but not supported by this build */
+#define EMB_ERR_UNSUPPORTED 4 /* valid but not supported by this library */
 
 /* gradient element types */
 #define EMB_F32 0  /* IEEE binary32 */
