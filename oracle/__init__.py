@@ -71,6 +71,8 @@ def _bind(lib):
     lib.orc_vertical_split.restype = I64
     lib.orc_sparse_adam.argtypes = [P, P, P, I64, I64, P, P, P, I32, I32, D, D, D, D, I64]
     lib.orc_sparse_adam.restype = I64
+    lib.orc_lookup_request.argtypes = [P, I64, I64, P, I32, P, P, P, P]
+    lib.orc_lookup_request.restype = I64
     lib.orc_pack_by_column.argtypes = [P, I64, I64, I64, I32, P]
     lib.orc_pack_by_column.restype = None
     lib.orc_gather_by_column.argtypes = [P, I64, I64, I32, P, I64, P]
@@ -219,3 +221,19 @@ COMM_SCHEMES = {"alltoall": 0, "allreduce": 1, "ps": 2, "allgather": 3}
 def comm_cost(scheme, N, M, alpha, B, beta, S=1):
     """Table 2 cost of one exchange by scheme name (alltoall, allreduce, ps, allgather)."""
     return float(_load().orc_comm_cost(COMM_SCHEMES[scheme], N, S, float(M), float(alpha), float(B), float(beta)))
+
+
+def lookup_request(ids, V, row_owner, P):
+    """Owner-grouped distinct ids of a batch and each token's index in them (-1: takes no part).
+
+    Returns dict(req_ids [U], req_counts [P], req_offsets [P+1], inverse [T], U)."""
+    ids = _c(ids, np.int32)
+    row_owner = _c(row_owner, np.int32)
+    T = ids.size
+    req_ids = np.empty(max(T, 1), np.int32)
+    counts = np.empty(P, np.int32)
+    offs = np.empty(P + 1, np.int32)
+    inv = np.empty(max(T, 1), np.int32)
+    U = int(_load().orc_lookup_request(_ptr(ids), T, V, _ptr(row_owner), P, _ptr(req_ids), _ptr(counts), _ptr(offs),
+                                       _ptr(inv)))
+    return dict(req_ids=req_ids[:U], req_counts=counts, req_offsets=offs, inverse=inv[:T], U=U)

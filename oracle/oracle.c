@@ -103,7 +103,7 @@ int64_t orc_pack_by_owner(const int32_t *uniq_ids, const float *uniq_grad,
                           int32_t *send_offsets) {
     int64_t bad = 0;
     int32_t *own = (int32_t *)malloc(sizeof(int32_t) * (size_t)(U > 0 ? U : 1));
-    int32_t *run = (int32_t *)calloc((size_t)P, sizeof(int32_t));
+    int32_t *run = (int32_t *)calloc((size_t)(P > 0 ? P : 1), sizeof(int32_t));
     for (int32_t p = 0; p < P; ++p) send_counts[p] = 0;
     for (int64_t k = 0; k < U; ++k) {
         int64_t id = uniq_ids[k];
@@ -174,6 +174,48 @@ int64_t orc_sparse_adam(float *W, float *m, float *v, int64_t V, int64_t D,
         }
     }
     return bad;
+}
+
+/* Lookup requests of the row-wise partition, Sec. 4.1.1. */
+int64_t orc_lookup_request(const int32_t *ids, int64_t T, int64_t V,
+                           const int32_t *row_owner, int32_t P,
+                           int32_t *req_ids, int32_t *req_counts,
+                           int32_t *req_offsets, int32_t *inverse) {
+    /* the distinct ids that take part, ascending */
+    int32_t *u = (int32_t *)malloc(sizeof(int32_t) * (size_t)(T > 0 ? T : 1));
+    int64_t n = 0;
+    for (int64_t t = 0; t < T; ++t) {
+        const int32_t id = ids[t];
+        if (id >= 0 && id < V && row_owner[id] >= 0 && row_owner[id] < P) u[n++] = id;
+    }
+    qsort(u, (size_t)n, sizeof(int32_t), orc_int32_cmp);
+    int64_t U = 0;
+    for (int64_t k = 0; k < n; ++k)
+        if (k == 0 || u[k] != u[k - 1]) u[U++] = u[k];
+    /* grouped by owner, ascending inside an owner */
+    for (int32_t p = 0; p < P; ++p) req_counts[p] = 0;
+    for (int64_t k = 0; k < U; ++k) req_counts[row_owner[u[k]]] += 1;
+    req_offsets[0] = 0;
+    for (int32_t p = 0; p < P; ++p) req_offsets[p + 1] = req_offsets[p] + req_counts[p];
+    int32_t *run = (int32_t *)calloc((size_t)(P > 0 ? P : 1), sizeof(int32_t));
+    for (int64_t k = 0; k < U; ++k) {
+        const int32_t p = row_owner[u[k]];
+        req_ids[req_offsets[p] + run[p]++] = u[k];
+    }
+    /* each token's place in the request */
+    for (int64_t t = 0; t < T; ++t) {
+        const int32_t id = ids[t];
+        inverse[t] = -1;
+        if (id < 0 || id >= V || row_owner[id] < 0 || row_owner[id] >= P) continue;
+        const int32_t p = row_owner[id];
+        const int32_t *blk = req_ids + req_offsets[p];
+        const int32_t *hit = (const int32_t *)bsearch(&id, blk, (size_t)(req_offsets[p + 1] - req_offsets[p]),
+                                                      sizeof(int32_t), orc_int32_cmp);
+        inverse[t] = hit != NULL ? (int32_t)(hit - req_ids) : -1;
+    }
+    free(run);
+    free(u);
+    return U;
 }
 
 /* Column-wise partition, Sec. 4.1.1.  First column of owner p. */

@@ -84,6 +84,21 @@ int64_t orc_sparse_adam(float *W, float *m, float *v, int64_t V, int64_t D,
                         int32_t shard_end, double lr, double beta1,
                         double beta2, double eps, int64_t step);
 
+/* Lookup requests of the row-wise partition (Sec. 4.1.1: every process looks
+ * up its training data in the embedding table; with rows partitioned by
+ * owner, a process asks each owner for the rows it needs).  A token takes
+ * part when its id is in [0, V) and row_owner[id] in [0, P).
+ *   req_ids[U]        the distinct ids of the tokens that take part, grouped by
+ *                     owner (owner 0 first), ascending inside an owner
+ *   req_counts[P], req_offsets[P+1]: the owner groups
+ *   inverse[T]        k with req_ids[k] = ids[t] for a token that takes part,
+ *                     -1 for one that does not
+ * Returns U. */
+int64_t orc_lookup_request(const int32_t *ids, int64_t T, int64_t V,
+                           const int32_t *row_owner, int32_t P,
+                           int32_t *req_ids, int32_t *req_counts,
+                           int32_t *req_offsets, int32_t *inverse);
+
 /* Column-wise partition (Sec. 4.1.1: the table is split along the embedding
  * dimension, every part keeping the whole vocabulary).  The paper does not say
  * how D columns split when P does not divide D; here owner p holds columns

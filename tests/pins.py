@@ -285,6 +285,92 @@ def pin_split_two_applies():
         assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
 
 
+# ------------------------------------------------------- lookup requests
+def pin_lookup_request_golden():
+    """Hand-worked requests of a worker in the row-wise partition (Sec. 4.1.1)."""
+    g = load_golden("lookup_request_worked.txt")
+    ids = np.array(g["ids"], np.int32)
+    for own, sfx in ((gen.owner_mod(g["V"], g["P"]), ""), (np.array(g["row_owner_b"], np.int32), "_b")):
+        r = oracle.lookup_request(ids, g["V"], own, g["P"])
+        assert r["req_ids"].tolist() == g["req_ids" + sfx]
+        assert r["req_counts"].tolist() == g["req_counts" + sfx]
+        assert r["req_offsets"].tolist() == g["req_offsets" + sfx]
+        assert r["inverse"].tolist() == g["inverse" + sfx]
+        assert r["U"] == len(g["req_ids" + sfx])
+
+
+def check_lookup_request(r, ids, V, row_owner, P):
+    """What the requests of a batch must be, checked against Python sets and numpy (shared by
+    oracle pins and GPU tests):
+      the requested ids are the set of the batch's ids that are rows with an owner in [0, P);
+      they come grouped by owner (ascending owners), ascending inside a group, and the counts
+      and offsets describe the groups;
+      every token that takes part points at its own id, every other token at -1."""
+    ids = np.asarray(ids, np.int64)
+    take = (ids >= 0) & (ids < V)
+    take[take] &= (row_owner[ids[take]] >= 0) & (row_owner[ids[take]] < P)
+    want = sorted(set(ids[take].tolist()))
+    req = np.asarray(r["req_ids"], np.int64)
+    assert r["U"] == len(want) == req.size
+    assert sorted(req.tolist()) == want
+    own = row_owner[req]
+    counts = np.bincount(own, minlength=P)[:P] if req.size else np.zeros(P, np.int64)
+    assert np.array_equal(r["req_counts"], counts)
+    assert np.array_equal(r["req_offsets"], np.concatenate([[0], np.cumsum(counts)]))
+    for p in range(P):
+        blk = req[r["req_offsets"][p]:r["req_offsets"][p + 1]]
+        assert np.all(row_owner[blk] == p) and np.all(np.diff(blk) > 0)
+    inv = np.asarray(r["inverse"], np.int64)
+    assert inv.size == ids.size
+    assert np.all(inv[~take] == -1)
+    assert np.all((inv[take] >= 0) & (inv[take] < req.size))
+    assert np.array_equal(req[inv[take]], ids[take])
+
+
+def pin_lookup_request_invariants():
+    for seed, (V, T, P, rule) in enumerate([(1000, 3000, 7, "mod"), (1000, 50, 16, "range"), (50, 500, 1, "mod"),
+                                            (4096, 2000, 1024, "rand"), (10, 0, 3, "mod"), (1, 9, 2, "mod")]):
+        ids = _rng_ids(400 + seed, T, V + 2)  # a few ids >= V
+        if T > 3:
+            ids[[0, T // 2]] = [-5, V + 1000]
+        if rule == "mod":
+            own = gen.owner_mod(V, P)
+        elif rule == "range":
+            own = gen.owner_range(V, P)
+        else:
+            own = np.random.default_rng(98).integers(0, P, V).astype(np.int32)
+            own[::17] = P  # rows without an owner
+        r = oracle.lookup_request(ids, V, own, P)
+        check_lookup_request(r, ids, V, own, P)
+        if P == 1 and r["U"]:  # a single owner: the request is the sorted distinct ids
+            assert np.array_equal(r["req_ids"], np.unique(ids[(ids >= 0) & (ids < V)]))
+
+
+def pin_lookup_request_serves_the_lookup():
+    """Row-wise forward exchange end to end (Sec. 4.1.1): P workers send their requests, each
+    owner answers with the rows of its shard (the owner's gather of the ids it received), and a
+    worker's gather through its inverse map of the rows it got back equals numpy's table[ids]
+    (zero rows for tokens that take part in nothing)."""
+    V, D, P = 200, 5, 4
+    table = _rng_normal(410, V * D, purpose=gen.PURPOSE_WEIGHTS).reshape(V, D)
+    own = gen.owner_range(V, P)
+    shard_of = {p: np.nonzero(own == p)[0] for p in range(P)}  # row ids of owner p, ascending
+    local = np.zeros(V, np.int32)
+    for p, rows in shard_of.items():
+        local[rows] = np.arange(rows.size)
+    shards = {p: table[rows] for p, rows in shard_of.items()}
+    batches = [_rng_ids(420 + q, n, V + 1) for q, n in enumerate((60, 0, 33, 1))]
+    for ids in batches:
+        r = oracle.lookup_request(ids, V, own, P)
+        back = np.zeros((r["U"], D), np.float32)
+        for p in range(P):
+            a, b = r["req_offsets"][p], r["req_offsets"][p + 1]
+            back[a:b] = oracle.gather(shards[p], local[r["req_ids"][a:b]])[0]
+        got = oracle.gather(back, r["inverse"])[0]
+        want = np.where((ids < V)[:, None], table[np.minimum(ids, V - 1)], 0).astype(np.float32)
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
 # ------------------------------------------------ receiver side of the exchange
 def pin_concat_coalesce_is_sum_of_workers():
     """The exchange delivers every worker's coalesced rows to their owner, who sums the rows of

@@ -33,6 +33,16 @@ MUTANTS = {
                        ["pin_split_golden", "pin_split_invariants"]),
     "split_drops_smallest_next_id": ("bsearch(&key, nx, (size_t)T_next,", "bsearch(&key, nx + 1, (size_t)(T_next > 0 ? T_next - 1 : 0),",
                                      ["pin_split_golden", "pin_split_invariants"]),
+    "request_keeps_duplicates": ("if (k == 0 || u[k] != u[k - 1]) u[U++] = u[k];", "u[U++] = u[k];",
+                                 ["pin_lookup_request_golden", "pin_lookup_request_invariants"]),
+    "request_skipped_token_reads_row_0": ("        inverse[t] = -1;\n", "        inverse[t] = 0;\n",
+                                          ["pin_lookup_request_golden", "pin_lookup_request_invariants"]),
+    "request_groups_by_id_only": ("req_ids[req_offsets[p] + run[p]++] = u[k];", "req_ids[k] = u[k];",
+                                  ["pin_lookup_request_golden", "pin_lookup_request_invariants"]),
+    "request_inverse_local_to_owner": ("inverse[t] = hit != NULL ? (int32_t)(hit - req_ids) : -1;",
+                                       "inverse[t] = hit != NULL ? (int32_t)(hit - blk) : -1;",
+                                       ["pin_lookup_request_golden", "pin_lookup_request_invariants",
+                                        "pin_lookup_request_serves_the_lookup"]),
     "column_split_rounds_up": ("return p * D / P;", "return (p * D + P - 1) / P;",
                                ["pin_column_golden", "pin_column_layout"]),
     "column_block_base_by_rows": ("blocks[C * a + r * w + j] = rows[r * D + a + j];",
