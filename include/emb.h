@@ -222,7 +222,9 @@ int emb_grad_coalesce_split(const int32_t *ids, int32_t T,
  *   recv_offsets[p][P]; receivers follow each other (owner-major).
  *   recv_ids [P * cap_rows], recv_rows [P * cap_rows][D]; recv_total [1] = rows received.
  * Offsets are clamped into [0, cap_rows]; rows outside a worker's blocks are
- * not sent.  Requires 1 <= P <= 1024, P * cap_rows < 2^30.
+ * not sent.  D == 0 moves the ids alone (send_rows and recv_rows may be NULL):
+ * the lookup requests of emb_lookup_request.  Requires 1 <= P <= 1024,
+ * P * cap_rows < 2^30, D >= 0.
  *
  * emb_receive_merge then coalesces the received rows of every owner (their
  * ids can repeat across senders): emb_grad_coalesce_by_owner over the first
@@ -244,6 +246,43 @@ int emb_receive_merge(const int32_t *recv_ids, const float *recv_rows,
                       int32_t *merged_offsets, int32_t *num_unique,
                       void *workspace, size_t workspace_bytes,
                       int32_t *dev_status, void *stream);
+
+/*
+ * Lookup requests of the row-wise partition (Sec. 4.1.1: every process looks
+ * up the embeddings of its own training data; with the rows partitioned, the
+ * rows a worker needs live with their owners, so the forward pass asks each
+ * owner for them and gets them back, the exchange that the column-wise
+ * partition replaces by the lookup-result AlltoAll).  Each distinct row is
+ * asked for once per worker, however many of its tokens use it.
+ *   ids [T] int32; row_owner [V] int32.  A token takes part when its id is in
+ *   [0, V) (else EMB_DEV_ID_OUT_OF_RANGE) and its owner in [0, P) (else
+ *   EMB_DEV_OWNER_OUT_OF_RANGE).
+ * Outputs (device):
+ *   req_ids     [T]     the U distinct ids of the tokens that take part,
+ *                       grouped by owner (owner 0 first), ascending inside a
+ *                       group: the send layout of emb_exchange_simulated (D = 0)
+ *   req_counts  [P], req_offsets [P + 1]: owner p's requests at
+ *                       [req_offsets[p], req_offsets[p + 1])
+ *   num_unique  [1]     U
+ *   inverse     [T]     k with req_ids[k] = ids[t] for a token that takes
+ *                       part, -1 for one that does not
+ * The owners answer with emb_gather of the ids they receive; the rows that
+ * come back in request order, [U][D], expand to the batch's lookup with
+ * emb_gather(rows, U, D, inverse, T, out) (tokens that take no part get zero
+ * rows).  Entries of req_ids past U are left unspecified.
+ * workspace: device memory of at least emb_lookup_request_workspace_bytes(T, V)
+ * bytes, 256-byte aligned; contents on entry do not matter.  T == 0 writes the
+ * empty result.  Requires 1 <= V < 2^31, 1 <= P <= 1024, 0 <= T < 2^30;
+ * EMB_ERR_UNSUPPORTED when bits(V) + bits(P) > 32 (the composite sort key of
+ * emb_grad_coalesce_by_owner).
+ */
+size_t emb_lookup_request_workspace_bytes(int32_t T, int64_t V);
+int emb_lookup_request(const int32_t *ids, int32_t T, int64_t V,
+                       const int32_t *row_owner, int32_t P, int32_t *req_ids,
+                       int32_t *req_counts, int32_t *req_offsets,
+                       int32_t *num_unique, int32_t *inverse, void *workspace,
+                       size_t workspace_bytes, int32_t *dev_status,
+                       void *stream);
 
 /*
  * Column-wise partition (Sec. 4.1.1: the table is split by columns before

@@ -46,6 +46,8 @@ SIGNATURES = {
     "emb_grad_coalesce_split_workspace_bytes": (_SZ, [_I32, _I32, _I64, _I32, _I32]),
     "emb_grad_coalesce_split": (ctypes.c_int, [_P, _I32, _P, _I32, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P,
                                                _P, _P, _SZ, _P, _P]),
+    "emb_lookup_request_workspace_bytes": (_SZ, [_I32, _I64]),
+    "emb_lookup_request": (ctypes.c_int, [_P, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_exchange_simulated": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]),
     "emb_receive_merge": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                          _P, _P]),
@@ -289,20 +291,47 @@ def grad_coalesce_split(ids, next_ids, grad, V, row_owner, P, out=None, workspac
     return out
 
 
+def lookup_request_workspace_bytes(T, V) -> int:
+    return int(lib.emb_lookup_request_workspace_bytes(T, V))
+
+
+def lookup_request(ids, V, row_owner, P, out=None, workspace=None, dev_status=None, stream=None):
+    """A worker's requests to the row owners (emb_lookup_request).
+
+    Returns (req_ids [T], req_counts [P], req_offsets [P+1], num_unique [1], inverse [T]); `out`
+    may pass those five tensors in."""
+    _need(ids, torch.int32, "ids")
+    _need(row_owner, torch.int32, "row_owner")
+    T = ids.numel()
+    dev = ids.device
+    if out is None:
+        out = (torch.empty(T, dtype=torch.int32, device=dev), torch.empty(P, dtype=torch.int32, device=dev),
+               torch.empty(P + 1, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev),
+               torch.empty(T, dtype=torch.int32, device=dev))
+    req_ids, counts, offsets, nu, inverse = out
+    if workspace is None:
+        workspace = new_workspace(lookup_request_workspace_bytes(T, V), dev)
+    _check(lib.emb_lookup_request(_ptr(ids), T, V, _ptr(row_owner), P, _ptr(req_ids), _ptr(counts), _ptr(offsets),
+                                  _ptr(nu), _ptr(inverse), _ptr(workspace), workspace.numel(), _ptr(dev_status),
+                                  _stream(stream)), "emb_lookup_request")
+    return out
+
+
 def exchange_simulated(send_ids, send_rows, send_offsets, out=None, stream=None):
     """Simulated AlltoAll of P workers' send layouts (emb_exchange_simulated).
 
-    send_ids [P, cap], send_rows [P, cap, D], send_offsets [P, P+1].  Returns (recv_ids [P*cap],
-    recv_rows [P*cap, D], recv_offsets [P, P+1], recv_total [1])."""
+    send_ids [P, cap], send_rows [P, cap, D] or None (ids only), send_offsets [P, P+1].  Returns
+    (recv_ids [P*cap], recv_rows [P*cap, D] or None, recv_offsets [P, P+1], recv_total [1])."""
     _need(send_ids, torch.int32, "send_ids")
-    _need(send_rows, torch.float32, "send_rows")
+    if send_rows is not None:
+        _need(send_rows, torch.float32, "send_rows")
     _need(send_offsets, torch.int32, "send_offsets")
     P, cap = send_ids.shape
-    D = send_rows.shape[-1]
+    D = send_rows.shape[-1] if send_rows is not None else 0
     dev = send_ids.device
     if out is None:
         out = (torch.empty(P * cap, dtype=torch.int32, device=dev),
-               torch.empty((P * cap, D), dtype=torch.float32, device=dev),
+               torch.empty((P * cap, D), dtype=torch.float32, device=dev) if D else None,
                torch.empty((P, P + 1), dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
     recv_ids, recv_rows, recv_offsets, recv_total = out
     _check(lib.emb_exchange_simulated(_ptr(send_ids), _ptr(send_rows), _ptr(send_offsets), P, cap, D, _ptr(recv_ids),

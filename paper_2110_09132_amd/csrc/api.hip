@@ -164,13 +164,34 @@ int emb_grad_coalesce_split(const int32_t* ids, int32_t T, const int32_t* next_i
                                             static_cast<hipStream_t>(stream)));
 }
 
+size_t emb_lookup_request_workspace_bytes(int32_t T, int64_t V) {
+  if (T < 0 || bad_table_dims(V, 1)) return 0;
+  return emb::coalesce_workspace_bytes(T, 0, -1, V);
+}
+
+int emb_lookup_request(const int32_t* ids, int32_t T, int64_t V, const int32_t* row_owner, int32_t P,
+                       int32_t* req_ids, int32_t* req_counts, int32_t* req_offsets, int32_t* num_unique,
+                       int32_t* inverse, void* workspace, size_t workspace_bytes, int32_t* dev_status,
+                       void* stream) {
+  if (T < 0 || T >= (1 << 30) || bad_table_dims(V, 1) || P < 1 || P > kMaxOwners) return EMB_ERR_INVALID_ARG;
+  if (!req_counts || !req_offsets || !num_unique) return EMB_ERR_INVALID_ARG;
+  if (!emb::coalesce_by_owner_supported(V, P, false)) return EMB_ERR_UNSUPPORTED;
+  if (T > 0 && (!ids || !row_owner || !req_ids || !inverse || !workspace)) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && reinterpret_cast<uintptr_t>(workspace) % 256 != 0) return EMB_ERR_INVALID_ARG;
+  if (T > 0 && workspace_bytes < emb::coalesce_workspace_bytes(T, 0, -1, V)) return EMB_ERR_WORKSPACE;
+  return launch_status(emb::launch_lookup_request(ids, T, V, row_owner, P, req_ids, req_counts, req_offsets,
+                                                  num_unique, inverse, workspace, dev_status,
+                                                  static_cast<hipStream_t>(stream)));
+}
+
 int emb_exchange_simulated(const int32_t* send_ids, const float* send_rows, const int32_t* send_offsets, int32_t P,
                            int32_t cap_rows, int32_t D, int32_t* recv_ids, float* recv_rows, int32_t* recv_offsets,
                            int32_t* recv_total, void* stream) {
-  if (P < 1 || P > kMaxOwners || cap_rows < 0 || D < 1) return EMB_ERR_INVALID_ARG;
+  if (P < 1 || P > kMaxOwners || cap_rows < 0 || D < 0) return EMB_ERR_INVALID_ARG;
   if (static_cast<int64_t>(P) * cap_rows >= (int64_t{1} << 30)) return EMB_ERR_INVALID_ARG;
   if (!send_offsets || !recv_offsets || !recv_total) return EMB_ERR_INVALID_ARG;
-  if (cap_rows > 0 && (!send_ids || !send_rows || !recv_ids || !recv_rows)) return EMB_ERR_INVALID_ARG;
+  if (cap_rows > 0 && (!send_ids || !recv_ids)) return EMB_ERR_INVALID_ARG;
+  if (cap_rows > 0 && D > 0 && (!send_rows || !recv_rows)) return EMB_ERR_INVALID_ARG;
   return launch_status(emb::launch_exchange(send_ids, send_rows, send_offsets, P, cap_rows, D, recv_ids, recv_rows,
                                             recv_offsets, recv_total, static_cast<hipStream_t>(stream)));
 }

@@ -6,18 +6,20 @@
 // over the gradient rows.
 //
 // Kernels (one stream, no host synchronisation):
-//  1. sort_upsweep: digit histograms of every radix pass at once (the digit
-//     totals do not depend on the order of the keys), one row per histogram
-//     tile; it also clears the look-back state used by the later kernels.
-//     Tokens whose id (or owner) is out of range take no part: they are left
-//     out of the histograms and so out of the sorted sequence.
-//  2. sort_pass, once per digit of the key bits (<= 8 bits each): a stable
-//     LSD radix pass over (key, token position).  Each tile ranks its keys in
-//     LDS with wave ballots, publishes its per-digit counts and reads the
-//     counts of the tiles before it (decoupled look-back, Merrill & Garland
-//     2016), so one launch per pass suffices.  Tiles take their index from a
-//     ticket counter, so a tile only waits for tiles that are already
-//     running.  The sorted sequence holds the n_valid tokens that take part.
+//  1. sort_keys_upsweep: the sort key of every token (owner and next-batch
+//     lookups done once) and the digit histograms of every radix pass at once
+//     (the digit totals do not depend on the order of the keys); it also
+//     clears the look-back state used by the later kernels.  Tokens whose id
+//     (or owner) is out of range take no part: they are left out of the
+//     histograms and so out of the sorted sequence.
+//  2. sort_pass, once per digit of the key bits (<= 8 bits each, 9 for 17-
+//     and 18-bit keys): a stable LSD radix pass over (key, token position).
+//     Each tile ranks its keys in LDS with wave ballots, publishes its
+//     per-digit counts and reads the counts of the tiles before it (decoupled
+//     look-back, Merrill & Garland 2016), so one launch per pass suffices.
+//     Tiles take their index from a ticket counter, so a tile only waits for
+//     tiles that are already running.  The sorted sequence holds the n_valid
+//     tokens that take part.
 //  3. seg_count: the number of first tokens of an id (heads) in each run of
 //     128 sorted tokens.
 //  4. seg_reduce: each wave owns 32 consecutive sorted tokens.  It finds the
@@ -28,8 +30,10 @@
 //     inside the chunk are final; the pieces of an id that crosses chunk
 //     boundaries go to a partials buffer.
 //  5. seg_combine: adds the pieces of each crossing id in chunk order
-//     (4 waves per id, each summing a contiguous range of pieces, then the
-//     4 results in wave order); by owner, it also forms the per-owner counts.
+//     (16 waves per id, each summing a contiguous range of pieces, then the
+//     results in wave order); by owner, it also forms the per-owner counts.
+// The lookup requests of the row-wise forward exchange reuse kernels 1-3 on
+// the owner-major keys and replace 4-5 by request_kernel (no rows to sum).
 // The order of every floating-point addition depends only on the ids, never
 // on scheduling, so results are bitwise reproducible.
 #include <hip/hip_ext.h>
@@ -684,6 +688,89 @@ __global__ __launch_bounds__(kCombineThreads) void seg_combine_kernel(const floa
   }
 }
 
+// Lookup requests of the row-wise partition, from the owner-major sorted
+// tokens: one thread per sorted token.  A token heads its id when its key
+// differs from the previous one; its unique index u is the number of heads up
+// to it (earlier workgroups' counts from seg_count, then the workgroup's own)
+// minus one.  Heads write req_ids[u] and the owner-group starts; every sorted
+// token writes inverse[its position] = u.  Token t = the same thread index
+// writes inverse[t] = -1 when it takes no part (those tokens are not in the
+// sorted sequence).
+__global__ __launch_bounds__(kRedTile) void request_kernel(const uint32_t* __restrict__ skeys,
+                                                           const int32_t* __restrict__ spos,
+                                                           const uint32_t* __restrict__ n_valid, int T,
+                                                           const uint32_t* __restrict__ tile_heads, KeySpec ks,
+                                                           const int32_t* __restrict__ ids,
+                                                           int32_t* __restrict__ req_ids,
+                                                           int32_t* __restrict__ req_offsets,
+                                                           int32_t* __restrict__ num_unique,
+                                                           int32_t* __restrict__ inverse) {
+  constexpr int NW = kRedTile / kWave;
+  __shared__ uint32_t wave_heads[NW];
+  __shared__ uint32_t red[NW];
+  const int tile = blockIdx.x;
+  const int w = threadIdx.x / kWave;
+  const int lane = static_cast<int>(lane_id());
+  const int tv = static_cast<int>(min(*n_valid, static_cast<uint32_t>(T)));
+  const int e = tile * kRedTile + static_cast<int>(threadIdx.x);
+  const int ec = min(e, T - 1);
+  const uint32_t key = skeys[ec];
+  const uint32_t key_prev = skeys[max(ec - 1, 0)];
+  const int32_t pos = spos[ec];
+  const bool valid = e < tv;
+  const bool head = valid && (e == 0 || key_prev != key);
+  const uint64_t heads = __ballot(head);
+  if (lane == 0) wave_heads[w] = static_cast<uint32_t>(__popcll(heads));
+  uint32_t before = 0;
+  for (int t = static_cast<int>(threadIdx.x); t < tile; t += kRedTile) before += tile_heads[t];
+  before = wave_sum(before);
+  if (lane == 0) red[w] = before;
+  __syncthreads();
+  uint32_t ubase = 0;
+#pragma unroll
+  for (int q = 0; q < NW; ++q) ubase += red[q];
+  for (int q = 0; q < w; ++q) ubase += wave_heads[q];
+  const uint64_t upto = (lane == kWave - 1) ? ~0ull : ((2ull << lane) - 1ull);
+  const int u = static_cast<int>(ubase + __popcll(heads & upto)) - 1;
+  if (valid && u >= 0 && u < T) {
+    if (pos >= 0 && pos < T) inverse[pos] = u;
+    if (head) {
+      req_ids[u] = static_cast<int32_t>(key & ks.id_mask);
+      const int o = min(group_of(key, ks), ks.G);  // owners o_prev < p <= o start here
+      const int o_prev = e == 0 ? -1 : group_of(key_prev, ks);
+      for (int p = o_prev + 1; p <= o; ++p) req_offsets[p] = u;
+    }
+    if (e + 1 == tv) {
+      num_unique[0] = u + 1;
+      for (int p = min(group_of(key, ks), ks.G) + 1; p <= ks.G; ++p) req_offsets[p] = u + 1;
+    }
+  }
+  if (e == 0 && !valid) {  // no token takes part
+    num_unique[0] = 0;
+    for (int p = 0; p <= ks.G; ++p) req_offsets[p] = 0;
+  }
+  if (e < T) {
+    const int32_t id = ids[e];
+    bool take = id >= 0 && static_cast<uint32_t>(id) < ks.V;
+    if (take) take = static_cast<uint32_t>(ks.row_owner[id]) < static_cast<uint32_t>(ks.P);
+    if (!take) inverse[e] = -1;
+  }
+}
+
+// Per-owner request counts from the offsets (one workgroup, P <= 1024); with
+// an empty batch it writes the empty result first.
+__global__ __launch_bounds__(1024) void request_counts_kernel(int32_t* __restrict__ req_offsets,
+                                                              int32_t* __restrict__ req_counts,
+                                                              int32_t* __restrict__ num_unique, int P, int empty) {
+  for (int p = threadIdx.x; p <= P; p += blockDim.x) {
+    if (empty) {
+      req_offsets[p] = 0;
+      if (p == 0) num_unique[0] = 0;
+    }
+    if (p < P) req_counts[p] = empty ? 0 : req_offsets[p + 1] - req_offsets[p];
+  }
+}
+
 __global__ void empty_batch_kernel(int32_t* seg_offsets, int32_t* num_unique, int32_t* owner_counts,
                                    int32_t* owner_offsets, int P) {
   if (threadIdx.x == 0) {
@@ -901,6 +988,32 @@ hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D
   }
 #undef EMB_REDUCE
 #undef EMB_COMBINE
+  return hipGetLastError();
+}
+
+hipError_t launch_lookup_request(const int32_t* ids, int T, int64_t V, const int32_t* row_owner, int P,
+                                 int32_t* req_ids, int32_t* req_counts, int32_t* req_offsets, int32_t* num_unique,
+                                 int32_t* inverse, void* workspace, int32_t* status, hipStream_t stream) {
+  if (T == 0) {
+    hipLaunchKernelGGL(request_counts_kernel, dim3(1), dim3(1024), 0, stream, req_offsets, req_counts, num_unique, P,
+                       1);
+    return hipGetLastError();
+  }
+  CoalesceVariant var;
+  var.row_owner = row_owner;
+  var.P = P;
+  const hipError_t e = launch_coalesce_sort(ids, T, V, 0, var, workspace, status, stream);
+  if (e != hipSuccess) return e;
+  const CoalesceWs ws = carve(workspace, T, 0, -1, V);
+  const KeySpec ks = key_spec(V, row_owner, P, false);
+  const RadixPlan plan = plan_for_call(V, var);
+  const uint32_t* kin = nullptr;
+  const int32_t* vin = nullptr;
+  sorted_arrays(ws, plan, &kin, &vin);
+  const int nred = (T + kRedTile - 1) / kRedTile;
+  hipLaunchKernelGGL(request_kernel, dim3(nred), dim3(kRedTile), 0, stream, kin, vin, ws.n_valid, T, ws.tile_heads, ks,
+                     ids, req_ids, req_offsets, num_unique, inverse);
+  hipLaunchKernelGGL(request_counts_kernel, dim3(1), dim3(1024), 0, stream, req_offsets, req_counts, num_unique, P, 0);
   return hipGetLastError();
 }
 

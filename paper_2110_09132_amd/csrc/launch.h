@@ -40,6 +40,12 @@ hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool gra
                            const CoalesceVariant& var, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
                            int32_t* num_unique, int32_t* group_counts, int32_t* group_offsets, void* workspace,
                            int32_t* status, hipStream_t stream);
+// Lookup requests of the row-wise partition: the owner-major sort of the
+// coalesce (workspace coalesce_workspace_bytes(T, 0, -1, V)), then the
+// distinct ids per owner and every token's index into them.
+hipError_t launch_lookup_request(const int32_t* ids, int T, int64_t V, const int32_t* row_owner, int P,
+                                 int32_t* req_ids, int32_t* req_counts, int32_t* req_offsets, int32_t* num_unique,
+                                 int32_t* inverse, void* workspace, int32_t* status, hipStream_t stream);
 // Host-side argument checks of emb_grad_coalesce, emb_grad_coalesce_by_owner and
 // emb_grad_coalesce_split (EMB_OK when the call is valid).
 int coalesce_args_status(const int32_t* ids, int32_t T, const void* grad, int32_t grad_dtype, int32_t D, int64_t V,

@@ -94,6 +94,35 @@ def test_coalesce_by_owner_validation():
     assert L.emb_grad_coalesce_by_owner(*args(V=(1 << 22) + 1, P=1024, **short)) == emb.EMB_ERR_UNSUPPORTED
 
 
+def test_lookup_request_validation_and_workspace_query():
+    L = emb.lib
+    need = L.emb_lookup_request_workspace_bytes(1000, 5000)
+    assert need > 0 and need % 256 == 0
+    assert need < L.emb_grad_coalesce_workspace_bytes(1000, 5000, 64, emb.EMB_F32)  # no gradient partials
+    assert L.emb_lookup_request_workspace_bytes(-1, 5000) == 0
+    assert L.emb_lookup_request_workspace_bytes(1000, 0) == 0
+    args = lambda T=1000, V=5000, own=FAKE, P=4, ids=FAKE, req=FAKE, counts=FAKE, offs=FAKE, nu=FAKE, inv=FAKE, \
+        ws=FAKE, wsb=need: (ids, T, V, own, P, req, counts, offs, nu, inv, ws, wsb, NULL, NULL)
+    assert L.emb_lookup_request(*args(wsb=need - 1)) == emb.EMB_ERR_WORKSPACE
+    for bad in (dict(P=0), dict(P=1025), dict(V=0), dict(V=1 << 31), dict(T=-1), dict(T=1 << 30), dict(own=NULL),
+                dict(ids=NULL), dict(req=NULL), dict(counts=NULL), dict(offs=NULL), dict(nu=NULL), dict(inv=NULL),
+                dict(ws=NULL)):
+        assert L.emb_lookup_request(*args(**bad)) == emb.EMB_ERR_INVALID_ARG, bad
+    # (owner, id) keys must fit 32 bits, checked before the workspace
+    short = dict(wsb=need - 1)
+    assert L.emb_lookup_request(*args(V=1 << 22, P=1024, **short)) == emb.EMB_ERR_WORKSPACE
+    assert L.emb_lookup_request(*args(V=(1 << 22) + 1, P=1024, **short)) == emb.EMB_ERR_UNSUPPORTED
+
+
+def test_exchange_validation_ids_only():
+    L = emb.lib
+    args = lambda D=0, rows=NULL, ids=FAKE, cap=10, P=4: (ids, rows, FAKE, P, cap, D, ids, rows, FAKE, FAKE, NULL)
+    assert L.emb_exchange_simulated(*args(D=-1)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_exchange_simulated(*args(D=8)) == emb.EMB_ERR_INVALID_ARG  # rows needed when D > 0
+    assert L.emb_exchange_simulated(*args(ids=NULL)) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_exchange_simulated(*args(P=0)) == emb.EMB_ERR_INVALID_ARG
+
+
 def test_coalesce_split_validation_and_workspace_query():
     L = emb.lib
     need = L.emb_grad_coalesce_split_workspace_bytes(1000, 3000, 5000, 64, emb.EMB_F32)
