@@ -262,6 +262,57 @@ def column_partition_report(torch, emb, sp, tb, batches, U, owner_rows, reps=20)
             "payload_rowwise": balance(row_b), "payload_columnwise": balance(col_b), "kernels": kern}
 
 
+def forward_exchange_report(torch, emb, sp, tb, batches, U, reps=20):
+    """The forward pass of the two partitions (Sec. 4.1.1) for the first table, one worker's batch of
+    T tokens: row-wise, the worker asks each owner for its U distinct rows (ids out, rows back) and
+    expands them to T rows; column-wise, every owner gets the worker's T ids and returns its w(p)
+    columns of all T rows.  Bytes the worker sends plus receives (ids int32, rows fp32, its own
+    owner's share included), and the row-wise kernels timed at the table's shape over `reps`
+    back-to-back launches (outside the timed steps): the request (emb_lookup_request), the answer
+    (emb_gather of the U requested rows) and the expansion (emb_gather through the inverse map).
+    Byte models count what the call must touch: the request reads the ids and their owners and
+    writes the requests and the inverse map (the sort passes are not counted); the answer reads
+    and writes U rows; the expansion reads the inverse map and U rows and writes T rows."""
+    V, D, P, T = sp.V, sp.D, sp.P, sp.T
+    nb = len(batches)
+    req = [emb.lookup_request(ids, V, tb.row_owner, P) for ids, _ in batches]
+    torch.cuda.synchronize()
+    Us = [int(r[3].item()) for r in req]
+    assert Us == [int(u) for u in U], "the requests ask for the coalesce's distinct rows"
+    ws = emb.new_workspace(emb.lookup_request_workspace_bytes(T, V))
+    out = tuple(torch.empty_like(x) for x in req[0])
+    ans = torch.empty((T, D), dtype=torch.float32, device="cuda")
+    look = torch.empty((T, D), dtype=torch.float32, device="cuda")
+    answers = [emb.gather(tb.W, r[0][:u]) for r, u in zip(req, Us)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        for i in range(3):
+            fn(i)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(reps):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    us_req = timed(lambda i: emb.lookup_request(batches[i % nb][0], V, tb.row_owner, P, out=out, workspace=ws))
+    us_ans = timed(lambda i: emb.gather(tb.W, req[i % nb][0][:Us[i % nb]], out=ans[:Us[i % nb]]))
+    us_exp = timed(lambda i: emb.gather(answers[i % nb], req[i % nb][4], out=look))
+    Um = float(np.mean(Us))
+    kern = {}
+    for name, us, nbytes in (("lookup_request", us_req, T * 4 * 3 + Um * 4),
+                             ("answer_gather", us_ans, 2 * Um * D * 4 + Um * 4),
+                             ("expand_gather", us_exp, T * 4 + Um * D * 4 + T * D * 4)):
+        kern[name] = {"avg_launch_us": us, "bytes_model": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9,
+                      "frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS}
+    return {"table": 0, "T": T, "distinct_rows": Um,
+            "rowwise_MB": {"requests": Um * 4 / 1e6, "answers": Um * D * 4 / 1e6},
+            "columnwise_MB": {"ids_to_owners": P * T * 4 / 1e6, "lookup_results": T * D * 4 / 1e6},
+            "kernels": kern}
+
+
 def cost_model_report(emb, sp, U, N=8):
     """Table 2 (Sec. 4.1.2) fed with the measured density alpha = U / V of the first table's batches,
     for N workers of one node with B = one xGMI link; the bandwidth terms (beta = 0) in microseconds
@@ -488,6 +539,8 @@ def main():
     column = column_partition_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches],
                                      [U[b][0] for b in range(args.batches)], owner_rows)
     cost = cost_model_report(emb, wl.tables[0], [U[b][0] for b in range(args.batches)])
+    forward = forward_exchange_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches],
+                                      [U[b][0] for b in range(args.batches)])
 
     # algorithmic bytes of the timed steps
     bytes_step = {k: 0.0 for k in ("gather", "coalesce", "pack", "adam")}
@@ -573,6 +626,7 @@ def main():
         "copy_GBps": copy_gbps,
         "gradient_sizes_table3": table3,
         "column_partition": column,
+        "forward_exchange": forward,
         "comm_cost_model": cost,
         "step_frac_of_copy": step_gbps / copy_gbps,
         "host": host_info(),
