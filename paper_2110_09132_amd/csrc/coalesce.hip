@@ -22,7 +22,9 @@
 //     tokens that take part.
 //  3. seg_count: the number of first tokens of an id (heads) in each run of
 //     128 sorted tokens.
-//  4. seg_reduce: each wave owns 32 consecutive sorted tokens.  It finds the
+//  4. seg_reduce: each wave owns 32 consecutive sorted tokens (for batches of
+//     few tokens with wide rows, several workgroups share them, each summing
+//     a slice of the columns).  It finds the
 //     heads with lane shuffles, adds up the head counts of the earlier
 //     workgroups, writes uniq_ids / seg_offsets / num_unique (and, by owner,
 //     where each owner's rows start), and sums the
@@ -506,6 +508,12 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const int lane = static_cast<int>(lane_id());
   const int chunk = tile * kWaves + w;
   const int a = chunk * kChunk;
+  // column blocks of kWave vectors: this workgroup sums blocks cb0, cb0 + cstep, ...
+  // (several workgroups share a chunk's columns when the batch has few chunks
+  // and wide rows); the segment bookkeeping is written by the cb0 == 0 one
+  const int cb0 = static_cast<int>(blockIdx.y) * kWave;
+  const int cstep = static_cast<int>(gridDim.y) * kWave;
+  const bool meta = blockIdx.y == 0;
 
   // lane L holds sorted element e = a - 1 + L, for L = 0 .. kChunk + 1
   // (workspace values are clamped so that no index can leave its array)
@@ -540,7 +548,8 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   Acc g[kChunk];
 #pragma unroll
   for (int k = 0; k < kChunk; ++k)
-    g[k] = Row::load(grad, static_cast<size_t>(__builtin_amdgcn_readlane(pos, min(k, last) + 1)), Dv, min(lane, Dv - 1));
+    g[k] = Row::load(grad, static_cast<size_t>(__builtin_amdgcn_readlane(pos, min(k, last) + 1)), Dv,
+                     min(cb0 + lane, Dv - 1));
   // heads before this workgroup: the sum of the earlier workgroups' counts
   uint32_t before = 0;
 #pragma unroll
@@ -562,7 +571,7 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const uint64_t upto = (lane == kWave - 1) ? ~0ull : ((2ull << lane) - 1ull);
   const int u = static_cast<int>(ubase + __popcll(heads & upto)) - 1;  // unique index of element e
   const bool u_ok = u >= 0 && u < T;
-  if (head && u_ok) {
+  if (meta && head && u_ok) {
     uniq_ids[u] = static_cast<int32_t>(key & ks.id_mask);
     seg_offsets[u] = e;
     if (owner_offsets != nullptr) {  // groups o' < p <= o start at this row
@@ -572,13 +581,13 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     }
   }
   const bool next_valid = __shfl_down(valid ? 1 : 0, 1, kWave) != 0;
-  if (in_chunk && valid && u_ok && (e + 1 == T || !next_valid)) {
+  if (meta && in_chunk && valid && u_ok && (e + 1 == T || !next_valid)) {
     seg_offsets[u + 1] = e + 1;  // the last valid token of the whole batch
     num_unique[0] = u + 1;
     if (owner_offsets != nullptr)
       for (int p = min(group_of(key, ks), ks.G) + 1; p <= ks.G; ++p) owner_offsets[p] = u + 1;
   }
-  if (chunk == 0 && lane == 1 && !valid) {  // no valid token at all
+  if (meta && chunk == 0 && lane == 1 && !valid) {  // no valid token at all
     seg_offsets[0] = 0;
     num_unique[0] = 0;
     if (owner_offsets != nullptr)
@@ -589,11 +598,11 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   // sum the rows of the chunk's tokens in sorted order, one run of equal ids at a time
   Acc* out_rows = reinterpret_cast<Acc*>(uniq_grad);
   Acc* part_rows = reinterpret_cast<Acc*>(partial);
-  for (int cb = 0; cb < Dv; cb += kWave) {
+  for (int cb = cb0; cb < Dv; cb += cstep) {
     const int c = cb + lane;
     const bool colok = c < Dv;
     const int cc = min(c, Dv - 1);
-    if (cb > 0) {  // the next column block of the same rows
+    if (cb > cb0) {  // the next column block of the same rows
 #pragma unroll
       for (int k = 0; k < kChunk; ++k)
         g[k] = Row::load(grad, static_cast<size_t>(__builtin_amdgcn_readlane(pos, min(k, last) + 1)), Dv, cc);
@@ -887,6 +896,16 @@ void launch_sort(const int32_t* ids, int T, const KeySpec& ks, const RadixPlan& 
   *spos = vin;
 }
 
+// Workgroups per chunk group of the reduction: batches with few chunks and wide
+// rows split the columns over several workgroups (one or more blocks of kWave
+// vectors each), so that the launch holds about kReduceTargetGroups groups.
+constexpr int kReduceTargetGroups = 1024;
+int reduce_col_split(int nred, int Dv) {
+  const int nblocks = (Dv + kWave - 1) / kWave;
+  const int want = (kReduceTargetGroups + nred - 1) / nred;
+  return max(1, min(nblocks, want));
+}
+
 bool is_split(const CoalesceVariant& var) { return var.row_owner != nullptr && var.T_next >= 0; }
 
 RadixPlan plan_for_call(int64_t V, const CoalesceVariant& var) {
@@ -965,7 +984,8 @@ hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D
                     (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
   const dim3 cgrid(grid_for(nchunks, 256));
 #define EMB_REDUCE(BF, VC)                                                                                          \
-  hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred), dim3(kThreads), 0, stream, kin, vin, ws.n_valid, T, \
+  hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred, reduce_col_split(nred, D / (VC))), dim3(kThreads), 0,   \
+                     stream, kin, vin, ws.n_valid, T,                                                                \
                      grad, D, ws.tile_heads, ks, uniq_ids, seg_offsets, num_unique, uniq_grad, group_offsets,        \
                      ws.partial, ws.span_list, ws.span_count, nchunks)
 #define EMB_COMBINE(VC)                                                                                             \
