@@ -650,7 +650,7 @@ __global__ __launch_bounds__(kCombineThreads) void seg_combine_kernel(const floa
                                                                int nchunks) {
   using Acc = typename GradRow<false, VEC>::Acc;
   __shared__ Acc red[kCombineWaves][kWave];
-  if (owner_counts != nullptr && blockIdx.x == 0)
+  if (owner_counts != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
     for (int p = threadIdx.x; p < P; p += kCombineThreads) owner_counts[p] = owner_offsets[p + 1] - owner_offsets[p];
   const int n = min(span_count[0], nchunks);
   const int Dv = D / VEC;
@@ -667,7 +667,8 @@ __global__ __launch_bounds__(kCombineThreads) void seg_combine_kernel(const floa
     const int first_slot = (S == c0 * kChunk) ? 0 : 1;
     const int p_beg = static_cast<int>((static_cast<long long>(w) * np) / kCombineWaves);
     const int p_end = static_cast<int>((static_cast<long long>(w + 1) * np) / kCombineWaves);
-    for (int cb = 0; cb < Dv; cb += kWave) {
+    // column blocks of kWave vectors, split over gridDim.y workgroups as in seg_reduce
+    for (int cb = static_cast<int>(blockIdx.y) * kWave; cb < Dv; cb += static_cast<int>(gridDim.y) * kWave) {
       const int c = cb + static_cast<int>(lane_id());
       const bool colok = c < Dv;
       const int cc = min(c, Dv - 1);
@@ -982,7 +983,7 @@ hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D
   // 5. segments and per-chunk sums; 6. pieces of ids that cross chunks
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(grad) % (grad_bf16 ? 8 : 16) == 0) &&
                     (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
-  const dim3 cgrid(grid_for(nchunks, 256));
+  const dim3 cgrid(grid_for(nchunks, 256), grid_for((D / (vec4 ? 4 : 1) + kWave - 1) / kWave, 8));
 #define EMB_REDUCE(BF, VC)                                                                                          \
   hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred, reduce_col_split(nred, D / (VC))), dim3(kThreads), 0,   \
                      stream, kin, vin, ws.n_valid, T,                                                                \
