@@ -38,10 +38,11 @@ __device__ __forceinline__ void adam_vec(const float& g, float& w, float& m, flo
   adam_elem(g, w, m, v, c);
 }
 
-// Each wave owns a contiguous range of the listed rows.  The row ids of 64
-// rows come in one coalesced load and reach their lanes by shuffle; rows are
-// processed in groups of kRowsInFlight steps, and the loads (g, w, m, v) of the
-// next group are issued before the current group is computed and stored.
+// Each wave owns a contiguous range of the listed rows (or, for few wide rows,
+// every cs-th column step of one).  The row ids of 64 rows come in one
+// coalesced load and reach their lanes by shuffle; rows are processed in
+// groups of kRowsInFlight steps, and the loads (g, w, m, v) of the next group
+// are issued before the current group is computed and stored.
 template <typename VecT>
 __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, VecT* __restrict__ M,
                                                         VecT* __restrict__ S, int64_t V, int Dv, int log2L,
@@ -57,9 +58,21 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
   const int lane = static_cast<int>(lane_id());
   const int sub = lane >> log2L;
   const int cl = lane & (L - 1);
-  const int wave = uniform(static_cast<int>(blockIdx.x) * (kThreads / kWave) + static_cast<int>(threadIdx.x / kWave));
-  const int nwaves = static_cast<int>(gridDim.x) * (kThreads / kWave);
   const int step_rows = rpw * kRowsInFlight;
+  // With few rows (a batch with many repeats) and wide rows, cs waves share a
+  // row range, each taking every cs-th column step, so that about every wave
+  // of the launch has work.
+  const int all_waves = static_cast<int>(gridDim.x) * (kThreads / kWave);
+  const int ncols = (Dv + L - 1) / L;
+  const int wave_all = uniform(static_cast<int>(blockIdx.x) * (kThreads / kWave) + static_cast<int>(threadIdx.x / kWave));
+  int cs = 1, wave = wave_all, part = 0, nwaves = all_waves;
+  if (ncols > 1) {
+    const float want = static_cast<float>(all_waves) * step_rows / static_cast<float>(max(hi - lo, 1));
+    cs = uniform(static_cast<int>(fminf(fmaxf(want, 1.0f), static_cast<float>(ncols))));
+    wave = wave_all / cs;  // row range (waves past the last range find it empty)
+    part = wave_all - wave * cs;
+    nwaves = all_waves / cs;
+  }
   int per = (hi - lo + nwaves - 1) / nwaves;
   per = (per + step_rows - 1) / step_rows * step_rows;
   const long long r0 = lo + static_cast<long long>(wave) * per;
@@ -70,7 +83,7 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
     const int32_t ridreg = row_ids[min(c0 + lane, static_cast<long long>(hi) - 1)];
     bad |= lane < n && (ridreg < 0 || ridreg >= V);
     const int ngroups = (n + step_rows - 1) / step_rows;
-    for (int cb = 0; cb < Dv; cb += L) {  // uniform column steps (the shuffles need every lane)
+    for (int cb = part * L; cb < Dv; cb += cs * L) {  // uniform column steps (the shuffles need every lane)
       const int col = min(cb + cl, Dv - 1);
       const bool cok = cb + cl < Dv;
       // two register buffers used in turn; every index below is a compile-time constant
