@@ -68,7 +68,8 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
   int cs = 1, wave = wave_all, part = 0, nwaves = all_waves;
   if (ncols > 1) {
     const float want = static_cast<float>(all_waves) * step_rows / static_cast<float>(max(hi - lo, 1));
-    cs = uniform(static_cast<int>(fminf(fmaxf(want, 1.0f), static_cast<float>(ncols))));
+    // at most all_waves, so that at least one wave takes each row range
+    cs = uniform(static_cast<int>(fminf(fmaxf(want, 1.0f), static_cast<float>(min(ncols, all_waves)))));
     wave = wave_all / cs;  // row range (waves past the last range find it empty)
     part = wave_all - wave * cs;
     nwaves = all_waves / cs;

@@ -207,6 +207,22 @@ def test_adam_parity_multi_step_by_shard(D):
             check_adam(state, pk["dev"], P, s, s + 1, HP, step)
 
 
+@pytest.mark.parametrize("cap,n,D", [(1, 1, 4096), (3, 3, 4096), (2, 2, 8192), (5, 3, 9001), (7, 5, 2048),
+                                     (4, 4, 16384), (16384, 4522, 1024), (300, 1, 4096), (50, 49, 1)])
+def test_adam_few_wide_rows(cap, n, D):
+    """Row capacities of a few rows with rows of many column steps (waves share a row's columns,
+    never more sharing waves than the launch has), and the 4.5k rows of 4 KB of the translation
+    workload."""
+    print(f"adam few wide rows cap={cap} n={n} D={D}", flush=True)
+    V = max(64, 2 * cap)
+    W0 = gen.normal_f32(gen.stream_key(D, cap, gen.PURPOSE_WEIGHTS), V * D).reshape(V, D)
+    state = [to_dev(W0), torch.zeros((V, D), device="cuda"), torch.zeros((V, D), device="cuda")]
+    ids = np.sort(np.random.default_rng(cap + D).choice(V, cap, replace=False)).astype(np.int32)
+    for step in (1, 2):
+        pack = (to_dev(ids), to_dev(grads_for(700 + step, cap, D)), None, to_dev(np.array([0, n], np.int32)))
+        check_adam(state, pack, 1, 0, 1, HP, step)
+
+
 def test_adam_out_of_range_row_is_skipped_and_flagged():
     V, D = 100, 4
     W = to_dev(np.ones((V, D), np.float32))
