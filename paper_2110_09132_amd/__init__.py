@@ -139,6 +139,31 @@ def _need(t, dtype, what):
         raise EmbError(f"{what} must be a contiguous {dtype} CUDA tensor (got {t.dtype}, {t.device})")
 
 
+def _out(t, dtype, n, what):
+    """An output (or input) buffer the call reads or writes n elements of."""
+    _need(t, dtype, what)
+    if t.numel() < n:
+        raise EmbError(f"{what} holds {t.numel()} elements; the call uses {n}")
+
+
+def _rows(t, n, D, what):
+    """A row buffer of at least n rows of width D (2-D [>= n, D], or flat with >= n * D elements)."""
+    if t.dim() == 2 and t.shape[1] != D:
+        raise EmbError(f"{what} has rows of {t.shape[1]} elements; the call uses {D}")
+    if t.numel() < n * D:
+        raise EmbError(f"{what} holds {t.numel()} elements; the call uses {n} rows of {D}")
+
+
+def _grad(grad, T, what="grad"):
+    """The per-token gradient [T, D] (fp32 or bf16); returns (dtype code, D)."""
+    code = _dtype_code(grad)
+    if not grad.is_cuda or not grad.is_contiguous() or grad.dim() != 2:
+        raise EmbError(f"{what} must be a contiguous 2-D CUDA tensor")
+    if grad.shape[0] != T:
+        raise EmbError(f"{what} has {grad.shape[0]} rows for {T} tokens")
+    return code, grad.shape[1]
+
+
 class Event:
     """A HIP event made by the library (emb_event_create); destroyed with the object."""
 
@@ -184,10 +209,14 @@ def gather(table, ids, out=None, dev_status=None, stream=None):
     """out[t] = table[ids[t]] (emb_gather)."""
     _need(table, torch.float32, "table")
     _need(ids, torch.int32, "ids")
+    if table.dim() != 2:
+        raise EmbError("table must be 2-D [V, D]")
     V, D = table.shape
     T = ids.numel()
     if out is None:
         out = torch.empty((T, D), dtype=torch.float32, device=table.device)
+    _out(out, torch.float32, 0, "out")
+    _rows(out, T, D, "out")
     _check(lib.emb_gather(_ptr(table), V, D, _ptr(ids), T, _ptr(out), _ptr(dev_status), _stream(stream)),
            "emb_gather")
     return out
@@ -201,6 +230,22 @@ def new_workspace(nbytes, device=None):
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device or "cuda")
 
 
+def _coalesce_outs(uniq_ids, seg_offsets, uniq_grad, num_unique, T, D):
+    _out(uniq_ids, torch.int32, T, "uniq_ids")
+    _out(seg_offsets, torch.int32, T + 1, "seg_offsets")
+    _out(uniq_grad, torch.float32, 0, "uniq_grad")
+    _rows(uniq_grad, T, D, "uniq_grad")
+    _out(num_unique, torch.int32, 1, "num_unique")
+
+
+def _owners(row_owner, V, P):
+    _need(row_owner, torch.int32, "row_owner")
+    if row_owner.numel() < V:
+        raise EmbError(f"row_owner holds {row_owner.numel()} owners for V = {V} rows")
+    if not 1 <= P <= 1024:
+        raise EmbError(f"P = {P} is outside [1, 1024]")
+
+
 def grad_coalesce(ids, grad, V, out=None, workspace=None, dev_status=None, stream=None):
     """COALESCE + UNIQUE (emb_grad_coalesce).
 
@@ -208,16 +253,14 @@ def grad_coalesce(ids, grad, V, out=None, workspace=None, dev_status=None, strea
     first num_unique entries are meaningful.  `out` may pass those four tensors in.
     """
     _need(ids, torch.int32, "ids")
-    code = _dtype_code(grad)
-    if not grad.is_cuda or not grad.is_contiguous():
-        raise EmbError("grad must be a contiguous CUDA tensor")
     T = ids.numel()
-    D = grad.shape[1]
+    code, D = _grad(grad, T)
     dev = ids.device
     if out is None:
         out = (torch.empty(T, dtype=torch.int32, device=dev), torch.empty(T + 1, dtype=torch.int32, device=dev),
                torch.empty((T, D), dtype=torch.float32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
     uniq_ids, seg_offsets, uniq_grad, num_unique = out
+    _coalesce_outs(uniq_ids, seg_offsets, uniq_grad, num_unique, T, D)
     nbytes = grad_coalesce_workspace_bytes(T, V, D, code)
     if workspace is None:
         workspace = new_workspace(nbytes, dev)
@@ -234,18 +277,18 @@ def grad_coalesce_by_owner(ids, grad, V, row_owner, P, out=None, workspace=None,
     num_unique [1]); `out` may pass those six tensors in.
     """
     _need(ids, torch.int32, "ids")
-    _need(row_owner, torch.int32, "row_owner")
-    code = _dtype_code(grad)
-    if not grad.is_cuda or not grad.is_contiguous():
-        raise EmbError("grad must be a contiguous CUDA tensor")
+    _owners(row_owner, V, P)
     T = ids.numel()
-    D = grad.shape[1]
+    code, D = _grad(grad, T)
     dev = ids.device
     if out is None:
         out = (torch.empty(T, dtype=torch.int32, device=dev), torch.empty(T + 1, dtype=torch.int32, device=dev),
                torch.empty((T, D), dtype=torch.float32, device=dev), torch.empty(P, dtype=torch.int32, device=dev),
                torch.empty(P + 1, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
     send_ids, seg_offsets, send_rows, send_counts, send_offsets, num_unique = out
+    _coalesce_outs(send_ids, seg_offsets, send_rows, num_unique, T, D)
+    _out(send_counts, torch.int32, P, "send_counts")
+    _out(send_offsets, torch.int32, P + 1, "send_offsets")
     if workspace is None:
         workspace = new_workspace(grad_coalesce_workspace_bytes(T, V, D, code), dev)
     _check(lib.emb_grad_coalesce_by_owner(_ptr(ids), T, _ptr(grad), code, D, V, _ptr(row_owner), P, _ptr(send_ids),
@@ -268,12 +311,9 @@ def grad_coalesce_split(ids, next_ids, grad, V, row_owner, P, out=None, workspac
     """
     _need(ids, torch.int32, "ids")
     _need(next_ids, torch.int32, "next_ids")
-    _need(row_owner, torch.int32, "row_owner")
-    code = _dtype_code(grad)
-    if not grad.is_cuda or not grad.is_contiguous():
-        raise EmbError("grad must be a contiguous CUDA tensor")
+    _owners(row_owner, V, P)
     T, T_next = ids.numel(), next_ids.numel()
-    D = grad.shape[1]
+    code, D = _grad(grad, T)
     dev = ids.device
     if out is None:
         out = (torch.empty(T, dtype=torch.int32, device=dev), torch.empty(T + 1, dtype=torch.int32, device=dev),
@@ -281,6 +321,9 @@ def grad_coalesce_split(ids, next_ids, grad, V, row_owner, P, out=None, workspac
                torch.empty(2 * P, dtype=torch.int32, device=dev),
                torch.empty(2 * P + 1, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
     send_ids, seg_offsets, send_rows, send_counts, send_offsets, num_unique = out
+    _coalesce_outs(send_ids, seg_offsets, send_rows, num_unique, T, D)
+    _out(send_counts, torch.int32, 2 * P, "send_counts")
+    _out(send_offsets, torch.int32, 2 * P + 1, "send_offsets")
     if workspace is None:
         workspace = new_workspace(grad_coalesce_split_workspace_bytes(T, T_next, V, D, code), dev)
     _check(lib.emb_grad_coalesce_split(_ptr(ids), T, _ptr(next_ids), T_next, _ptr(grad), code, D, V,
@@ -301,7 +344,7 @@ def lookup_request(ids, V, row_owner, P, out=None, workspace=None, dev_status=No
     Returns (req_ids [T], req_counts [P], req_offsets [P+1], num_unique [1], inverse [T]); `out`
     may pass those five tensors in."""
     _need(ids, torch.int32, "ids")
-    _need(row_owner, torch.int32, "row_owner")
+    _owners(row_owner, V, P)
     T = ids.numel()
     dev = ids.device
     if out is None:
@@ -309,6 +352,9 @@ def lookup_request(ids, V, row_owner, P, out=None, workspace=None, dev_status=No
                torch.empty(P + 1, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev),
                torch.empty(T, dtype=torch.int32, device=dev))
     req_ids, counts, offsets, nu, inverse = out
+    for t, n, what in ((req_ids, T, "req_ids"), (counts, P, "req_counts"), (offsets, P + 1, "req_offsets"),
+                       (nu, 1, "num_unique"), (inverse, T, "inverse")):
+        _out(t, torch.int32, n, what)
     if workspace is None:
         workspace = new_workspace(lookup_request_workspace_bytes(T, V), dev)
     _check(lib.emb_lookup_request(_ptr(ids), T, V, _ptr(row_owner), P, _ptr(req_ids), _ptr(counts), _ptr(offsets),
@@ -326,14 +372,25 @@ def exchange_simulated(send_ids, send_rows, send_offsets, out=None, stream=None)
     if send_rows is not None:
         _need(send_rows, torch.float32, "send_rows")
     _need(send_offsets, torch.int32, "send_offsets")
+    if send_ids.dim() != 2:
+        raise EmbError("send_ids must be 2-D [P, cap]")
     P, cap = send_ids.shape
     D = send_rows.shape[-1] if send_rows is not None else 0
+    if send_rows is not None:
+        _rows(send_rows, P * cap, D, "send_rows")
+    _out(send_offsets, torch.int32, P * (P + 1), "send_offsets")
     dev = send_ids.device
     if out is None:
         out = (torch.empty(P * cap, dtype=torch.int32, device=dev),
                torch.empty((P * cap, D), dtype=torch.float32, device=dev) if D else None,
                torch.empty((P, P + 1), dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
     recv_ids, recv_rows, recv_offsets, recv_total = out
+    _out(recv_ids, torch.int32, P * cap, "recv_ids")
+    if D:
+        _out(recv_rows, torch.float32, 0, "recv_rows")
+        _rows(recv_rows, P * cap, D, "recv_rows")
+    _out(recv_offsets, torch.int32, P * (P + 1), "recv_offsets")
+    _out(recv_total, torch.int32, 1, "recv_total")
     _check(lib.emb_exchange_simulated(_ptr(send_ids), _ptr(send_rows), _ptr(send_offsets), P, cap, D, _ptr(recv_ids),
                                       _ptr(recv_rows), _ptr(recv_offsets), _ptr(recv_total), _stream(stream)),
            "emb_exchange_simulated")
@@ -348,15 +405,21 @@ def receive_merge(recv_ids, recv_rows, recv_total, V, row_owner, P, out=None, wo
     _need(recv_ids, torch.int32, "recv_ids")
     _need(recv_rows, torch.float32, "recv_rows")
     _need(recv_total, torch.int32, "recv_total")
-    _need(row_owner, torch.int32, "row_owner")
+    _owners(row_owner, V, P)
     cap = recv_ids.numel()
+    if recv_rows.dim() != 2:
+        raise EmbError("recv_rows must be 2-D [cap, D]")
     D = recv_rows.shape[1]
+    _rows(recv_rows, cap, D, "recv_rows")
     dev = recv_ids.device
     if out is None:
         out = (torch.empty(cap, dtype=torch.int32, device=dev), torch.empty(cap + 1, dtype=torch.int32, device=dev),
                torch.empty((cap, D), dtype=torch.float32, device=dev), torch.empty(P, dtype=torch.int32, device=dev),
                torch.empty(P + 1, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
     merged_ids, seg, rows, counts, offs, nu = out
+    _coalesce_outs(merged_ids, seg, rows, nu, cap, D)
+    _out(counts, torch.int32, P, "merged_counts")
+    _out(offs, torch.int32, P + 1, "merged_offsets")
     if workspace is None:
         workspace = new_workspace(grad_coalesce_workspace_bytes(cap, V, D, EMB_F32), dev)
     _check(lib.emb_receive_merge(_ptr(recv_ids), _ptr(recv_rows), _ptr(recv_total), cap, D, V, _ptr(row_owner), P,
@@ -381,13 +444,22 @@ def pack_by_owner(uniq_ids, uniq_grad, num_unique, row_owner, P, out=None, works
     _need(num_unique, torch.int32, "num_unique")
     _need(row_owner, torch.int32, "row_owner")
     cap = uniq_ids.numel()
+    if uniq_grad.dim() != 2:
+        raise EmbError("uniq_grad must be 2-D [cap, D]")
     D = uniq_grad.shape[1]
+    _rows(uniq_grad, cap, D, "uniq_grad")
+    _out(num_unique, torch.int32, 1, "num_unique")
     V = row_owner.numel()
     dev = uniq_ids.device
     if out is None:
         out = (torch.empty(cap, dtype=torch.int32, device=dev), torch.empty((cap, D), dtype=torch.float32, device=dev),
                torch.empty(P, dtype=torch.int32, device=dev), torch.empty(P + 1, dtype=torch.int32, device=dev))
     send_ids, send_rows, send_counts, send_offsets = out
+    _out(send_ids, torch.int32, cap, "send_ids")
+    _out(send_rows, torch.float32, 0, "send_rows")
+    _rows(send_rows, cap, D, "send_rows")
+    _out(send_counts, torch.int32, P, "send_counts")
+    _out(send_offsets, torch.int32, P + 1, "send_offsets")
     if workspace is None:
         workspace = new_workspace(pack_by_owner_workspace_bytes(cap, P), dev)
     _check(lib.emb_pack_by_owner(_ptr(uniq_ids), _ptr(uniq_grad), _ptr(num_unique), cap, D, _ptr(row_owner), V, P,
@@ -415,12 +487,17 @@ def pack_by_column(rows, P, num_rows=None, out=None, stream=None):
     Returns (blocks [cap * D] flat, send_counts [P])."""
     _need(rows, torch.float32, "rows")
     if num_rows is not None:
-        _need(num_rows, torch.int32, "num_rows")
+        _out(num_rows, torch.int32, 1, "num_rows")
+    if rows.dim() != 2:
+        raise EmbError("rows must be 2-D [cap, D]")
     cap, D = rows.shape
     dev = rows.device
     if out is None:
         out = (torch.empty(cap * D, dtype=torch.float32, device=dev), torch.empty(P, dtype=torch.int32, device=dev))
     blocks, counts = out
+    _out(blocks, torch.float32, cap * D, "blocks")
+    if counts is not None:
+        _out(counts, torch.int32, P, "send_counts")
     _check(lib.emb_pack_by_column(_ptr(rows), _ptr(num_rows), cap, D, P, _ptr(blocks), _ptr(counts), _stream(stream)),
            "emb_pack_by_column")
     return out
@@ -432,9 +509,11 @@ def gather_by_column(shards, V, D, P, ids, out=None, dev_status=None, stream=Non
     shards: flat column-block layout of capacity V.  Returns blocks [T * D] flat (capacity T)."""
     _need(shards, torch.float32, "shards")
     _need(ids, torch.int32, "ids")
+    _out(shards, torch.float32, V * D, "shards")
     T = ids.numel()
     if out is None:
         out = torch.empty(T * D, dtype=torch.float32, device=ids.device)
+    _out(out, torch.float32, T * D, "out")
     _check(lib.emb_gather_by_column(_ptr(shards), V, D, P, _ptr(ids), T, _ptr(out), _ptr(dev_status),
                                     _stream(stream)), "emb_gather_by_column")
     return out
@@ -443,9 +522,12 @@ def gather_by_column(shards, V, D, P, ids, out=None, dev_status=None, stream=Non
 def assemble_by_column(blocks, C, D, P, row0=0, R=None, out=None, stream=None):
     """Rows [row0, row0 + R) of a column-block layout of capacity C, joined (emb_assemble_by_column)."""
     _need(blocks, torch.float32, "blocks")
+    _out(blocks, torch.float32, C * D, "blocks")
     R = C - row0 if R is None else R
     if out is None:
         out = torch.empty((R, D), dtype=torch.float32, device=blocks.device)
+    _out(out, torch.float32, 0, "out")
+    _rows(out, max(R, 0), D, "out")
     _check(lib.emb_assemble_by_column(_ptr(blocks), C, row0, R, D, P, _ptr(out), _stream(stream)),
            "emb_assemble_by_column")
     return out
@@ -466,7 +548,14 @@ def sparse_adam_apply(table, exp_avg, exp_avg_sq, row_ids, rows, offsets, P, sha
         _need(t, torch.float32, n)
     _need(row_ids, torch.int32, "row_ids")
     _need(offsets, torch.int32, "offsets")
+    if table.dim() != 2:
+        raise EmbError("table must be 2-D [V, D]")
     V, D = table.shape
+    for t, n in ((exp_avg, "exp_avg"), (exp_avg_sq, "exp_avg_sq")):
+        if t.shape != table.shape:
+            raise EmbError(f"{n} has shape {tuple(t.shape)}, the table {tuple(table.shape)}")
+    _rows(rows, row_ids.numel(), D, "rows")
+    _out(offsets, torch.int32, max(P, 0) + 1, "offsets")
     _check(lib.emb_sparse_adam_apply(_ptr(table), _ptr(exp_avg), _ptr(exp_avg_sq), V, D, _ptr(row_ids), _ptr(rows),
                                      _ptr(offsets), P, shard_begin, shard_end, row_ids.numel(), float(lr),
                                      float(beta1), float(beta2), float(eps), int(step), _ptr(dev_status),

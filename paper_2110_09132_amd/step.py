@@ -25,8 +25,8 @@ import ctypes
 
 import torch
 
-from . import (EMB_BF16, EMB_F32, Event, StepArgs, StepSchedule, StepSignals, _check,
-               grad_coalesce_split_workspace_bytes, lib, new_workspace, pack_by_owner_workspace_bytes)
+from . import (EMB_BF16, EMB_F32, EmbError, Event, StepArgs, StepSchedule, StepSignals, _check, _grad, _need,
+               _owners, grad_coalesce_split_workspace_bytes, lib, new_workspace, pack_by_owner_workspace_bytes)
 
 # timing pairs of emb_step_schedule.timing; with the split, "pack" times the
 # prior update and "adam" the delayed one
@@ -38,6 +38,10 @@ class EmbeddingTable:
 
     def __init__(self, W: torch.Tensor, row_owner: torch.Tensor, P: int, T_cap: int,
                  grad_dtype: torch.dtype = torch.float32, sets: int = 2):
+        _need(W, torch.float32, "W")
+        if W.dim() != 2:
+            raise EmbError("W must be 2-D [V, D]")
+        _owners(row_owner, W.shape[0], P)
         dev = W.device
         self.V, self.D = W.shape
         self.P, self.T_cap = P, T_cap
@@ -166,6 +170,20 @@ class StepPipeline:
                 side.wait_stream(self.main)
         if self.split and (next_ids is None or len(next_ids) != len(batches)):
             raise ValueError("the split schedule needs the next step's ids of every table")
+        if len(batches) != len(self.tables):
+            raise EmbError(f"{len(batches)} batches for {len(self.tables)} tables")
+        for k, (ids, grad) in enumerate(batches):  # the kernels trust these sizes: check them first
+            tb = self.tables[k]
+            _need(ids, torch.int32, "ids")
+            if ids.numel() > tb.T_cap:
+                raise EmbError(f"{ids.numel()} tokens exceed the table's capacity of {tb.T_cap}")
+            _, D = _grad(grad, ids.numel())
+            if D != tb.D:
+                raise EmbError(f"grad rows of {D} elements for a table of D = {tb.D}")
+            if self.split:
+                _need(next_ids[k], torch.int32, "next_ids")
+                if next_ids[k].numel() > tb.T_cap:
+                    raise EmbError(f"{next_ids[k].numel()} next ids exceed the table's capacity of {tb.T_cap}")
         for k, (ids, grad) in enumerate(batches):
             a, s = self.args[k][i], self.sched[k][i]
             a.ids = ids.data_ptr()

@@ -5,6 +5,8 @@ two tokens bit-exact, token counts per row equal to the oracle's segment
 lengths.  Sizes span several sort tiles and reduction chunks with ragged
 tails; owner maps by id mod P, by range and at random; bad ids and owners;
 empty and degenerate batches; the key-width limit."""
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -170,8 +172,18 @@ def test_by_owner_key_width_limit_is_unsupported():
     V, P, T, D = (1 << 31) - 1, 4, 16, 4
     ids = to_dev(np.arange(T, dtype=np.int32))
     own = torch.zeros(1, dtype=torch.int32, device="cuda")  # never read: the host check fails first
-    with pytest.raises(emb.EmbError, match="unsupported"):
-        emb.grad_coalesce_by_owner(ids, to_dev(grads_for(1, T, D)), V, own, P)
+    g = to_dev(grads_for(1, T, D))
+    outs = [torch.zeros(T + 1, dtype=torch.int32, device="cuda") for _ in range(5)]
+    out_rows = torch.zeros((T, D), dtype=torch.float32, device="cuda")
+    ws = emb.new_workspace(1 << 20)
+    p = lambda t: ctypes.c_void_p(t.data_ptr())
+    code = emb.lib.emb_grad_coalesce_by_owner(p(ids), T, p(g), emb.EMB_F32, D, V, p(own), P, p(outs[0]), p(outs[1]),
+                                              p(out_rows), p(outs[2]), p(outs[3]), p(outs[4]), p(ws), ws.numel(),
+                                              None, None)
+    assert code == emb.EMB_ERR_UNSUPPORTED
+    # the binding refuses the owner map, one owner for 2^31 - 1 rows, before that
+    with pytest.raises(emb.EmbError, match="row_owner"):
+        emb.grad_coalesce_by_owner(ids, g, V, own, P)
 
 
 # ------------------------------------------------------ vertical split (Algorithm 1)
@@ -272,7 +284,7 @@ def test_split_key_width_limit_is_unsupported():
     # bits(V) + bits(P) + 1 = 22 + 10 + 1 > 32: refused on the host
     V, P, T, D = (1 << 22) - 1, 1024, 16, 4
     ids = to_dev(np.arange(T, dtype=np.int32))
-    own = torch.zeros(1, dtype=torch.int32, device="cuda")  # never read
+    own = torch.zeros(V, dtype=torch.int32, device="cuda")  # never read: the host check fails first
     with pytest.raises(emb.EmbError, match="unsupported"):
         emb.grad_coalesce_split(ids, ids, to_dev(grads_for(1, T, D)), V, own, P)
 
