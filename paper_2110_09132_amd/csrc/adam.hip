@@ -38,12 +38,28 @@ __device__ __forceinline__ void adam_vec(const float& g, float& w, float& m, flo
   adam_elem(g, w, m, v, c);
 }
 
-// Each wave owns a contiguous range of the listed rows (or, for few wide rows,
-// every cs-th column step of one).  The row ids of 64 rows come in one
-// coalesced load and reach their lanes by shuffle; rows are processed in
-// groups of kRowsInFlight steps, and the loads (g, w, m, v) of the next group
-// are issued before the current group is computed and stored.
-template <typename VecT>
+// Waves of this kernel that can be resident at once: 256 CUs x 4 SIMDs x 2
+// waves (its register use allows two per SIMD).
+constexpr int kResidentWaves = 2048;
+
+// Row ranges of few wide rows are shared by cs waves, each taking every cs-th
+// column step, so that about kResidentWaves waves have work; each wave keeps
+// at least two column steps where the rows allow it, so that its loads of the
+// next step are in flight while the current one is stored.
+__device__ __forceinline__ int column_share(int rows, int step_rows, int ncols, int all_waves) {
+  const int ranges = max((rows + step_rows - 1) / step_rows, 1);
+  const float want = static_cast<float>(kResidentWaves) / static_cast<float>(ranges);
+  return static_cast<int>(fminf(fmaxf(rintf(want), 1.0f), static_cast<float>(min(ncols, all_waves))));
+}
+
+// Each wave owns a contiguous range of the listed rows (with wide rows, every
+// cs-th column step of one).  The row ids of 64 rows come in one coalesced
+// load and reach their lanes by shuffle; rows are processed in tiles of
+// kRowsInFlight row steps, and the loads (g, w, m, v) of the next tile are
+// issued before the current tile is computed and stored.  kWide: rows of more
+// than one column step (Dv > 64); the tiles then run over the wave's column
+// steps as well, one sequence.
+template <typename VecT, bool kWide>
 __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, VecT* __restrict__ M,
                                                         VecT* __restrict__ S, int64_t V, int Dv, int log2L,
                                                         const int32_t* __restrict__ row_ids,
@@ -59,17 +75,12 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
   const int sub = lane >> log2L;
   const int cl = lane & (L - 1);
   const int step_rows = rpw * kRowsInFlight;
-  // With few rows (a batch with many repeats) and wide rows, cs waves share a
-  // row range, each taking every cs-th column step, so that about every wave
-  // of the launch has work.
   const int all_waves = static_cast<int>(gridDim.x) * (kThreads / kWave);
-  const int ncols = (Dv + L - 1) / L;
   const int wave_all = uniform(static_cast<int>(blockIdx.x) * (kThreads / kWave) + static_cast<int>(threadIdx.x / kWave));
+  const int ncols = kWide ? (Dv + L - 1) / L : 1;
   int cs = 1, wave = wave_all, part = 0, nwaves = all_waves;
-  if (ncols > 1) {
-    const float want = static_cast<float>(all_waves) * step_rows / static_cast<float>(max(hi - lo, 1));
-    // at most all_waves, so that at least one wave takes each row range
-    cs = uniform(static_cast<int>(fminf(fmaxf(want, 1.0f), static_cast<float>(min(ncols, all_waves)))));
+  if (kWide) {
+    cs = uniform(column_share(hi - lo, step_rows, ncols, all_waves));  // 1 <= cs <= all_waves
     wave = wave_all / cs;  // row range (waves past the last range find it empty)
     part = wave_all - wave * cs;
     nwaves = all_waves / cs;
@@ -78,20 +89,39 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
   per = (per + step_rows - 1) / step_rows * step_rows;
   const long long r0 = lo + static_cast<long long>(wave) * per;
   const long long r1 = min(static_cast<long long>(hi), r0 + per);
+  // two register buffers used in turn; every index below is a compile-time constant
+  struct Buf {
+    VecT g[kRowsInFlight], w[kRowsInFlight], m[kRowsInFlight], s[kRowsInFlight];
+    int rid[kRowsInFlight];
+    int col;
+    bool cok;
+  } A, B;
   bool bad = false;
   for (long long c0 = r0; c0 < r1; c0 += kWave) {  // 64 rows per id load
     const int n = static_cast<int>(min(static_cast<long long>(kWave), r1 - c0));
     const int32_t ridreg = row_ids[min(c0 + lane, static_cast<long long>(hi) - 1)];
     bad |= lane < n && (ridreg < 0 || ridreg >= V);
     const int ngroups = (n + step_rows - 1) / step_rows;
-    for (int cb = part * L; cb < Dv; cb += cs * L) {  // uniform column steps (the shuffles need every lane)
-      const int col = min(cb + cl, Dv - 1);
-      const bool cok = cb + cl < Dv;
-      // two register buffers used in turn; every index below is a compile-time constant
-      struct Buf {
-        VecT g[kRowsInFlight], w[kRowsInFlight], m[kRowsInFlight], s[kRowsInFlight];
-        int rid[kRowsInFlight];
-      } A, B;
+    auto apply = [&](Buf& x, int col, bool cok) {
+#pragma unroll
+      for (int u = 0; u < kRowsInFlight; ++u) {
+        if (x.rid[u] >= 0 && cok) {
+          adam_vec(x.g[u], x.w[u], x.m[u], x.s[u], c);
+          const size_t e = static_cast<size_t>(x.rid[u]) * Dv + col;
+          store_stream(&W[e], x.w[u]);
+          store_stream(&M[e], x.m[u]);
+          store_stream(&S[e], x.s[u]);
+        }
+      }
+    };
+    // Loads are unconditional (a group or tile past the last one reads row 0 of
+    // the table, one cached line for every wave, and stores nothing): with a
+    // branch around them the compiler could not count the loads in flight and
+    // would wait for all of them.  (Re-reading real rows instead would fetch
+    // the moments twice: they come in with streaming loads.)
+    if constexpr (!kWide) {  // one column step: the row groups in turn
+      const int col = min(cl, Dv - 1);
+      const bool cok = cl < Dv;
       auto load = [&](int grp, Buf& x) {
 #pragma unroll
         for (int u = 0; u < kRowsInFlight; ++u) {
@@ -105,27 +135,47 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
           x.s[u] = load_stream(&S[e]);
         }
       };
-      auto apply = [&](Buf& x) {
-#pragma unroll
-        for (int u = 0; u < kRowsInFlight; ++u) {
-          if (x.rid[u] >= 0 && cok) {
-            adam_vec(x.g[u], x.w[u], x.m[u], x.s[u], c);
-            const size_t e = static_cast<size_t>(x.rid[u]) * Dv + col;
-            store_stream(&W[e], x.w[u]);
-            store_stream(&M[e], x.m[u]);
-            store_stream(&S[e], x.s[u]);
-          }
-        }
-      };
-      // Loads are unconditional (a group past the last one reads clamped
-      // addresses and stores nothing): with a branch around them the compiler
-      // could not count the loads in flight and would wait for all of them.
       load(0, A);
       for (int grp = 0; grp < ngroups; grp += 2) {
         load(grp + 1, B);
-        apply(A);
+        apply(A, col, cok);
         load(grp + 2, A);
-        apply(B);
+        apply(B, col, cok);
+      }
+    } else {  // tiles (column step k: cb = (part + k * cs) * L; row group grp) in one sequence
+      const int nsteps = (ncols - part + cs - 1) / cs;
+      const int ntiles = nsteps * ngroups;
+      int lk = 0, lg = 0, lq = 0;  // the next tile to load
+      auto load = [&](Buf& x) {
+        const bool live = lq < ntiles;
+        const int k = live ? lk : nsteps - 1;
+        const int grp = live ? lg : ngroups - 1;
+        const int cb = (part + k * cs) * L;
+        x.col = min(cb + cl, Dv - 1);
+        x.cok = live && cb + cl < Dv;
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+          const int j = grp * step_rows + u * rpw + sub;
+          const int r = __shfl(ridreg, min(j, kWave - 1), kWave);
+          x.rid[u] = (live && j < n && r >= 0 && r < V) ? r : -1;
+          const size_t e = static_cast<size_t>(x.rid[u] < 0 ? 0 : x.rid[u]) * Dv + x.col;
+          x.g[u] = rows[static_cast<size_t>(c0 + min(j, n - 1)) * Dv + x.col];
+          x.w[u] = W[e];
+          x.m[u] = load_stream(&M[e]);
+          x.s[u] = load_stream(&S[e]);
+        }
+        ++lq;
+        if (++lg == ngroups) {
+          lg = 0;
+          ++lk;
+        }
+      };
+      load(A);
+      for (int q = 0; q < ntiles; q += 2) {
+        load(B);
+        apply(A, A.col, A.cok);
+        load(A);
+        apply(B, B.col, B.cok);
       }
     }
   }
@@ -147,15 +197,24 @@ hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t 
   // Both events are attached to the dispatch, so they time the kernel itself
   // (an attached start event idles the stream a few microseconds longer than a
   // marker before the launch, which would also count the dispatch latency).
-  if (vec4)
-    hipExtLaunchKernelGGL(adam_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream, start, stop, 0,
-                          reinterpret_cast<float4*>(table), reinterpret_cast<float4*>(exp_avg),
-                          reinterpret_cast<float4*>(exp_avg_sq), V, Dv, rl.log2_lanes, row_ids,
-                          reinterpret_cast<const float4*>(rows), offsets, shard_begin, shard_end, cap_rows, c, status);
-  else
-    hipExtLaunchKernelGGL(adam_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, start, stop, 0, table, exp_avg,
-                          exp_avg_sq, V, Dv, rl.log2_lanes, row_ids, rows, offsets, shard_begin, shard_end, cap_rows, c,
-                          status);
+  const bool wide = Dv > kWave;  // more than one column step per row
+#define EMB_ADAM(VT, WIDE)                                                                                        \
+  hipExtLaunchKernelGGL((adam_kernel<VT, WIDE>), dim3(grid), dim3(kThreads), 0, stream, start, stop, 0,           \
+                        reinterpret_cast<VT*>(table), reinterpret_cast<VT*>(exp_avg),                              \
+                        reinterpret_cast<VT*>(exp_avg_sq), V, Dv, rl.log2_lanes, row_ids,                          \
+                        reinterpret_cast<const VT*>(rows), offsets, shard_begin, shard_end, cap_rows, c, status)
+  if (vec4) {
+    if (wide)
+      EMB_ADAM(float4, true);
+    else
+      EMB_ADAM(float4, false);
+  } else {
+    if (wide)
+      EMB_ADAM(float, true);
+    else
+      EMB_ADAM(float, false);
+  }
+#undef EMB_ADAM
   return hipGetLastError();
 }
 
