@@ -223,3 +223,13 @@ def test_comm_cost_matches_oracle():
                         got = emb.comm_cost(code, N, M, alpha, B, beta, S=S)
                         want = oracle.comm_cost(name, N, M, alpha, B, beta, S=S)
                         assert got == pytest.approx(want, rel=1e-15, abs=0.0)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The benchmark measures one GPU's share; asked for several it says so and exits before touching a GPU."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
