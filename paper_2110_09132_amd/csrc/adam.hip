@@ -42,6 +42,15 @@ __device__ __forceinline__ void adam_vec(const float& g, float& w, float& m, flo
 // waves (its register use allows two per SIMD).
 constexpr int kResidentWaves = 2048;
 
+// LDS reserved (and not used) by each workgroup of the narrow-row update with
+// vector rows (the scalar path, for odd D, uses few registers and is left alone): with
+// 160 KB of LDS per CU, at most two of its workgroups, two waves per SIMD,
+// share a CU.  Its registers alone would allow three; at three the update
+// crowds out the reduction of the next step that runs beside it on another
+// stream, and the step gets slower (measured: 167 -> 200 us per step with
+// coalesce and pack as separate calls, 147 -> 149 us with the owner-major call).
+constexpr size_t kNarrowOccupancyLds = 56 * 1024;
+
 // Row ranges of few wide rows are shared by cs waves, each taking every cs-th
 // column step, so that about kResidentWaves waves have work; each wave keeps
 // at least two column steps where the rows allow it, so that its loads of the
@@ -199,7 +208,8 @@ hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t 
   // marker before the launch, which would also count the dispatch latency).
   const bool wide = Dv > kWave;  // more than one column step per row
 #define EMB_ADAM(VT, WIDE)                                                                                        \
-  hipExtLaunchKernelGGL((adam_kernel<VT, WIDE>), dim3(grid), dim3(kThreads), 0, stream, start, stop, 0,           \
+  hipExtLaunchKernelGGL((adam_kernel<VT, WIDE>), dim3(grid), dim3(kThreads),                                      \
+                        (WIDE) || sizeof(VT) != 16 ? 0 : kNarrowOccupancyLds, stream, start, stop, 0,              \
                         reinterpret_cast<VT*>(table), reinterpret_cast<VT*>(exp_avg),                              \
                         reinterpret_cast<VT*>(exp_avg_sq), V, Dv, rl.log2_lanes, row_ids,                          \
                         reinterpret_cast<const VT*>(rows), offsets, shard_begin, shard_end, cap_rows, c, status)
