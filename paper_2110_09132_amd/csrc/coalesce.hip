@@ -698,6 +698,157 @@ __global__ __launch_bounds__(kCombineThreads) void seg_combine_kernel(const floa
   }
 }
 
+// ------------------------------------------------------- one-workgroup path
+// Batches of at most kSmallMax tokens are coalesced by one workgroup in one
+// launch: the keys (built as in sort_keys_upsweep) are compacted to the
+// tokens that take part, sorted by an LSD radix sort in LDS (8-bit digits,
+// stable ranking as in the radix passes), and the segments are summed, each
+// by a group of lanes, over its tokens in sorted order.  The outputs are those
+// of the multi-kernel path; the fp32 sums of segments that would cross a
+// 32-token chunk there are rounded in another order (a plain sorted-order sum
+// here), within the same bound.  For small batches the launches and the gaps
+// between them are most of the multi-kernel path's time.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallItems = 2;
+constexpr int kSmallMax = kSmallThreads * kSmallItems;
+constexpr int kSmallGroupsMax = 2 * 1024;  // owner groups, times two with the split
+
+template <bool BF16, int VEC>
+__global__ __launch_bounds__(kSmallThreads) void small_coalesce_kernel(
+    const int32_t* __restrict__ ids, int T, KeySpec ks, int npass, const void* __restrict__ grad, int D, int log2L,
+    int32_t* __restrict__ uniq_ids, int32_t* __restrict__ seg_offsets, int32_t* __restrict__ num_unique,
+    float* __restrict__ uniq_grad, int32_t* __restrict__ group_counts, int32_t* __restrict__ group_offsets,
+    int32_t* status) {
+  constexpr int NT = kSmallThreads, NW = NT / kWave, IT = kSmallItems;
+  __shared__ uint32_t key_s[2][kSmallMax];
+  __shared__ int32_t pos_s[2][kSmallMax];
+  __shared__ uint32_t cnt[NW * 256];
+  __shared__ uint32_t dstart[256];
+  __shared__ uint32_t wsum[NW];
+  __shared__ uint32_t hs[kSmallMax];              // head flags, then their exclusive scan
+  __shared__ int32_t sstart[kSmallMax + 1];       // first sorted token of each segment, and n
+  __shared__ int32_t goff[kSmallGroupsMax + 1];   // group offsets
+  const int w = threadIdx.x / kWave;
+  const int lane = static_cast<int>(lane_id());
+  const int Tc = ks.count_dev != nullptr ? min(max(*ks.count_dev, 0), T) : T;  // tokens that exist
+  // 1. keys of the tokens, element e = (wave, round, lane) as the ranking walks them
+  uint32_t key[IT], dig[IT], lpos[IT];
+  bool inb[IT], take[IT];
+  bool bad_id = false, bad_owner = false;
+#pragma unroll
+  for (int r = 0; r < IT; ++r) {
+    const int e = w * IT * kWave + r * kWave + lane;
+    inb[r] = e < Tc;
+    const int32_t id = ids[min(e, T - 1)];
+    const bool idok = id >= 0 && static_cast<uint32_t>(id) < ks.V;
+    uint32_t own = 0;
+    if (ks.row_owner != nullptr) own = static_cast<uint32_t>(ks.row_owner[idok ? id : 0]);
+    const bool ownok = own < static_cast<uint32_t>(ks.P);
+    take[r] = inb[r] && idok && ownok;
+    bad_id |= inb[r] && !idok;
+    bad_owner |= inb[r] && idok && !ownok;
+    key[r] = (own << ks.ib) | static_cast<uint32_t>(idok ? id : 0);
+    if (ks.next_tab != nullptr && take[r] && !in_next(static_cast<uint32_t>(id), ks)) key[r] |= 1u << ks.cls_shift;
+    dig[r] = take[r] ? 0u : 1u;
+  }
+  if (__any(bad_id) && lane == 0) raise_flag(status, EMB_DEV_ID_OUT_OF_RANGE);
+  if (__any(bad_owner) && lane == 0) raise_flag(status, EMB_DEV_OWNER_OUT_OF_RANGE);
+  // 2. the tokens that take part, first and in token order
+  (void)tile_stable_rank<NT, IT>(dig, inb, 2, 1, cnt, dstart, wsum, lpos);
+  const int n = static_cast<int>(dstart[1]);  // tokens that take part
+#pragma unroll
+  for (int r = 0; r < IT; ++r) {
+    if (take[r]) {
+      key_s[0][lpos[r]] = key[r];
+      pos_s[0][lpos[r]] = w * IT * kWave + r * kWave + lane;
+    }
+  }
+  __syncthreads();
+  // 3. LSD radix passes of 8-bit digits in LDS
+  int cur = 0;
+  for (int p = 0; p < npass; ++p) {
+    bool valid[IT];
+    int32_t pos[IT];
+#pragma unroll
+    for (int r = 0; r < IT; ++r) {
+      const int e = w * IT * kWave + r * kWave + lane;
+      valid[r] = e < n;
+      key[r] = key_s[cur][min(e, kSmallMax - 1)];
+      pos[r] = pos_s[cur][min(e, kSmallMax - 1)];
+      dig[r] = valid[r] ? (key[r] >> (8 * p)) & 255u : 0u;
+    }
+    (void)tile_stable_rank<NT, IT>(dig, valid, 256, 8, cnt, dstart, wsum, lpos);
+#pragma unroll
+    for (int r = 0; r < IT; ++r) {
+      if (valid[r]) {
+        key_s[cur ^ 1][lpos[r]] = key[r];
+        pos_s[cur ^ 1][lpos[r]] = pos[r];
+      }
+    }
+    cur ^= 1;
+    __syncthreads();
+  }
+  const uint32_t* sk = key_s[cur];
+  const int32_t* sp = pos_s[cur];
+  // 4. segments: heads, unique indices, ids, starts, offsets of the owner groups
+  for (int e = threadIdx.x; e < n; e += NT) hs[e] = (e == 0 || sk[e] != sk[e - 1]) ? 1u : 0u;
+  __syncthreads();
+  const int U = static_cast<int>(block_exclusive_scan<NT>(hs, n, wsum));
+  for (int e = threadIdx.x; e < n; e += NT) {
+    if (e > 0 && sk[e] == sk[e - 1]) continue;  // not a head
+    const int u = static_cast<int>(hs[e]);
+    uniq_ids[u] = static_cast<int32_t>(sk[e] & ks.id_mask);
+    seg_offsets[u] = e;
+    sstart[u] = e;
+    const int o = min(group_of(sk[e], ks), ks.G);  // groups o_prev < q <= o start at this row
+    const int o_prev = e == 0 ? -1 : group_of(sk[e - 1], ks);
+    for (int q = o_prev + 1; q <= o; ++q) goff[q] = u;
+  }
+  if (threadIdx.x == 0) {
+    seg_offsets[U] = n;
+    sstart[U] = n;
+    num_unique[0] = U;
+    const int o_last = n > 0 ? min(group_of(sk[n - 1], ks), ks.G) : -1;
+    for (int q = o_last + 1; q <= ks.G; ++q) goff[q] = U;
+  }
+  __syncthreads();
+  if (group_offsets != nullptr)
+    for (int q = threadIdx.x; q <= ks.G; q += NT) {
+      group_offsets[q] = goff[q];
+      if (q < ks.G) group_counts[q] = goff[q + 1] - goff[q];
+    }
+  // 5. the sums: L lanes per segment, each segment's rows in sorted order
+  using Row = GradRow<BF16, VEC>;
+  using Acc = typename Row::Acc;
+  const int Dv = D / VEC;
+  const int L = 1 << log2L;
+  const int rpw = kWave >> log2L;
+  const int sub = lane >> log2L;
+  const int cl = lane & (L - 1);
+  Acc* out = reinterpret_cast<Acc*>(uniq_grad);
+  for (int u = w * rpw + sub; u < U; u += NW * rpw) {
+    const int S = sstart[u], E = sstart[u + 1];
+    for (int cb = 0; cb < Dv; cb += L) {
+      const int c = cb + cl;
+      if (c >= Dv) continue;
+      Acc acc = Acc{};
+      int i = S;
+      for (; i + 4 <= E; i += 4) {  // four rows in flight, added in order
+        const Acc g0 = Row::load(grad, static_cast<size_t>(sp[i]), Dv, c);
+        const Acc g1 = Row::load(grad, static_cast<size_t>(sp[i + 1]), Dv, c);
+        const Acc g2 = Row::load(grad, static_cast<size_t>(sp[i + 2]), Dv, c);
+        const Acc g3 = Row::load(grad, static_cast<size_t>(sp[i + 3]), Dv, c);
+        acc += g0;
+        acc += g1;
+        acc += g2;
+        acc += g3;
+      }
+      for (; i < E; ++i) acc += Row::load(grad, static_cast<size_t>(sp[i]), Dv, c);
+      out[static_cast<size_t>(u) * Dv + c] = acc;
+    }
+  }
+}
+
 // Lookup requests of the row-wise partition, from the owner-major sorted
 // tokens: one thread per sorted token.  A token heads its id when its key
 // differs from the previous one; its unique index u is the number of heads up
@@ -929,8 +1080,15 @@ bool coalesce_by_owner_supported(int64_t V, int P, bool split) {
   return key_bits(V, true, P, split) <= 8 * kMaxPasses;
 }
 
-hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const CoalesceVariant& var,
-                                void* workspace, int32_t* status, hipStream_t stream) {
+namespace {
+
+// Batches the one-workgroup kernel coalesces (its groups fit its LDS table).
+bool small_batch(int T, const KeySpec& ks) { return T <= kSmallMax && ks.G <= kSmallGroupsMax; }
+
+// full: the radix passes and head counts even for a small batch (the lookup
+// requests read the sorted keys).
+hipError_t sort_chain(const int32_t* ids, int T, int64_t V, int D, const CoalesceVariant& var, void* workspace,
+                      int32_t* status, hipStream_t stream, bool full) {
   if (T == 0) return hipSuccess;
   CoalesceWs ws = carve(workspace, T, D, is_split(var) ? var.T_next : -1, V);
   KeySpec ks = key_spec(V, var.row_owner, var.P, is_split(var));
@@ -948,6 +1106,8 @@ hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, con
     ks.next_bytemap = ws.tab_bytemap;
     ks.tab_shift = ws.tab_shift;
   }
+  // a small batch is sorted and summed by the one-workgroup kernel of the reduction half
+  if (!full && small_batch(T, ks)) return hipGetLastError();
   // 1-3. the key of every token (owner and next-batch lookups once) with the digit
   // histograms of all passes, then the radix passes over (key, position)
   const uint32_t* kin = nullptr;
@@ -962,15 +1122,54 @@ hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, con
   return hipGetLastError();
 }
 
-hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V,
+}  // namespace
+
+hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const CoalesceVariant& var,
+                                void* workspace, int32_t* status, hipStream_t stream) {
+  return sort_chain(ids, T, V, D, var, workspace, status, stream, false);
+}
+
+hipError_t launch_coalesce_reduce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
                                   const CoalesceVariant& var, int32_t* uniq_ids, int32_t* seg_offsets,
                                   float* uniq_grad, int32_t* num_unique, int32_t* group_counts,
-                                  int32_t* group_offsets, void* workspace, hipStream_t stream, hipEvent_t done) {
+                                  int32_t* group_offsets, void* workspace, int32_t* status, hipStream_t stream,
+                                  hipEvent_t done) {
   // group_offsets / group_counts are given exactly for the owner-major variants
   const KeySpec ks = key_spec(V, var.row_owner, var.P, is_split(var));
   if (T == 0) {
     hipExtLaunchKernelGGL(empty_batch_kernel, dim3(1), dim3(kThreads), 0, stream, nullptr, done, 0, seg_offsets,
                           num_unique, group_counts, group_offsets, ks.G);
+    return hipGetLastError();
+  }
+  if (small_batch(T, ks)) {  // sort and sums in one workgroup (the sort half built only the next-id set)
+    const CoalesceWs wsn = carve(workspace, T, D, is_split(var) ? var.T_next : -1, V);
+    KeySpec kss = ks;
+    kss.count_dev = var.count_dev;
+    if (is_split(var)) {
+      kss.next_tab = wsn.next_tab;
+      kss.next_bytemap = wsn.tab_bytemap;
+      kss.tab_shift = wsn.tab_shift;
+    }
+    const int npass = (max(key_bits(V, var.row_owner != nullptr, var.P, is_split(var)), 1) + 7) / 8;
+    const bool v4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(grad) % (grad_bf16 ? 8 : 16) == 0) &&
+                    (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
+    const int log2L = row_lanes_for(v4 ? D / 4 : D).log2_lanes;
+#define EMB_SMALL(BF, VC)                                                                                           \
+  hipExtLaunchKernelGGL((small_coalesce_kernel<BF, VC>), dim3(1), dim3(kSmallThreads), 0, stream, nullptr, done, 0, \
+                        ids, T, kss, npass, grad, D, log2L, uniq_ids, seg_offsets, num_unique, uniq_grad,  \
+                        group_counts, group_offsets, status)
+    if (v4) {
+      if (grad_bf16)
+        EMB_SMALL(true, 4);
+      else
+        EMB_SMALL(false, 4);
+    } else {
+      if (grad_bf16)
+        EMB_SMALL(true, 1);
+      else
+        EMB_SMALL(false, 1);
+    }
+#undef EMB_SMALL
     return hipGetLastError();
   }
   CoalesceWs ws = carve(workspace, T, D, -1, V);  // the next-id set, if any, lies past everything used here
@@ -1023,7 +1222,7 @@ hipError_t launch_lookup_request(const int32_t* ids, int T, int64_t V, const int
   CoalesceVariant var;
   var.row_owner = row_owner;
   var.P = P;
-  const hipError_t e = launch_coalesce_sort(ids, T, V, 0, var, workspace, status, stream);
+  const hipError_t e = sort_chain(ids, T, V, 0, var, workspace, status, stream, true);
   if (e != hipSuccess) return e;
   const CoalesceWs ws = carve(workspace, T, 0, -1, V);
   const KeySpec ks = key_spec(V, row_owner, P, false);
@@ -1044,8 +1243,8 @@ hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool gra
                            int32_t* status, hipStream_t stream) {
   const hipError_t e = launch_coalesce_sort(ids, T, V, D, var, workspace, status, stream);
   if (e != hipSuccess) return e;
-  return launch_coalesce_reduce(T, grad, grad_bf16, D, V, var, uniq_ids, seg_offsets, uniq_grad, num_unique,
-                                group_counts, group_offsets, workspace, stream, nullptr);
+  return launch_coalesce_reduce(ids, T, grad, grad_bf16, D, V, var, uniq_ids, seg_offsets, uniq_grad, num_unique,
+                                group_counts, group_offsets, workspace, status, stream, nullptr);
 }
 
 }  // namespace emb

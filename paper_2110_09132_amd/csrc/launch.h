@@ -28,14 +28,18 @@ struct CoalesceVariant {
 size_t coalesce_workspace_bytes(int T, int D, int T_next, int64_t V);
 bool coalesce_by_owner_supported(int64_t V, int P, bool split);  // the composite keys fit the radix passes
 // The two halves of launch_coalesce, for schedules that run them on different
-// streams (same workspace and variant; the reduce half must follow the sort
-// half).  done (may be null): an event attached to the reduce half's last kernel.
+// streams (same ids, workspace and variant; the reduce half must follow the
+// sort half).  A batch of at most 2048 tokens is sorted and summed by one
+// kernel of the reduce half (the sort half then only builds the next-id set
+// of the split).  done (may be null): an event attached to the reduce half's
+// last kernel.
 hipError_t launch_coalesce_sort(const int32_t* ids, int T, int64_t V, int D, const CoalesceVariant& var,
                                 void* workspace, int32_t* status, hipStream_t stream);
-hipError_t launch_coalesce_reduce(int T, const void* grad, bool grad_bf16, int D, int64_t V,
+hipError_t launch_coalesce_reduce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
                                   const CoalesceVariant& var, int32_t* uniq_ids, int32_t* seg_offsets,
                                   float* uniq_grad, int32_t* num_unique, int32_t* group_counts,
-                                  int32_t* group_offsets, void* workspace, hipStream_t stream, hipEvent_t done);
+                                  int32_t* group_offsets, void* workspace, int32_t* status, hipStream_t stream,
+                                  hipEvent_t done);
 hipError_t launch_coalesce(const int32_t* ids, int T, const void* grad, bool grad_bf16, int D, int64_t V,
                            const CoalesceVariant& var, int32_t* uniq_ids, int32_t* seg_offsets, float* uniq_grad,
                            int32_t* num_unique, int32_t* group_counts, int32_t* group_offsets, void* workspace,

@@ -164,10 +164,10 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     if (sep_sr && !ok(order.after(s->pack, kSorted, 0))) return st;
     if (sep_p && !chained && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
     if (s->split && s->delayed != s->pack && !ok(order.after(s->pack, kDelayedDone, order.sets))) return st;
-    if (!ok(launched(emb::launch_coalesce_reduce(a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, var,
+    if (!ok(launched(emb::launch_coalesce_reduce(a->ids, a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, var,
                                                  a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
-                                                 a->send_counts, a->send_offsets, a->ws_coalesce, S(s->pack),
-                                                 order.attach(kCoalesced)))))
+                                                 a->send_counts, a->send_offsets, a->ws_coalesce, a->dev_status,
+                                                 S(s->pack), order.attach(kCoalesced)))))
       return st;
     if (!ok(order.done(kCoalesced, s->pack, true))) return st;
     if (!ok(record(s->timing[3], s->pack))) return st;

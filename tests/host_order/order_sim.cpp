@@ -153,8 +153,9 @@ hipError_t launch_coalesce_sort(const int32_t*, int, int64_t, int, const Coalesc
   push(stream, Op{kLaunch, 0, 0, "sort"});
   return hipSuccess;
 }
-hipError_t launch_coalesce_reduce(int, const void*, bool, int, int64_t, const CoalesceVariant&, int32_t*, int32_t*,
-                                  float*, int32_t*, int32_t*, int32_t*, void*, hipStream_t stream, hipEvent_t done) {
+hipError_t launch_coalesce_reduce(const int32_t*, int, const void*, bool, int, int64_t, const CoalesceVariant&, int32_t*,
+                                  int32_t*, float*, int32_t*, int32_t*, int32_t*, void*, int32_t*, hipStream_t stream,
+                                  hipEvent_t done) {
   push(stream, Op{kLaunch, 0, 0, "reduce"});
   if (done) fail("an attached event with signals");
   return hipSuccess;
