@@ -87,6 +87,10 @@ def check_by_owner(ids_np, grad_np, V, own_np, P, bf16=False, grad_dev=None):
     ("uniform", 50000, 9000, 20, 1024, "range"),
     ("uniform", (1 << 22) - 1, 9000, 4, 1024, "rand"),  # 22 + 10 = 32 key bits: four passes
     ("uniform", (1 << 24) + 3, 9000, 4, 128, "mod"),    # 25 + 7 = 32 key bits, the widest that fits
+    # the one-workgroup path (at most 2048 tokens): the most owners, 32 key bits, a device-side count
+    ("uniform", 50000, 2048, 20, 1024, "rand"),
+    ("uniform", (1 << 22) - 1, 1500, 4, 1024, "rand"),
+    ("zipf", 5000, 1000, 256, 16, "mod"),
 ])
 def test_by_owner_parity(law, V, T, D, P, rule):
     ids = ids_for(law, V + T + P, T, V)
@@ -226,6 +230,9 @@ def check_split(ids_np, next_np, grad_np, V, own_np, P, bf16=False):
     ("zipf", 1, 777, 4, 1, "mod"),                # V = 1, P = 1: keys 0 and 1 only
     ("uniform", 50000, 9000, 20, 1024, "mod"),    # the most owners: 16 + 10 + 1 key bits
     ("uniform", (1 << 21) - 1, 9000, 4, 1024, "rand"),  # 21 + 10 + 1 = 32 key bits
+    # the one-workgroup path: 2048 groups (the most), a hash set of next ids (V > 2^24)
+    ("uniform", 50000, 2048, 20, 1024, "mod"),
+    ("uniform", (1 << 24) + 5, 1800, 4, 4, "mod"),
 ])
 def test_split_parity(law, V, T, D, P, rule):
     ids = ids_for(law, V + T + P, T, V)

@@ -65,10 +65,12 @@ def check_exchange(send_ids, send_rows, send_offs, P, cap):
     return recv_ids, recv_rows, total
 
 
-@pytest.mark.parametrize("P,law,D,rule", [(1, "zipf", 16, "mod"), (2, "uniform", 64, "mod"), (4, "zipf", 3, "range"),
-                                          (16, "uniform", 32, "mod"), (7, "zipf", 8, "rand")])
-def test_exchange_then_merge_equals_coalesce_of_all_tokens(P, law, D, rule):
-    V, T = 20000, 3000
+@pytest.mark.parametrize("P,law,D,rule,T", [(1, "zipf", 16, "mod", 3000), (2, "uniform", 64, "mod", 3000),
+                                            (4, "zipf", 3, "range", 3000), (16, "uniform", 32, "mod", 3000),
+                                            (7, "zipf", 8, "rand", 3000),
+                                            (2, "zipf", 16, "mod", 1000)])  # merge of 1903 of 2000 rows: one workgroup
+def test_exchange_then_merge_equals_coalesce_of_all_tokens(P, law, D, rule, T):
+    V = 20000
     sizes = [T - 97 * w for w in range(P)]  # ragged worker batches
     batches = [worker_batch(law, 900 + 31 * P + w, sizes[w], V, D) for w in range(P)]
     own_np = {"mod": gen.owner_mod(V, P), "range": gen.owner_range(V, P),

@@ -73,6 +73,12 @@ def test_gather_empty():
     ("zipf", 65535, 12000, 16),      # 16 key bits: two 8-bit passes
     ("zipf", 65537, 12000, 16),      # 17 key bits: three passes of 6 bits
     ("uniform", (1 << 22) - 1, 20000, 4),  # 22 key bits
+    # batches of at most 2048 tokens (the one-workgroup path): four 8-bit passes in LDS, one
+    # segment of all 2048 tokens, a hot row over many of them, a single token
+    ("uniform", (1 << 31) - 1, 2000, 4),
+    ("zipf", 1, 2048, 4),
+    ("zipf", 300, 1999, 256),
+    ("uniform", 7, 1, 5),
 ])
 def test_coalesce_parity_fp32(law, V, T, D):
     ids = ids_for(law, V + T + D, T, V)
@@ -80,7 +86,8 @@ def test_coalesce_parity_fp32(law, V, T, D):
     check_coalesce(ids, G, V)
 
 
-@pytest.mark.parametrize("V,T,D", [(262144, 16384, 1024), (1000, 3000, 12), (1000, 3000, 10)])
+@pytest.mark.parametrize("V,T,D", [(262144, 16384, 1024), (1000, 3000, 12), (1000, 3000, 10), (1000, 2000, 12),
+                                   (1000, 2048, 16)])
 def test_coalesce_parity_bf16(V, T, D):
     ids = ids_for("zipf", V + T, T, V, 1.0)
     G = grads_for(V + D, T, D, 0.01, bf16=True)
