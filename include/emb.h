@@ -95,7 +95,9 @@ int emb_gather(const float *table, int64_t V, int32_t D, const int32_t *ids,
  * left out and set EMB_DEV_ID_OUT_OF_RANGE.
  * Sums are accumulated in fp32 in a fixed order that depends only on the ids
  * (sorted position order, in chunks of 32 tokens, then an ordered combine of
- * the chunk partials): results are bitwise reproducible run to run.
+ * the chunk partials; a batch of at most 2048 tokens is summed by one
+ * workgroup in plain sorted position order): results are bitwise
+ * reproducible run to run.
  * Workgroups of one launch hand prefix sums to each other (decoupled
  * look-back); every wait is bounded and a timeout sets EMB_DEV_STALLED.
  * workspace: device memory of at least
@@ -156,8 +158,9 @@ int emb_pack_by_owner(const int32_t *uniq_ids, const float *uniq_grad,
  *   seg_offsets [T + 1]: seg_offsets[k + 1] - seg_offsets[k] tokens were summed
  *             into send row k (offsets in the owner-major token order)
  * except that the order of the fp32 additions inside a row may differ (same
- * rule: position order in chunks of 32 sorted tokens, then an ordered combine;
- * bitwise reproducible run to run).  A token whose id is outside [0, V) or
+ * rule: position order in chunks of 32 sorted tokens, then an ordered combine,
+ * or plain position order for at most 2048 tokens; bitwise reproducible run to
+ * run).  A token whose id is outside [0, V) or
  * whose owner is outside [0, P) is left out and sets EMB_DEV_ID_OUT_OF_RANGE /
  * EMB_DEV_OWNER_OUT_OF_RANGE.
  * workspace: emb_grad_coalesce_workspace_bytes(T, V, D, grad_dtype) bytes,
