@@ -313,6 +313,56 @@ def forward_exchange_report(torch, emb, sp, tb, batches, U, reps=20):
             "kernels": kern}
 
 
+def exchange_report(torch, emb, sp, tb, batches, reps=10):
+    """The receiver side of the gradient exchange (Sec. 4.1.1 / 4.1.2) for P simulated workers of the
+    first table's shape: every worker's owner-major coalesce into its own send layout (worker w takes
+    batch w mod 8 of the rotation; not timed), then the simulated AlltoAll (emb_exchange_simulated: a
+    P x P block transpose of ids and rows) and every owner's merge of what it received
+    (emb_receive_merge), each timed over `reps` back-to-back launches.  Byte models: the exchange reads
+    and writes every sent row and id; the merge reads the received rows and ids and writes the merged
+    rows and ids (its sort passes are not counted)."""
+    V, D, P, T = sp.V, sp.D, sp.P, sp.T
+    i32, f32 = torch.int32, torch.float32
+    send_ids = torch.empty((P, T), dtype=i32, device="cuda")
+    send_rows = torch.empty((P, T, D), dtype=f32, device="cuda")
+    send_offs = torch.empty((P, P + 1), dtype=i32, device="cuda")
+    seg = torch.empty(T + 1, dtype=i32, device="cuda")
+    cnt = torch.empty(P, dtype=i32, device="cuda")
+    nu = torch.empty(1, dtype=i32, device="cuda")
+    ws = emb.new_workspace(emb.grad_coalesce_workspace_bytes(T, V, D))
+    for w in range(P):
+        ids, g = batches[w % len(batches)]
+        emb.grad_coalesce_by_owner(ids, g, V, tb.row_owner, P, out=(send_ids[w], seg, send_rows[w], cnt, send_offs[w], nu),
+                                   workspace=ws)
+    recv = emb.exchange_simulated(send_ids, send_rows, send_offs)
+    merged = emb.receive_merge(recv[0], recv[1], recv[3], V, tb.row_owner, P)
+    torch.cuda.synchronize()
+    R, Um = int(recv[3].item()), int(merged[5].item())
+    mws = emb.new_workspace(emb.grad_coalesce_workspace_bytes(P * T, V, D))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    us_x = timed(lambda: emb.exchange_simulated(send_ids, send_rows, send_offs, out=recv))
+    us_m = timed(lambda: emb.receive_merge(recv[0], recv[1], recv[3], V, tb.row_owner, P, out=merged, workspace=mws))
+    kern = {}
+    for name, us, nbytes in (("exchange_simulated", us_x, 2 * R * (4 * D + 4)),
+                             ("receive_merge", us_m, R * (4 * D + 4) + Um * (4 * D + 4))):
+        kern[name] = {"avg_call_us": us, "bytes_model": nbytes, "GBps": nbytes / (us * 1e-6) / 1e9,
+                      "frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS}
+    del send_rows, recv, merged, mws
+    return {"table": 0, "workers": P, "rows_sent": R, "rows_merged": Um,
+            "merge_per_owner_mean_rows": Um / P, "calls": kern}
+
+
 def cost_model_report(emb, sp, U, N=8):
     """Table 2 (Sec. 4.1.2) fed with the measured density alpha = U / V of the first table's batches,
     for N workers of one node with B = one xGMI link; the bandwidth terms (beta = 0) in microseconds
@@ -541,6 +591,7 @@ def main():
     cost = cost_model_report(emb, wl.tables[0], [U[b][0] for b in range(args.batches)])
     forward = forward_exchange_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches],
                                       [U[b][0] for b in range(args.batches)])
+    exchange = exchange_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches])
 
     # algorithmic bytes of the timed steps
     bytes_step = {k: 0.0 for k in ("gather", "coalesce", "pack", "adam")}
@@ -627,6 +678,7 @@ def main():
         "gradient_sizes_table3": table3,
         "column_partition": column,
         "forward_exchange": forward,
+        "gradient_exchange": exchange,
         "comm_cost_model": cost,
         "step_frac_of_copy": step_gbps / copy_gbps,
         "host": host_info(),

@@ -7,7 +7,8 @@
 //     at its receiver: owner-major, senders in order inside an owner.  One
 //     workgroup; P <= 1024.
 //  2. exchange_rows: a P x P block transpose of ids and rows.  Each row finds
-//     its owner block by binary search over its sender's offsets.
+//     its owner block by binary search over its sender's offsets, which each
+//     workgroup first copies to LDS with the receivers' destinations.
 // The merge of the received runs is the owner-major coalesce with a token
 // count read on the device (the received total), in coalesce.hip.
 #include "common.h"
@@ -59,13 +60,26 @@ __global__ __launch_bounds__(kRowThreads) void exchange_rows_kernel(
     const int32_t* __restrict__ send_ids, const VecT* __restrict__ send_rows, const int32_t* __restrict__ send_offsets,
     int P, int cap, int Dv, int log2L, const int32_t* __restrict__ recv_offsets, int32_t* __restrict__ recv_ids,
     VecT* __restrict__ recv_rows) {
+  // the sender's offsets, block sizes and destinations, once per workgroup in LDS
+  // (a row then finds its block by a binary search in LDS, not in memory)
+  __shared__ int32_t s_o[kThreads + 1];   // send_offsets[w][p]
+  __shared__ int32_t s_cnt[kThreads];     // rows of block p (clamped)
+  __shared__ int32_t s_dst[kThreads];     // where receiver p puts them: recv_offsets[p][w]
   const int L = 1 << log2L;
   const int rpw = kWave >> log2L;
   const int sub = static_cast<int>(lane_id()) >> log2L;
   const int cl = static_cast<int>(lane_id()) & (L - 1);
   const int w = blockIdx.y;  // the sender
   const int32_t* o = send_offsets + static_cast<size_t>(w) * (P + 1);
-  const int sent = min(max(o[P], 0), cap);
+  for (int p = threadIdx.x; p <= P; p += kRowThreads) {
+    s_o[p] = o[p];
+    if (p < P) {
+      s_cnt[p] = block_count(send_offsets, P, cap, w, p);
+      s_dst[p] = recv_offsets[static_cast<size_t>(p) * (P + 1) + w];
+    }
+  }
+  __syncthreads();
+  const int sent = min(max(s_o[P], 0), cap);
   const long long wave = (static_cast<long long>(blockIdx.x) * kRowThreads + threadIdx.x) / kWave;
   const long long nwaves = static_cast<long long>(gridDim.x) * (kRowThreads / kWave);
   const long long step = static_cast<long long>(rpw) * kRowsInFlight;
@@ -80,15 +94,12 @@ __global__ __launch_bounds__(kRowThreads) void exchange_rows_kernel(
       int lo = 0, hi = P - 1;
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (o[mid] <= kc) lo = mid; else hi = mid - 1;
+        if (s_o[mid] <= kc) lo = mid; else hi = mid - 1;
       }
-      const int32_t* r = recv_offsets + static_cast<size_t>(lo) * (P + 1);
-      const int a = min(max(o[lo], 0), cap);
+      const int a = min(max(s_o[lo], 0), cap);
       const int off = kc - a;  // inside the block unless the offsets are malformed
       src[u] = static_cast<int64_t>(w) * cap + kc;
-      dst[u] = (k < sent && off >= 0 && off < block_count(send_offsets, P, cap, w, lo))
-                   ? static_cast<int64_t>(r[w]) + off
-                   : -1;
+      dst[u] = (k < sent && off >= 0 && off < s_cnt[lo]) ? static_cast<int64_t>(s_dst[lo]) + off : -1;
     }
     if (cl == 0) {
 #pragma unroll

@@ -126,3 +126,36 @@ def test_merge_of_nothing():
     merged = emb.receive_merge(recv_ids, recv_rows, total, V, to_dev(gen.owner_mod(V, P)), P)
     torch.cuda.synchronize()
     assert int(merged[5].item()) == 0 and host(merged[4]).tolist() == [0, 0, 0]
+
+
+def test_exchange_and_merge_at_the_benchmark_shape():
+    """The launch configuration the benchmark times: 16 workers, each the owner-major coalesce of a
+    65536-token batch over 2^20 rows of 256 floats (worker w takes batch w mod 8, as there).  The
+    merge's ids, counts and offsets bit for bit against the oracle's owner-major pack of the coalesce
+    of all 16 batches together; rows sampled within the summation bound."""
+    V, D, P, T = 1 << 20, 256, 16, 65536
+    print(f"exchange + merge at V={V} D={D} P={P} T={T}", flush=True)
+    own_np = gen.owner_mod(V, P)
+    base = [worker_batch("uniform", 1500 + b, T, V, D) for b in range(8)]
+    batches = [base[w % 8] for w in range(P)]
+    send_ids, send_rows, send_offs = run_workers(batches, V, D, own_np, P, T)
+    recv_ids, recv_rows, recv_offs, total = emb.exchange_simulated(send_ids, send_rows, send_offs)
+    del send_rows
+    st = emb.new_status()
+    m_ids, m_seg, m_rows, m_cnt, m_offs, m_nu = emb.receive_merge(recv_ids, recv_rows, total, V, to_dev(own_np), P,
+                                                                 dev_status=st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    U = int(m_nu.item())
+    all_ids = np.concatenate([b[0] for b in batches])
+    all_g = np.concatenate([b[1] for b in batches])
+    orc = oracle.coalesce(all_ids, all_g, V)
+    del all_g
+    pk = oracle.pack_by_owner(orc["uniq_ids"], orc["uniq_grad"], own_np, P)
+    assert U == int(pk["send_offsets"][P])
+    assert np.array_equal(host(m_ids[:U]), pk["send_ids"])
+    assert np.array_equal(host(m_cnt), pk["send_counts"]) and np.array_equal(host(m_offs), pk["send_offsets"])
+    sample = np.sort(np.random.default_rng(5).choice(U, 4096, replace=False))
+    idx = np.searchsorted(orc["uniq_ids"], pk["send_ids"][sample])
+    got = host(m_rows[torch.from_numpy(sample).to(m_rows.device)])
+    tolerance.assert_grad_close(got, orc["sum_f64"][idx], orc["absum"][idx], tolerance.RTOL_F32)
