@@ -36,6 +36,8 @@
 //     results in wave order); by owner, it also forms the per-owner counts.
 // The lookup requests of the row-wise forward exchange reuse kernels 1-3 on
 // the owner-major keys and replace 4-5 by request_kernel (no rows to sum).
+// Batches of at most 2048 tokens take one kernel instead of all five
+// (small_coalesce_kernel: the same keys, sort and sums in one workgroup).
 // The order of every floating-point addition depends only on the ids, never
 // on scheduling, so results are bitwise reproducible.
 #include <hip/hip_ext.h>
