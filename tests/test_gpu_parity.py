@@ -79,6 +79,9 @@ def test_gather_empty():
     ("zipf", 1, 2048, 4),
     ("zipf", 300, 1999, 256),
     ("uniform", 7, 1, 5),
+    # more than 1024 reduction workgroups: the head counts are scanned once by their own kernel
+    ("zipf", 1 << 20, 200000, 8),
+    ("uniform", 1 << 18, 131073, 4),
 ])
 def test_coalesce_parity_fp32(law, V, T, D):
     ids = ids_for(law, V + T + D, T, V)
