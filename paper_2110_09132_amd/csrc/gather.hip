@@ -19,7 +19,12 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kRowsInFlight = 8;
 
-template <typename VecT>
+// kWide: rows of more than one column step (Dv > 64).  The wave's column steps
+// and row groups then run as one sequence of tiles, so that the loads of the
+// next column step are in flight while the current one is stored (with few
+// rows per wave, a single group per column step would otherwise wait for its
+// loads step after step).
+template <typename VecT, bool kWide>
 __global__ __launch_bounds__(kThreads) void gather_kernel(const VecT* __restrict__ table, int64_t V, int Dv,
                                                           int log2L, const int32_t* __restrict__ ids, int T,
                                                           VecT* __restrict__ out, int32_t* status) {
@@ -48,6 +53,53 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const VecT* __restrict
       const int id = __shfl(idreg, min(j, kWave - 1), kWave);
       return (j < n && id >= 0 && id < V) ? id : -1;
     };
+    if constexpr (kWide) {
+      // tiles (column step k: cb = k * L; row group g) in one sequence, two buffers in turn
+      struct Tile {
+        VecT v[kRowsInFlight];
+        int id[kRowsInFlight];
+        int c, g;
+        bool live;
+      } A, B;
+      const int nsteps = (Dv + L - 1) / L;
+      const int ntiles = nsteps * ngroups;
+      int lk = 0, lg = 0, lq = 0;  // the next tile to load
+      // a tile past the last one reads row 0 (one cached line) and is not stored
+      auto load = [&](Tile& x) {
+        x.live = lq < ntiles;
+        x.g = x.live ? lg : 0;
+        const int cb = (x.live ? lk : 0) * L;
+        x.c = min(cb + cl, Dv - 1);
+        const bool cok = cb + cl < Dv;
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+          x.id[u] = x.live ? row_id(x.g, u) : -1;
+          x.v[u] = table[static_cast<size_t>(x.id[u] < 0 ? 0 : x.id[u]) * Dv + x.c];
+        }
+        x.live = x.live && cok;
+        ++lq;
+        if (++lg == ngroups) {
+          lg = 0;
+          ++lk;
+        }
+      };
+      auto store = [&](const Tile& x) {
+        if (!x.live) return;
+#pragma unroll
+        for (int u = 0; u < kRowsInFlight; ++u) {
+          const int j = x.g * static_cast<int>(step_rows) + u * rpw + sub;
+          if (j < n) store_stream(&out[static_cast<size_t>(c0 + j) * Dv + x.c], x.id[u] < 0 ? VecT{} : x.v[u]);
+        }
+      };
+      load(A);
+      for (int q = 0; q < ntiles; q += 2) {
+        load(B);
+        store(A);
+        load(A);
+        store(B);
+      }
+      continue;
+    }
     // column steps are uniform across the wave (the shuffles need every lane)
     for (int cb = 0; cb < Dv; cb += L) {
       const int c = min(cb + cl, Dv - 1);
@@ -96,13 +148,23 @@ hipError_t launch_gather(const float* table, int64_t V, int D, const int32_t* id
   const RowLanes rl = row_lanes_for(Dv);
   const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * kRowsInFlight * (kThreads / kWave);
   const unsigned grid = grid_for((T + rows_per_block - 1) / rows_per_block, kMaxBlocks);
+  const bool wide = Dv > kWave;
   if (vec4) {
-    hipExtLaunchKernelGGL(gather_kernel<float4>, dim3(grid), dim3(kThreads), 0, stream, nullptr, done, 0,
-                          reinterpret_cast<const float4*>(table), V, Dv, rl.log2_lanes, ids, T,
-                          reinterpret_cast<float4*>(out), status);
+    const auto* tv = reinterpret_cast<const float4*>(table);
+    auto* ov = reinterpret_cast<float4*>(out);
+    if (wide)
+      hipExtLaunchKernelGGL((gather_kernel<float4, true>), dim3(grid), dim3(kThreads), 0, stream, nullptr, done, 0, tv,
+                            V, Dv, rl.log2_lanes, ids, T, ov, status);
+    else
+      hipExtLaunchKernelGGL((gather_kernel<float4, false>), dim3(grid), dim3(kThreads), 0, stream, nullptr, done, 0, tv,
+                            V, Dv, rl.log2_lanes, ids, T, ov, status);
   } else {
-    hipExtLaunchKernelGGL(gather_kernel<float>, dim3(grid), dim3(kThreads), 0, stream, nullptr, done, 0, table, V,
-                          Dv, rl.log2_lanes, ids, T, out, status);
+    if (wide)
+      hipExtLaunchKernelGGL((gather_kernel<float, true>), dim3(grid), dim3(kThreads), 0, stream, nullptr, done, 0,
+                            table, V, Dv, rl.log2_lanes, ids, T, out, status);
+    else
+      hipExtLaunchKernelGGL((gather_kernel<float, false>), dim3(grid), dim3(kThreads), 0, stream, nullptr, done, 0,
+                            table, V, Dv, rl.log2_lanes, ids, T, out, status);
   }
   return hipGetLastError();
 }
