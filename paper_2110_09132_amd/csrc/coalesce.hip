@@ -62,7 +62,7 @@ struct SortCfg {
   static constexpr int kNT = NT;
   static constexpr int kBins = 1 << BITS;
   static constexpr int kTile = NT * kItems;      // keys per sort tile
-  static constexpr int kUpTile = NT * 16;        // keys per histogram tile
+  static constexpr int kUpTile = NT * 8;         // keys per histogram tile
   static constexpr int kPasses = kMaxPasses;  // most passes this configuration runs
 };
 using Narrow = SortCfg<256, 8>;
