@@ -12,8 +12,8 @@
 //     clears the look-back state used by the later kernels.  Tokens whose id
 //     (or owner) is out of range take no part: they are left out of the
 //     histograms and so out of the sorted sequence.
-//  2. sort_pass, once per digit of the key bits (<= 8 bits each, 9 for 17-
-//     and 18-bit keys): a stable LSD radix pass over (key, token position).
+//  2. sort_pass, once per digit of the key bits (<= 8 bits each, 9 where that
+//     saves a pass): a stable LSD radix pass over (key, token position).
 //     Each tile ranks its keys in LDS with wave ballots, publishes its
 //     per-digit counts and reads the counts of the tiles before it (decoupled
 //     look-back, Merrill & Garland 2016), so one launch per pass suffices.
@@ -54,9 +54,10 @@ constexpr int kItems = 8;
 constexpr int kMaxPasses = 4;  // up to 31 key bits
 
 // Radix configuration: 256-thread tiles of 2048 keys, digits of at most 8 bits,
-// or 9 bits for keys of 17 or 18 bits (two passes instead of three).  (Two
-// passes of 11-bit digits were measured slower than three of 8 bits for 24-bit
-// keys: the 2048-bin ranking is LDS-bound and runs on half as many tiles.)
+// or 9 bits where that saves a pass (keys of 9, 17-18 or 25-27 bits: one, two or
+// three passes instead of two, three or four).  (Two passes of 11-bit digits
+// were measured slower than three of 8 bits for 24-bit keys: the 2048-bin
+// ranking is LDS-bound and runs on half as many tiles.)
 template <int NT, int BITS>
 struct SortCfg {
   static constexpr int kNT = NT;
@@ -66,7 +67,12 @@ struct SortCfg {
   static constexpr int kPasses = kMaxPasses;  // most passes this configuration runs
 };
 using Narrow = SortCfg<256, 8>;
-using Wide9 = SortCfg<256, 9>;  // same workspace sizes as Narrow for its two passes
+using Wide9 = SortCfg<256, 9>;
+constexpr int kWide9Passes = 3;  // most passes of 9-bit digits
+// Histogram and look-back words per tile, for every pass of either configuration.
+constexpr int kHistPerTile = kMaxPasses * Narrow::kBins > kWide9Passes * Wide9::kBins ? kMaxPasses * Narrow::kBins
+                                                                                      : kWide9Passes * Wide9::kBins;
+static_assert(Narrow::kTile == Wide9::kTile && Narrow::kUpTile == Wide9::kUpTile, "one tiling for both");
 constexpr int kChunk = 32;                    // sorted tokens per reduction wave
 constexpr int kRedTile = kChunk * kWaves;     // sorted tokens per reduction workgroup
 constexpr int kLoadsInFlight = 8;
@@ -249,7 +255,7 @@ int key_bits(int64_t V, bool by_owner, int P, bool split) {
 
 RadixPlan plan_for(int B) {
   B = max(B, 1);  // one pass even when every key is 0
-  const int digit = (B == 17 || B == 18) ? 9 : 8;
+  const int digit = ((B + 8) / 9 < (B + 7) / 8 && (B + 8) / 9 <= kWide9Passes) ? 9 : 8;
   const int npass = (B + digit - 1) / digit;
   return RadixPlan{npass, (B + npass - 1) / npass, B, digit};
 }
@@ -993,10 +999,10 @@ CoalesceWs carve_with(void* base, int T, int D, int T_next, int64_t V) {
   w.keys_b = cv.take<uint32_t>(n);
   w.vals_a = cv.take<int32_t>(n);
   w.vals_b = cv.take<int32_t>(n);
-  w.up_hist = cv.take<uint32_t>(nup * kMaxPasses * C::kBins);
+  w.up_hist = cv.take<uint32_t>(nup * kHistPerTile);
   w.tickets = cv.take<uint32_t>(kMaxPasses);
   w.span_count = cv.take<int32_t>(1);
-  w.sort_lb = cv.take<uint32_t>(static_cast<size_t>(kMaxPasses) * ntiles * C::kBins);
+  w.sort_lb = cv.take<uint32_t>(static_cast<size_t>(kHistPerTile) * ntiles);
   w.n_valid = cv.take<uint32_t>(1);
   w.span_list = cv.take<int32_t>(nchunks);
   w.tile_heads = cv.take<uint32_t>(nred);

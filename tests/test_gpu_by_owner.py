@@ -83,9 +83,11 @@ def check_by_owner(ids_np, grad_np, V, own_np, P, bf16=False, grad_dev=None):
     ("uniform", 50, 33, 1, 3, "mod"),               # one chunk + 1, D = 1
     ("zipf", 1, 777, 4, 1, "mod"),                  # V = 1, P = 1: every key 0
     ("zipf", 1, 777, 4, 9, "rand"),                 # V = 1, one owner of nine
-    ("uniform", 50000, 9000, 20, 1024, "mod"),      # the most owners: 16 + 10 key bits
+    ("uniform", 50000, 9000, 20, 1024, "mod"),      # the most owners: 16 + 10 key bits, three 9-bit passes
     ("uniform", 50000, 9000, 20, 1024, "range"),
     ("uniform", (1 << 22) - 1, 9000, 4, 1024, "rand"),  # 22 + 10 = 32 key bits: four passes
+    ("uniform", 1 << 21, 20000, 8, 16, "mod"),     # 21 + 4 = 25 key bits: three 9-bit passes (9, 9, 7)
+    ("zipf", 256, 5000, 8, 2, "mod"),              # 8 + 1 = 9 key bits: one 9-bit pass
     ("uniform", (1 << 24) + 3, 9000, 4, 128, "mod"),    # 25 + 7 = 32 key bits, the widest that fits
     # the one-workgroup path (at most 2048 tokens): the most owners, 32 key bits, a device-side count
     ("uniform", 50000, 2048, 20, 1024, "rand"),
@@ -225,10 +227,10 @@ def check_split(ids_np, next_np, grad_np, V, own_np, P, bf16=False):
 @pytest.mark.parametrize("law,V,T,D,P,rule", [
     ("zipf", 1000, 512, 64, 2, "mod"),            # the tiny workload's shape
     ("zipf", 32768, 25000, 64, 4, "range"),       # shared-vocab shape, narrower rows
-    ("uniform", 1 << 20, 20000, 16, 16, "mod"),   # 20 + 4 + 1 key bits: four passes
+    ("uniform", 1 << 20, 20000, 16, 16, "mod"),   # 20 + 4 + 1 key bits: three 9-bit passes
     ("zipf", 5000, 2049, 3, 7, "rand"),           # ragged tile, scalar width path
     ("zipf", 1, 777, 4, 1, "mod"),                # V = 1, P = 1: keys 0 and 1 only
-    ("uniform", 50000, 9000, 20, 1024, "mod"),    # the most owners: 16 + 10 + 1 key bits
+    ("uniform", 50000, 9000, 20, 1024, "mod"),    # the most owners: 16 + 10 + 1 = 27 key bits, 9 bits a pass
     ("uniform", (1 << 21) - 1, 9000, 4, 1024, "rand"),  # 21 + 10 + 1 = 32 key bits
     # the one-workgroup path: 2048 groups (the most), a hash set of next ids (V > 2^24)
     ("uniform", 50000, 2048, 20, 1024, "mod"),

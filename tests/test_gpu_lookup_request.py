@@ -71,7 +71,8 @@ def check_request(ids, V, own, P):
 CASES = [(1000, 100, 4, "mod", "uniform"), (5000, 3001, 7, "range", "uniform"), (1 << 16, 20000, 1, "mod", "uniform"),
          (4096, 9000, 1024, "rand", "uniform"), (1 << 14, 12345, 8, "mod", "zipf13"),
          (1 << 15, 40000, 4, "range", "zipf11"), (1, 300, 3, "mod", "uniform"), (1 << 22, 5000, 1024, "range", "uniform"),
-         (100003, 65536, 16, "mod", "zipf13"), (1 << 20, 200000, 16, "mod", "uniform")]  # scanned head counts
+         (100003, 65536, 16, "mod", "zipf13"), (1 << 20, 200000, 16, "mod", "uniform"),  # scanned head counts
+         (1 << 21, 30000, 16, "mod", "uniform"), (256, 5000, 2, "mod", "zipf11")]  # 25 and 9 key bits
 
 
 @pytest.mark.parametrize("V,T,P,rule,law", CASES)

@@ -65,14 +65,16 @@ def test_gather_empty():
     ("zipf", 5000, 2049, 3),         # ragged second tile, scalar width path
     ("uniform", 1 << 20, 10000, 16),  # 20 key bits: three passes of 7 bits
     ("zipf", 32768, 25000, 65),      # odd width (scalar path), many chunks
-    ("zipf", 300, 4001, 256),        # very heavy duplication
+    ("zipf", 300, 4001, 256),        # very heavy duplication; 9 key bits: one 9-bit pass
     ("uniform", 50, 33, 1),          # one chunk + 1, D = 1
     ("zipf", 1, 777, 4),             # V = 1: every key 0 (one pass), one segment over 25 chunks
     ("uniform", 5_000_000, 9000, 8),  # 23 key bits: three 8-bit passes
     ("uniform", (1 << 31) - 1, 5000, 4),  # 31 key bits: four passes
     ("zipf", 65535, 12000, 16),      # 16 key bits: two 8-bit passes
-    ("zipf", 65537, 12000, 16),      # 17 key bits: three passes of 6 bits
+    ("zipf", 65537, 12000, 16),      # 17 key bits: two 9-bit passes
     ("uniform", (1 << 22) - 1, 20000, 4),  # 22 key bits
+    ("uniform", 1 << 25, 20000, 4),  # 25 key bits: three 9-bit passes (9, 9, 7)
+    ("uniform", (1 << 27) - 1, 9000, 4),  # 27 key bits: three 9-bit passes
     # batches of at most 2048 tokens (the one-workgroup path): four 8-bit passes in LDS, one
     # segment of all 2048 tokens, a hot row over many of them, a single token
     ("uniform", (1 << 31) - 1, 2000, 4),
