@@ -22,7 +22,10 @@
  * Conventions for every call:
  *  - Array arguments are DEVICE pointers (memory of the current HIP device);
  *    scalars are passed by value.  The caller allocates and owns every buffer;
- *    the library never allocates, frees or keeps a pointer after returning.
+ *    the calls of the path never allocate, free or keep a pointer after
+ *    returning.  The one allocation of the library is the signal memory of
+ *    emb_step_signals_create (a few words per handle, kept in a pool for reuse
+ *    and never returned to the runtime).
  *  - Tables and gradient rows are dense row-major [rows][D] arrays.  Ids are
  *    int32 row indices in [0, V).
  *  - `stream` is a hipStream_t (NULL: the null stream).  Calls only enqueue
@@ -403,12 +406,18 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  * Sec. 4.2.2, here on one GPU).  One host call per step keeps the host ahead
  * of the GPU.
  *
- * The caller rotates buffer sets (coalesce workspace, uniq_* and send_*
- * outputs; two unless `sets` says more) between consecutive steps and gives
- * each set its own events; `reuse` is nonzero when the set was used before.
- * Below, "s-2" is the set's previous step, s - sets.  The streams may differ
- * between sets: with the `coalesce` stream alternating between two streams,
- * the sorts of consecutive steps run side by side.
+ * The caller rotates buffer sets (coalesce and pack workspaces, uniq_* and
+ * send_* outputs; two unless `sets` says more) between consecutive steps and
+ * gives each set its own events; `reuse` is nonzero when the set was used
+ * before.  Below, "s-2" is the set's previous step, s - sets.  The streams may
+ * differ between sets, and a set's streams may change from one use to the
+ * next (with the `coalesce` stream alternating between two streams, the sorts
+ * of consecutive steps run side by side): the waits on a set's previous use
+ * are issued whatever the streams, and cost nothing when the stage waited for
+ * ran on the waiting stream.  `lookup_update` must be the same stream for
+ * every step of a table (the lookup of a step follows the previous update in
+ * stream order), and a table's steps change between split and not split only
+ * once the work enqueued so far has completed.
  *
  * by_owner == 0: emb_grad_coalesce on the `coalesce` stream, emb_pack_by_owner
  * on the `pack` stream, lookup and update on `lookup_update`, with the waits

@@ -87,7 +87,9 @@ struct Order {
     sig->writer[k][q] = stream;
     return EMB_OK;
   }
-  // `stream` waits for stage k of the step `lag` steps back (lag 0: this step).
+  // `stream` waits for stage k of the step `lag` steps back (lag 0: this step).  A wait on a stage
+  // that ran on the waiting stream itself is implied by stream order and costs nothing: the runtime
+  // skips a wait on an event recorded on the waiting stream, and with signals it is left out below.
   // With events, a lag > 0 means the step that last used this buffer set (the
   // set's own event), so it must equal `sets`.
   // With signals the wait uses the word of that step's parity, and the target
@@ -103,6 +105,10 @@ struct Order {
       const int q = n & 1;
       const uint32_t target = n < sig->written[k][q] ? n : sig->written[k][q];
       if (target == 0) return EMB_OK;  // the stage never ran in a step of that parity
+      // The word's last write was enqueued on this stream: every write to the word is ordered before
+      // it (a write on another stream than the previous one waits for that one first), so the word
+      // holds at least the target by the time this stream gets here.
+      if (sig->writer[k][q] == stream) return EMB_OK;
       return status_of(hipStreamWaitValue32(S(stream), sig->word[k][q], target, hipStreamWaitValueGte, 0xFFFFFFFFu));
     }
     if (lag > 0 && !s->reuse) return EMB_OK;  // the buffer set was not used before
@@ -117,22 +123,26 @@ struct Order {
   }
 };
 
+// Waits on the earlier use of this buffer set (and the split's wait two steps back) are issued
+// whatever the streams, since a set's streams may differ from one use to the next; the stage ends
+// they refer to are always announced.  Waits inside one step are issued between different streams
+// only.
 int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order& order) {
   const bool sep_p = s->pack != s->lookup_update;
   int st = EMB_OK;
   // each step stops the sequence at the first failing call
   auto ok = [&st](int r) { return (st = r) == EMB_OK; };
   auto launched = [](hipError_t e) { return status_of(e); };
-  auto update = [&](int32_t groups_from, void* stream, void* t0, void* t1, Stage end_stage, bool announce) {
+  auto update = [&](int32_t groups_from, void* stream, void* t0, void* t1, Stage end_stage) {
     // Adam on the groups [groups_from, groups_from + P) of the send layout.  An
     // event after the kernel is attached to its dispatch (less idle time on the
     // stream than a separate marker): the timing event if any, else the end event.
-    const hipEvent_t end_ev = announce ? order.attach(end_stage) : nullptr;
+    const hipEvent_t end_ev = order.attach(end_stage);
     const hipEvent_t first = t1 != nullptr ? E(t1) : end_ev;
     return ok(emb::sparse_adam_call(a->table, a->exp_avg, a->exp_avg_sq, a->V, a->D, a->send_ids, a->send_rows,
                                     a->send_offsets + groups_from, a->P, 0, a->P, a->cap_rows, a->lr, a->beta1,
                                     a->beta2, a->eps, a->step, a->dev_status, S(stream), E(t0), first)) &&
-           (!announce || ok(order.done(end_stage, stream, t1 == nullptr && end_ev != nullptr)));
+           ok(order.done(end_stage, stream, t1 == nullptr && end_ev != nullptr));
   };
   if (s->by_owner) {
     // owner-major coalesce in its two halves: the sort on the coalesce stream,
@@ -154,7 +164,7 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     // with two sets it would hold the sort back by a whole update).
     const bool chained = order.sets >= 4 && !s->split && sep_sr && sep_p;
     // sort(s): after the reduction of the set's last step (s - sets) has finished with its workspace
-    if (sep_sr && !ok(order.after(s->coalesce, chained ? kUpdated : kCoalesced, order.sets))) return st;
+    if (!ok(order.after(s->coalesce, chained ? kUpdated : kCoalesced, order.sets))) return st;
     if (!ok(record(s->timing[2], s->coalesce))) return st;
     if (!ok(launched(emb::launch_coalesce_sort(a->ids, a->T, a->V, a->D, var, a->ws_coalesce, a->dev_status,
                                                S(s->coalesce)))))
@@ -162,8 +172,8 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     if (sep_sr && !ok(order.done(kSorted, s->coalesce))) return st;
     // reduction(s): after the sort, and after the updates of step s - sets have read this set's send buffers
     if (sep_sr && !ok(order.after(s->pack, kSorted, 0))) return st;
-    if (sep_p && !chained && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
-    if (s->split && s->delayed != s->pack && !ok(order.after(s->pack, kDelayedDone, order.sets))) return st;
+    if (!chained && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
+    if (s->split && !ok(order.after(s->pack, kDelayedDone, order.sets))) return st;
     if (!ok(launched(emb::launch_coalesce_reduce(a->ids, a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, var,
                                                  a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
                                                  a->send_counts, a->send_offsets, a->ws_coalesce, a->dev_status,
@@ -175,7 +185,7 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
       // lookup(s): after the delayed update of step s-2 (its rows may be in this
       // batch; those of step s-1 are not, by construction)
       const bool sep_d = s->delayed != s->lookup_update;
-      if (sep_d && !ok(order.after(s->lookup_update, kDelayedDone, 2))) return st;
+      if (!ok(order.after(s->lookup_update, kDelayedDone, 2))) return st;
       if (!ok(record(s->timing[0], s->lookup_update))) return st;
       if (!ok(launched(emb::launch_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status,
                                           S(s->lookup_update), order.attach(kGathered)))))
@@ -184,12 +194,12 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
       if (!ok(record(s->timing[1], s->lookup_update))) return st;
       // prior update(s): the rows the next lookup reads, right after this lookup
       if (sep_p && !ok(order.after(s->lookup_update, kCoalesced, 0))) return st;
-      if (!update(0, s->lookup_update, s->timing[4], s->timing[5], kUpdated, true)) return st;
+      if (!update(0, s->lookup_update, s->timing[4], s->timing[5], kUpdated)) return st;
       // delayed update(s): beside the next lookup (it reads none of these rows),
       // after this step's lookup has read them and the reduction has written them
       if (sep_d && !ok(order.after(s->delayed, kGathered, 0))) return st;
       if (s->delayed != s->pack && !ok(order.after(s->delayed, kCoalesced, 0))) return st;
-      if (!update(a->P, s->delayed, s->timing[6], s->timing[7], kDelayedDone, true)) return st;
+      if (!update(a->P, s->delayed, s->timing[6], s->timing[7], kDelayedDone)) return st;
       return EMB_OK;
     }
     // lookup(s), then update(s) once the rows are reduced
@@ -199,7 +209,7 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     if (sep_p && !ok(order.after(s->lookup_update, kCoalesced, 0))) return st;
   } else {
     // coalesce(s): after pack(s - sets) has read this buffer set's unique rows
-    if (s->coalesce != s->pack && !ok(order.after(s->coalesce, kPacked, order.sets))) return st;
+    if (!ok(order.after(s->coalesce, kPacked, order.sets))) return st;
     if (!ok(record(s->timing[2], s->coalesce))) return st;
     if (!ok(emb_grad_coalesce(a->ids, a->T, a->grad, a->grad_dtype, a->D, a->V, a->uniq_ids, a->seg_offsets,
                               a->uniq_grad, a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes, a->dev_status,
@@ -208,7 +218,7 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     if (!ok(record(s->timing[3], s->coalesce)) || !ok(order.done(kCoalesced, s->coalesce))) return st;
     // pack(s): after coalesce(s), and after update(s - sets) has read this set's send rows
     if (s->pack != s->coalesce && !ok(order.after(s->pack, kCoalesced, 0))) return st;
-    if (sep_p && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
+    if (!ok(order.after(s->pack, kUpdated, order.sets))) return st;
     if (!ok(record(s->timing[4], s->pack))) return st;
     if (!ok(emb_pack_by_owner(a->uniq_ids, a->uniq_grad, a->num_unique, a->cap_rows, a->D, a->row_owner, a->V, a->P,
                               a->send_ids, a->send_rows, a->send_counts, a->send_offsets, a->ws_pack,
@@ -221,8 +231,8 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     if (!ok(record(s->timing[1], s->lookup_update))) return st;
     if (sep_p && !ok(order.after(s->lookup_update, kPacked, 0))) return st;
   }
-  // the pack stream's next use of this set waits for `updated`
-  if (!update(0, s->lookup_update, s->timing[6], s->timing[7], kUpdated, sep_p)) return st;
+  // the next use of this set waits for `updated`
+  if (!update(0, s->lookup_update, s->timing[6], s->timing[7], kUpdated)) return st;
   return EMB_OK;
 }
 

@@ -65,7 +65,8 @@ class EmbeddingTable:
         nb = grad_coalesce_split_workspace_bytes(T_cap, T_cap, self.V, self.D, self.grad_code)  # serves every variant
         self.ws_coalesces = [new_workspace(nb, dev) for _ in range(sets)]
         self.ws_coalesce = self.ws_coalesces[0]
-        self.ws_pack = new_workspace(pack_by_owner_workspace_bytes(T_cap, P), dev)
+        self.ws_packs = [new_workspace(pack_by_owner_workspace_bytes(T_cap, P), dev) for _ in range(sets)]
+        self.ws_pack = self.ws_packs[0]
 
 
 def _stream_handle(s: torch.cuda.Stream) -> int:
@@ -140,7 +141,8 @@ class StepPipeline:
                              send_counts=cnt.data_ptr(), send_offsets=offs.data_ptr(), send_rows=srows.data_ptr(),
                              ws_coalesce=tb.ws_coalesces[i].data_ptr(),
                              ws_coalesce_bytes=tb.ws_coalesces[i].numel(),
-                             ws_pack=tb.ws_pack.data_ptr(), ws_pack_bytes=tb.ws_pack.numel(), lr=lr, beta1=beta1,
+                             ws_pack=tb.ws_packs[i].data_ptr(), ws_pack_bytes=tb.ws_packs[i].numel(), lr=lr,
+                             beta1=beta1,
                              beta2=beta2, eps=eps, dev_status=st)
                 evs = [Event() for _ in range(6)]
                 self.events += evs

@@ -1,9 +1,12 @@
-"""The step executor's cross-stream order with step signals, checked on the host: step.hip is
-linked against stand-ins that record every launch, signal write and wait, and event record and wait per stream, and a
-model of the device runs the recorded work (tests/host_order/order_sim.cpp).  It must never wait
-for a value that no write enqueued before it supplies, never let a signal word decrease, and never
-deadlock: across handles reused between modes, a call that fails part-way, and a long random mix
-of modes and single-stream schedules.  No GPU is used."""
+"""The step executor's cross-stream order, checked on the host: step.hip is linked against stand-ins
+that record every launch, signal write and wait, and event record and wait per stream, and a model of
+the device runs the recorded work (tests/host_order/order_sim.cpp).  It must never wait for a value
+that no write enqueued before it supplies, never let a signal word decrease, and never deadlock:
+across handles reused between modes, a call that fails part-way, and a long random mix of modes and
+single-stream schedules.  With a vector clock per stream it also checks happens-before: every two
+launches that touch the same buffer of a set, or overlapping table rows, one of them writing, run in
+the order the executor enqueued them, for every mode, events and signals, two to six buffer sets, and
+stream choices that include a set's streams changing between its uses.  No GPU is used."""
 import os
 import shutil
 import subprocess
@@ -24,4 +27,5 @@ def test_step_signals_order_model(tmp_path):
     subprocess.run(cmd, check=True, capture_output=True, cwd=str(tmp_path))
     r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
-    assert r.stdout.startswith("ok:"), r.stdout
+    lines = r.stdout.splitlines()
+    assert lines[0].startswith("happens-before:") and lines[-1].startswith("ok:"), r.stdout
