@@ -146,9 +146,10 @@ def _find(directory, suffix):
 
 def summarize_trace(directory, command, skip=20, steps=200, every=20):
     """Text summary of a rocprofv3 --kernel-trace --stats run (kernel_stats.csv), plus the
-    average duration of the update kernel over the timed steps of the bench run (its
+    average duration of the update kernel over the steps of the bench run's roofline window (its
     dispatches skip+1 .. skip+steps in launch order, from kernel_trace.csv; skip counts the
-    untimed steps before them: the order tuning and the warm-up)."""
+    steps before them: the order tuning, the warm-up and the timed steps), every `every`-th of
+    which the bench times with events."""
     trace = [r for r in _read_csv(_find(directory, "kernel_trace.csv")) if ADAM_KERNEL in r["Kernel_Name"]]
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
     durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace[skip:skip + steps]]
@@ -162,9 +163,10 @@ def summarize_trace(directory, command, skip=20, steps=200, every=20):
                    f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):5.1f}%")
     if durs:
         out += ["", f"{ADAM_KERNEL} over the {len(sampled)} launches the bench times with events (every "
-                    f"{every}th timed step): avg {sum(sampled) / len(sampled):.2f} us",
-                f"{ADAM_KERNEL} over the {len(durs)} timed steps (dispatches {skip + 1}..{skip + len(durs)}): "
-                    f"avg {sum(durs) / len(durs):.2f} us, min {min(durs):.2f} us, max {max(durs):.2f} us"]
+                    f"{every}th step of the roofline window): avg {sum(sampled) / len(sampled):.2f} us",
+                f"{ADAM_KERNEL} over the {len(durs)} steps of the roofline window (dispatches {skip + 1}.."
+                    f"{skip + len(durs)}): avg {sum(durs) / len(durs):.2f} us, min {min(durs):.2f} us, "
+                    f"max {max(durs):.2f} us"]
     return "\n".join(out) + "\n"
 
 
@@ -197,6 +199,61 @@ def summarize_pmc(fetch_dir, write_dir, command_fetch, command_write):
             "traffic_bytes_per_launch": fetch_b + write_b,
             "adam_source_sha256_16": source_hash(ADAM_SOURCE),
             "command_fetch": command_fetch, "command_write": command_write}
+
+
+CU_NUM = 256  # MI355X compute units
+
+
+def summarize_counters(dirs, command):
+    """Per-kernel figures from rocprofv3 --pmc runs (counter_collection.csv of each directory; a kernel's
+    counters averaged over its dispatches, which the profiler runs one at a time).  The derived figures
+    follow the profiler's own definitions for gfx950 (CU_NUM = 256):
+      occupancy  mean resident waves per CU: 4 SQ_WAVE_CYCLES / (GRBM_GUI_ACTIVE CU_NUM), of 32
+      VALU busy  100 SQ_ACTIVE_INST_VALU / (CU_NUM GRBM_GUI_ACTIVE)
+      LDS util   100 SQ_LDS_IDX_ACTIVE / (GRBM_GUI_ACTIVE CU_NUM)
+      LDS bank conflict  100 SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE (conflict cycles per LDS-active cycle)
+      L2 hit     100 TCC_HIT / (TCC_HIT + TCC_MISS)
+    plus VALU and LDS instructions per wave and the mean duration of a dispatch under the profiler."""
+    per = {}  # kernel -> counter -> [values]
+    durs = {}
+    for d in dirs:
+        for r in _read_csv(_find(d, "counter_collection.csv")):
+            name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            name = name.replace("void ", "").replace("emb::", "")[:60]
+            per.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            durs.setdefault(name, {})[(d, r["Dispatch_Id"])] = \
+                (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+
+    def mean(k, c):
+        v = per[k].get(c)
+        return sum(v) / len(v) if v else None
+
+    def ratio(a, b, scale=1.0):
+        return None if a is None or not b else scale * a / b
+
+    def fmt(x, w=8, p=1):
+        return f"{'-':>{w}s}" if x is None else f"{x:{w}.{p}f}"
+
+    rows = []
+    for k in per:
+        gui = mean(k, "GRBM_GUI_ACTIVE")
+        waves = mean(k, "SQ_WAVES")
+        hit, miss = mean(k, "TCC_HIT_sum"), mean(k, "TCC_MISS_sum")
+        rows.append((k, len(durs[k]), sum(durs[k].values()) / len(durs[k]), waves,
+                     ratio(mean(k, "SQ_WAVE_CYCLES"), None if gui is None else gui * CU_NUM, 4.0),
+                     ratio(mean(k, "SQ_ACTIVE_INST_VALU"), None if gui is None else gui * CU_NUM, 100.0),
+                     ratio(mean(k, "SQ_LDS_IDX_ACTIVE"), None if gui is None else gui * CU_NUM, 100.0),
+                     ratio(mean(k, "SQ_LDS_BANK_CONFLICT"), mean(k, "SQ_LDS_IDX_ACTIVE"), 100.0),
+                     ratio(hit, None if hit is None or miss is None else hit + miss, 100.0),
+                     ratio(mean(k, "SQ_INSTS_VALU"), waves), ratio(mean(k, "SQ_INSTS_LDS"), waves)))
+    rows.sort(key=lambda r: -r[1] * r[2])
+    out = [f"command: {command}", "",
+           f"{'kernel':60s} {'disp':>5s} {'us':>8s} {'waves':>8s} {'occ/CU':>7s} {'VALU%':>6s} {'LDS%':>6s} "
+           f"{'bankc%':>6s} {'L2hit%':>6s} {'VALUi/w':>8s} {'LDSi/w':>7s}"]
+    for k, n, us, waves, occ, valu, lds, bank, l2, vi, li in rows:
+        out.append(f"{k:60s} {n:5d} {us:8.2f} {fmt(waves, 8, 0)} {fmt(occ, 7, 2)} {fmt(valu, 6)} {fmt(lds, 6)} "
+                   f"{fmt(bank, 6)} {fmt(l2, 6)} {fmt(vi, 8)} {fmt(li, 7)}")
+    return "\n".join(out) + "\n"
 
 
 XGMI_LINK_GBPS = 153.0  # one MI355X xGMI link, per direction (one link per peer in an 8-GPU node)
@@ -378,9 +435,13 @@ def cost_model_report(emb, sp, U, N=8):
 
 
 def schedule_candidates(args):
-    """(cross-stream order, buffer sets) pairs the bench chooses among: those the options leave open."""
+    """(cross-stream order, buffer sets, paired) triples the bench chooses among: those the options leave
+    open (--candidate names one)."""
     if args.sequential:
         return [("events", 2, False)]
+    if args.candidate:
+        parts = args.candidate.split("/")
+        return [(parts[0], int(parts[1]), len(parts) > 2 and parts[2] == "paired")]
     orders = ("events", "signals") if args.order == "auto" else (args.order,)
     sets = (2, 4) if args.sets == 0 else (args.sets,)
     # with events the split needs two sets (its lookup waits for the delayed update two steps back)
@@ -390,6 +451,10 @@ def schedule_candidates(args):
     if args.schedule == "by_owner":
         cands += [(o, 4, True) for o in orders if 4 in sets]
     return cands
+
+
+def cand_name(c):
+    return f"{c[0]}/{c[1]} sets{'/paired' if c[2] else ''}"
 
 
 def host_info():
@@ -405,6 +470,258 @@ def host_info():
     return dict(cpu=model, nproc=os.cpu_count())
 
 
+def spread(xs):
+    """Median, 10th and 90th percentile of a list of times."""
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median": float(np.median(a)), "p10": float(np.percentile(a, 10)),
+            "p90": float(np.percentile(a, 90)), "n": int(a.size)}
+
+
+FLUSH_BYTES = 1 << 30  # written between the steps of the cold runs: four times the 256 MB last-level cache
+
+
+class WorkloadRun:
+    """One workload resident on the GPU: its tables (W, Adam moments, four buffer sets), `nbatches`
+    pre-generated batches of every table, and each batch's distinct and prior row counts (taken with
+    the library before any timing; the next batch of the split is the next one in the rotation)."""
+
+    def __init__(self, torch, emb, wl, nbatches, schedule):
+        from paper_2110_09132_amd.step import EmbeddingTable
+        from workloads import configs
+        self.torch, self.emb, self.wl = torch, emb, wl
+        self.nb = nbatches
+        self.split = schedule == "split"
+        self.by_owner = schedule != "unfused"
+        self.schedule = schedule
+        self.t = 0  # Adam step counter, advanced by every step enqueued on the tables
+        dev = "cuda"
+        self.tables, batches = [], []
+        for sp in wl.tables:
+            gdt = torch.bfloat16 if sp.grad_dtype == "bf16" else torch.float32
+            W = torch.from_numpy(configs.make_weights(sp)).to(dev)
+            self.tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).to(dev), sp.P, sp.T, gdt,
+                                              sets=4))
+            tb_batches = []
+            for b in range(nbatches):
+                ids, G = configs.make_batch(sp, 1000 + b)
+                g = torch.from_numpy(G.view(np.int16)).to(dev).view(torch.bfloat16) if sp.grad_dtype == "bf16" \
+                    else torch.from_numpy(G).to(dev)
+                tb_batches.append((torch.from_numpy(ids).to(dev), g))
+            batches.append(tb_batches)
+        self.step_batches = [[batches[k][b] for k in range(len(self.tables))] for b in range(nbatches)]
+        nt = len(self.tables)
+        self.U = [[0] * nt for _ in range(nbatches)]
+        self.U_prior = [[0] * nt for _ in range(nbatches)]
+        self.owner_rows = [None] * nbatches  # rows per owner of the first table (prior + delayed)
+        for b in range(nbatches):
+            for k, tb in enumerate(self.tables):
+                ids, g = self.step_batches[b][k]
+                nxt = self.step_batches[(b + 1) % nbatches][k][0]
+                out = emb.grad_coalesce_split(ids, nxt, g, tb.V, tb.row_owner, tb.P, workspace=tb.ws_coalesce)
+                torch.cuda.synchronize()
+                self.U[b][k] = int(out[5].item())
+                self.U_prior[b][k] = int(out[4][tb.P].item())
+                if k == 0:
+                    self.owner_rows[b] = out[3].view(2, tb.P).sum(0).cpu().numpy()
+
+    def make_pipe(self, cand, sequential=False):
+        from paper_2110_09132_amd.step import StepPipeline
+        wl = self.wl
+        if sequential:
+            return StepPipeline(self.tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=False,
+                                by_owner=self.by_owner, split=self.split)
+        order, sets, paired = cand
+        return StepPipeline(self.tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=True, by_owner=self.by_owner,
+                            split=self.split, signals=order == "signals",
+                            sort_streams=2 if (sets == 4 and self.by_owner and not self.split) else 1, sets=sets,
+                            paired=paired)
+
+    def next_ids(self, t):
+        return [x[0] for x in self.step_batches[(t + 1) % self.nb]] if self.split else None
+
+    def step(self, pipe, timing=None):
+        """Enqueue the next step; returns the index of the batch it used."""
+        self.t += 1
+        b = self.t % self.nb
+        pipe.step(self.step_batches[b], self.t, timing=timing, next_ids=self.next_ids(self.t))
+        return b
+
+    def settle(self, pipe):
+        pipe.finish()
+        self.torch.cuda.synchronize()
+
+    def tune(self, cands, tune_steps):
+        """Time `tune_steps` untimed steps of each candidate schedule (after 5 more) and keep the fastest.
+        Events cost the GPU nothing but the host tens of microseconds per overlapped step; step signals
+        halve the host's cost but add small runtime kernels to the streams.  Four sets (sorts on two
+        streams) free the sorts of latency-bound steps; two interfere less with the bandwidth-bound ones."""
+        tune_ms = {}
+        if len(cands) == 1:
+            return cands[0], tune_ms
+        for c in cands:
+            trial = self.make_pipe(c)
+            for k in range(5 + tune_steps):
+                if k == 5:
+                    self.settle(trial)
+                    t_start = time.perf_counter()
+                self.step(trial)
+            self.settle(trial)
+            tune_ms[cand_name(c)] = (time.perf_counter() - t_start) * 1e3 / tune_steps
+            del trial
+        best = min(range(len(cands)), key=lambda i: tune_ms[cand_name(cands[i])])
+        return cands[best], tune_ms
+
+    def timed(self, pipe, K, time_every):
+        """Exactly K steps between two synchronisations, timed with events on the main stream; the update
+        kernel of the first table is timed on its own stream (a pair of events attached to its dispatch)
+        on every time_every-th step (0: on none; each pair costs the step about 9 us)."""
+        torch, emb = self.torch, self.emb
+        main = torch.cuda.current_stream()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        timed_steps = [s for s in range(K) if time_every > 0 and s % time_every == 0]
+        adam_ev = {s: (emb.Event(timing=True), emb.Event(timing=True)) for s in timed_steps}
+        used = []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        start.record(main)
+        for s in range(K):
+            used.append(self.step(pipe, timing={"adam": adam_ev[s]} if s in adam_ev else None))
+        pipe.finish()
+        end.record(main)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms_total = start.elapsed_time(end)
+        adam_us = [1e3 * adam_ev[s][0].elapsed_ms(adam_ev[s][1]) for s in timed_steps]
+        rows = sum(sum(self.U[b]) for b in used)
+        return dict(ms_total=ms_total, wall=wall, used=used, rows=rows, adam_us=adam_us,
+                    adam_steps=timed_steps)
+
+    def sequential(self, n, cold):
+        """n steps one after another on one stream, an event pair around each step and each stage.  cold:
+        a 1 GiB buffer is written between the steps, outside the events, so that each step starts with
+        the caches (L2 and the last-level cache) holding none of its data."""
+        torch, emb = self.torch, self.emb
+        main = torch.cuda.current_stream()
+        stages = ("gather", "coalesce", "pack", "adam") if (self.split or not self.by_owner) else \
+            ("gather", "coalesce", "adam")
+        seq = self.make_pipe(None, sequential=True)
+        flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device="cuda") if cold else None
+        evs = []
+        for s in range(n):
+            if flush is not None:
+                flush.fill_(s)
+            ev = {k: (emb.Event(timing=True), emb.Event(timing=True)) for k in stages}
+            s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s0.record(main)
+            b = self.step(seq, timing=ev)
+            s1.record(main)
+            evs.append((b, s0, s1, ev))
+            if s % 25 == 24:  # bounded numbers of live events
+                torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        step_ms = [s0.elapsed_time(s1) for _, s0, s1, _ in evs]
+        stage_ms = {k: [ev[k][0].elapsed_ms(ev[k][1]) for _, _, _, ev in evs] for k in stages}
+        if self.split:  # the timing pairs' names under the split
+            stage_ms = {"gather": stage_ms["gather"], "coalesce": stage_ms["coalesce"],
+                        "update_prior": stage_ms["pack"], "update_delayed": stage_ms["adam"]}
+        used = [b for b, _, _, _ in evs]
+        del flush
+        return dict(step_ms=step_ms, stage_ms=stage_ms, used=used)
+
+    def step_bytes(self, used):
+        """Mean algorithmic bytes per step (per stage) over the batches `used`."""
+        out = {k: 0.0 for k in ("gather", "coalesce", "pack", "adam")}
+        for b in used:
+            for k, tb in enumerate(self.tables):
+                sp = self.wl.tables[k]
+                bm = byte_model(sp.T, self.U[b][k], sp.D, 2 if sp.grad_dtype == "bf16" else 4, sp.P, self.by_owner,
+                                sp.T if self.split else 0)
+                for name in out:
+                    out[name] += bm[name] / len(used)
+        return out
+
+    def update_bytes(self, b):
+        """Algorithmic bytes of the first table's update launch of batch b (with the split: the delayed part)."""
+        sp0 = self.wl.tables[0]
+        rows = self.U[b][0] - (self.U_prior[b][0] if self.split else 0)
+        return byte_model(sp0.T, rows, sp0.D, 4, sp0.P)["adam"]
+
+    def release(self):
+        del self.tables, self.step_batches
+        self.torch.cuda.synchronize()
+        self.torch.cuda.empty_cache()
+
+
+def sequential_report(run, n):
+    """Warm and cold figures of the step run call after call on one stream (median, p10, p90 over n
+    steps): the step, each call, and the step's effective bandwidth at the median."""
+    out = {}
+    for kind, cold in (("warm", False), ("cold", True)):
+        r = run.sequential(n, cold)
+        nbytes = sum(run.step_bytes(r["used"]).values())
+        st = spread(r["step_ms"])
+        out[kind] = {"step_ms": st, "stage_ms": {k: spread(v) for k, v in r["stage_ms"].items()},
+                     "step_hbm_frac_at_median": nbytes / (st["median"] * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+    out["flush_bytes_cold"] = FLUSH_BYTES
+    return out
+
+
+def pipelined_report(run, args, K):
+    """Tune the schedule, warm up, then exactly K timed steps (no event pairs among them); then the
+    roofline window: --roofline-steps more steps of the same schedule, the update kernel timed with
+    events attached to its dispatch on every --roofline-every-th of them.  The step figures and the
+    update kernel's live duration.  With --sequential: one stream, calls one after another."""
+    cands = schedule_candidates(args)
+    cand, tune_ms = run.tune(cands, args.tune_steps)
+    pipe = run.make_pipe(cand, sequential=args.sequential)
+    for _ in range(args.warmup):
+        run.step(pipe)
+    run.settle(pipe)
+    r = run.timed(pipe, K, 0)
+    w = run.timed(pipe, args.roofline_steps, args.roofline_every)
+    ms_step = r["ms_total"] / K
+    bytes_step = run.step_bytes(r["used"])
+    total = sum(bytes_step.values())
+    adam_us = float(np.mean(w["adam_us"]))
+    adam_bytes = float(np.mean([run.update_bytes(w["used"][s]) for s in w["adam_steps"]]))
+    del pipe
+    return dict(cand=cand, tune_ms=tune_ms, ms_step=ms_step, ms_total=r["ms_total"], wall=r["wall"],
+                rows=r["rows"], used=r["used"], bytes_step=bytes_step, total_bytes=total,
+                step_gbps=total / (ms_step * 1e-3) / 1e9, adam_us=adam_us, adam_us_all=w["adam_us"],
+                adam_bytes=adam_bytes, adam_gbps=adam_bytes / (adam_us * 1e-6) / 1e9,
+                window_ms_step=w["ms_total"] / args.roofline_steps)
+
+
+def config_report(torch, emb, name, args, K, run=None, pl=None):
+    """One workload's entry of the `configs` object: pipelined steps (tuned schedule), the update
+    kernel's live duration, and the sequential warm and cold spreads."""
+    from workloads import configs
+    wl = configs.WORKLOADS[name]
+    own = run is None
+    if own:
+        log(f"config {name}: {wl.description}")
+        run = WorkloadRun(torch, emb, wl, args.batches, args.schedule)
+        pl = pipelined_report(run, args, K)
+    seqr = sequential_report(run, args.seq_steps)
+    entry = {
+        "tables": [dict(V=sp.V, D=sp.D, T=sp.T, P=sp.P, ids=sp.id_law + (f" s={sp.zipf_s}" if sp.id_law == "zipf"
+                                                                          else ""), owner=sp.owner_rule,
+                        grad=sp.grad_dtype) for sp in wl.tables],
+        "schedule": cand_name(pl["cand"]), "timed_steps": K,
+        "ms_per_step": pl["ms_step"], "unique_rows_per_s": pl["rows"] / (pl["ms_total"] * 1e-3),
+        "mean_unique_rows_per_step": pl["rows"] / K,
+        "step_bytes_model": pl["total_bytes"], "step_hbm_GBps": pl["step_gbps"],
+        "step_hbm_frac": pl["step_gbps"] / HBM_PEAK_GBPS,
+        "update_kernel": {"avg_launch_us": pl["adam_us"], "launches_timed": len(pl["adam_us_all"]),
+                          "bytes_per_launch": pl["adam_bytes"], "GBps": pl["adam_gbps"],
+                          "frac": pl["adam_gbps"] / HBM_PEAK_GBPS},
+        "sequential": seqr,
+    }
+    if own:
+        run.release()
+    return entry
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -412,7 +729,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="lowdup_uniform")
     ap.add_argument("--batches", type=int, default=8)
-    ap.add_argument("--time-every", type=int, default=20, help="time the update kernel on every n-th timed step")
+    ap.add_argument("--roofline-steps", type=int, default=200,
+                    help="steps of the roofline window that follows the timed steps")
+    ap.add_argument("--roofline-every", type=int, default=10,
+                    help="time the update kernel on every n-th step of the roofline window")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one stream, calls one after another")
@@ -427,21 +747,35 @@ def main():
     ap.add_argument("--order", choices=("auto", "signals", "events"), default="auto",
                     help="cross-stream order of the overlapped schedule: step signals (stream memory operations), "
                          "events, or auto (tuned)")
+    ap.add_argument("--candidate", default="",
+                    help="one schedule, ORDER/SETS[/paired] (e.g. events/4/paired): no tuning")
     ap.add_argument("--tune-steps", type=int, default=30)
+    ap.add_argument("--seq-steps", type=int, default=100,
+                    help="steps of each sequential (warm, cold) run of the timing protocol")
+    ap.add_argument("--config-steps", type=int, default=100,
+                    help="timed steps of each workload of the `configs` object (at least --steps)")
+    ap.add_argument("--only-steps", action="store_true",
+                    help="tuning, warm-up and the timed steps only (for profiler runs)")
+    ap.add_argument("--no-configs", action="store_true", help="leave out the `configs` object")
     ap.add_argument("--summarize-trace", metavar="DIR", help="print a summary of a rocprofv3 kernel-stats run")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the scaled HBM traffic of the update kernel from two rocprofv3 --pmc runs")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="DIR",
+                    help="print per-kernel occupancy, VALU, LDS and L2 figures from rocprofv3 --pmc runs")
     ap.add_argument("--command", default="", help="the command recorded in a summary")
     ap.add_argument("--command2", default="", help="the second command recorded in a summary")
     args = ap.parse_args()
     if args.summarize_trace:
-        tuned = len(schedule_candidates(args)) * (5 + args.tune_steps) if not args.sequential else 0
-        tuned = tuned if tuned > 5 + args.tune_steps else 0
-        print(summarize_trace(args.summarize_trace, args.command, tuned + args.warmup, args.steps, args.time_every),
-              end="")
+        n = len(schedule_candidates(args))
+        tuned = n * (5 + args.tune_steps) if n > 1 else 0
+        print(summarize_trace(args.summarize_trace, args.command, tuned + args.warmup + args.steps,
+                              args.roofline_steps, args.roofline_every), end="")
         return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc, args.command, args.command2), indent=1))
+        return
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters, args.command), end="")
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -453,181 +787,39 @@ def main():
     import torch
 
     import paper_2110_09132_amd as emb
-    from paper_2110_09132_amd.step import EmbeddingTable, StepPipeline
     from workloads import configs
 
     wl = configs.WORKLOADS[args.workload]
     log(f"workload {wl.name}: {wl.description}")
-    dev = "cuda"
-    tables, batches = [], []
-    for sp in wl.tables:
-        gdt = torch.bfloat16 if sp.grad_dtype == "bf16" else torch.float32
-        W = torch.from_numpy(configs.make_weights(sp)).to(dev)
-        tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).to(dev), sp.P, sp.T, gdt,
-                                     sets=4))
-        tb_batches = []
-        for b in range(args.batches):
-            ids, G = configs.make_batch(sp, 1000 + b)
-            g = torch.from_numpy(G.view(np.int16)).to(dev).view(torch.bfloat16) if sp.grad_dtype == "bf16" \
-                else torch.from_numpy(G).to(dev)
-            tb_batches.append((torch.from_numpy(ids).to(dev), g))
-        batches.append(tb_batches)
-    step_batches = [[batches[k][b] for k in range(len(tables))] for b in range(args.batches)]
+    run = WorkloadRun(torch, emb, wl, args.batches, args.schedule)
+    pl = pipelined_report(run, args, args.steps)
+    order, nsets, paired = pl["cand"]
+    log(f"schedule: {cand_name(pl['cand'])} {pl['tune_ms'] or ''}")
+    log(f"timed {args.steps} steps: {pl['ms_step']:.4f} ms/step")
+    split, by_owner = run.split, run.by_owner
+    used = pl["used"]
+    U, U_prior = run.U, run.U_prior
+    ms_step = pl["ms_step"]
 
-    # unique and prior row counts of each batch (the next batch is the next one in rotation),
-    # outside any timed region
-    U = [[0] * len(tables) for _ in range(args.batches)]
-    U_prior = [[0] * len(tables) for _ in range(args.batches)]
-    owner_rows = [None] * args.batches  # rows per owner of the first table (prior + delayed)
-    for b in range(args.batches):
-        for k, tb in enumerate(tables):
-            ids, g = step_batches[b][k]
-            nxt = step_batches[(b + 1) % args.batches][k][0]
-            out = emb.grad_coalesce_split(ids, nxt, g, tb.V, tb.row_owner, tb.P, workspace=tb.ws_coalesce)
-            torch.cuda.synchronize()
-            U[b][k] = int(out[5].item())
-            U_prior[b][k] = int(out[4][tb.P].item())
-            if k == 0:
-                owner_rows[b] = out[3].view(2, tb.P).sum(0).cpu().numpy()
-
-    split = args.schedule == "split"
-    by_owner = args.schedule != "unfused"
-    def make_pipe(cand):
-        order, sets, paired = cand
-        return StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=not args.sequential,
-                            by_owner=by_owner, split=split, signals=order == "signals",
-                            sort_streams=2 if (sets == 4 and by_owner and not split) else 1, sets=sets,
-                            paired=paired)
-
-    def next_ids(t):
-        return [x[0] for x in step_batches[(t + 1) % args.batches]] if split else None
-
-    t = 0
-    # the schedule: time a few untimed steps of each candidate (cross-stream order x buffer sets)
-    # and keep the fastest.  Events cost the GPU nothing but the host ~85 us per overlapped step;
-    # step signals halve the host's cost but add small runtime kernels to the streams.  Four sets
-    # (sorts on two streams) free the sorts of latency-bound steps; two interfere less with the
-    # bandwidth-bound ones.
-    tune_ms = {}
-    cands = schedule_candidates(args)
-    cand = cands[0]
-    if len(cands) > 1:
-        for c in cands:
-            trial = make_pipe(c)
-            for k in range(5 + args.tune_steps):
-                if k == 5:
-                    trial.finish()
-                    torch.cuda.synchronize()
-                    t_start = time.perf_counter()
-                t += 1
-                trial.step(step_batches[t % args.batches], t, next_ids=next_ids(t))
-            trial.finish()
-            torch.cuda.synchronize()
-            tune_ms[f"{c[0]}/{c[1]} sets{'/paired' if c[2] else ''}"] = \
-                (time.perf_counter() - t_start) * 1e3 / args.tune_steps
-            del trial
-        cand = cands[min(range(len(cands)), key=lambda i: list(tune_ms.values())[i])]
-    order, nsets, paired = cand
-    log(f"schedule: {order}, {nsets} buffer sets{', paired' if paired else ''} {tune_ms or ''}")
-    pipe = make_pipe(cand)
-    for _ in range(args.warmup):
-        t += 1
-        pipe.step(step_batches[t % args.batches], t, next_ids=next_ids(t))
-    pipe.finish()
-    torch.cuda.synchronize()
-
-    # timed region: exactly K steps; the update's duration is recorded on its own stream
-    main = torch.cuda.current_stream()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    # the update's own duration, on its stream, on every time_every-th step (an event pair
-    # costs the stream a few microseconds of idle time)
-    timed = [s for s in range(args.steps) if s % args.time_every == 0]
-    adam_ev = {s: (emb.Event(timing=True), emb.Event(timing=True)) for s in timed}
-    rows, used = 0, []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start.record(main)
-    for s in range(args.steps):
-        t += 1
-        b = t % args.batches
-        pipe.step(step_batches[b], t, timing={"adam": adam_ev[s]} if s in adam_ev else None, next_ids=next_ids(t))
-        rows += sum(U[b])
-        used.append(b)
-    pipe.finish()
-    end.record(main)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_total = start.elapsed_time(end)
-    log(f"timed {args.steps} steps: {ms_total / args.steps:.4f} ms/step")
-    ms_step = ms_total / args.steps
-    adam_us = 1e3 * sum(a.elapsed_ms(z) for a, z in adam_ev.values()) / len(adam_ev)
-
-    # per-stage breakdown: the same steps run one call after another on one stream (with the
-    # split, the "pack" pair of timing events times the prior update, "adam" the delayed one)
-    seq = StepPipeline(tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=False, by_owner=by_owner, split=split)
-    stage_ms = {k: 0.0 for k in (("gather", "coalesce", "pack", "adam") if split or not by_owner
-                                 else ("gather", "coalesce", "adam"))}
-    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    seq_total = 0.0
-    for s in range(args.steps):
-        t += 1
-        ev = {k: (emb.Event(timing=True), emb.Event(timing=True)) for k in stage_ms}
-        s0.record(main)
-        seq.step(step_batches[t % args.batches], t, timing=ev, next_ids=next_ids(t))
-        s1.record(main)
-        torch.cuda.synchronize()
-        seq_total += s0.elapsed_time(s1) / args.steps
-        for k in stage_ms:
-            stage_ms[k] += ev[k][0].elapsed_ms(ev[k][1]) / args.steps
-
-    if split:  # name the timing pairs for what they time under the split
-        stage_ms = {"gather": stage_ms["gather"], "coalesce": stage_ms["coalesce"],
-                    "update_prior": stage_ms["pack"], "update_delayed": stage_ms["adam"]}
-
-    log("per-stage breakdown done; copy reference, column partition, cost model ...")
-    copy_gbps = copy_reference(torch)
-    column = column_partition_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches],
-                                     [U[b][0] for b in range(args.batches)], owner_rows)
-    cost = cost_model_report(emb, wl.tables[0], [U[b][0] for b in range(args.batches)])
-    forward = forward_exchange_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches],
-                                      [U[b][0] for b in range(args.batches)])
-    exchange = exchange_report(torch, emb, wl.tables[0], tables[0], [x[0] for x in step_batches])
-
-    # algorithmic bytes of the timed steps
-    bytes_step = {k: 0.0 for k in ("gather", "coalesce", "pack", "adam")}
-    for b in used:
-        for k, tb in enumerate(tables):
-            sp = wl.tables[k]
-            bm = byte_model(sp.T, U[b][k], sp.D, 2 if sp.grad_dtype == "bf16" else 4, sp.P, by_owner,
-                            sp.T if split else 0)
-            for name in bytes_step:
-                bytes_step[name] += bm[name] / args.steps
-    total_bytes = sum(bytes_step.values())
-    step_gbps = total_bytes / (ms_step * 1e-3) / 1e9
-    # the roofline kernel: the update launch of the first table (with the split, its delayed part,
-    # the larger one), every time_every-th step
-    sp0 = wl.tables[0]
-    upd_rows = [U[used[s]][0] - (U_prior[used[s]][0] if split else 0) for s in timed]
-    adam_bytes = sum(byte_model(sp0.T, r, sp0.D, 4, sp0.P)["adam"] for r in upd_rows) / len(timed)
-    adam_gbps = adam_bytes / (adam_us * 1e-6) / 1e9
     # sizes of the sparse gradient as Table 3 reports them (per step, all tables): the per-token
     # COO gradient (original), after COALESCE (coalesced), and the prior part of the vertical split
     # (prioritized: rows whose id is in the next batch, the part that must arrive before the next
     # forward pass); ids int32, rows in the gradient's element type
     def mb(rows, sp):
         return rows * (4 + sp.D * (2 if sp.grad_dtype == "bf16" else 4)) / 1e6
+    nt, nb = len(run.tables), args.batches
     orig = sum(mb(sp.T, sp) for sp in wl.tables)
-    coal = sum(mb(U[b][k], wl.tables[k]) for b in range(args.batches) for k in range(len(tables))) / args.batches
-    prio = sum(mb(U_prior[b][k], wl.tables[k]) for b in range(args.batches) for k in range(len(tables))) / args.batches
+    coal = sum(mb(U[b][k], wl.tables[k]) for b in range(nb) for k in range(nt)) / nb
+    prio = sum(mb(U_prior[b][k], wl.tables[k]) for b in range(nb) for k in range(nt)) / nb
     table3 = {"original_MB": orig, "coalesced_MB": coal, "prioritized_MB": prio,
               "reduction_by_coalescing": 1 - coal / orig, "further_reduction_by_prioritizing": 1 - prio / coal,
               "next_batch": "the next batch of the rotation"}
-    prior_frac = sum(U_prior[b][k] for b in used for k in range(len(tables))) / max(1, sum(
-        U[b][k] for b in used for k in range(len(tables))))
+    prior_frac = sum(U_prior[b][k] for b in used for k in range(nt)) / max(1, sum(
+        U[b][k] for b in used for k in range(nt)))
 
     result = {
         "metric": "unique grad rows/sec for coalesce+pack+update; achieved HBM GB/s vs peak",
-        "value": rows / (ms_total * 1e-3),
+        "value": pl["rows"] / (pl["ms_total"] * 1e-3),
         "unit": "unique grad rows/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -641,7 +833,7 @@ def main():
         "config": {"workload": wl.name,
                    "tables": [dict(V=sp.V, D=sp.D, T=sp.T, P=sp.P, ids=sp.id_law, owner=sp.owner_rule)
                               for sp in wl.tables],
-                   "mean_unique_rows_per_step": rows / args.steps, "batches_rotated": args.batches,
+                   "mean_unique_rows_per_step": pl["rows"] / args.steps, "batches_rotated": args.batches,
                    "coalesce": {"split": "emb_grad_coalesce_split (owner-major, prior/delayed split)",
                                 "by_owner": "emb_grad_coalesce_by_owner (coalesce straight into the send layout)",
                                 "unfused": "emb_grad_coalesce + emb_pack_by_owner"}[args.schedule],
@@ -657,33 +849,63 @@ def main():
                    "cross_stream_order": None if args.sequential else
                    {"signals": "step signals (hipStreamWriteValue32 / hipStreamWaitValue32)",
                     "events": "events (hipEventRecord / hipStreamWaitEvent)"}[order],
-                   "schedule_tuning_ms_per_step": tune_ms or None,
+                   "schedule_tuning_ms_per_step": pl["tune_ms"] or None,
                    "prior_rows_frac": prior_frac if split else None},
-        "step_bytes_model": total_bytes,
+        "step_bytes_model": pl["total_bytes"],
         "step_bytes_model_kind": "fused minimum (pack folded into coalesce)" if by_owner else "four calls",
-        "stage_bytes_model": bytes_step,
-        "step_hbm_GBps": step_gbps,
-        "step_hbm_frac": step_gbps / HBM_PEAK_GBPS,
-        "sequential_ms_per_step": seq_total,
-        "stage_ms_sequential": stage_ms,
-        "wall_s_timed": wall,
+        "stage_bytes_model": pl["bytes_step"],
+        "step_hbm_GBps": pl["step_gbps"],
+        "step_hbm_frac": pl["step_gbps"] / HBM_PEAK_GBPS,
+        "wall_s_timed": pl["wall"],
         "roofline": {"bound": "hbm",
                      "kernel": "adam_kernel (emb_sparse_adam_apply)" + (", delayed rows" if split else ""),
-                     "achieved": adam_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": adam_gbps / HBM_PEAK_GBPS,
+                     "achieved": pl["adam_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": pl["adam_gbps"] / HBM_PEAK_GBPS,
                      "traffic": measured_traffic() if args.workload == "lowdup_uniform" else None,
-                     "bytes_per_launch": adam_bytes, "avg_launch_us": adam_us,
-                     "launches_timed": len(adam_ev)},
-        "copy_GBps": copy_gbps,
+                     "bytes_per_launch": pl["adam_bytes"], "avg_launch_us": pl["adam_us"],
+                     "launches_timed": len(pl["adam_us_all"]),
+                     "launch_us_spread": spread(pl["adam_us_all"]),
+                     "window": f"{args.roofline_steps} steps after the timed ones, same schedule, the update "
+                               f"timed on every {args.roofline_every}th",
+                     "window_ms_per_step": pl["window_ms_step"]},
         "gradient_sizes_table3": table3,
-        "column_partition": column,
-        "forward_exchange": forward,
-        "gradient_exchange": exchange,
-        "comm_cost_model": cost,
-        "step_frac_of_copy": step_gbps / copy_gbps,
         "host": host_info(),
     }
-    if not args.no_cpu_baseline:
+    if not args.only_steps:
+        log("sequential warm and cold runs ...")
+        seqr = sequential_report(run, args.seq_steps)
+        result["timing_protocol"] = seqr
+        result["stage_ms_sequential"] = {k: v["median"] for k, v in seqr["warm"]["stage_ms"].items()}
+        result["sequential_ms_per_step"] = seqr["warm"]["step_ms"]["median"]
+        log("copy reference, column partition, cost model, exchanges ...")
+        copy_gbps = copy_reference(torch)
+        sp0, tb0 = wl.tables[0], run.tables[0]
+        batches0 = [x[0] for x in run.step_batches]
+        U0 = [U[b][0] for b in range(nb)]
+        result["copy_GBps"] = copy_gbps
+        result["step_frac_of_copy"] = pl["step_gbps"] / copy_gbps
+        result["column_partition"] = column_partition_report(torch, emb, sp0, tb0, batches0, U0, run.owner_rows)
+        result["forward_exchange"] = forward_exchange_report(torch, emb, sp0, tb0, batches0, U0)
+        result["gradient_exchange"] = exchange_report(torch, emb, sp0, tb0, batches0)
+        result["comm_cost_model"] = cost_model_report(emb, sp0, U0)
+        if not args.no_configs and not args.sequential:
+            # every workload, at least config_steps timed steps each (the headline workload again,
+            # in a fresh run, unless its timed steps were that many)
+            K = max(args.steps, args.config_steps)
+            reuse = K == args.steps
+            if not reuse:
+                run.release()
+                run = None
+            cfgs = {}
+            for name in configs.WORKLOADS:
+                if reuse and name == wl.name:
+                    cfgs[name] = config_report(torch, emb, name, args, K, run=run, pl=pl)
+                else:
+                    cfgs[name] = config_report(torch, emb, name, args, K)
+            result["configs"] = cfgs
+    if run is not None:
+        run.release()
+    if not args.no_cpu_baseline and not args.only_steps:
         log("timing the CPU oracle ...")
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -87,7 +87,8 @@ def check_pack(coal_dev, U, row_owner_np, P):
 
 def check_adam(state_dev, pack_dev, P, shard_begin, shard_end, hp, step, rtol=tolerance.RTOL_F32):
     """GPU Adam vs the oracle on identical inputs (the GPU's pre-call state of the
-    touched rows and the GPU pack output).  Rows not listed must stay bit-identical."""
+    touched rows and the GPU pack output): W, m, v rows, and the update W_after - W_before on
+    its own scale.  Rows not listed must stay bit-identical."""
     W, M, S = state_dev
     send_ids, send_rows, _, offs = pack_dev
     offs_h = host(offs)
@@ -103,13 +104,15 @@ def check_adam(state_dev, pack_dev, P, shard_begin, shard_end, hp, step, rtol=to
     assert int(st.item()) == 0
     # oracle on a compact table holding just the touched rows
     n = rid.size
-    Wc, Mc, Sc = (np.ascontiguousarray(b.reshape(n, -1)) for b in before)
+    Wc, Mc, Sc = (np.array(b.reshape(n, -1), copy=True) for b in before)  # `before` stays as it was
     oracle.sparse_adam(Wc, Mc, Sc, np.arange(n, dtype=np.int32), rows_h, np.array([0, n], np.int32), 0, 1,
                        hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], step)
     idx = torch.from_numpy(rid).to(DEV)
     ratios = []
     for t, ref, name in ((W, Wc, "table"), (M, Mc, "exp_avg"), (S, Sc, "exp_avg_sq")):
         ratios.append(tolerance.assert_rows_close(host(t[idx]), ref, rtol, name))
+    # the update itself, on its own scale (Sec. 5.7; Kingma & Ba, Algorithm 1)
+    ratios.append(tolerance.assert_update_close(host(W[idx]), before[0], Wc, rtol, what="table update"))
     mask = torch.ones(W.shape[0], dtype=torch.bool, device=DEV)
     mask[idx] = False
     for t, s in zip((W, M, S), snap):

@@ -15,7 +15,7 @@ import oracle
 import paper_2110_09132_amd as emb
 import tolerance
 from gpu_helpers import host, to_dev
-from workloads import gen
+from workloads import configs, gen
 
 pytestmark = pytest.mark.gpu
 
@@ -104,6 +104,18 @@ def test_by_owner_parity_bf16(V, T, D, P):
     ids = ids_for("zipf", V + T, T, V, 1.0)
     G = grads_for(V + D, T, D, 0.01, bf16=True)
     check_by_owner(ids, G, V, gen.owner_range(V, P), P, bf16=True)
+
+
+@pytest.mark.parametrize("name", ["tiny", "transformer_shared_vocab", "two_table_translation",
+                                  "lm_large_vocab_bf16", "lowdup_zipf13"])
+def test_by_owner_workload_full_shape(name):
+    """The call the benchmark's steps make, on each workload's own batches at full shape, every table:
+    rows of 512 fp32 (shared vocabulary), 1024 fp32 (two tables), 1024 bf16 (large vocabulary)."""
+    wl = configs.WORKLOADS[name]
+    for k, sp in enumerate(wl.tables):
+        print(f"[{name}] table {k}: V={sp.V} D={sp.D} T={sp.T} P={sp.P} {sp.owner_rule}", flush=True)
+        ids, G = configs.make_batch(sp, 900 + k)
+        check_by_owner(ids, G, sp.V, configs.row_owner(sp), sp.P, bf16=sp.grad_dtype == "bf16")
 
 
 def test_by_owner_hot_row_spans_many_chunks():

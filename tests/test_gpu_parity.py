@@ -9,6 +9,7 @@ import torch
 import oracle
 import paper_2110_09132_amd as emb
 import tolerance
+from adam_inputs import eps_regime_grads
 from gpu_helpers import (check_adam, check_coalesce, check_pack, gpu_coalesce, gpu_gather, host, to_dev)
 from workloads import gen
 
@@ -217,6 +218,25 @@ def test_adam_parity_multi_step_by_shard(D):
         pk = check_pack(gpu["dev"], gpu["U"], own, P)
         for s in range(P):  # each simulated owner applies its own block
             check_adam(state, pk["dev"], P, s, s + 1, HP, step)
+
+
+@pytest.mark.parametrize("D", [1, 4, 64, 256, 1024])
+def test_adam_eps_regime(D):
+    """Gradients where the placement of eps decides the update (|g| near eps / sqrt(1 - b2^t)), zero
+    gradients and whole zero rows, over three steps on the same rows, some rows skipped at step 2
+    (lazy moments): each call against the oracle on the GPU's own pre-call state, W, m, v and the
+    update W_after - W_before on its own scale (Sec. 5.7; Kingma & Ba, Algorithm 1)."""
+    print(f"adam eps regime D={D}", flush=True)
+    rng = np.random.default_rng(D)
+    V, n = 3000, 700
+    W0 = rng.normal(0.0, 1.0, (V, D)).astype(np.float32)
+    state = [to_dev(W0), torch.zeros((V, D), device="cuda"), torch.zeros((V, D), device="cuda")]
+    rows = np.sort(rng.choice(V, n, replace=False)).astype(np.int32)
+    for step in (1, 2, 3):
+        ids = rows if step != 2 else rows[::2]
+        g = eps_regime_grads(rng, ids.size, D)
+        pack = (to_dev(ids), to_dev(g), None, to_dev(np.array([0, ids.size], np.int32)))
+        check_adam(state, pack, 1, 0, 1, HP, step)
 
 
 @pytest.mark.parametrize("cap,n,D", [(1, 1, 4096), (3, 3, 4096), (2, 2, 8192), (5, 3, 9001), (7, 5, 2048),
