@@ -182,6 +182,33 @@ int emb_grad_coalesce_by_owner(const int32_t *ids, int32_t T,
                                int32_t *dev_status, void *stream);
 
 /*
+ * emb_grad_coalesce_by_owner for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments, outputs and rules, without the workspace.
+ * The call allocates nothing and calls no allocating routine; its workspace is
+ * a static device array of EMB_NOALLOC_SCRATCH_BYTES (16 MiB) that each device
+ * the library runs on holds until the process ends (its address is looked up
+ * once per device, at the first call on it).
+ * Returns EMB_ERR_WORKSPACE, before anything touches the device, when
+ * emb_grad_coalesce_workspace_bytes(T, V, D, grad_dtype) exceeds
+ * EMB_NOALLOC_SCRATCH_BYTES (e.g. more than about 190k tokens of 256 floats, or
+ * 60k of 1024).  Every call on one device shares the array, which keeps the
+ * last call's contents (the call clears what must start at zero itself): calls
+ * in order on one stream are safe; calls that can overlap on one device
+ * (different streams, nothing ordering them) race on it.
+ */
+#define EMB_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+int emb_grad_coalesce_by_owner_noalloc(const int32_t *ids, int32_t T,
+                                       const void *grad, int32_t grad_dtype,
+                                       int32_t D, int64_t V,
+                                       const int32_t *row_owner, int32_t P,
+                                       int32_t *send_ids, int32_t *seg_offsets,
+                                       float *send_rows, int32_t *send_counts,
+                                       int32_t *send_offsets,
+                                       int32_t *num_unique,
+                                       int32_t *dev_status, void *stream);
+
+/*
  * emb_grad_coalesce_by_owner with the set split of Vertical Sparse Scheduling
  * (Algorithm 1; Sec. 4.2.2, "Minimum Dependency of Embedding").  With the next
  * batch's ids known in advance (next_ids [T_next]), a coalesced row is prior

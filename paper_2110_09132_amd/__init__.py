@@ -43,6 +43,8 @@ SIGNATURES = {
     "emb_grad_coalesce": (ctypes.c_int, [_P, _I32, _P, _I32, _I32, _I64, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_grad_coalesce_by_owner": (ctypes.c_int, [_P, _I32, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P, _P,
                                                   _P, _SZ, _P, _P]),
+    "emb_grad_coalesce_by_owner_noalloc": (ctypes.c_int, [_P, _I32, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P,
+                                                          _P, _P, _P, _P]),
     "emb_grad_coalesce_split_workspace_bytes": (_SZ, [_I32, _I32, _I64, _I32, _I32]),
     "emb_grad_coalesce_split": (ctypes.c_int, [_P, _I32, _P, _I32, _P, _I32, _I32, _I64, _P, _I32, _P, _P, _P, _P, _P,
                                                _P, _P, _SZ, _P, _P]),
@@ -295,6 +297,29 @@ def grad_coalesce_by_owner(ids, grad, V, row_owner, P, out=None, workspace=None,
                                           _ptr(seg_offsets), _ptr(send_rows), _ptr(send_counts), _ptr(send_offsets),
                                           _ptr(num_unique), _ptr(workspace), workspace.numel(), _ptr(dev_status),
                                           _stream(stream)), "emb_grad_coalesce_by_owner")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # EMB_NOALLOC_SCRATCH_BYTES
+
+
+def grad_coalesce_by_owner_noalloc(ids, grad, V, row_owner, P, out, dev_status=None, stream=None):
+    """grad_coalesce_by_owner without a workspace (emb_grad_coalesce_by_owner_noalloc: the library's
+    static device array serves as the workspace; calls that may overlap on one device race on it).
+    `out` passes the six output tensors in (nothing is allocated here either)."""
+    _need(ids, torch.int32, "ids")
+    _owners(row_owner, V, P)
+    T = ids.numel()
+    code, D = _grad(grad, T)
+    send_ids, seg_offsets, send_rows, send_counts, send_offsets, num_unique = out
+    _coalesce_outs(send_ids, seg_offsets, send_rows, num_unique, T, D)
+    _out(send_counts, torch.int32, P, "send_counts")
+    _out(send_offsets, torch.int32, P + 1, "send_offsets")
+    _check(lib.emb_grad_coalesce_by_owner_noalloc(_ptr(ids), T, _ptr(grad), code, D, V, _ptr(row_owner), P,
+                                                  _ptr(send_ids), _ptr(seg_offsets), _ptr(send_rows),
+                                                  _ptr(send_counts), _ptr(send_offsets), _ptr(num_unique),
+                                                  _ptr(dev_status), _stream(stream)),
+           "emb_grad_coalesce_by_owner_noalloc")
     return out
 
 

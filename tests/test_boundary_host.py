@@ -94,6 +94,20 @@ def test_coalesce_by_owner_validation():
     assert L.emb_grad_coalesce_by_owner(*args(V=(1 << 22) + 1, P=1024, **short)) == emb.EMB_ERR_UNSUPPORTED
 
 
+def test_coalesce_by_owner_noalloc_size_limit():
+    # the allocation-free call refuses, on the host, a batch whose workspace exceeds its static array
+    L = emb.lib
+    assert emb.NOALLOC_SCRATCH_BYTES == 16 << 20
+    T, D, V, P = 65536, 4096, 1 << 20, 16
+    assert L.emb_grad_coalesce_workspace_bytes(T, V, D, emb.EMB_F32) > emb.NOALLOC_SCRATCH_BYTES
+    assert L.emb_grad_coalesce_by_owner_noalloc(FAKE, T, FAKE, 0, D, V, FAKE, P, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                                NULL, NULL) == emb.EMB_ERR_WORKSPACE
+    # the largest workload batches fit
+    for T, V, D, g in ((65536, 1 << 20, 256, 0), (16384, 262144, 1024, 1), (25000, 32768, 512, 0),
+                       (16384, 32000, 1024, 0)):
+        assert L.emb_grad_coalesce_workspace_bytes(T, V, D, g) <= emb.NOALLOC_SCRATCH_BYTES
+
+
 def test_lookup_request_validation_and_workspace_query():
     L = emb.lib
     need = L.emb_lookup_request_workspace_bytes(1000, 5000)
