@@ -586,6 +586,7 @@ class WorkloadRun:
         start.record(main)
         for s in range(K):
             used.append(self.step(pipe, timing={"adam": adam_ev[s]} if s in adam_ev else None))
+        host_enqueue = time.perf_counter() - t0
         pipe.finish()
         end.record(main)
         torch.cuda.synchronize()
@@ -594,7 +595,7 @@ class WorkloadRun:
         adam_us = [1e3 * adam_ev[s][0].elapsed_ms(adam_ev[s][1]) for s in timed_steps]
         rows = sum(sum(self.U[b]) for b in used)
         return dict(ms_total=ms_total, wall=wall, used=used, rows=rows, adam_us=adam_us,
-                    adam_steps=timed_steps)
+                    adam_steps=timed_steps, host_enqueue_ms=host_enqueue * 1e3)
 
     def sequential(self, n, cold):
         """n steps one after another on one stream, an event pair around each step and each stage.  cold:
@@ -689,7 +690,7 @@ def pipelined_report(run, args, K):
                 rows=r["rows"], used=r["used"], bytes_step=bytes_step, total_bytes=total,
                 step_gbps=total / (ms_step * 1e-3) / 1e9, adam_us=adam_us, adam_us_all=w["adam_us"],
                 adam_bytes=adam_bytes, adam_gbps=adam_bytes / (adam_us * 1e-6) / 1e9,
-                window_ms_step=w["ms_total"] / args.roofline_steps)
+                window_ms_step=w["ms_total"] / args.roofline_steps, host_enqueue_ms=r["host_enqueue_ms"])
 
 
 def config_report(torch, emb, name, args, K, run=None, pl=None):
@@ -857,6 +858,7 @@ def main():
         "step_hbm_GBps": pl["step_gbps"],
         "step_hbm_frac": pl["step_gbps"] / HBM_PEAK_GBPS,
         "wall_s_timed": pl["wall"],
+        "host_enqueue_ms_timed": pl["host_enqueue_ms"],
         "roofline": {"bound": "hbm",
                      "kernel": "adam_kernel (emb_sparse_adam_apply)" + (", delayed rows" if split else ""),
                      "achieved": pl["adam_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
