@@ -443,13 +443,15 @@ def schedule_candidates(args):
         parts = args.candidate.split("/")
         return [(parts[0], int(parts[1]), len(parts) > 2 and parts[2] == "paired")]
     orders = ("events", "signals") if args.order == "auto" else (args.order,)
-    sets = (2, 4) if args.sets == 0 else (args.sets,)
+    sets = (2, 4, 6) if args.sets == 0 else (args.sets,)
     # with events the split needs two sets (its lookup waits for the delayed update two steps back)
     cands = [(o, n, False) for o in orders for n in sets
-             if not (args.schedule == "split" and o == "events" and n != 2)]
-    # owner-major with four sets: also with each sort stream running its steps' reductions
+             if n != 6 and not (args.schedule == "split" and o == "events" and n != 2)]
+    # owner-major with four sets: also with each sort stream running its steps' reductions; with six,
+    # three such streams
     if args.schedule == "by_owner":
         cands += [(o, 4, True) for o in orders if 4 in sets]
+        cands += [(o, 6, True) for o in orders if 6 in sets]
     return cands
 
 
@@ -500,7 +502,7 @@ class WorkloadRun:
             gdt = torch.bfloat16 if sp.grad_dtype == "bf16" else torch.float32
             W = torch.from_numpy(configs.make_weights(sp)).to(dev)
             self.tables.append(EmbeddingTable(W, torch.from_numpy(configs.row_owner(sp)).to(dev), sp.P, sp.T, gdt,
-                                              sets=4))
+                                              sets=6))
             tb_batches = []
             for b in range(nbatches):
                 ids, G = configs.make_batch(sp, 1000 + b)
@@ -533,8 +535,8 @@ class WorkloadRun:
         order, sets, paired = cand
         return StepPipeline(self.tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=True, by_owner=self.by_owner,
                             split=self.split, signals=order == "signals",
-                            sort_streams=2 if (sets == 4 and self.by_owner and not self.split) else 1, sets=sets,
-                            paired=paired)
+                            sort_streams=(sets // 2 if sets in (4, 6) else 1) if (self.by_owner and not self.split)
+                            else 1, sets=sets, paired=paired)
 
     def next_ids(self, t):
         return [x[0] for x in self.step_batches[(t + 1) % self.nb]] if self.split else None
@@ -742,7 +744,7 @@ def main():
                          "the prior/delayed split of Vertical Sparse Scheduling (emb_grad_coalesce_split; the "
                          "delayed update beside the next lookup); unfused: emb_grad_coalesce then "
                          "emb_pack_by_owner")
-    ap.add_argument("--sets", type=int, choices=(0, 2, 4), default=0,
+    ap.add_argument("--sets", type=int, choices=(0, 2, 4, 6), default=0,
                     help="buffer sets rotated between steps, with the sorts of odd and even sets on two side "
                          "streams when 4 and not split (0: tuned; the split with events uses 2)")
     ap.add_argument("--order", choices=("auto", "signals", "events"), default="auto",
@@ -844,7 +846,8 @@ def main():
                     "by_owner": "sort and reduction on two side streams; lookup and update on the main stream",
                     "unfused": "coalesce and pack on two side streams; lookup and update on the main stream"}[
                        args.schedule],
-                   "sort_streams": None if (args.sequential or split or not by_owner) else (2 if nsets == 4 else 1),
+                   "sort_streams": None if (args.sequential or split or not by_owner) else
+                   (nsets // 2 if nsets in (4, 6) else 1),
                    "buffer_sets": nsets,
                    "sort_and_reduce_paired": paired,
                    "cross_stream_order": None if args.sequential else

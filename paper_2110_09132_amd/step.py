@@ -98,12 +98,14 @@ class StepPipeline:
         split: the prior / delayed split (implies by_owner); step() then needs the next ids.
         sort_streams (by_owner without the split, overlap=True): 2 runs the sorts of odd and even
         buffer sets on two side streams, so that a step's sort can run beside the previous step's
-        (they share nothing; each waits only for the reduction of its own set's previous step).
+        (they share nothing; each waits only for the reduction of its own set's previous step);
+        3 (with paired) runs sort and reduction of set i on side stream i mod 3, all three side
+        streams (sets a multiple of 3).
         sets: buffer sets rotated between steps (every table needs at least this many; the split
         with events needs 2).  More sets let a step's sort start before the reduction of the step
         two back has finished.
-        paired (with sort_streams=2): each of the two sort streams also runs the reductions of its
-        steps, right after their sorts (no cross-stream wait between the two halves).
+        paired (with sort_streams >= 2): each sort stream also runs the reductions of its steps,
+        right after their sorts (no cross-stream wait between the two halves).
         signals (with overlap=True): keep the cross-stream order with step signals (stream memory
         operations: about half the host time per step, for host-bound pipelines of small
         batches; with large batches events keep the GPU a few percent busier) instead of events."""
@@ -119,8 +121,11 @@ class StepPipeline:
         # the sorts of buffer set 1 (by_owner without the split): the third side stream
         self.side3_sort = s3 if (overlap and self.by_owner and not split and sort_streams >= 2) else None
         self.paired = paired and self.side3_sort is not None
-        if sort_streams >= 2 and sets % 2:
-            raise ValueError("two sort streams need an even number of buffer sets")
+        self.sort_streams = sort_streams if self.side3_sort is not None else 1
+        if self.sort_streams >= 3 and not self.paired:
+            raise ValueError("three sort streams run paired")
+        if self.sort_streams >= 2 and sets % self.sort_streams:
+            raise ValueError("the buffer sets must be a multiple of the sort streams")
         if any(tb.sets < sets for tb in self.tables):
             raise ValueError("a table has fewer buffer sets than the pipeline rotates")
         self.sets = sets
@@ -146,7 +151,10 @@ class StepPipeline:
                              beta2=beta2, eps=eps, dev_status=st)
                 evs = [Event() for _ in range(6)]
                 self.events += evs
-                sort_side = self.side3_sort if (i % 2 == 1 and self.side3_sort is not None) else self.side
+                if self.sort_streams >= 3:
+                    sort_side = (self.side, self.side2, self.side3_sort)[i % 3]
+                else:
+                    sort_side = self.side3_sort if (i % 2 == 1 and self.side3_sort is not None) else self.side
                 red_side = sort_side if self.paired else self.side2
                 s = StepSchedule(lookup_update=_stream_handle(self.main), coalesce=_stream_handle(sort_side),
                                  pack=_stream_handle(red_side), delayed=_stream_handle(self.side3),

@@ -1,7 +1,8 @@
 """The step exactly as the benchmark runs it, at the full size of every workload and for every table
 of it: the step executor (owner-major coalesce, sort and reduction on side streams) under each
 schedule the benchmark's tuner may pick (events or step signals; two buffer sets with one sort
-stream, or four with two, with or without each sort stream running its own reductions), and the
+stream, four with two, with or without each sort stream running its own reductions, or six with
+three sort streams running their own reductions), and the
 split schedule of Vertical Sparse Scheduling (Algorithm 1: prior rows updated before the next
 lookup, delayed rows beside it), a few steps in a row, checked against the oracle:
   - each step's send layout (ids, counts, offsets; with the split, the 2P groups of the prior and
@@ -31,6 +32,7 @@ pytestmark = pytest.mark.gpu
 SCHEDULES = [("by_owner", "events", 2, False), ("by_owner", "events", 4, False),
              ("by_owner", "signals", 2, False), ("by_owner", "signals", 4, False),
              ("by_owner", "events", 4, True), ("by_owner", "signals", 4, True),
+             ("by_owner", "events", 6, True), ("by_owner", "signals", 6, True),
              ("split", "events", 2, False), ("split", "signals", 2, False), ("split", "signals", 4, False)]
 CASES = [(w,) + s for w in configs.WORKLOADS for s in SCHEDULES]
 
@@ -62,7 +64,7 @@ def test_bench_schedule_full_size(name, kind, order, sets, paired):
     st = emb.new_status()
     pipe = StepPipeline(tbs, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=True, dev_status=st, split=split,
                         signals=order == "signals", sets=sets,
-                        sort_streams=2 if (sets == 4 and not split) else 1, paired=paired)
+                        sort_streams=(sets // 2 if sets in (4, 6) else 1) if not split else 1, paired=paired)
     # batches of steps 0 .. steps (the last one is only the split's next batch)
     host_batches = [[batch(name, k, s) for k in range(nt)] for s in range(steps + 1)]
     dev_batches = [[(to_dev(ids), to_dev(G)) for ids, G in hb] for hb in host_batches]
