@@ -201,6 +201,46 @@ def summarize_pmc(fetch_dir, write_dir, command_fetch, command_write):
             "command_fetch": command_fetch, "command_write": command_write}
 
 
+def summarize_traffic(fetch_dir, write_dir, bench_json, command_fetch, command_write):
+    """HBM traffic per kernel from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE in KiB per dispatch,
+    averaged over each kernel's dispatches), each scaled by what the counter reads for the reference
+    stream of the same run (torch.bitwise_not over COPY_MIB MiB: reads and writes that many bytes);
+    beside the algorithmic bytes of the lookup, the reduction and the update for the run's mean
+    distinct-row count (from its bench line, `bench_json`)."""
+    def per_kernel(directory, counter):
+        vals = {}
+        for r in _read_csv(_find(directory, "counter_collection.csv")):
+            if r.get("Counter_Name") != counter:
+                continue
+            name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            name = name.replace("void ", "").replace("emb::", "")
+            vals.setdefault(name, []).append(float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in vals.items()}, {k: len(v) for k, v in vals.items()}
+    f, nf = per_kernel(fetch_dir, "FETCH_SIZE")
+    w, _ = per_kernel(write_dir, "WRITE_SIZE")
+    copy = next(k for k in f if COPY_KERNEL in k)
+    copy_bytes = COPY_MIB * (1 << 20)
+    fs, ws = copy_bytes / (f[copy] * 1024.0), copy_bytes / (w[copy] * 1024.0)
+    with open(bench_json) as fh:
+        b = json.loads(fh.read().strip().splitlines()[-1])
+    t = b["config"]["tables"][0]
+    T, D, U = t["T"], t["D"], b["config"]["mean_unique_rows_per_step"]
+    model = {"adam_kernel": (4 * U + 16 * D * U, 12 * D * U), "gather_kernel": (4 * T + 4 * D * U, 4 * D * T),
+             "seg_reduce_kernel": (8 * T + 4 * D * T, 8 * U + 4 * D * U + 4)}  # sorted keys and positions in
+    out = [f"command_fetch: {command_fetch}", f"command_write: {command_write}",
+           f"scales (reference stream of {COPY_MIB} MiB each way): FETCH x{fs:.4f}, WRITE x{ws:.4f}; "
+           f"mean distinct rows U = {U:.0f} of T = {T}, D = {D}", "",
+           f"{'kernel':56s} {'disp':>5s} {'read MB':>9s} {'write MB':>9s} {'model r/w MB':>15s} {'ratio':>6s}"]
+    for k in sorted(f, key=lambda k: -f[k] * nf[k]):
+        if k == copy or k not in w:
+            continue
+        rd, wr = f[k] * 1024.0 * fs / 1e6, w[k] * 1024.0 * ws / 1e6
+        m = next((v for key, v in model.items() if key in k), None)
+        ms = f"{m[0] / 1e6:7.1f}/{m[1] / 1e6:7.1f}" if m else ""
+        ratio = f"{(rd + wr) * 1e6 / (m[0] + m[1]):6.3f}" if m else ""
+        out.append(f"{k[:56]:56s} {nf[k]:5d} {rd:9.1f} {wr:9.1f} {ms:>15s} {ratio:>6s}")
+    return "\n".join(out) + "\n"
+
 CU_NUM = 256  # MI355X compute units
 
 
@@ -239,7 +279,8 @@ def summarize_counters(dirs, command):
         gui = mean(k, "GRBM_GUI_ACTIVE")
         waves = mean(k, "SQ_WAVES")
         hit, miss = mean(k, "TCC_HIT_sum"), mean(k, "TCC_MISS_sum")
-        rows.append((k, len(durs[k]), sum(durs[k].values()) / len(durs[k]), waves,
+        per_dir = max(sum(1 for key in durs[k] if key[0] == d) for d in dirs)  # dispatches of one run
+        rows.append((k, per_dir, sum(durs[k].values()) / len(durs[k]), waves,
                      ratio(mean(k, "SQ_WAVE_CYCLES"), None if gui is None else gui * CU_NUM, 4.0),
                      ratio(mean(k, "SQ_ACTIVE_INST_VALU"), None if gui is None else gui * CU_NUM, 100.0),
                      ratio(mean(k, "SQ_LDS_IDX_ACTIVE"), None if gui is None else gui * CU_NUM, 100.0),
@@ -763,6 +804,8 @@ def main():
     ap.add_argument("--summarize-trace", metavar="DIR", help="print a summary of a rocprofv3 kernel-stats run")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the scaled HBM traffic of the update kernel from two rocprofv3 --pmc runs")
+    ap.add_argument("--summarize-traffic", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
+                    help="print the scaled HBM traffic of every kernel from two rocprofv3 --pmc runs")
     ap.add_argument("--summarize-counters", nargs="+", metavar="DIR",
                     help="print per-kernel occupancy, VALU, LDS and L2 figures from rocprofv3 --pmc runs")
     ap.add_argument("--command", default="", help="the command recorded in a summary")
@@ -776,6 +819,9 @@ def main():
         return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc, args.command, args.command2), indent=1))
+        return
+    if args.summarize_traffic:
+        print(summarize_traffic(*args.summarize_traffic, args.command, args.command2), end="")
         return
     if args.summarize_counters:
         print(summarize_counters(args.summarize_counters, args.command), end="")
@@ -876,19 +922,19 @@ def main():
         "gradient_sizes_table3": table3,
         "host": host_info(),
     }
+    copy_gbps = copy_reference(torch)  # also the calibration dispatch of the byte counters
+    result["copy_GBps"] = copy_gbps
+    result["step_frac_of_copy"] = pl["step_gbps"] / copy_gbps
     if not args.only_steps:
         log("sequential warm and cold runs ...")
         seqr = sequential_report(run, args.seq_steps)
         result["timing_protocol"] = seqr
         result["stage_ms_sequential"] = {k: v["median"] for k, v in seqr["warm"]["stage_ms"].items()}
         result["sequential_ms_per_step"] = seqr["warm"]["step_ms"]["median"]
-        log("copy reference, column partition, cost model, exchanges ...")
-        copy_gbps = copy_reference(torch)
+        log("column partition, cost model, exchanges ...")
         sp0, tb0 = wl.tables[0], run.tables[0]
         batches0 = [x[0] for x in run.step_batches]
         U0 = [U[b][0] for b in range(nb)]
-        result["copy_GBps"] = copy_gbps
-        result["step_frac_of_copy"] = pl["step_gbps"] / copy_gbps
         result["column_partition"] = column_partition_report(torch, emb, sp0, tb0, batches0, U0, run.owner_rows)
         result["forward_exchange"] = forward_exchange_report(torch, emb, sp0, tb0, batches0, U0)
         result["gradient_exchange"] = exchange_report(torch, emb, sp0, tb0, batches0)
