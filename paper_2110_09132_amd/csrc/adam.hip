@@ -18,15 +18,15 @@ namespace emb {
 namespace {
 
 constexpr int kThreads = 256;
-// Row steps per tile: two for rows of one column step, each wave then taking
-// four tiles' worth of rows (its loads of the next tile in flight while the
-// current one is stored); four for wider rows, whose waves share column steps.
-// Measured in the overlapped step of the low-duplication workload (63.5k rows
-// of 1 KB, update beside the next step's reduction): 144.0 us per step with
-// four-row tiles and one tile's worth of rows per wave, 138.3 us with two-row
-// tiles and four; eight, sixteen or three-row variants were in between.
-template <bool kWide>
-constexpr int rows_in_flight() { return kWide ? 4 : 2; }
+// Row steps per tile: two (the loads of the next tile are in flight while the
+// current one is stored); with rows of one column step each wave takes four
+// tiles' worth of rows.  Measured in the overlapped steps (update beside the
+// next step's reduction): the low-duplication workload (63.5k rows of 1 KB)
+// 144.0 us per step with four-row tiles and one tile's worth of rows per wave,
+// 138.3 us with two-row tiles and four (eight, sixteen or three-row variants
+// in between); the shared-vocabulary workload (7.1k rows of 2 KB) 56.1 -> 53.7
+// us with two-row tiles for wide rows too, the 4 KB-row workloads unchanged.
+constexpr int kRowsInFlight = 2;
 constexpr int kNarrowTilesPerWave = 4;
 
 __device__ __forceinline__ float adam_elem(float g, float& w, float& m, float& v, const AdamCoeffs& c) {
@@ -73,7 +73,7 @@ __device__ __forceinline__ int column_share(int rows, int step_rows, int ncols, 
 // Each wave owns a contiguous range of the listed rows (with wide rows, every
 // cs-th column step of one).  The row ids of 64 rows come in one coalesced
 // load and reach their lanes by shuffle; rows are processed in tiles of
-// rows_in_flight() row steps, and the loads (g, w, m, v) of the next tile are
+// kRowsInFlight row steps, and the loads (g, w, m, v) of the next tile are
 // issued before the current tile is computed and stored.  kWide: rows of more
 // than one column step (Dv > 64); the tiles then run over the wave's column
 // steps as well, one sequence.
@@ -92,7 +92,6 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
   const int lane = static_cast<int>(lane_id());
   const int sub = lane >> log2L;
   const int cl = lane & (L - 1);
-  constexpr int kRowsInFlight = rows_in_flight<kWide>();
   const int step_rows = rpw * kRowsInFlight;
   const int all_waves = static_cast<int>(gridDim.x) * (kThreads / kWave);
   const int wave_all = uniform(static_cast<int>(blockIdx.x) * (kThreads / kWave) + static_cast<int>(threadIdx.x / kWave));
@@ -212,8 +211,8 @@ hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t 
   const int Dv = vec4 ? D / 4 : D;
   const RowLanes rl = row_lanes_for(Dv);
   const bool wide = Dv > kWave;  // more than one column step per row
-  const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * (kThreads / kWave) *
-                                   (wide ? rows_in_flight<true>() : rows_in_flight<false>() * kNarrowTilesPerWave);
+  const long long rows_per_block = static_cast<long long>(rl.rows_per_wave()) * (kThreads / kWave) * kRowsInFlight *
+                                   (wide ? 1 : kNarrowTilesPerWave);
   const unsigned grid = grid_for((cap_rows + rows_per_block - 1) / rows_per_block, kMaxBlocks);
   // Both events are attached to the dispatch, so they time the kernel itself
   // (an attached start event idles the stream a few microseconds longer than a
