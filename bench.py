@@ -640,10 +640,12 @@ class WorkloadRun:
         return dict(ms_total=ms_total, wall=wall, used=used, rows=rows, adam_us=adam_us,
                     adam_steps=timed_steps, host_enqueue_ms=host_enqueue * 1e3)
 
-    def sequential(self, n, cold):
-        """n steps one after another on one stream, an event pair around each step and each stage.  cold:
-        a 1 GiB buffer is written between the steps, outside the events, so that each step starts with
-        the caches (L2 and the last-level cache) holding none of its data."""
+    def sequential(self, n, cold, per_call):
+        """n steps one after another on one stream, an event pair around each step, and with per_call
+        around each call as well (their records sit between the calls and lengthen the step, so the
+        step's own spread comes from a run without them).  cold: a 1 GiB buffer is written between the
+        steps, outside the events, so that each step starts with the caches (L2 and the last-level
+        cache) holding none of its data."""
         torch, emb = self.torch, self.emb
         main = torch.cuda.current_stream()
         stages = ("gather", "coalesce", "pack", "adam") if (self.split or not self.by_owner) else \
@@ -654,7 +656,7 @@ class WorkloadRun:
         for s in range(n):
             if flush is not None:
                 flush.fill_(s)
-            ev = {k: (emb.Event(timing=True), emb.Event(timing=True)) for k in stages}
+            ev = {k: (emb.Event(timing=True), emb.Event(timing=True)) for k in stages} if per_call else None
             s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             s0.record(main)
             b = self.step(seq, timing=ev)
@@ -664,8 +666,8 @@ class WorkloadRun:
                 torch.cuda.synchronize()
         torch.cuda.synchronize()
         step_ms = [s0.elapsed_time(s1) for _, s0, s1, _ in evs]
-        stage_ms = {k: [ev[k][0].elapsed_ms(ev[k][1]) for _, _, _, ev in evs] for k in stages}
-        if self.split:  # the timing pairs' names under the split
+        stage_ms = {k: [ev[k][0].elapsed_ms(ev[k][1]) for _, _, _, ev in evs] for k in stages} if per_call else {}
+        if self.split and per_call:  # the timing pairs' names under the split
             stage_ms = {"gather": stage_ms["gather"], "coalesce": stage_ms["coalesce"],
                         "update_prior": stage_ms["pack"], "update_delayed": stage_ms["adam"]}
         used = [b for b, _, _, _ in evs]
@@ -698,13 +700,16 @@ class WorkloadRun:
 
 def sequential_report(run, n):
     """Warm and cold figures of the step run call after call on one stream (median, p10, p90 over n
-    steps): the step, each call, and the step's effective bandwidth at the median."""
+    steps): the step (event pairs around the steps only), each call (a second run with event pairs
+    around the calls too), and the step's effective bandwidth at the median."""
     out = {}
     for kind, cold in (("warm", False), ("cold", True)):
-        r = run.sequential(n, cold)
+        r = run.sequential(n, cold, per_call=False)
+        c = run.sequential(n, cold, per_call=True)
         nbytes = sum(run.step_bytes(r["used"]).values())
         st = spread(r["step_ms"])
-        out[kind] = {"step_ms": st, "stage_ms": {k: spread(v) for k, v in r["stage_ms"].items()},
+        out[kind] = {"step_ms": st, "stage_ms": {k: spread(v) for k, v in c["stage_ms"].items()},
+                     "step_ms_with_call_events": spread(c["step_ms"]),
                      "step_hbm_frac_at_median": nbytes / (st["median"] * 1e-3) / 1e9 / HBM_PEAK_GBPS}
     out["flush_bytes_cold"] = FLUSH_BYTES
     return out
