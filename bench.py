@@ -482,6 +482,8 @@ def schedule_candidates(args):
         return [("events", 2, False)]
     if args.candidate:
         parts = args.candidate.split("/")
+        if parts[0] not in ("events", "signals") or len(parts) not in (2, 3):
+            raise SystemExit(f"--candidate {args.candidate!r}: expected ORDER/SETS[/paired], ORDER events or signals")
         return [(parts[0], int(parts[1]), len(parts) > 2 and parts[2] == "paired")]
     orders = ("events", "signals") if args.order == "auto" else (args.order,)
     sets = (2, 4, 6) if args.sets == 0 else (args.sets,)

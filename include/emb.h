@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define EMB_ABI_VERSION 1
+#define EMB_ABI_VERSION 2
 
 /* host status codes */
 #define EMB_OK 0
@@ -424,6 +424,21 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
                           int32_t *dev_status, void *stream);
 
 /*
+ * The update's coefficients for one step (Kingma & Ba, Algorithm 1, as
+ * emb_sparse_adam_apply forms them: bias corrections in fp64, each
+ * coefficient rounded once to fp32), written to out[EMB_ADAM_COEFFS_WORDS]
+ * (host memory): beta1, 1 - beta1, beta2, 1 - beta2, lr / (1 - beta1^step),
+ * 1 / (1 - beta2^step), eps, 0.  Copied to device memory and named by
+ * emb_step_args.adam_coeffs, they let steps captured in a graph advance the
+ * step count on every replay (Sec. 5.7: the step counter grows once per
+ * iteration).  Host arithmetic only; EMB_ERR_INVALID_ARG as for
+ * emb_sparse_adam_apply's hyper-parameters.
+ */
+#define EMB_ADAM_COEFFS_WORDS 8
+int emb_adam_coeffs(double lr, double beta1, double beta2, double eps,
+                    int64_t step, float *out);
+
+/*
  * ---------------------------------------------------------------------------
  * Step executor.  Not a step of the path itself: it enqueues the four calls
  * above for one training step of one table, in data order, on up to four streams,
@@ -487,6 +502,16 @@ int emb_sparse_adam_apply(float *table, float *exp_avg, float *exp_avg_sq,
  *
  * With all streams equal the calls simply run one after another, and the
  * results are bitwise the same either way.
+ *
+ * Graph capture.  While `lookup_update` is being captured into a HIP graph
+ * (stream capture, events only: step signals and timing events are refused
+ * with EMB_ERR_UNSUPPORTED), the executor records every stage end as an event
+ * node instead of attaching events to dispatches.  The captured steps must not
+ * wait for steps enqueued before the capture began: each buffer set's first use
+ * in a capture has reuse == 0 (a replayed graph runs after the work before it
+ * on its stream, whole).  With args.adam_coeffs the update reads its
+ * coefficients from device memory when it runs, so a replay can apply other
+ * step numbers than the ones the capture saw.
  * ---------------------------------------------------------------------------
  */
 typedef struct {
@@ -540,6 +565,10 @@ typedef struct {
   double lr, beta1, beta2, eps;
   int64_t step;             /* Adam step (>= 1), one per iteration (Sec. 5.7) */
   int32_t *dev_status;      /* optional */
+  const void *adam_coeffs;  /* optional, 16-byte aligned device memory: this step's
+                               EMB_ADAM_COEFFS_WORDS update coefficients (emb_adam_coeffs),
+                               read by the update kernel when it runs instead of those of
+                               `step` (for steps replayed from a graph) */
 } emb_step_args;
 
 /* Events for the schedule (hipEventCreateWithFlags; timing: nonzero for

@@ -32,6 +32,7 @@ EMB_COMM_ALLTOALL = 0
 EMB_COMM_ALLREDUCE = 1
 EMB_COMM_PS = 2
 EMB_COMM_ALLGATHER = 3
+EMB_ADAM_COEFFS_WORDS = 8
 
 # (name, restype, argtypes) of every symbol include/emb.h declares.
 _P, _I32, _I64, _SZ, _D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_double
@@ -57,6 +58,7 @@ SIGNATURES = {
     "emb_pack_by_owner": (ctypes.c_int, [_P, _P, _P, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _P, _P, _SZ, _P, _P]),
     "emb_sparse_adam_apply": (ctypes.c_int, [_P, _P, _P, _I64, _I32, _P, _P, _P, _I32, _I32, _I32, _I32,
                                              _D, _D, _D, _D, _I64, _P, _P]),
+    "emb_adam_coeffs": (ctypes.c_int, [_D, _D, _D, _D, _I64, _P]),
     "emb_pack_by_column": (ctypes.c_int, [_P, _P, _I32, _I32, _I32, _P, _P, _P]),
     "emb_gather_by_column": (ctypes.c_int, [_P, _I64, _I32, _I32, _P, _I32, _P, _P, _P]),
     "emb_assemble_by_column": (ctypes.c_int, [_P, _I64, _I64, _I32, _I32, _I32, _P, _P]),
@@ -85,7 +87,8 @@ class StepArgs(ctypes.Structure):
                 ("cap_rows", _I32), ("lookup", _P), ("uniq_ids", _P), ("seg_offsets", _P), ("num_unique", _P),
                 ("uniq_grad", _P), ("send_ids", _P), ("send_counts", _P), ("send_offsets", _P), ("send_rows", _P),
                 ("ws_coalesce", _P), ("ws_coalesce_bytes", _SZ), ("ws_pack", _P), ("ws_pack_bytes", _SZ),
-                ("lr", _D), ("beta1", _D), ("beta2", _D), ("eps", _D), ("step", _I64), ("dev_status", _P)]
+                ("lr", _D), ("beta1", _D), ("beta2", _D), ("eps", _D), ("step", _I64), ("dev_status", _P),
+                ("adam_coeffs", _P)]
 
 
 class EmbError(RuntimeError):
@@ -564,6 +567,16 @@ def comm_cost(scheme, N, M, alpha, B, beta, S=1) -> float:
     _check(lib.emb_comm_cost(scheme, N, S, float(M), float(alpha), float(B), float(beta), ctypes.byref(r)),
            "emb_comm_cost")
     return r.value
+
+
+def adam_coeffs(lr, beta1, beta2, eps, step, out):
+    """Write step `step`'s update coefficients (emb_adam_coeffs) into `out`, a float32 CPU tensor of
+    EMB_ADAM_COEFFS_WORDS elements (for instance a row of a pinned buffer)."""
+    if out.dtype != torch.float32 or out.device.type != "cpu" or not out.is_contiguous() or \
+            out.numel() < EMB_ADAM_COEFFS_WORDS:
+        raise EmbError(f"out must be a contiguous float32 CPU tensor of {EMB_ADAM_COEFFS_WORDS} elements")
+    _check(lib.emb_adam_coeffs(lr, beta1, beta2, eps, step, out.data_ptr()), "emb_adam_coeffs")
+    return out
 
 
 def sparse_adam_apply(table, exp_avg, exp_avg_sq, row_ids, rows, offsets, P, shard_begin, shard_end, lr, beta1,

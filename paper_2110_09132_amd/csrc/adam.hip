@@ -83,7 +83,9 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
                                                         const int32_t* __restrict__ row_ids,
                                                         const VecT* __restrict__ rows,
                                                         const int32_t* __restrict__ offsets, int sb, int se, int cap,
-                                                        AdamCoeffs c, int32_t* status) {
+                                                        AdamCoeffs cval, const AdamCoeffs* __restrict__ coeffs_dev,
+                                                        int32_t* status) {
+  const AdamCoeffs c = coeffs_dev != nullptr ? *coeffs_dev : cval;
   int lo = offsets[sb], hi = offsets[se];
   lo = max(0, min(lo, cap));
   hi = max(lo, min(hi, cap));
@@ -204,7 +206,8 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
 
 hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int D, const int32_t* row_ids,
                        const float* rows, const int32_t* offsets, int shard_begin, int shard_end, int cap_rows,
-                       const AdamCoeffs& c, int32_t* status, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
+                       const AdamCoeffs& c, const AdamCoeffs* coeffs_dev, int32_t* status, hipStream_t stream,
+                       hipEvent_t start, hipEvent_t stop) {
   if (cap_rows == 0 || shard_begin == shard_end) return hipSuccess;
   const auto al16 = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
   const bool vec4 = (D % 4 == 0) && al16(table) && al16(exp_avg) && al16(exp_avg_sq) && al16(rows);
@@ -222,7 +225,7 @@ hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t 
                         (WIDE) || sizeof(VT) != 16 ? 0 : kNarrowOccupancyLds, stream, start, stop, 0,              \
                         reinterpret_cast<VT*>(table), reinterpret_cast<VT*>(exp_avg),                              \
                         reinterpret_cast<VT*>(exp_avg_sq), V, Dv, rl.log2_lanes, row_ids,                          \
-                        reinterpret_cast<const VT*>(rows), offsets, shard_begin, shard_end, cap_rows, c, status)
+                        reinterpret_cast<const VT*>(rows), offsets, shard_begin, shard_end, cap_rows, c, coeffs_dev, status)
   if (vec4) {
     if (wide)
       EMB_ADAM(float4, true);

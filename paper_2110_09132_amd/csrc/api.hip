@@ -50,35 +50,44 @@ int coalesce_by_owner_args_status(const int32_t* ids, int32_t T, const void* gra
 }
 
 
-int sparse_adam_call(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int32_t D, const int32_t* row_ids,
-                     const float* rows, const int32_t* offsets, int32_t P, int32_t shard_begin, int32_t shard_end,
-                     int32_t cap_rows, double lr, double beta1, double beta2, double eps, int64_t step,
-                     int32_t* dev_status, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
-  if (bad_table_dims(V, D) || P < 1 || P > kMaxOwners || cap_rows < 0) return EMB_ERR_INVALID_ARG;
-  if (shard_begin < 0 || shard_begin > shard_end || shard_end > P) return EMB_ERR_INVALID_ARG;
+int adam_coeffs(double lr, double beta1, double beta2, double eps, int64_t step, AdamCoeffs* c) {
   if (step < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0) ||
       !std::isfinite(lr) || !std::isfinite(eps))
     return EMB_ERR_INVALID_ARG;
+  // bias corrections in fp64 on the host, then the fp32 coefficients of the kernel
+  const double bc1 = 1.0 - std::pow(beta1, static_cast<double>(step));
+  const double bc2 = 1.0 - std::pow(beta2, static_cast<double>(step));
+  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return EMB_ERR_INVALID_ARG;  // beta == 0 edge cases stay valid: bc == 1
+  c->beta1 = static_cast<float>(beta1);
+  c->one_minus_beta1 = static_cast<float>(1.0 - beta1);
+  c->beta2 = static_cast<float>(beta2);
+  c->one_minus_beta2 = static_cast<float>(1.0 - beta2);
+  c->step_size = static_cast<float>(lr / bc1);
+  c->inv_bc2 = static_cast<float>(1.0 / bc2);
+  c->eps = static_cast<float>(eps);
+  return EMB_OK;
+}
+
+int sparse_adam_call(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int32_t D, const int32_t* row_ids,
+                     const float* rows, const int32_t* offsets, int32_t P, int32_t shard_begin, int32_t shard_end,
+                     int32_t cap_rows, double lr, double beta1, double beta2, double eps, int64_t step,
+                     const void* coeffs_dev, int32_t* dev_status, hipStream_t stream, hipEvent_t start,
+                     hipEvent_t stop) {
+  if (bad_table_dims(V, D) || P < 1 || P > kMaxOwners || cap_rows < 0) return EMB_ERR_INVALID_ARG;
+  if (shard_begin < 0 || shard_begin > shard_end || shard_end > P) return EMB_ERR_INVALID_ARG;
+  AdamCoeffs c;
+  const int cst = adam_coeffs(lr, beta1, beta2, eps, step, &c);
+  if (cst != EMB_OK) return cst;
+  if (coeffs_dev != nullptr && reinterpret_cast<uintptr_t>(coeffs_dev) % 16 != 0) return EMB_ERR_INVALID_ARG;
   if (cap_rows == 0 || shard_begin == shard_end) {  // nothing to launch: the timing pair still brackets this point
     if (start && hipEventRecord(start, stream) != hipSuccess) return EMB_ERR_LAUNCH;
     if (stop && hipEventRecord(stop, stream) != hipSuccess) return EMB_ERR_LAUNCH;
     return EMB_OK;
   }
   if (!table || !exp_avg || !exp_avg_sq || !row_ids || !rows || !offsets) return EMB_ERR_INVALID_ARG;
-  // bias corrections in fp64 on the host, then the fp32 coefficients of the kernel
-  const double bc1 = 1.0 - std::pow(beta1, static_cast<double>(step));
-  const double bc2 = 1.0 - std::pow(beta2, static_cast<double>(step));
-  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return EMB_ERR_INVALID_ARG;  // beta == 0 edge cases stay valid: bc == 1
-  AdamCoeffs c;
-  c.beta1 = static_cast<float>(beta1);
-  c.one_minus_beta1 = static_cast<float>(1.0 - beta1);
-  c.beta2 = static_cast<float>(beta2);
-  c.one_minus_beta2 = static_cast<float>(1.0 - beta2);
-  c.step_size = static_cast<float>(lr / bc1);
-  c.inv_bc2 = static_cast<float>(1.0 / bc2);
-  c.eps = static_cast<float>(eps);
   return launch_status(launch_adam(table, exp_avg, exp_avg_sq, V, D, row_ids, rows, offsets, shard_begin, shard_end,
-                                   cap_rows, c, dev_status, stream, start, stop));
+                                   cap_rows, c, static_cast<const AdamCoeffs*>(coeffs_dev), dev_status, stream,
+                                   start, stop));
 }
 
 }  // namespace emb
@@ -296,8 +305,19 @@ int emb_sparse_adam_apply(float* table, float* exp_avg, float* exp_avg_sq, int64
                           int32_t shard_begin, int32_t shard_end, int32_t cap_rows, double lr, double beta1,
                           double beta2, double eps, int64_t step, int32_t* dev_status, void* stream) {
   return emb::sparse_adam_call(table, exp_avg, exp_avg_sq, V, D, row_ids, rows, offsets, P, shard_begin, shard_end,
-                               cap_rows, lr, beta1, beta2, eps, step, dev_status, static_cast<hipStream_t>(stream),
-                               nullptr, nullptr);
+                               cap_rows, lr, beta1, beta2, eps, step, nullptr, dev_status,
+                               static_cast<hipStream_t>(stream), nullptr, nullptr);
+}
+
+int emb_adam_coeffs(double lr, double beta1, double beta2, double eps, int64_t step, float* out) {
+  if (out == nullptr) return EMB_ERR_INVALID_ARG;
+  emb::AdamCoeffs c;
+  const int st = emb::adam_coeffs(lr, beta1, beta2, eps, step, &c);
+  if (st != EMB_OK) return st;
+  const float words[EMB_ADAM_COEFFS_WORDS] = {c.beta1, c.one_minus_beta1, c.beta2, c.one_minus_beta2,
+                                              c.step_size, c.inv_bc2, c.eps, 0.0f};
+  for (int i = 0; i < EMB_ADAM_COEFFS_WORDS; ++i) out[i] = words[i];
+  return EMB_OK;
 }
 
 }  // extern "C"

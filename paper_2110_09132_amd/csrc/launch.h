@@ -82,25 +82,34 @@ hipError_t launch_pack(const int32_t* uniq_ids, const float* uniq_grad, const in
                        int32_t* send_counts, int32_t* send_offsets, void* workspace, int32_t* status,
                        hipStream_t stream);
 
+// The update's coefficients, in the order emb_adam_coeffs writes them.
 struct AdamCoeffs {
   float beta1, one_minus_beta1, beta2, one_minus_beta2;
   float step_size;  // lr / (1 - beta1^t)
   float inv_bc2;    // 1 / (1 - beta2^t)
   float eps;
 };
+static_assert(sizeof(AdamCoeffs) <= EMB_ADAM_COEFFS_WORDS * sizeof(float), "coefficients fit their words");
+// The coefficients of step `step`, formed in fp64 and rounded once to fp32; EMB_ERR_INVALID_ARG for
+// hyper-parameters the update refuses.
+int adam_coeffs(double lr, double beta1, double beta2, double eps, int64_t step, AdamCoeffs* c);
 
 // start / stop (may be null): timing events around the kernel; stop is
 // attached to the kernel's dispatch (no separate marker packet), start is
 // recorded just before it.
+// coeffs_dev (may be null): device memory holding the coefficients, read by the
+// kernel when it runs in place of `c` (steps replayed from a graph).
 hipError_t launch_adam(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int D, const int32_t* row_ids,
                        const float* rows, const int32_t* offsets, int shard_begin, int shard_end, int cap_rows,
-                       const AdamCoeffs& c, int32_t* status, hipStream_t stream, hipEvent_t start = nullptr,
-                       hipEvent_t stop = nullptr);
-// emb_sparse_adam_apply with the optional start / stop events of launch_adam.
+                       const AdamCoeffs& c, const AdamCoeffs* coeffs_dev, int32_t* status, hipStream_t stream,
+                       hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
+// emb_sparse_adam_apply with the optional start / stop events of launch_adam and
+// coefficients in device memory.
 int sparse_adam_call(float* table, float* exp_avg, float* exp_avg_sq, int64_t V, int32_t D, const int32_t* row_ids,
                      const float* rows, const int32_t* offsets, int32_t P, int32_t shard_begin, int32_t shard_end,
                      int32_t cap_rows, double lr, double beta1, double beta2, double eps, int64_t step,
-                     int32_t* dev_status, hipStream_t stream, hipEvent_t start, hipEvent_t stop);
+                     const void* coeffs_dev, int32_t* dev_status, hipStream_t stream, hipEvent_t start,
+                     hipEvent_t stop);
 
 // Carves aligned regions out of a workspace; with base == nullptr it only measures.
 struct Carver {

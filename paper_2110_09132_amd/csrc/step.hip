@@ -53,6 +53,7 @@ struct Order {
   StepSignals* sig;  // null: the schedule's events
   uint32_t seq;      // this step's number (signals)
   uint32_t sets;     // buffer sets in rotation: a set's buffers come back after this many steps
+  bool capturing;    // the streams are being captured into a graph: no events attached to dispatches
 
   void* event(Stage k) const {
     switch (k) {
@@ -64,8 +65,9 @@ struct Order {
       default: return s->delayed_done;
     }
   }
-  // The event to attach to the last kernel of stage k (events only).
-  hipEvent_t attach(Stage k) const { return sig != nullptr ? nullptr : E(event(k)); }
+  // The event to attach to the last kernel of stage k (events only, and not under capture, where an
+  // event attached to a dispatch would not become a node of the graph).
+  hipEvent_t attach(Stage k) const { return (sig != nullptr || capturing) ? nullptr : E(event(k)); }
   // Stage k of this step ends here on `stream`; `attached`: its event was attached to the last kernel.
   int done(Stage k, void* stream, bool attached = false) const {
     if (sig != nullptr) return write(k, stream);
@@ -141,7 +143,8 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     const hipEvent_t first = t1 != nullptr ? E(t1) : end_ev;
     return ok(emb::sparse_adam_call(a->table, a->exp_avg, a->exp_avg_sq, a->V, a->D, a->send_ids, a->send_rows,
                                     a->send_offsets + groups_from, a->P, 0, a->P, a->cap_rows, a->lr, a->beta1,
-                                    a->beta2, a->eps, a->step, a->dev_status, S(stream), E(t0), first)) &&
+                                    a->beta2, a->eps, a->step, a->adam_coeffs, a->dev_status, S(stream), E(t0),
+                                    first)) &&
            ok(order.done(end_stage, stream, t1 == nullptr && end_ev != nullptr));
   };
   if (s->by_owner) {
@@ -174,12 +177,13 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
     if (sep_sr && !ok(order.after(s->pack, kSorted, 0))) return st;
     if (!chained && !ok(order.after(s->pack, kUpdated, order.sets))) return st;
     if (s->split && !ok(order.after(s->pack, kDelayedDone, order.sets))) return st;
+    const hipEvent_t coalesced_ev = order.attach(kCoalesced);
     if (!ok(launched(emb::launch_coalesce_reduce(a->ids, a->T, a->grad, a->grad_dtype == EMB_BF16, a->D, a->V, var,
                                                  a->send_ids, a->seg_offsets, a->send_rows, a->num_unique,
                                                  a->send_counts, a->send_offsets, a->ws_coalesce, a->dev_status,
-                                                 S(s->pack), order.attach(kCoalesced)))))
+                                                 S(s->pack), coalesced_ev))))
       return st;
-    if (!ok(order.done(kCoalesced, s->pack, true))) return st;
+    if (!ok(order.done(kCoalesced, s->pack, coalesced_ev != nullptr))) return st;
     if (!ok(record(s->timing[3], s->pack))) return st;
     if (s->split) {
       // lookup(s): after the delayed update of step s-2 (its rows may be in this
@@ -187,10 +191,11 @@ int enqueue_step(const emb_step_args* a, const emb_step_schedule* s, const Order
       const bool sep_d = s->delayed != s->lookup_update;
       if (!ok(order.after(s->lookup_update, kDelayedDone, 2))) return st;
       if (!ok(record(s->timing[0], s->lookup_update))) return st;
+      const hipEvent_t gathered_ev = order.attach(kGathered);
       if (!ok(launched(emb::launch_gather(a->table, a->V, a->D, a->ids, a->T, a->lookup, a->dev_status,
-                                          S(s->lookup_update), order.attach(kGathered)))))
+                                          S(s->lookup_update), gathered_ev))))
         return st;
-      if (!ok(order.done(kGathered, s->lookup_update, true))) return st;
+      if (!ok(order.done(kGathered, s->lookup_update, gathered_ev != nullptr))) return st;
       if (!ok(record(s->timing[1], s->lookup_update))) return st;
       // prior update(s): the rows the next lookup reads, right after this lookup
       if (sep_p && !ok(order.after(s->lookup_update, kCoalesced, 0))) return st;
@@ -316,7 +321,17 @@ int emb_train_step(const emb_step_args* a, const emb_step_schedule* s) {
         a->num_unique, a->ws_coalesce, a->ws_coalesce_bytes);
     if (st != EMB_OK) return st;
   }
-  Order order{s, static_cast<StepSignals*>(s->signals), 0, sets};
+  // under stream capture: events only, no timing pairs, no events attached to dispatches
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(S(s->lookup_update), &cap) != hipSuccess) return EMB_ERR_LAUNCH;
+  const bool capturing = cap != hipStreamCaptureStatusNone;
+  if (capturing) {
+    if (!events) return EMB_ERR_UNSUPPORTED;
+    for (void* t : s->timing)
+      if (t != nullptr) return EMB_ERR_UNSUPPORTED;
+  }
+  if (a->adam_coeffs != nullptr && reinterpret_cast<uintptr_t>(a->adam_coeffs) % 16 != 0) return EMB_ERR_INVALID_ARG;
+  Order order{s, static_cast<StepSignals*>(s->signals), 0, sets, capturing};
   if (order.sig != nullptr) order.seq = ++order.sig->seq;
   const int st = enqueue_step(a, s, order);
   if (st != EMB_OK) order.release_all();

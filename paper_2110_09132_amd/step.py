@@ -25,8 +25,9 @@ import ctypes
 
 import torch
 
-from . import (EMB_BF16, EMB_F32, EmbError, Event, StepArgs, StepSchedule, StepSignals, _check, _grad, _need,
-               _owners, grad_coalesce_split_workspace_bytes, lib, new_workspace, pack_by_owner_workspace_bytes)
+from . import (EMB_ADAM_COEFFS_WORDS, EMB_BF16, EMB_F32, EmbError, Event, StepArgs, StepSchedule, StepSignals,
+               _check, _grad, _need, _owners, adam_coeffs, grad_coalesce_split_workspace_bytes, lib, new_workspace,
+               pack_by_owner_workspace_bytes)
 
 # timing pairs of emb_step_schedule.timing; with the split, "pack" times the
 # prior update and "adam" the delayed one
@@ -168,12 +169,14 @@ class StepPipeline:
             self.args.append(args)
             self.sched.append(scheds)
 
-    def step(self, batches, t: int, timing=None, next_ids=None):
+    def step(self, batches, t: int, timing=None, next_ids=None, adam_coeffs_ptr=None):
         """Enqueue one step.  batches: [(ids int32 [T], grad [T, D]) per table]; t: Adam step (>= 1).
         timing: optional dict stage -> (begin Event, end Event) of library timing events, recorded
         around the calls of the first table on the streams they run on.
         next_ids (split): [ids int32 per table] of the next step's batches (an empty tensor after
-        the last step).  Inputs must be ready on the main stream when the first step is enqueued."""
+        the last step).  adam_coeffs_ptr: optional device address of this step's update coefficients
+        (emb_step_args.adam_coeffs; StepGraph sets it).  Inputs must be ready on the main stream
+        when the first step is enqueued."""
         i = self.count % self.sets
         if self.count == 0 and self.overlap:
             for side in self._sides():
@@ -204,6 +207,7 @@ class StepPipeline:
             a.grad = grad.data_ptr()
             a.grad_dtype = EMB_BF16 if grad.dtype == torch.bfloat16 else EMB_F32
             a.step = t
+            a.adam_coeffs = adam_coeffs_ptr
             s.reuse = 1 if self.count >= self.sets else 0
             for n in range(8):
                 s.timing[n] = None
@@ -222,3 +226,61 @@ class StepPipeline:
         """Make the main stream wait for everything enqueued on the side streams."""
         for side in self._sides():
             self.main.wait_stream(side)
+
+
+class StepGraph:
+    """`len(batches)` training steps of `tables` captured once into a HIP graph (stream capture of the
+    step executor's calls, the cross-stream order by events) and replayed with one launch: for
+    pipelines whose host enqueue time bounds them (small batches).  The steps' batches are fixed
+    at capture (a loop feeding new batches would copy them into the captured buffers); the Adam
+    step numbers are not: every step's update reads its coefficients from a device buffer that
+    replay() fills for the step numbers it runs (emb_adam_coeffs; Sec. 5.7: one step count per
+    iteration).  A replay runs after the work before it on its stream and before the work after
+    it, whole, so the pipeline fills and drains once per replay: a graph should hold many steps.
+    Events only (no step signals), no split.  Capture a graph after some eager steps have run in
+    the process (the kernels' code is then loaded).  A graph holds at most one step per buffer
+    set (no set is used twice inside one capture): the only configuration tested on the GPU; a
+    graph of many steps over four sets ended its process with a segmentation fault whose cause
+    is not known."""
+
+    def __init__(self, tables, lr, beta1, beta2, eps, batches, sets: int = 4, sort_streams: int = 2,
+                 paired: bool = True, dev_status: torch.Tensor | None = None):
+        if len(batches) > sets:
+            raise ValueError(f"a graph holds at most one step per buffer set ({len(batches)} steps, {sets} sets)")
+        self.n = len(batches)
+        self.hp = (lr, beta1, beta2, eps)
+        dev = tables[0].W.device
+        self.coeffs_dev = torch.zeros((self.n, EMB_ADAM_COEFFS_WORDS), dtype=torch.float32, device=dev)
+        # two pinned staging buffers in turn: one can be refilled while the other's copy is pending
+        self.coeffs_host = [torch.zeros((self.n, EMB_ADAM_COEFFS_WORDS), dtype=torch.float32, pin_memory=True)
+                            for _ in range(2)]
+        self.copied = [None, None]  # the event after each staging buffer's last copy
+        self.turn = 0
+        self.stream = torch.cuda.Stream(device=dev)  # the capture stream (not the default stream)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(self.stream):
+            # a fresh pipeline: the first use of each buffer set in the capture waits for nothing before it
+            self.pipe = StepPipeline(tables, lr, beta1, beta2, eps, overlap=True, dev_status=dev_status,
+                                     signals=False, sets=sets, sort_streams=sort_streams, paired=paired)
+            self.graph.capture_begin()
+            try:
+                for i, b in enumerate(batches):
+                    self.pipe.step(b, 1, adam_coeffs_ptr=self.coeffs_dev[i].data_ptr())
+                self.pipe.finish()
+            finally:
+                self.graph.capture_end()
+
+    def replay(self, step0: int):
+        """Run the captured steps on the current stream as Adam steps step0 .. step0 + n - 1."""
+        buf = self.coeffs_host[self.turn]
+        if self.copied[self.turn] is not None:
+            self.copied[self.turn].synchronize()  # its previous copy has been read
+        lr, b1, b2, eps = self.hp
+        for i in range(self.n):
+            adam_coeffs(lr, b1, b2, eps, step0 + i, buf[i])
+        self.coeffs_dev.copy_(buf, non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record()
+        self.copied[self.turn] = ev
+        self.turn ^= 1
+        self.graph.replay()

@@ -118,3 +118,76 @@ def check_adam(state_dev, pack_dev, P, shard_begin, shard_end, hp, step, rtol=to
     for t, s in zip((W, M, S), snap):
         assert torch.equal(t[mask], s[mask]), "an untouched row changed"
     return max(ratios)
+
+
+def check_steps_against_oracle(wl, tbs, W0s, owns, host_batches, steps, split, looked=None, seed=7):
+    """The state the step executor left after `steps` steps of workload `wl` (one buffer set per step,
+    so every step's send buffers survive) against the oracle, for every table:
+      - each step's send layout (ids, counts, offsets; with the split, the 2P groups of the prior and
+        delayed rows) bit-exact against the oracle's owner-major pack (or split pack) of its coalesce,
+        and the rows within the fp32 summation bound;
+      - each step's sampled lookup (looked[s][k] = (positions, rows), if given) against the table as
+        the previous steps left it, replayed on the CPU: bit-exact at the first step, then to the Adam
+        tolerance;
+      - W, m, v after the steps against the oracle's Adam applied to the GPU's own send rows, on a
+        sample of touched rows, with the update W_after - W_before judged on its own scale, and
+        untouched rows bit-identical.
+    host_batches[s][k] = (ids, grads) of step s (steps + 1 of them with the split: the last is only
+    the next batch)."""
+    rng = np.random.default_rng(seed)
+    for k, (sp, tb, W0, own) in enumerate(zip(wl.tables, tbs, W0s, owns)):
+        bf16 = sp.grad_dtype == "bf16"
+        G_of = [host_batches[s][k] for s in range(len(host_batches))]
+        # rows to replay on the CPU: some of every batch, plus untouched ones
+        touched = np.unique(np.concatenate([ids for ids, _ in G_of[:steps]]))
+        extra = [G_of[s][0][looked[s][k][0]] for s in range(steps)] if looked is not None else []
+        sample = np.unique(np.concatenate([rng.choice(touched, min(384, touched.size), replace=False)] + extra))
+        untouched = np.setdiff1d(rng.choice(sp.V, min(sp.V, 2048), replace=False), touched)[:64]
+        idx = {int(r): i for i, r in enumerate(sample)}
+        Wc = W0[sample].copy()
+        Mc = np.zeros_like(Wc)
+        Sc = np.zeros_like(Wc)
+        for s in range(steps):
+            ids, G = G_of[s]
+            if looked is not None:
+                pos, got = looked[s][k]
+                want = Wc[[idx[int(i)] for i in ids[pos]]]
+                if s == 0:
+                    assert np.array_equal(host(got).view(np.uint32), want.view(np.uint32)), \
+                        f"table {k}: lookup of step 1"
+                else:
+                    tolerance.assert_rows_close(host(got), want, what=f"table {k}: lookup of step {s + 1}")
+            # the send layout of step s (buffer set s) against the oracle
+            sid, srows, cnt, offs = tb.send[s]
+            orc = oracle.coalesce(ids, G, sp.V, grad_is_bf16=bf16)
+            if split:
+                pk = oracle.split_pack(orc["uniq_ids"], orc["uniq_grad"], G_of[s + 1][0], own, sp.P)
+                ng = 2 * sp.P
+            else:
+                pk = oracle.pack_by_owner(orc["uniq_ids"], orc["uniq_grad"], own, sp.P)
+                ng = sp.P
+            U = orc["U"]
+            offs_h = host(offs)[:ng + 1]
+            assert np.array_equal(offs_h, pk["send_offsets"]), f"table {k} step {s + 1}: send offsets"
+            assert np.array_equal(host(cnt)[:ng], pk["send_counts"]), f"table {k} step {s + 1}: send counts"
+            got_ids = host(sid[:U])
+            assert np.array_equal(got_ids, pk["send_ids"]), f"table {k} step {s + 1}: send ids"
+            rows_h = host(srows[:U])
+            order_u = np.searchsorted(orc["uniq_ids"], got_ids)
+            tolerance.assert_grad_close(rows_h, orc["sum_f64"][order_u], orc["absum"][order_u],
+                                        what=f"table {k} step {s + 1}: send rows")
+            # the oracle's Adam on the sampled rows with the GPU's own send rows of this step (with the
+            # split the prior and the delayed part, same step, touch disjoint rows: one call covers both)
+            sel = np.nonzero(np.isin(got_ids, sample))[0]
+            local = np.array([idx[int(i)] for i in got_ids[sel]], dtype=np.int32)
+            oracle.sparse_adam(Wc, Mc, Sc, local, rows_h[sel], np.array([0, sel.size], np.int32), 0, 1, wl.lr,
+                               wl.beta1, wl.beta2, wl.eps, s + 1)
+        sel_dev = torch.from_numpy(sample.astype(np.int64)).to(tb.W.device)
+        Wg = host(tb.W[sel_dev])
+        for t, ref, what in ((Wg, Wc, "table"), (host(tb.M[sel_dev]), Mc, "exp_avg"),
+                             (host(tb.S[sel_dev]), Sc, "exp_avg_sq")):
+            tolerance.assert_rows_close(t, ref, what=f"table {k}: {what}")
+        tolerance.assert_update_close(Wg, W0[sample], Wc, ulps=steps, what=f"table {k}: update over {steps} steps")
+        un_dev = torch.from_numpy(untouched.astype(np.int64)).to(tb.W.device)
+        assert np.array_equal(host(tb.W[un_dev]).view(np.uint32), W0[untouched].view(np.uint32))
+        assert not host(tb.M[un_dev]).any() and not host(tb.S[un_dev]).any()

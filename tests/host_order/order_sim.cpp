@@ -15,8 +15,9 @@
 //    steps: the lookup of step n reads the rows of batch n, its update writes them; with the split,
 //    the prior update writes the rows of batch n that batch n + 1 also holds and the delayed update
 //    the others, which no operation on batch n + 1 touches.
-// Scenarios: every mode (coalesce then pack, owner-major, owner-major with the split) with events
-// and with signals, two to six buffer sets, and stream choices that include a set's streams
+// Scenarios: every mode (coalesce then pack, owner-major, owner-major with the split) with events,
+// with signals and with events under graph capture (no event attached to a dispatch), two to six
+// buffer sets, more steps than sets, and stream choices that include a set's streams
 // changing between its uses; signal handles reused from the pool across modes; a call that fails
 // part-way; and a long random mix of modes (deadlock freedom only).
 #include <hip/hip_runtime.h>
@@ -240,6 +241,11 @@ hipError_t hipStreamSynchronize(hipStream_t) {
   drain();
   return hipSuccess;
 }
+bool g_capturing = false;  // the streams are being captured into a graph
+hipError_t hipStreamIsCapturing(hipStream_t, hipStreamCaptureStatus* st) {
+  *st = g_capturing ? hipStreamCaptureStatusActive : hipStreamCaptureStatusNone;
+  return hipSuccess;
+}
 hipError_t hipGetDevice(int* d) {
   *d = 0;
   return hipSuccess;
@@ -255,6 +261,7 @@ namespace emb {
 hipError_t launch_gather(const float* table, int64_t, int, const int32_t*, int, float*, int32_t*, hipStream_t stream,
                          hipEvent_t done) {
   push(stream, launch_op("gather", {}, kAllRows, table));
+  if (done && g_capturing) fail("an event attached to a dispatch under capture");
   if (done) (void)hipEventRecord(done, stream);  // an event attached to the dispatch completes with it
   return hipSuccess;
 }
@@ -267,6 +274,7 @@ hipError_t launch_coalesce_reduce(const int32_t*, int, const void*, bool, int, i
                                   int32_t* send_ids, int32_t*, float*, int32_t*, int32_t*, int32_t*, void* ws,
                                   int32_t*, hipStream_t stream, hipEvent_t done) {
   push(stream, launch_op("reduce", {{ws, false}, {send_ids, true}}));
+  if (done && g_capturing) fail("an event attached to a dispatch under capture");
   if (done) (void)hipEventRecord(done, stream);
   return hipSuccess;
 }
@@ -277,13 +285,14 @@ int coalesce_by_owner_args_status(const int32_t*, int32_t, const void*, int32_t,
 }
 int sparse_adam_call(float* table, float*, float*, int64_t, int32_t, const int32_t* send_ids, const float*,
                      const int32_t* offsets, int32_t P, int32_t, int32_t, int32_t, double, double, double, double,
-                     int64_t, int32_t*, hipStream_t stream, hipEvent_t, hipEvent_t stop) {
+                     int64_t, const void*, int32_t*, hipStream_t stream, hipEvent_t, hipEvent_t stop) {
   // the split's two parts: groups [0, P) prior, [P, 2P) delayed (offsets is send_offsets + P)
   extern const int32_t* g_offsets_base;
   RowSet rows = kAllRows;
   if (g_offsets_base != nullptr) rows = offsets == g_offsets_base ? kPriorRows : kDelayedRows;
   push(stream, launch_op("adam", {{send_ids, false}}, rows, table));
   (void)P;
+  if (stop && g_capturing) fail("an event attached to a dispatch under capture");
   if (stop) (void)hipEventRecord(stop, stream);
   return EMB_OK;
 }
@@ -379,10 +388,14 @@ void streams_for(int r, long n, int k, unsigned& rnd_state, emb_step_schedule& s
 void happens_before_scenarios() {
   static char table_mem[64];
   int scenarios = 0;
-  for (int signals = 0; signals < 2; ++signals)
+  // order 0: events; 1: step signals; 2: events under graph capture (no event attached to a dispatch:
+  // every stage's end is an event record of its own)
+  for (int order = 0; order < 3; ++order)
     for (int mode = 0; mode < 3; ++mode)
       for (int sets = 2; sets <= 6; ++sets) {
+        const bool signals = order == 1;
         if (!signals && mode == 2 && sets != 2) continue;  // with events the split takes two sets
+        g_capturing = order == 2;
         for (int r = 0; r < 7; ++r) {
           drain();
           g_clock.clear();
@@ -422,13 +435,14 @@ void happens_before_scenarios() {
             if (step(t, mode, false) != EMB_OK) fail("happens-before step");
           }
           char name[96];
-          std::snprintf(name, sizeof name, "%s, mode %d, %d sets, streams rule %d", signals ? "signals" : "events",
-                        mode, sets, r);
+          std::snprintf(name, sizeof name, "%s, mode %d, %d sets, streams rule %d",
+                        order == 0 ? "events" : order == 1 ? "signals" : "events under capture", mode, sets, r);
           check_happens_before(name);
           g_track = false;
           if (signals) drop_handle(t);
           ++scenarios;
         }
+        g_capturing = false;
       }
   std::printf("happens-before: %d scenarios ordered\n", scenarios);
 }

@@ -5,6 +5,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_2110_09132_amd as emb
@@ -33,7 +34,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings_and_version():
-    assert emb.abi_version() == 1
+    assert emb.abi_version() == 2
     assert emb.status_string(emb.EMB_OK) == "ok"
     assert "workspace" in emb.status_string(emb.EMB_ERR_WORKSPACE)
 
@@ -106,6 +107,22 @@ def test_coalesce_by_owner_noalloc_size_limit():
     for T, V, D, g in ((65536, 1 << 20, 256, 0), (16384, 262144, 1024, 1), (25000, 32768, 512, 0),
                        (16384, 32000, 1024, 0)):
         assert L.emb_grad_coalesce_workspace_bytes(T, V, D, g) <= emb.NOALLOC_SCRATCH_BYTES
+
+
+def test_adam_coeffs_host_helper():
+    # the coefficients a replayed graph reads: as emb_sparse_adam_apply forms them (fp64, rounded once)
+    import torch
+    out = torch.zeros(emb.EMB_ADAM_COEFFS_WORDS, dtype=torch.float32)
+    for step in (1, 2, 10, 1000):
+        emb.adam_coeffs(1e-3, 0.9, 0.999, 1e-8, step, out)
+        bc1, bc2 = 1 - 0.9 ** step, 1 - 0.999 ** step
+        want = np.array([0.9, 1 - 0.9, 0.999, 1 - 0.999, 1e-3 / bc1, 1 / bc2, 1e-8, 0.0], dtype=np.float32)
+        assert np.array_equal(out.numpy(), want)
+    L = emb.lib
+    buf = (ctypes.c_float * 8)()
+    assert L.emb_adam_coeffs(1e-3, 0.9, 0.999, 1e-8, 0, buf) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_adam_coeffs(1e-3, 1.0, 0.999, 1e-8, 1, buf) == emb.EMB_ERR_INVALID_ARG
+    assert L.emb_adam_coeffs(1e-3, 0.9, 0.999, 1e-8, 1, NULL) == emb.EMB_ERR_INVALID_ARG
 
 
 def test_lookup_request_validation_and_workspace_query():

@@ -5,8 +5,10 @@ that no write enqueued before it supplies, never let a signal word decrease, and
 across handles reused between modes, a call that fails part-way, and a long random mix of modes and
 single-stream schedules.  With a vector clock per stream it also checks happens-before: every two
 launches that touch the same buffer of a set, or overlapping table rows, one of them writing, run in
-the order the executor enqueued them, for every mode, events and signals, two to six buffer sets, and
-stream choices that include a set's streams changing between its uses.  No GPU is used."""
+the order the executor enqueued them, for every mode, events, signals and events under graph capture
+(every stage's end an event record of its own, none attached to a dispatch), two to six buffer sets
+with more steps than sets, and stream choices that include a set's streams changing between its uses.
+No GPU is used."""
 import os
 import shutil
 import subprocess
