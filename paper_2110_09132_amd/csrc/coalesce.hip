@@ -50,24 +50,31 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kItems = 8;
 constexpr int kMaxPasses = 4;  // up to 31 key bits
 
-// Radix configuration: 256-thread tiles of 2048 keys, digits of at most 8 bits,
-// or 9 bits where that saves a pass (keys of 9, 17-18 or 25-27 bits: one, two or
-// three passes instead of two, three or four).  (Two passes of 11-bit digits
-// were measured slower than three of 8 bits for 24-bit keys: the 2048-bin
-// ranking is LDS-bound and runs on half as many tiles.)
+// Radix configuration: sort tiles of 1024 keys on 512 threads (two keys per
+// thread), key-build tiles of 2048 tokens (four per thread), digits of at most
+// 8 bits, or 9 bits where that saves a pass (keys of 9, 17-18 or 25-27 bits:
+// one, two or three passes instead of two, three or four).  The passes are
+// latency-bound (a few dozen tiles on 256 CUs), so short per-thread chains win:
+// measured per owner-major call against 256-thread tiles of 2048 keys with
+// 2048-token key-build tiles, 4.5 to 8.8 us less on every workload (72.6 ->
+// 68.2 us for 65536 tokens of 24-bit keys); 1024 threads, or 4096- and
+// 8192-token key-build tiles, were slower.  (Two passes of 11-bit digits were
+// measured slower than three of 8 bits for 24-bit keys: the 2048-bin ranking
+// is LDS-bound and runs on half as many tiles.)
 template <int NT, int BITS>
 struct SortCfg {
   static constexpr int kNT = NT;
   static constexpr int kBins = 1 << BITS;
+  static constexpr int kItems = 2;               // keys per thread of a sort tile
   static constexpr int kTile = NT * kItems;      // keys per sort tile
-  static constexpr int kUpTile = NT * 8;         // keys per histogram tile
-  static constexpr int kPasses = kMaxPasses;  // most passes this configuration runs
+  static constexpr int kUpTile = 2048;           // tokens per key-build (histogram) tile
+  static constexpr int kPasses = kMaxPasses;     // most passes this configuration runs
+  static_assert(kUpTile % NT == 0, "whole key-build rounds");
 };
-using Narrow = SortCfg<256, 8>;
-using Wide9 = SortCfg<256, 9>;
+using Narrow = SortCfg<512, 8>;
+using Wide9 = SortCfg<512, 9>;
 constexpr int kWide9Passes = 3;  // most passes of 9-bit digits
 // Histogram and look-back words per tile, for every pass of either configuration.
 constexpr int kHistPerTile = kMaxPasses * Narrow::kBins > kWide9Passes * Wide9::kBins ? kMaxPasses * Narrow::kBins
@@ -346,7 +353,7 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     const uint32_t* __restrict__ up_hist, int nup, uint32_t* lookback,
     uint32_t* ticket, int ntiles, uint32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out,
     uint32_t* __restrict__ n_valid, int32_t* status) {
-  constexpr int NT = C::kNT, kBins = C::kBins, kTile = C::kTile, NW = NT / kWave;
+  constexpr int NT = C::kNT, kBins = C::kBins, kTile = C::kTile, NW = NT / kWave, kItems = C::kItems;
   constexpr int kDigitsPerThread = (kBins + NT - 1) / NT;
   __shared__ uint32_t cnt[NW * kBins];
   __shared__ uint32_t dstart[kBins], gbase[kBins];

@@ -1,5 +1,5 @@
 """Parity of each C ABI call with the oracle at sizes the oracle finishes in
-seconds: several sort tiles (2048 keys) and reduction chunks (32 tokens) with
+seconds: several sort tiles (1024 keys) and reduction chunks (32 tokens) with
 ragged tails, every gradient width path (vector and scalar), bf16 gradients,
 hot rows spanning many chunks, empty and degenerate inputs."""
 import numpy as np
@@ -62,8 +62,9 @@ def test_gather_empty():
 # -------------------------------------------------------------------- coalesce
 @pytest.mark.parametrize("law,V,T,D", [
     ("zipf", 1000, 512, 64),         # the tiny workload's shape
-    ("zipf", 5000, 2048, 8),         # exactly one sort tile
-    ("zipf", 5000, 2049, 3),         # ragged second tile, scalar width path
+    ("zipf", 5000, 2048, 8),         # the most tokens of the one-workgroup path
+    ("zipf", 5000, 3072, 8),         # exactly three sort tiles
+    ("zipf", 5000, 2049, 3),         # two whole sort tiles and one key, scalar width path
     ("uniform", 1 << 20, 10000, 16),  # 20 key bits: three passes of 7 bits
     ("zipf", 32768, 25000, 65),      # odd width (scalar path), many chunks
     ("zipf", 300, 4001, 256),        # very heavy duplication; 9 key bits: one 9-bit pass
