@@ -15,8 +15,12 @@
 //  2. sort_pass, once per digit of the key bits (<= 8 bits each, 9 where that
 //     saves a pass): a stable LSD radix pass over (key, token position).
 //     Each tile ranks its keys in LDS with wave ballots, publishes its
-//     per-digit counts and reads the counts of the tiles before it (decoupled
+//     per-digit counts (before the ranking, so that the tiles after it find
+//     them early) and reads the counts of the tiles before it (decoupled
 //     look-back, Merrill & Garland 2016), so one launch per pass suffices.
+//     Pass 0 sums the key build's histograms into digit totals; its first
+//     tiles, once done, leave the digit starts of the later passes, which then
+//     read one word per digit instead of every histogram.
 //     Tiles take their index from a ticket counter, so a tile only waits for
 //     tiles that are already running.  The sorted sequence holds the n_valid
 //     tokens that take part.
@@ -89,6 +93,8 @@ constexpr int kLoadsInFlight = 8;
 constexpr int kCombineThreads = 1024;
 constexpr int kCombineWaves = kCombineThreads / kWave;
 constexpr uint32_t kSpinLimit = 1u << 22;
+constexpr int kTotalsBatch = 32;     // digit-total loads in flight per thread (tiles of the key build)
+constexpr int kLookBackWindow = 16;  // look-back status words in flight per thread
 
 // Look-back status word: value in the low 30 bits, state in the top 2 bits.
 constexpr uint32_t kAggregate = 1u << 30;  // the tile's own count
@@ -198,8 +204,11 @@ __global__ __launch_bounds__(kThreads) void tab_insert_kernel(const int32_t* __r
 // status words lb[t * stride] (nearest first, kWindow at a time) until a tile with
 // an inclusive count is found.  Every tile publishes its aggregate before it
 // waits, so the wait ends; it is bounded anyway and reports EMB_DEV_STALLED.
+// The status words of tiles on other XCDs are read from beyond their L2: a
+// window costs about a microsecond, and wider windows (32, 64 words per thread)
+// were measured slower than 16.
+template <int kWindow>
 __device__ uint32_t digit_look_back(uint32_t* lb, int tile, int stride, int32_t* status) {
-  constexpr int kWindow = 16;
   uint32_t excl = 0;
   int j = tile - 1;
   uint32_t spins = 0;
@@ -347,30 +356,66 @@ __global__ __launch_bounds__(C::kNT) void sort_keys_upsweep_kernel(const int32_t
   for (int i = blockIdx.x * NT + threadIdx.x; i < zero_words; i += gridDim.x * NT) zero_begin[i] = 0;
 }
 
+// The count of digit d (clamped to a valid digit) of pass p over the key
+// build's nup histograms, kTotalsBatch loads in flight.
+template <int kBins>
+__device__ __forceinline__ uint32_t digit_total(const uint32_t* __restrict__ up_hist, int nup, int npass, int p, int d) {
+  uint32_t tot = 0;
+  for (int u0 = 0; u0 < nup; u0 += kTotalsBatch) {
+    uint32_t v[kTotalsBatch];
+#pragma unroll
+    for (int z = 0; z < kTotalsBatch; ++z)
+      v[z] = up_hist[(static_cast<size_t>(min(u0 + z, nup - 1)) * npass + p) * kBins + min(d, kBins - 1)];
+#pragma unroll
+    for (int z = 0; z < kTotalsBatch; ++z) tot += (u0 + z < nup) ? v[z] : 0u;
+  }
+  return tot;
+}
+
 template <class C>
 __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int T, RadixPlan plan, int pass,
     const uint32_t* __restrict__ up_hist, int nup, uint32_t* lookback,
     uint32_t* ticket, int ntiles, uint32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out,
-    uint32_t* __restrict__ n_valid, int32_t* status) {
+    uint32_t* __restrict__ n_valid, uint32_t* __restrict__ starts, int32_t* status) {
   constexpr int NT = C::kNT, kBins = C::kBins, kTile = C::kTile, NW = NT / kWave, kItems = C::kItems;
   constexpr int kDigitsPerThread = (kBins + NT - 1) / NT;
   __shared__ uint32_t cnt[NW * kBins];
-  __shared__ uint32_t dstart[kBins], gbase[kBins];
+  __shared__ uint32_t dstart[kBins], gbase[kBins], thist[kBins];
   __shared__ uint32_t wsum[NW];
   __shared__ uint32_t skeys[kTile];
   __shared__ int32_t svals[kTile];
   __shared__ int tile_s;
-  if (threadIdx.x == 0) tile_s = static_cast<int>(atomicAdd(ticket, 1u));
+  // The ticket's round trip overlaps the loads of the digit totals, which do
+  // not depend on the tile.
+  uint32_t ticket_v = 0;
+  if (threadIdx.x == 0) ticket_v = atomicAdd(ticket, 1u);
+  const int shift = plan.shift(pass);
+  const int bits = plan.bits(pass);
+  const int bins = 1 << bits;
+  // where each digit starts in the sorted output: pass 0 sums the digit totals
+  // of the key build's histograms and scans them; the later passes read the
+  // starts that pass 0 left, and the number of tokens that take part
+  uint32_t tot[kDigitsPerThread];
+  uint32_t tv_later = 0;
+  if (pass == 0) {
+#pragma unroll
+    for (int q = 0; q < kDigitsPerThread; ++q)
+      tot[q] = digit_total<kBins>(up_hist, nup, plan.npass, pass, static_cast<int>(threadIdx.x) + q * NT);
+  } else {
+#pragma unroll
+    for (int q = 0; q < kDigitsPerThread; ++q)
+      tot[q] = starts[pass * kBins + min(static_cast<int>(threadIdx.x) + q * NT, kBins - 1)];
+    tv_later = *n_valid;
+  }
+  for (int i = threadIdx.x; i < kBins; i += NT) thist[i] = 0;
+  if (threadIdx.x == 0) tile_s = static_cast<int>(ticket_v);
   __syncthreads();
   const int tile = tile_s;
   if (tile < 0 || tile >= ntiles) {  // the ticket counter was not cleared: never index with it
     if (threadIdx.x == 0) raise_flag(status, EMB_DEV_STALLED);
     return;
   }
-  const int shift = plan.shift(pass);
-  const int bits = plan.bits(pass);
-  const int bins = 1 << bits;
   const int base = tile * kTile;
   const int w = threadIdx.x / kWave;
 
@@ -389,48 +434,40 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     key[r] = keys_in[idx[r]];
   }
 #pragma unroll
-  for (int r = 0; r < kItems; ++r) dig[r] = (key[r] >> shift) & (bins - 1);
-  // where each digit starts in the sorted output: exclusive scan of the digit totals
-#pragma unroll
   for (int q = 0; q < kDigitsPerThread; ++q) {
     const int d = static_cast<int>(threadIdx.x) + q * NT;
-    uint32_t tot = 0;
-    for (int u0 = 0; u0 < nup; u0 += 16) {
-      uint32_t v[16];
-#pragma unroll
-      for (int z = 0; z < 16; ++z)
-        v[z] = up_hist[(static_cast<size_t>(min(u0 + z, nup - 1)) * plan.npass + pass) * kBins + min(d, kBins - 1)];
-#pragma unroll
-      for (int z = 0; z < 16; ++z) tot += (u0 + z < nup) ? v[z] : 0u;
-    }
-    if (d < kBins) gbase[d] = d < bins ? tot : 0u;
+    if (d < kBins) gbase[d] = d < bins ? tot[q] : 0u;
   }
   __syncthreads();
   // the sorted sequence holds the tokens that take part: the sum of the totals
-  const uint32_t tv = block_exclusive_scan<NT>(gbase, bins, wsum);
+  const uint32_t tv = pass == 0 ? block_exclusive_scan<NT>(gbase, bins, wsum) : tv_later;
+#pragma unroll
+  for (int r = 0; r < kItems; ++r) dig[r] = (key[r] >> shift) & (bins - 1);
   // the first pass reads every token (those that take part have a position);
   // later passes read the tv sorted tokens
 #pragma unroll
   for (int r = 0; r < kItems; ++r)
     valid[r] = inb[r] && (pass == 0 ? val[r] >= 0 : static_cast<uint32_t>(idx[r]) < tv);
   if (tile == 0 && threadIdx.x == 0) *n_valid = tv;
+  // This tile's count of each digit, published before the ranking so that the
+  // tiles after it find it when they look back.
+#pragma unroll
+  for (int r = 0; r < kItems; ++r)
+    if (valid[r]) atomicAdd(&thist[dig[r]], 1u);
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kDigitsPerThread; ++q) {
+    const int d = static_cast<int>(threadIdx.x) + q * NT;
+    if (d < bins) publish(lookback + static_cast<size_t>(tile) * kBins + d, (tile == 0 ? kInclusive : kAggregate) | thist[d]);
+  }
 
   const uint32_t nvalid = tile_stable_rank<NT, kItems>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
 #pragma unroll
   for (int q = 0; q < kDigitsPerThread; ++q) {
     const int d = static_cast<int>(threadIdx.x) + q * NT;
-    if (d < bins) {
-      const uint32_t mine = (d + 1 < bins ? dstart[d + 1] : nvalid) - dstart[d];
-      uint32_t* slot = lookback + static_cast<size_t>(tile) * kBins + d;
-      publish(slot, (tile == 0 ? kInclusive : kAggregate) | mine);
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < kDigitsPerThread; ++q) {
-    const int d = static_cast<int>(threadIdx.x) + q * NT;
     if (d < bins && tile > 0) {
-      const uint32_t mine = (d + 1 < bins ? dstart[d + 1] : nvalid) - dstart[d];
-      const uint32_t excl = digit_look_back(lookback + d, tile, kBins, status);
+      const uint32_t mine = thist[d];
+      const uint32_t excl = digit_look_back<kLookBackWindow>(lookback + d, tile, kBins, status);
       publish(lookback + static_cast<size_t>(tile) * kBins + d, kInclusive | (excl + mine));
       gbase[d] += excl;
     }
@@ -452,6 +489,23 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
       keys_out[dest] = k;
       vals_out[dest] = svals[i];
     }
+  }
+  // After its own tile, tile t of pass 0 scans the digit totals of passes
+  // t + 1, t + 1 + ntiles, ... (off the look-back chain: the first tiles finish
+  // first).
+  if (pass != 0) return;
+  for (int later = tile + 1; later < plan.npass; later += ntiles) {
+    const int lbins = 1 << plan.bits(later);
+    __syncthreads();  // gbase has been read (by the scatter, or by the previous round's stores)
+#pragma unroll
+    for (int q = 0; q < kDigitsPerThread; ++q) {
+      const int d = static_cast<int>(threadIdx.x) + q * NT;
+      const uint32_t t = digit_total<kBins>(up_hist, nup, plan.npass, later, d);
+      if (d < kBins) gbase[d] = d < lbins ? t : 0u;
+    }
+    __syncthreads();
+    block_exclusive_scan<NT>(gbase, lbins, wsum);
+    for (int d = threadIdx.x; d < kBins; d += NT) starts[later * kBins + d] = gbase[d];
   }
 }
 
@@ -969,6 +1023,7 @@ struct CoalesceWs {
   int32_t* span_count;
   uint32_t* sort_lb;     // [npass][ntiles][kBins]; ends that region (npass of the call)
   uint32_t* n_valid;     // tokens that take part (written by the radix passes)
+  uint32_t* starts;      // [kMaxPasses][512]: where each digit of passes 1.. starts (written by pass 0)
   int32_t* span_list;
   uint32_t* tile_heads;  // [nred]
   float* partial;
@@ -1011,6 +1066,7 @@ CoalesceWs carve_with(void* base, int T, int D, int T_next, int64_t V) {
   w.span_count = cv.take<int32_t>(1);
   w.sort_lb = cv.take<uint32_t>(static_cast<size_t>(kHistPerTile) * ntiles);
   w.n_valid = cv.take<uint32_t>(1);
+  w.starts = cv.take<uint32_t>(static_cast<size_t>(kMaxPasses) * Wide9::kBins);
   w.span_list = cv.take<int32_t>(nchunks);
   w.tile_heads = cv.take<uint32_t>(nred);
   w.partial = cv.take<float>(nchunks * 2 * static_cast<size_t>(D));
@@ -1053,7 +1109,7 @@ void launch_sort(const int32_t* ids, int T, const KeySpec& ks, const RadixPlan& 
   for (int p = 0; p < plan.npass; ++p) {
     hipLaunchKernelGGL(sort_pass_kernel<C>, dim3(ntiles), dim3(C::kNT), 0, stream, kin, vin, T, plan, p, ws.up_hist,
                        nup, ws.sort_lb + static_cast<size_t>(p) * ntiles * C::kBins, ws.tickets + p, ntiles, kout,
-                       vout, ws.n_valid, status);
+                       vout, ws.n_valid, ws.starts, status);
     kin = kout;
     vin = vout;
     kout = (kout == ws.keys_a) ? ws.keys_b : ws.keys_a;
