@@ -24,13 +24,19 @@ CXXFLAGS = [
 ]
 
 
+# Per-file flags.  coalesce.hip: no atomic optimizer (it turns a one-lane
+# atomic into a wave-wide form that waits for the result at once, which would
+# keep the sort passes' ticket from overlapping their first loads).
+FILE_FLAGS = {"coalesce.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
 def _compile(src, verbose):
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *CXXFLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *CXXFLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

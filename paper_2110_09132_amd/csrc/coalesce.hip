@@ -372,7 +372,10 @@ __device__ __forceinline__ uint32_t digit_total(const uint32_t* __restrict__ up_
   return tot;
 }
 
-template <class C>
+// kFirst: pass 0 (sums the key build's histograms); else a later pass (reads
+// the starts pass 0 left).  Two kernels rather than a branch, so that the
+// compiler keeps the ticket in flight beside the loads of either.
+template <class C, bool kFirst>
 __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     const uint32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in, int T, RadixPlan plan, int pass,
     const uint32_t* __restrict__ up_hist, int nup, uint32_t* lookback,
@@ -386,8 +389,9 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
   __shared__ uint32_t skeys[kTile];
   __shared__ int32_t svals[kTile];
   __shared__ int tile_s;
-  // The ticket's round trip overlaps the loads of the digit totals, which do
-  // not depend on the tile.
+  // The ticket's round trip overlaps the loads below, which do not depend on
+  // the tile (this file is built without the compiler's atomic optimizer, whose
+  // wave-wide form of an atomic waits for the result right away).
   uint32_t ticket_v = 0;
   if (threadIdx.x == 0) ticket_v = atomicAdd(ticket, 1u);
   const int shift = plan.shift(pass);
@@ -398,7 +402,7 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
   // starts that pass 0 left, and the number of tokens that take part
   uint32_t tot[kDigitsPerThread];
   uint32_t tv_later = 0;
-  if (pass == 0) {
+  if constexpr (kFirst) {
 #pragma unroll
     for (int q = 0; q < kDigitsPerThread; ++q)
       tot[q] = digit_total<kBins>(up_hist, nup, plan.npass, pass, static_cast<int>(threadIdx.x) + q * NT);
@@ -408,6 +412,7 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
       tot[q] = starts[pass * kBins + min(static_cast<int>(threadIdx.x) + q * NT, kBins - 1)];
     tv_later = *n_valid;
   }
+
   for (int i = threadIdx.x; i < kBins; i += NT) thist[i] = 0;
   if (threadIdx.x == 0) tile_s = static_cast<int>(ticket_v);
   __syncthreads();
@@ -440,14 +445,14 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
   }
   __syncthreads();
   // the sorted sequence holds the tokens that take part: the sum of the totals
-  const uint32_t tv = pass == 0 ? block_exclusive_scan<NT>(gbase, bins, wsum) : tv_later;
+  const uint32_t tv = kFirst ? block_exclusive_scan<NT>(gbase, bins, wsum) : tv_later;
 #pragma unroll
   for (int r = 0; r < kItems; ++r) dig[r] = (key[r] >> shift) & (bins - 1);
   // the first pass reads every token (those that take part have a position);
   // later passes read the tv sorted tokens
 #pragma unroll
   for (int r = 0; r < kItems; ++r)
-    valid[r] = inb[r] && (pass == 0 ? val[r] >= 0 : static_cast<uint32_t>(idx[r]) < tv);
+    valid[r] = inb[r] && (kFirst ? val[r] >= 0 : static_cast<uint32_t>(idx[r]) < tv);
   if (tile == 0 && threadIdx.x == 0) *n_valid = tv;
   // This tile's count of each digit, published before the ranking so that the
   // tiles after it find it when they look back.
@@ -493,7 +498,7 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
   // After its own tile, tile t of pass 0 scans the digit totals of passes
   // t + 1, t + 1 + ntiles, ... (off the look-back chain: the first tiles finish
   // first).
-  if (pass != 0) return;
+  if constexpr (!kFirst) return;
   for (int later = tile + 1; later < plan.npass; later += ntiles) {
     const int lbins = 1 << plan.bits(later);
     __syncthreads();  // gbase has been read (by the scatter, or by the previous round's stores)
@@ -1107,9 +1112,10 @@ void launch_sort(const int32_t* ids, int T, const KeySpec& ks, const RadixPlan& 
   uint32_t* kout = ws.keys_a;
   int32_t* vout = ws.vals_a;
   for (int p = 0; p < plan.npass; ++p) {
-    hipLaunchKernelGGL(sort_pass_kernel<C>, dim3(ntiles), dim3(C::kNT), 0, stream, kin, vin, T, plan, p, ws.up_hist,
-                       nup, ws.sort_lb + static_cast<size_t>(p) * ntiles * C::kBins, ws.tickets + p, ntiles, kout,
-                       vout, ws.n_valid, ws.starts, status);
+    hipLaunchKernelGGL((p == 0 ? sort_pass_kernel<C, true> : sort_pass_kernel<C, false>), dim3(ntiles), dim3(C::kNT), 0,
+                       stream, kin, vin, T, plan, p, ws.up_hist, nup,
+                       ws.sort_lb + static_cast<size_t>(p) * ntiles * C::kBins, ws.tickets + p, ntiles, kout, vout,
+                       ws.n_valid, ws.starts, status);
     kin = kout;
     vin = vout;
     kout = (kout == ws.keys_a) ? ws.keys_b : ws.keys_a;
