@@ -57,14 +57,15 @@ constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxPasses = 4;  // up to 31 key bits
 
 // Radix configuration: sort tiles of 1024 keys on 512 threads (two keys per
-// thread), key-build tiles of 2048 tokens (four per thread), digits of at most
+// thread), key-build tiles of 1024 tokens (two per thread), digits of at most
 // 8 bits, or 9 bits where that saves a pass (keys of 9, 17-18 or 25-27 bits:
 // one, two or three passes instead of two, three or four).  The passes are
 // latency-bound (a few dozen tiles on 256 CUs), so short per-thread chains win:
 // measured per owner-major call against 256-thread tiles of 2048 keys with
 // 2048-token key-build tiles, 4.5 to 8.8 us less on every workload (72.6 ->
 // 68.2 us for 65536 tokens of 24-bit keys); 1024 threads, or 4096- and
-// 8192-token key-build tiles, were slower.  (Two passes of 11-bit digits were
+// 8192-token key-build tiles, were slower.  Once only pass 0 summed the key
+// build's histograms, 1024-token key-build tiles gained up to 1.8 us more.  (Two passes of 11-bit digits were
 // measured slower than three of 8 bits for 24-bit keys: the 2048-bin ranking
 // is LDS-bound and runs on half as many tiles.)
 template <int NT, int BITS>
@@ -73,7 +74,7 @@ struct SortCfg {
   static constexpr int kBins = 1 << BITS;
   static constexpr int kItems = 2;               // keys per thread of a sort tile
   static constexpr int kTile = NT * kItems;      // keys per sort tile
-  static constexpr int kUpTile = 2048;           // tokens per key-build (histogram) tile
+  static constexpr int kUpTile = 1024;           // tokens per key-build (histogram) tile
   static constexpr int kPasses = kMaxPasses;     // most passes this configuration runs
   static_assert(kUpTile % NT == 0, "whole key-build rounds");
 };
