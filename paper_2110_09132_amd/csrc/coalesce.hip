@@ -357,20 +357,43 @@ __global__ __launch_bounds__(C::kNT) void sort_keys_upsweep_kernel(const int32_t
   for (int i = blockIdx.x * NT + threadIdx.x; i < zero_words; i += gridDim.x * NT) zero_begin[i] = 0;
 }
 
-// The count of digit d (clamped to a valid digit) of pass p over the key
-// build's nup histograms, kTotalsBatch loads in flight.
-template <int kBins>
-__device__ __forceinline__ uint32_t digit_total(const uint32_t* __restrict__ up_hist, int nup, int npass, int p, int d) {
+// Digit totals of pass p over the key build's nup histograms, by NT = G * kBins
+// threads: thread i sums digit i mod kBins over histograms g, g + G, ... where
+// g = i / kBins (kTotalsBatch loads in flight), so that with 8-bit digits both
+// halves of the workgroup load; digit_totals_combine adds the G parts up.
+template <int NT, int kBins>
+__device__ __forceinline__ uint32_t digit_total_part(const uint32_t* __restrict__ up_hist, int nup, int npass, int p) {
+  static_assert(NT % kBins == 0, "whole groups of digits");
+  constexpr int G = NT / kBins;
+  const int d = static_cast<int>(threadIdx.x) % kBins;
+  const int g = static_cast<int>(threadIdx.x) / kBins;
   uint32_t tot = 0;
-  for (int u0 = 0; u0 < nup; u0 += kTotalsBatch) {
+  for (int u0 = g; u0 < nup; u0 += kTotalsBatch * G) {
     uint32_t v[kTotalsBatch];
 #pragma unroll
     for (int z = 0; z < kTotalsBatch; ++z)
-      v[z] = up_hist[(static_cast<size_t>(min(u0 + z, nup - 1)) * npass + p) * kBins + min(d, kBins - 1)];
+      v[z] = up_hist[(static_cast<size_t>(min(u0 + z * G, nup - 1)) * npass + p) * kBins + d];
 #pragma unroll
-    for (int z = 0; z < kTotalsBatch; ++z) tot += (u0 + z < nup) ? v[z] : 0u;
+    for (int z = 0; z < kTotalsBatch; ++z) tot += (u0 + z * G < nup) ? v[z] : 0u;
   }
   return tot;
+}
+
+// out[d] = the sum of the G parts of digit d for d < bins, 0 for bins <= d <
+// kBins; scratch: LDS of NT words, written before the first barrier (no thread
+// may still read it), out after it.  Ends with a barrier.
+template <int NT, int kBins>
+__device__ __forceinline__ void digit_totals_combine(uint32_t part, uint32_t* scratch, uint32_t* out, int bins) {
+  constexpr int G = NT / kBins;
+  scratch[threadIdx.x] = part;
+  __syncthreads();
+  for (int d = threadIdx.x; d < kBins; d += NT) {
+    uint32_t t = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g) t += scratch[g * kBins + d];
+    out[d] = d < bins ? t : 0u;
+  }
+  __syncthreads();
 }
 
 // kFirst: pass 0 (sums the key build's histograms); else a later pass (reads
@@ -401,16 +424,13 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
   // where each digit starts in the sorted output: pass 0 sums the digit totals
   // of the key build's histograms and scans them; the later passes read the
   // starts that pass 0 left, and the number of tokens that take part
-  uint32_t tot[kDigitsPerThread];
+  static_assert(NT % kBins == 0, "a whole number of threads per digit");
+  uint32_t tot;  // pass 0: this thread's part of its digit's total; later passes: its digit's start
   uint32_t tv_later = 0;
   if constexpr (kFirst) {
-#pragma unroll
-    for (int q = 0; q < kDigitsPerThread; ++q)
-      tot[q] = digit_total<kBins>(up_hist, nup, plan.npass, pass, static_cast<int>(threadIdx.x) + q * NT);
+    tot = digit_total_part<NT, kBins>(up_hist, nup, plan.npass, pass);
   } else {
-#pragma unroll
-    for (int q = 0; q < kDigitsPerThread; ++q)
-      tot[q] = starts[pass * kBins + min(static_cast<int>(threadIdx.x) + q * NT, kBins - 1)];
+    tot = starts[pass * kBins + static_cast<int>(threadIdx.x) % kBins];
     tv_later = *n_valid;
   }
 
@@ -439,14 +459,15 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     val[r] = vals_in[idx[r]];
     key[r] = keys_in[idx[r]];
   }
-#pragma unroll
-  for (int q = 0; q < kDigitsPerThread; ++q) {
-    const int d = static_cast<int>(threadIdx.x) + q * NT;
-    if (d < kBins) gbase[d] = d < bins ? tot[q] : 0u;
-  }
-  __syncthreads();
   // the sorted sequence holds the tokens that take part: the sum of the totals
-  const uint32_t tv = kFirst ? block_exclusive_scan<NT>(gbase, bins, wsum) : tv_later;
+  uint32_t tv = tv_later;
+  if constexpr (kFirst) {
+    digit_totals_combine<NT, kBins>(tot, cnt, gbase, bins);
+    tv = block_exclusive_scan<NT>(gbase, bins, wsum);
+  } else {
+    if (threadIdx.x < kBins) gbase[threadIdx.x] = threadIdx.x < static_cast<unsigned>(bins) ? tot : 0u;
+    __syncthreads();
+  }
 #pragma unroll
   for (int r = 0; r < kItems; ++r) dig[r] = (key[r] >> shift) & (bins - 1);
   // the first pass reads every token (those that take part have a position);
@@ -502,14 +523,10 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
   if constexpr (!kFirst) return;
   for (int later = tile + 1; later < plan.npass; later += ntiles) {
     const int lbins = 1 << plan.bits(later);
-    __syncthreads();  // gbase has been read (by the scatter, or by the previous round's stores)
-#pragma unroll
-    for (int q = 0; q < kDigitsPerThread; ++q) {
-      const int d = static_cast<int>(threadIdx.x) + q * NT;
-      const uint32_t t = digit_total<kBins>(up_hist, nup, plan.npass, later, d);
-      if (d < kBins) gbase[d] = d < lbins ? t : 0u;
-    }
-    __syncthreads();
+    const uint32_t part = digit_total_part<NT, kBins>(up_hist, nup, plan.npass, later);
+    // cnt was last read by the ranking (before the scatter's barrier), gbase by
+    // the scatter or the previous round's stores (before the combine's barrier)
+    digit_totals_combine<NT, kBins>(part, cnt, gbase, lbins);
     block_exclusive_scan<NT>(gbase, lbins, wsum);
     for (int d = threadIdx.x; d < kBins; d += NT) starts[later * kBins + d] = gbase[d];
   }
