@@ -46,20 +46,24 @@ __device__ __forceinline__ uint16_t load_stream(const uint16_t* p) { return __bu
 // Wave-uniform value as an SGPR (lets the compiler use scalar loads).
 __device__ __forceinline__ int32_t uniform(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
 
-// Inclusive prefix sum across the 64 lanes of a wave.
+// Inclusive prefix sum across the 64 lanes of a wave, with DPP moves (no LDS
+// traffic, unlike lane shuffles): shifts by 1, 2, 4 and 8 lanes inside each row
+// of 16, then each row's total broadcast to the rows above it (row_bcast:15 to
+// rows 1 and 3, row_bcast:31 to rows 2 and 3).  Lanes a move does not reach
+// read 0.
 __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    uint32_t y = __shfl_up(x, o, kWave);
-    if (lane_id() >= static_cast<uint32_t>(o)) x += y;
-  }
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x111, 0xf, 0xf, false));  // row_shr:1
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x112, 0xf, 0xf, false));  // row_shr:2
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x114, 0xf, 0xf, false));  // row_shr:4
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x118, 0xf, 0xf, false));  // row_shr:8
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x142, 0xa, 0xf, false));  // row_bcast:15
+  x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x143, 0xc, 0xf, false));  // row_bcast:31
   return x;
 }
 
+// Sum over the 64 lanes of a wave, in every lane.
 __device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
-  return x;
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(wave_inclusive_scan(x)), kWave - 1));
 }
 
 // Exclusive scan, in place, of a[0..n) in LDS by a block of NT threads.
