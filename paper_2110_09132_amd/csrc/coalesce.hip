@@ -71,6 +71,7 @@ constexpr int kMaxPasses = 4;  // up to 31 key bits
 template <int NT, int BITS>
 struct SortCfg {
   static constexpr int kNT = NT;
+  static constexpr int kBits = BITS;
   static constexpr int kBins = 1 << BITS;
   static constexpr int kItems = 2;               // keys per thread of a sort tile
   static constexpr int kTile = NT * kItems;      // keys per sort tile
@@ -488,7 +489,7 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
     if (d < bins) publish(lookback + static_cast<size_t>(tile) * kBins + d, (tile == 0 ? kInclusive : kAggregate) | thist[d]);
   }
 
-  const uint32_t nvalid = tile_stable_rank<NT, kItems>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
+  const uint32_t nvalid = tile_stable_rank<NT, kItems, C::kBits>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
 #pragma unroll
   for (int q = 0; q < kDigitsPerThread; ++q) {
     const int d = static_cast<int>(threadIdx.x) + q * NT;

@@ -109,7 +109,10 @@ __device__ uint32_t block_exclusive_scan(uint32_t* a, int n, uint32_t* wsum) {
 // cnt: LDS [NT/64][bins]; dstart: LDS [bins]; wsum: LDS [NT/64].
 // On return dstart[d] is the tile-local start of digit d, lpos[] the tile
 // position of each valid key, and the function returns the number of valid keys.
-template <int NT, int ITEMS>
+// MAXBITS > 0: digits have at most MAXBITS bits, and the ballots run over all
+// MAXBITS of them, unrolled (the bits above `bits` are 0 in every lane, so
+// their ballots leave the peers unchanged); 0: a loop over `bits`.
+template <int NT, int ITEMS, int MAXBITS = 0>
 __device__ uint32_t tile_stable_rank(const uint32_t (&dig)[ITEMS], const bool (&valid)[ITEMS], int bins,
                                      int bits, uint32_t* cnt, uint32_t* dstart, uint32_t* wsum,
                                      uint32_t (&lpos)[ITEMS]) {
@@ -123,10 +126,19 @@ __device__ uint32_t tile_stable_rank(const uint32_t (&dig)[ITEMS], const bool (&
   for (int r = 0; r < ITEMS; ++r) {
     const uint32_t d = dig[r];
     uint64_t peers = __ballot(valid[r]);
-    for (int b = 0; b < bits; ++b) {
-      const bool set = (d >> b) & 1u;
-      const uint64_t m = __ballot(set);
-      peers &= set ? m : ~m;
+    if constexpr (MAXBITS > 0) {
+#pragma unroll
+      for (int b = 0; b < MAXBITS; ++b) {
+        const bool set = (d >> b) & 1u;
+        const uint64_t m = __ballot(set);
+        peers &= set ? m : ~m;
+      }
+    } else {
+      for (int b = 0; b < bits; ++b) {
+        const bool set = (d >> b) & 1u;
+        const uint64_t m = __ballot(set);
+        peers &= set ? m : ~m;
+      }
     }
     const uint32_t below = __popcll(peers & lanemask_lt());
     const uint32_t old = valid[r] ? mine[d] : 0u;
