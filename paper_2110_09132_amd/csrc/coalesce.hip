@@ -56,8 +56,9 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxPasses = 4;  // up to 31 key bits
 
-// Radix configuration: sort tiles of 1024 keys on 512 threads (two keys per
-// thread), key-build tiles of 1024 tokens (two per thread), digits of at most
+// Radix configuration: sort tiles on 512 threads, of 1024 keys (two per
+// thread), or of 1536 keys (three per thread) for batches of more than 32768
+// tokens; key-build tiles of 1024 tokens (two per thread); digits of at most
 // 8 bits, or 9 bits where that saves a pass (keys of 9, 17-18 or 25-27 bits:
 // one, two or three passes instead of two, three or four).  The passes are
 // latency-bound (a few dozen tiles on 256 CUs), so short per-thread chains win:
@@ -65,27 +66,38 @@ constexpr int kMaxPasses = 4;  // up to 31 key bits
 // 2048-token key-build tiles, 4.5 to 8.8 us less on every workload (72.6 ->
 // 68.2 us for 65536 tokens of 24-bit keys); 1024 threads, or 4096- and
 // 8192-token key-build tiles, were slower.  Once only pass 0 summed the key
-// build's histograms, 1024-token key-build tiles gained up to 1.8 us more.  (Two passes of 11-bit digits were
-// measured slower than three of 8 bits for 24-bit keys: the 2048-bin ranking
-// is LDS-bound and runs on half as many tiles.)
-template <int NT, int BITS>
+// build's histograms, 1024-token key-build tiles gained up to 1.8 us more.
+// The look-back of a tile reads its predecessors 16 at a time from beyond
+// L2, so on 65536 tokens fewer, larger tiles pay (three keys per thread: 60.5
+// -> 58.7 us; four: 59.0), while on 16384 tokens they cost 1 to 2 us.  (Two
+// passes of 11-bit digits were measured slower than three of 8 bits for
+// 24-bit keys: the 2048-bin ranking is LDS-bound and runs on half as many
+// tiles.)
+template <int NT, int BITS, int ITEMS>
 struct SortCfg {
   static constexpr int kNT = NT;
   static constexpr int kBits = BITS;
   static constexpr int kBins = 1 << BITS;
-  static constexpr int kItems = 2;               // keys per thread of a sort tile
+  static constexpr int kItems = ITEMS;           // keys per thread of a sort tile
   static constexpr int kTile = NT * kItems;      // keys per sort tile
   static constexpr int kUpTile = 1024;           // tokens per key-build (histogram) tile
   static constexpr int kPasses = kMaxPasses;     // most passes this configuration runs
   static_assert(kUpTile % NT == 0, "whole key-build rounds");
 };
-using Narrow = SortCfg<512, 8>;
-using Wide9 = SortCfg<512, 9>;
+using Narrow = SortCfg<512, 8, 2>;
+using Wide9 = SortCfg<512, 9, 2>;
+using NarrowBig = SortCfg<512, 8, 3>;
+using Wide9Big = SortCfg<512, 9, 3>;
+constexpr int kBigTileAbove = 32768;  // batches of more tokens take the 1536-key tiles
 constexpr int kWide9Passes = 3;  // most passes of 9-bit digits
 // Histogram and look-back words per tile, for every pass of either configuration.
 constexpr int kHistPerTile = kMaxPasses * Narrow::kBins > kWide9Passes * Wide9::kBins ? kMaxPasses * Narrow::kBins
                                                                                       : kWide9Passes * Wide9::kBins;
-static_assert(Narrow::kTile == Wide9::kTile && Narrow::kUpTile == Wide9::kUpTile, "one tiling for both");
+// The workspace is laid out for the configuration with the most tiles.
+static_assert(Narrow::kTile == Wide9::kTile && Narrow::kTile <= NarrowBig::kTile && Narrow::kTile <= Wide9Big::kTile,
+              "the workspace's tile count is the largest");
+static_assert(Narrow::kUpTile == Wide9::kUpTile && Narrow::kUpTile == NarrowBig::kUpTile &&
+              Narrow::kUpTile == Wide9Big::kUpTile, "one key-build tiling");
 constexpr int kChunk = 32;                    // sorted tokens per reduction wave
 constexpr int kRedTile = kChunk * kWaves;     // sorted tokens per reduction workgroup
 constexpr int kLoadsInFlight = 8;
@@ -1208,10 +1220,18 @@ hipError_t sort_chain(const int32_t* ids, int T, int64_t V, int D, const Coalesc
   // histograms of all passes, then the radix passes over (key, position)
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
-  if (plan.digit == 9)
-    launch_sort<Wide9>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
-  else
-    launch_sort<Narrow>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
+  const bool big = T > kBigTileAbove;
+  if (plan.digit == 9) {
+    if (big)
+      launch_sort<Wide9Big>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
+    else
+      launch_sort<Wide9>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
+  } else {
+    if (big)
+      launch_sort<NarrowBig>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
+    else
+      launch_sort<Narrow>(ids, T, ks, plan, ws, status, stream, &kin, &vin);
+  }
   // 4. heads per reduction workgroup
   hipLaunchKernelGGL(seg_count_kernel, dim3((nred + kWaves - 1) / kWaves), dim3(kThreads), 0, stream, kin, ws.n_valid,
                      ws.tile_heads, nred);

@@ -1,5 +1,5 @@
 """Parity of each C ABI call with the oracle at sizes the oracle finishes in
-seconds: several sort tiles (1024 keys) and reduction chunks (32 tokens) with
+seconds: several sort tiles (1024 keys, 1536 above 32768 tokens) and reduction chunks (32 tokens) with
 ragged tails, every gradient width path (vector and scalar), bf16 gradients,
 hot rows spanning many chunks, empty and degenerate inputs."""
 import numpy as np
@@ -83,6 +83,10 @@ def test_gather_empty():
     ("zipf", 1, 2048, 4),
     ("zipf", 300, 1999, 256),
     ("uniform", 7, 1, 5),
+    # the largest batch of 1024-key sort tiles, and the smallest of 1536-key tiles (ragged: 21 whole
+    # tiles and 513 keys)
+    ("uniform", 1 << 20, 32768, 4),
+    ("zipf", 1 << 20, 32769, 4),
     # more than 1024 reduction workgroups: the head counts are scanned once by their own kernel
     ("zipf", 1 << 20, 200000, 8),
     ("uniform", 1 << 18, 131073, 4),
