@@ -89,6 +89,10 @@ def check_by_owner(ids_np, grad_np, V, own_np, P, bf16=False, grad_dev=None):
     ("uniform", 1 << 21, 20000, 8, 16, "mod"),     # 21 + 4 = 25 key bits: three 9-bit passes (9, 9, 7)
     ("zipf", 256, 5000, 8, 2, "mod"),              # 8 + 1 = 9 key bits: one 9-bit pass
     ("uniform", (1 << 24) + 3, 9000, 4, 128, "mod"),    # 25 + 7 = 32 key bits, the widest that fits
+    # 1536-key sort tiles (more than 32768 tokens): 8-bit digits, 9-bit digits, four passes
+    ("zipf", 1 << 16, 40001, 8, 4, "range"),        # 16 + 2 = 18 key bits: two 9-bit passes
+    ("uniform", 1 << 20, 33000, 8, 64, "rand"),     # 20 + 6 = 26 key bits: three 9-bit passes
+    ("uniform", (1 << 22) - 1, 50000, 4, 1024, "rand"),  # 32 key bits: four 8-bit passes
     # the one-workgroup path (at most 2048 tokens): the most owners, 32 key bits, a device-side count
     ("uniform", 50000, 2048, 20, 1024, "rand"),
     ("uniform", (1 << 22) - 1, 1500, 4, 1024, "rand"),

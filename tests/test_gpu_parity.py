@@ -87,6 +87,10 @@ def test_gather_empty():
     # tiles and 513 keys)
     ("uniform", 1 << 20, 32768, 4),
     ("zipf", 1 << 20, 32769, 4),
+    # 1536-key tiles with 9-bit digits: 17 key bits (two passes), 26 key bits (three passes), one
+    # and a ragged tail of 1535 keys
+    ("zipf", 65537, 49151, 8),
+    ("uniform", (1 << 26) - 3, 40000, 4),
     # more than 1024 reduction workgroups: the head counts are scanned once by their own kernel
     ("zipf", 1 << 20, 200000, 8),
     ("uniform", 1 << 18, 131073, 4),
