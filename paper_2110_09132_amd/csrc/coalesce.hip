@@ -498,7 +498,8 @@ __global__ __launch_bounds__(C::kNT) void sort_pass_kernel(
 #pragma unroll
   for (int q = 0; q < kDigitsPerThread; ++q) {
     const int d = static_cast<int>(threadIdx.x) + q * NT;
-    if (d < bins) publish(lookback + static_cast<size_t>(tile) * kBins + d, (tile == 0 ? kInclusive : kAggregate) | thist[d]);
+    if (d < bins)
+      publish(lookback + static_cast<size_t>(tile) * kBins + d, (tile == 0 ? kInclusive : kAggregate) | thist[d]);
   }
 
   const uint32_t nvalid = tile_stable_rank<NT, kItems, C::kBits>(dig, valid, bins, bits, cnt, dstart, wsum, lpos);
