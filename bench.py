@@ -483,19 +483,24 @@ def schedule_candidates(args):
         return [("events", 2, False)]
     if args.candidate:
         parts = args.candidate.split("/")
-        if parts[0] not in ("events", "signals") or len(parts) not in (2, 3):
-            raise SystemExit(f"--candidate {args.candidate!r}: expected ORDER/SETS[/paired], ORDER events or signals")
+        if parts[0] not in ("events", "signals", "queued") or len(parts) not in (2, 3):
+            raise SystemExit(f"--candidate {args.candidate!r}: expected ORDER/SETS[/paired], ORDER events, signals "
+                             f"or queued")
         return [(parts[0], int(parts[1]), len(parts) > 2 and parts[2] == "paired")]
     orders = ("events", "signals") if args.order == "auto" else (args.order,)
+    if args.order == "queued" and args.schedule != "by_owner":
+        raise SystemExit("--order queued takes the owner-major schedule")
     sets = (2, 4, 6) if args.sets == 0 else (args.sets,)
     # with events the split needs two sets (its lookup waits for the delayed update two steps back)
     cands = [(o, n, False) for o in orders for n in sets
              if n != 6 and not (args.schedule == "split" and o == "events" and n != 2)]
     # owner-major with four sets: also with each sort stream running its steps' reductions; with six,
-    # three such streams
+    # three such streams; and, tuned, those two with the two-thread enqueue
     if args.schedule == "by_owner":
         cands += [(o, 4, True) for o in orders if 4 in sets]
         cands += [(o, 6, True) for o in orders if 6 in sets]
+        if args.order == "auto":
+            cands += [("queued", n, True) for n in (4, 6) if n in sets]
     return cands
 
 
@@ -578,7 +583,7 @@ class WorkloadRun:
                                 by_owner=self.by_owner, split=self.split)
         order, sets, paired = cand
         return StepPipeline(self.tables, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=True, by_owner=self.by_owner,
-                            split=self.split, signals=order == "signals",
+                            split=self.split, signals=order == "signals", queued=order == "queued",
                             sort_streams=(sets // 2 if sets in (4, 6) else 1) if (self.by_owner and not self.split)
                             else 1, sets=sets, paired=paired)
 
@@ -807,9 +812,9 @@ def main():
     ap.add_argument("--sets", type=int, choices=(0, 2, 4, 6), default=0,
                     help="buffer sets rotated between steps, with the sorts of odd and even sets on two side "
                          "streams when 4 and not split (0: tuned; the split with events uses 2)")
-    ap.add_argument("--order", choices=("auto", "signals", "events"), default="auto",
+    ap.add_argument("--order", choices=("auto", "signals", "events", "queued"), default="auto",
                     help="cross-stream order of the overlapped schedule: step signals (stream memory operations), "
-                         "events, or auto (tuned)")
+                         "events, events with the two-thread enqueue (queued; owner-major), or auto (tuned)")
     ap.add_argument("--candidate", default="",
                     help="one schedule, ORDER/SETS[/paired] (e.g. events/4/paired): no tuning")
     ap.add_argument("--tune-steps", type=int, default=30)
@@ -917,7 +922,8 @@ def main():
                    "sort_and_reduce_paired": paired,
                    "cross_stream_order": None if args.sequential else
                    {"signals": "step signals (hipStreamWriteValue32 / hipStreamWaitValue32)",
-                    "events": "events (hipEventRecord / hipStreamWaitEvent)"}[order],
+                    "events": "events (hipEventRecord / hipStreamWaitEvent)",
+                    "queued": "events, each step enqueued from two host threads (emb_train_step_queued)"}[order],
                    "schedule_tuning_ms_per_step": pl["tune_ms"] or None,
                    "prior_rows_frac": prior_frac if split else None},
         "step_bytes_model": pl["total_bytes"],

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define EMB_ABI_VERSION 2
+#define EMB_ABI_VERSION 3
 
 /* host status codes */
 #define EMB_OK 0
@@ -610,6 +610,36 @@ int emb_step_signals_destroy(void *signals);
 /* Enqueue one training step of one table (see above).  Returns the first
  * failing call's status; nothing after it is enqueued. */
 int emb_train_step(const emb_step_args *args, const emb_step_schedule *sched);
+
+/* Two-thread enqueue.  Not a step of the method: a host-side way to enqueue
+ * the same steps for callers whose host time per step bounds them (small
+ * batches: the executor issues a dozen HIP calls per step, and a wait on an
+ * event still pending on another stream alone costs the host about 10 us).
+ * emb_train_step_queued enqueues the sort and the reduction of the step (on
+ * `coalesce` and `pack`) from the calling thread and hands the rest (the
+ * lookup, the wait for the reduction and the update, on `lookup_update`) to
+ * the queue's worker thread, which enqueues the handed steps in call order on
+ * the device that was current at the call.  The stream order is exactly the
+ * one emb_train_step gives.  Before the calling thread waits on a buffer
+ * set's earlier use, it waits (on the host, at most 30 s, else
+ * EMB_ERR_LAUNCH) until the worker has enqueued that use's update.
+ * Restrictions: events (no step signals), by_owner without the split, not
+ * under graph capture, `coalesce` and `pack` other streams than
+ * `lookup_update` (each stream is fed by one thread; EMB_ERR_UNSUPPORTED
+ * otherwise); one queue per table,
+ * used from one thread; timing events in `sched` are recorded as usual, those
+ * of the lookup and the update by the worker.
+ * Until emb_step_queue_flush has returned, the handed parts of the steps may
+ * not be enqueued yet: call it before enqueuing anything on `lookup_update`
+ * that must follow them, and before reading what they write.  flush and
+ * destroy return the first error of a handed part (a failed part stops its
+ * own step only, as in emb_train_step); destroy enqueues what was handed
+ * before it stops the worker.  The queue is host memory and a thread; the
+ * library allocates nothing on the device for it. */
+int emb_step_queue_create(void **queue);
+int emb_step_queue_flush(void *queue);
+int emb_step_queue_destroy(void *queue);
+int emb_train_step_queued(void *queue, const emb_step_args *args, const emb_step_schedule *sched);
 
 #ifdef __cplusplus
 }

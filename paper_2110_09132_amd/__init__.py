@@ -69,6 +69,10 @@ SIGNATURES = {
     "emb_step_signals_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p)]),
     "emb_step_signals_destroy": (ctypes.c_int, [_P]),
     "emb_train_step": (ctypes.c_int, [_P, _P]),
+    "emb_step_queue_create": (ctypes.c_int, [ctypes.POINTER(ctypes.c_void_p)]),
+    "emb_step_queue_flush": (ctypes.c_int, [_P]),
+    "emb_step_queue_destroy": (ctypes.c_int, [_P]),
+    "emb_train_step_queued": (ctypes.c_int, [_P, _P, _P]),
 }
 
 
@@ -202,6 +206,28 @@ class StepSignals:
     def __del__(self):
         if getattr(self, "handle", None):
             self._lib.emb_step_signals_destroy(self.handle)
+            self.handle = None
+
+
+class StepQueue:
+    """Two-thread enqueue of owner-major steps (emb_step_queue_create): emb_train_step_queued
+    enqueues a step's sort and reduction on the calling thread and hands its lookup and update to
+    the library's worker thread.  flush() returns once the worker has enqueued everything handed
+    to it (the steps then run in stream order like any other work); the worker is stopped when
+    the object goes away."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check(lib.emb_step_queue_create(ctypes.byref(h)), "emb_step_queue_create")
+        self.handle = h.value
+        self._lib = lib
+
+    def flush(self):
+        _check(self._lib.emb_step_queue_flush(self.handle), "emb_step_queue_flush")
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            self._lib.emb_step_queue_destroy(self.handle)
             self.handle = None
 
 

@@ -25,7 +25,8 @@ import ctypes
 
 import torch
 
-from . import (EMB_ADAM_COEFFS_WORDS, EMB_BF16, EMB_F32, EmbError, Event, StepArgs, StepSchedule, StepSignals,
+from . import (EMB_ADAM_COEFFS_WORDS, EMB_BF16, EMB_F32, EmbError, Event, StepArgs, StepQueue, StepSchedule,
+               StepSignals,
                _check, _grad, _need, _owners, adam_coeffs, grad_coalesce_split_workspace_bytes, lib, new_workspace,
                pack_by_owner_workspace_bytes)
 
@@ -92,7 +93,7 @@ class StepPipeline:
 
     def __init__(self, tables, lr, beta1, beta2, eps, overlap: bool = True, dev_status: torch.Tensor | None = None,
                  streams: int = 3, by_owner: bool = True, split: bool = False, signals: bool = False,
-                 sort_streams: int = 1, sets: int = 2, paired: bool = False):
+                 sort_streams: int = 1, sets: int = 2, paired: bool = False, queued: bool = False):
         """streams (with overlap=True and by_owner=False): 2 puts coalesce and pack on one side
         stream, 3 gives each its own (more concurrency, one more cross-stream wait per step).
         by_owner: coalesce straight into the send layout (emb_grad_coalesce_by_owner).
@@ -109,7 +110,11 @@ class StepPipeline:
         right after their sorts (no cross-stream wait between the two halves).
         signals (with overlap=True): keep the cross-stream order with step signals (stream memory
         operations: about half the host time per step, for host-bound pipelines of small
-        batches; with large batches events keep the GPU a few percent busier) instead of events."""
+        batches; with large batches events keep the GPU a few percent busier) instead of events.
+        queued (overlap=True, events, by_owner without the split): enqueue each step from two host
+        threads (StepQueue): the sort and the reduction from this one, the lookup and the update
+        from the library's worker, so that a step costs the host about the larger half of its
+        enqueue instead of both."""
         self.tables = list(tables)
         self.overlap = overlap
         self.main = torch.cuda.current_stream()
@@ -133,6 +138,9 @@ class StepPipeline:
         self.count = 0
         self.events = []  # keeps the library events alive
         self.signals = [StepSignals() for _ in self.tables] if (overlap and signals) else []
+        if queued and (not overlap or signals or split or not self.by_owner):
+            raise ValueError("the two-thread enqueue takes overlapped owner-major steps with events, no split")
+        self.queue = StepQueue() if queued else None
         self.args, self.sched = [], []
         st = 0 if dev_status is None else dev_status.data_ptr()
         for tb in self.tables:
@@ -216,14 +224,21 @@ class StepPipeline:
                     if name in timing:
                         s.timing[2 * j] = timing[name][0].handle
                         s.timing[2 * j + 1] = timing[name][1].handle
-            _check(lib.emb_train_step(ctypes.byref(a), ctypes.byref(s)), "emb_train_step")
+            if self.queue is not None:
+                _check(lib.emb_train_step_queued(self.queue.handle, ctypes.byref(a), ctypes.byref(s)),
+                       "emb_train_step_queued")
+            else:
+                _check(lib.emb_train_step(ctypes.byref(a), ctypes.byref(s)), "emb_train_step")
         self.count += 1
 
     def _sides(self):
         return {x for x in (self.side, self.side2, self.side3, self.side3_sort) if x is not None} - {self.main}
 
     def finish(self):
-        """Make the main stream wait for everything enqueued on the side streams."""
+        """Make the main stream wait for everything enqueued on the side streams (with the
+        two-thread enqueue, once the worker has enqueued every step handed to it)."""
+        if self.queue is not None:
+            self.queue.flush()
         for side in self._sides():
             self.main.wait_stream(side)
 

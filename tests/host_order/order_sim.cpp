@@ -27,6 +27,7 @@
 #include <cstdlib>
 #include <deque>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -80,11 +81,20 @@ bool g_track = false;  // record launches for the happens-before check
 
 // What the next launches touch (set by the stand-ins from their arguments).
 long g_cur_step = 0;                      // step number of the call being enqueued
+// Two-thread enqueue: the worker enqueues a step's main half after the caller has moved on, so the
+// step of a launch is read from its arguments instead (ids = kIdsBase + 16 * step, Adam step = step + 1).
+bool g_step_from_args = false;
+constexpr uintptr_t kIdsBase = 0x100000;
+std::recursive_mutex g_sim_mu;  // the stand-ins are called from two host threads
+long step_of_ids(const int32_t* ids) {
+  return g_step_from_args ? static_cast<long>((reinterpret_cast<uintptr_t>(ids) - kIdsBase) / 16) : g_cur_step;
+}
 std::map<const void*, bool> g_is_table;   // table pointers
 
 long sid(hipStream_t s) { return reinterpret_cast<long>(s); }
 
 void push(hipStream_t s, Op op) {
+  std::lock_guard<std::recursive_mutex> lock(g_sim_mu);
   if (op.kind == kLaunch) op.seq = g_seq++;
   g_streams[sid(s)].push_back(op);
   ++g_ops;
@@ -188,9 +198,10 @@ void check_happens_before(const char* scenario) {
   g_launches.clear();
 }
 
-Op launch_op(const char* what, std::vector<Access> acc, RowSet rows = kNoRows, const void* table = nullptr) {
+Op launch_op(const char* what, std::vector<Access> acc, RowSet rows = kNoRows, const void* table = nullptr,
+             long step = -1) {
   Op o{kLaunch, 0, 0, what, std::move(acc)};
-  o.step = g_cur_step;
+  o.step = step >= 0 ? step : g_cur_step;
   o.rows = rows;
   o.table = table;
   return o;
@@ -201,12 +212,14 @@ Op launch_op(const char* what, std::vector<Access> acc, RowSet rows = kNoRows, c
 // ---- stand-ins for the HIP runtime calls the executor makes
 extern "C" {
 hipError_t hipStreamWriteValue32(hipStream_t stream, void* ptr, uint32_t value, unsigned int) {
+  std::lock_guard<std::recursive_mutex> lock(g_sim_mu);
   const long w = g_word_of.at(ptr);
   if (value > g_enqueued_max[w]) g_enqueued_max[w] = value;
   push(stream, Op{kWrite, w, value, "write"});
   return hipSuccess;
 }
 hipError_t hipStreamWaitValue32(hipStream_t stream, void* ptr, uint32_t value, unsigned int flags, uint32_t mask) {
+  std::lock_guard<std::recursive_mutex> lock(g_sim_mu);
   if (flags != hipStreamWaitValueGte || mask != 0xFFFFFFFFu) fail("unexpected wait form");
   const long w = g_word_of.at(ptr);
   if (value > g_enqueued_max[w]) fail("a wait targets a value no enqueued write supplies");
@@ -214,6 +227,7 @@ hipError_t hipStreamWaitValue32(hipStream_t stream, void* ptr, uint32_t value, u
   return hipSuccess;
 }
 hipError_t hipEventRecord(hipEvent_t event, hipStream_t stream) {
+  std::lock_guard<std::recursive_mutex> lock(g_sim_mu);
   const long n = static_cast<long>(g_record_done.size());
   g_record_done.push_back(false);
   g_record_clock.push_back(Clock{});
@@ -222,6 +236,7 @@ hipError_t hipEventRecord(hipEvent_t event, hipStream_t stream) {
   return hipSuccess;
 }
 hipError_t hipStreamWaitEvent(hipStream_t stream, hipEvent_t event, unsigned int) {
+  std::lock_guard<std::recursive_mutex> lock(g_sim_mu);
   if (event == nullptr) fail("a wait on a null event");
   // HIP semantics: wait for the event's latest record at the time of the call (none: no wait)
   auto it = g_last_record.find(event);
@@ -250,6 +265,7 @@ hipError_t hipGetDevice(int* d) {
   *d = 0;
   return hipSuccess;
 }
+hipError_t hipSetDevice(int) { return hipSuccess; }
 hipError_t hipDeviceGetAttribute(int* v, hipDeviceAttribute_t, int) {
   *v = 1;
   return hipSuccess;
@@ -258,22 +274,24 @@ hipError_t hipDeviceGetAttribute(int* v, hipDeviceAttribute_t, int) {
 
 // ---- stand-ins for the launchers and calls the executor enqueues
 namespace emb {
-hipError_t launch_gather(const float* table, int64_t, int, const int32_t*, int, float*, int32_t*, hipStream_t stream,
-                         hipEvent_t done) {
-  push(stream, launch_op("gather", {}, kAllRows, table));
+hipError_t launch_gather(const float* table, int64_t, int, const int32_t* ids, int, float*, int32_t*,
+                         hipStream_t stream, hipEvent_t done) {
+  std::lock_guard<std::recursive_mutex> lock(g_sim_mu);
+  push(stream, launch_op("gather", {}, kAllRows, table, step_of_ids(ids)));
   if (done && g_capturing) fail("an event attached to a dispatch under capture");
   if (done) (void)hipEventRecord(done, stream);  // an event attached to the dispatch completes with it
   return hipSuccess;
 }
-hipError_t launch_coalesce_sort(const int32_t*, int, int64_t, int, const CoalesceVariant&, void* ws, int32_t*,
+hipError_t launch_coalesce_sort(const int32_t* ids, int, int64_t, int, const CoalesceVariant&, void* ws, int32_t*,
                                 hipStream_t stream) {
-  push(stream, launch_op("sort", {{ws, true}}));
+  push(stream, launch_op("sort", {{ws, true}}, kNoRows, nullptr, step_of_ids(ids)));
   return hipSuccess;
 }
-hipError_t launch_coalesce_reduce(const int32_t*, int, const void*, bool, int, int64_t, const CoalesceVariant&,
+hipError_t launch_coalesce_reduce(const int32_t* ids, int, const void*, bool, int, int64_t, const CoalesceVariant&,
                                   int32_t* send_ids, int32_t*, float*, int32_t*, int32_t*, int32_t*, void* ws,
                                   int32_t*, hipStream_t stream, hipEvent_t done) {
-  push(stream, launch_op("reduce", {{ws, false}, {send_ids, true}}));
+  std::lock_guard<std::recursive_mutex> lock(g_sim_mu);
+  push(stream, launch_op("reduce", {{ws, false}, {send_ids, true}}, kNoRows, nullptr, step_of_ids(ids)));
   if (done && g_capturing) fail("an event attached to a dispatch under capture");
   if (done) (void)hipEventRecord(done, stream);
   return hipSuccess;
@@ -285,12 +303,13 @@ int coalesce_by_owner_args_status(const int32_t*, int32_t, const void*, int32_t,
 }
 int sparse_adam_call(float* table, float*, float*, int64_t, int32_t, const int32_t* send_ids, const float*,
                      const int32_t* offsets, int32_t P, int32_t, int32_t, int32_t, double, double, double, double,
-                     int64_t, const void*, int32_t*, hipStream_t stream, hipEvent_t, hipEvent_t stop) {
+                     int64_t adam_step, const void*, int32_t*, hipStream_t stream, hipEvent_t, hipEvent_t stop) {
+  std::lock_guard<std::recursive_mutex> lock(g_sim_mu);
   // the split's two parts: groups [0, P) prior, [P, 2P) delayed (offsets is send_offsets + P)
   extern const int32_t* g_offsets_base;
   RowSet rows = kAllRows;
   if (g_offsets_base != nullptr) rows = offsets == g_offsets_base ? kPriorRows : kDelayedRows;
-  push(stream, launch_op("adam", {{send_ids, false}}, rows, table));
+  push(stream, launch_op("adam", {{send_ids, false}}, rows, table, g_step_from_args ? adam_step - 1 : -1));
   (void)P;
   if (stop && g_capturing) fail("an event attached to a dispatch under capture");
   if (stop) (void)hipEventRecord(stop, stream);
@@ -300,8 +319,8 @@ const int32_t* g_offsets_base = nullptr;  // the split's send_offsets while a sp
 }  // namespace emb
 
 extern "C" {
-int emb_gather(const float* table, int64_t, int32_t, const int32_t*, int32_t, float*, int32_t*, void* stream) {
-  push(static_cast<hipStream_t>(stream), launch_op("gather", {}, kAllRows, table));
+int emb_gather(const float* table, int64_t, int32_t, const int32_t* ids, int32_t, float*, int32_t*, void* stream) {
+  push(static_cast<hipStream_t>(stream), launch_op("gather", {}, kAllRows, table, step_of_ids(ids)));
   return EMB_OK;
 }
 int emb_grad_coalesce(const int32_t*, int32_t, const void*, int32_t, int32_t, int64_t, int32_t* uniq_ids, int32_t*,
@@ -447,10 +466,89 @@ void happens_before_scenarios() {
   std::printf("happens-before: %d scenarios ordered\n", scenarios);
 }
 
+// The two-thread enqueue (emb_train_step_queued): the worker thread enqueues each step's lookup and
+// update while this thread goes on with the next steps' sorts and reductions.  Each scenario runs
+// several times, so that the two threads meet in different interleavings.
+void queued_scenarios() {
+  static char table_mem[64];
+  int scenarios = 0;
+  g_step_from_args = true;
+  for (int sets = 2; sets <= 6; ++sets)
+    for (int r = 0; r < 4; ++r)  // stream rules with the sort and the reduction off the main stream
+      for (int rep = 0; rep < 5; ++rep) {
+        drain();
+        g_clock.clear();
+        g_launches.clear();
+        g_track = true;
+        std::vector<SetBuffers> bufs(sets);
+        Table t;
+        t.args.T = 100;
+        t.args.cap_rows = 100;
+        t.args.table = reinterpret_cast<float*>(table_mem);
+        t.args.P = 4;
+        t.sched.sets = sets;
+        t.sched.by_owner = 1;
+        t.sched.split = 0;
+        t.sched.signals = nullptr;
+        void* q = nullptr;
+        if (emb_step_queue_create(&q) != EMB_OK) fail("queue create");
+        unsigned rs = 901u + static_cast<unsigned>(r * 31 + sets);
+        for (long n = 0; n < 24; ++n) {
+          const int k = static_cast<int>(n % sets);
+          SetBuffers& b = bufs[k];
+          t.args.ws_coalesce = b.ws;
+          t.args.ws_coalesce_bytes = sizeof b.ws;
+          t.args.send_ids = b.send_ids;
+          t.args.send_offsets = b.send_offsets;
+          t.args.ids = reinterpret_cast<const int32_t*>(kIdsBase + 16 * static_cast<uintptr_t>(n));
+          t.args.step = n + 1;
+          t.sched.sorted = &b.ev[0];
+          t.sched.coalesced = &b.ev[1];
+          t.sched.updated = &b.ev[3];
+          t.sched.reuse = n >= sets;
+          streams_for(r, n, k, rs, t.sched);
+          if (emb_train_step_queued(q, &t.args, &t.sched) != EMB_OK) fail("queued step");
+        }
+        if (emb_step_queue_flush(q) != EMB_OK) fail("queue flush");
+        if (emb_step_queue_destroy(q) != EMB_OK) fail("queue destroy");
+        char name[96];
+        std::snprintf(name, sizeof name, "queued, %d sets, streams rule %d, run %d", sets, r, rep);
+        check_happens_before(name);
+        g_track = false;
+        ++scenarios;
+      }
+  // a schedule with the reduction on the main stream is refused
+  {
+    void* q = nullptr;
+    if (emb_step_queue_create(&q) != EMB_OK) fail("queue create");
+    Table t;
+    static char ws[256];
+    static int32_t ids_dummy[4], offs_dummy[8];
+    static char ev[6];
+    t.args.T = 4;
+    t.args.cap_rows = 4;
+    t.args.ws_coalesce = ws;
+    t.args.send_ids = ids_dummy;
+    t.args.send_offsets = offs_dummy;
+    t.sched.by_owner = 1;
+    t.sched.sorted = &ev[0];
+    t.sched.coalesced = &ev[1];
+    t.sched.updated = &ev[3];
+    t.sched.lookup_update = fake_stream(1);
+    t.sched.coalesce = fake_stream(2);
+    t.sched.pack = fake_stream(1);
+    if (emb_train_step_queued(q, &t.args, &t.sched) != EMB_ERR_UNSUPPORTED) fail("queued step on the main stream");
+    if (emb_step_queue_destroy(q) != EMB_OK) fail("queue destroy");
+  }
+  g_step_from_args = false;
+  std::printf("queued: %d scenarios ordered\n", scenarios);
+}
+
 }  // namespace
 
 int main() {
   happens_before_scenarios();
+  queued_scenarios();
   static char dummy[256];
   static int32_t ids_dummy[4], offs_dummy[8];
   Table tabs[2];

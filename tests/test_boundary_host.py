@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings_and_version():
-    assert emb.abi_version() == 2
+    assert emb.abi_version() == 3
     assert emb.status_string(emb.EMB_OK) == "ok"
     assert "workspace" in emb.status_string(emb.EMB_ERR_WORKSPACE)
 

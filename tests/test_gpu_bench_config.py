@@ -2,7 +2,8 @@
 of it: the step executor (owner-major coalesce, sort and reduction on side streams) under each
 schedule the benchmark's tuner may pick (events or step signals; two buffer sets with one sort
 stream, four with two, with or without each sort stream running its own reductions, or six with
-three sort streams running their own reductions), and the
+three sort streams running their own reductions; four or six with each step enqueued from two host
+threads), and the
 split schedule of Vertical Sparse Scheduling (Algorithm 1: prior rows updated before the next
 lookup, delayed rows beside it), a few steps in a row, checked against the oracle:
   - each step's send layout (ids, counts, offsets; with the split, the 2P groups of the prior and
@@ -31,6 +32,7 @@ SCHEDULES = [("by_owner", "events", 2, False), ("by_owner", "events", 4, False),
              ("by_owner", "signals", 2, False), ("by_owner", "signals", 4, False),
              ("by_owner", "events", 4, True), ("by_owner", "signals", 4, True),
              ("by_owner", "events", 6, True), ("by_owner", "signals", 6, True),
+             ("by_owner", "queued", 4, True), ("by_owner", "queued", 6, True),
              ("split", "events", 2, False), ("split", "signals", 2, False), ("split", "signals", 4, False)]
 CASES = [(w,) + s for w in configs.WORKLOADS for s in SCHEDULES]
 
@@ -61,7 +63,7 @@ def test_bench_schedule_full_size(name, kind, order, sets, paired):
         tbs.append(EmbeddingTable(to_dev(W0s[k]), to_dev(owns[k]), sp.P, sp.T, gdt, sets=sets))
     st = emb.new_status()
     pipe = StepPipeline(tbs, wl.lr, wl.beta1, wl.beta2, wl.eps, overlap=True, dev_status=st, split=split,
-                        signals=order == "signals", sets=sets,
+                        signals=order == "signals", queued=order == "queued", sets=sets,
                         sort_streams=(sets // 2 if sets in (4, 6) else 1) if not split else 1, paired=paired)
     # batches of steps 0 .. steps (the last one is only the split's next batch)
     host_batches = [[batch(name, k, s) for k in range(nt)] for s in range(steps + 1)]
@@ -70,6 +72,8 @@ def test_bench_schedule_full_size(name, kind, order, sets, paired):
     looked = []
     for s in range(steps):
         pipe.step(dev_batches[s], s + 1, next_ids=[x[0] for x in dev_batches[s + 1]] if split else None)
+        if pipe.queue is not None:
+            pipe.queue.flush()  # the worker has enqueued this step's lookup, read below
         # the lookups of step s, sampled, read on the main stream before the next step's lookup overwrites them
         pos = np.sort(rng.choice(wl.tables[0].T, 256, replace=False))
         looked.append([(pos, tb.lookup[torch.from_numpy(pos).to(tb.lookup.device)].clone()) for tb in tbs])

@@ -1,6 +1,7 @@
 """The overlapped step schedules give bitwise the same table, moments and
 lookups as running their calls one after another on one stream, with the
-cross-stream order kept by events or by step signals; the
+cross-stream order kept by events or by step signals, and with each step
+enqueued from two host threads (emb_train_step_queued); the
 owner-major schedule (coalesce straight into the send layout) agrees with
 coalesce-then-pack, and the prior / delayed split with one update, to the
 fp32 tolerance (their sums add in another grouping)."""
@@ -15,7 +16,10 @@ from workloads import configs, gen
 pytestmark = pytest.mark.gpu
 
 
-def run(overlap, by_owner, steps=9, split=False, signals=False, sort_streams=1, sets=2, paired=False):
+def run(overlap, by_owner, steps=9, split=False, signals=False, sort_streams=1, sets=2, paired=False, queued=False,
+        flush_each=True):
+    """flush_each (queued): wait for the worker after every step, so that its lookup can be read; else only
+    the last step's lookup is read, and the worker's enqueue runs beside the next steps' sorts."""
     torch.cuda.synchronize()
     specs = [configs.TableSpec(20000, 128, 6000, "zipf", 1.05, "f32", 0.01, 8, "mod", 61),
              configs.TableSpec(5000, 64, 3000, "uniform", 0.0, "bf16", 0.01, 3, "range", 62)]
@@ -34,12 +38,16 @@ def run(overlap, by_owner, steps=9, split=False, signals=False, sort_streams=1, 
         batches.append(per)
     torch.cuda.synchronize()
     pipe = StepPipeline(tables, 1e-3, 0.9, 0.999, 1e-8, overlap=overlap, by_owner=by_owner, split=split,
-                        signals=signals, sort_streams=sort_streams, sets=sets, paired=paired)
+                        signals=signals, sort_streams=sort_streams, sets=sets, paired=paired, queued=queued)
     lookups = []
     empty = torch.zeros(0, dtype=torch.int32, device="cuda")
     for t in range(1, steps + 1):
         nxt = [batches[k][(t + 1) % 3][0] if t < steps else empty for k in range(len(specs))]
         pipe.step([batches[k][t % 3] for k in range(len(specs))], t, next_ids=nxt if split else None)
+        if queued:
+            if not flush_each and t < steps:
+                continue
+            pipe.queue.flush()  # the worker has enqueued this step's lookup
         # the lookup of step t is read on the main stream before step t+1's lookup overwrites it
         lookups.append([tb.lookup[: batches[k][t % 3][0].numel()].clone() for k, tb in enumerate(tables)])
     pipe.finish()
@@ -71,6 +79,23 @@ def test_two_sort_streams_equal_sequential(signals, sets, paired):
     for x, y in zip(a, b):
         for u, v in zip(x, y):
             assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
+    for x, y in zip(la, lb):
+        for u, v in zip(x, y):
+            assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
+
+
+@pytest.mark.parametrize("sets,sort_streams,paired", [(2, 1, False), (4, 2, False), (4, 2, True), (6, 3, True)])
+@pytest.mark.parametrize("flush_each", [True, False], ids=["flush-each", "flush-last"])
+def test_queued_enqueue_equals_sequential(sets, sort_streams, paired, flush_each):
+    print(f"queued, sets={sets}, sort streams={sort_streams}, paired={paired}, flush_each={flush_each}", flush=True)
+    a, la = run(True, True, steps=12, sort_streams=sort_streams, sets=sets, paired=paired, queued=True,
+                flush_each=flush_each)
+    b, lb = run(False, True, steps=12)
+    for x, y in zip(a, b):
+        for u, v in zip(x, y):
+            assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
+    lb = lb if flush_each else lb[-1:]
+    assert len(la) == len(lb)
     for x, y in zip(la, lb):
         for u, v in zip(x, y):
             assert np.array_equal(u.view(np.uint32), v.view(np.uint32))

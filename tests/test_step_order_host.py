@@ -7,8 +7,10 @@ single-stream schedules.  With a vector clock per stream it also checks happens-
 launches that touch the same buffer of a set, or overlapping table rows, one of them writing, run in
 the order the executor enqueued them, for every mode, events, signals and events under graph capture
 (every stage's end an event record of its own, none attached to a dispatch), two to six buffer sets
-with more steps than sets, and stream choices that include a set's streams changing between its uses.
-No GPU is used."""
+with more steps than sets, and stream choices that include a set's streams changing between its uses;
+and the two-thread enqueue (emb_train_step_queued: the library's worker thread enqueues each step's
+lookup and update), each scenario several times so that the threads meet in different interleavings,
+the steps' launches tagged from their arguments.  No GPU is used."""
 import os
 import shutil
 import subprocess
@@ -31,3 +33,4 @@ def test_step_signals_order_model(tmp_path):
     assert r.returncode == 0, r.stdout + r.stderr
     lines = r.stdout.splitlines()
     assert lines[0].startswith("happens-before:") and lines[-1].startswith("ok:"), r.stdout
+    assert any(l.startswith("queued:") for l in lines), r.stdout
