@@ -32,10 +32,11 @@
 //     heads with lane shuffles, adds up the head counts of the earlier
 //     workgroups, writes uniq_ids / seg_offsets / num_unique (and, by owner,
 //     where each owner's rows start), and sums the
-//     gradient rows of its tokens in sorted order.  Sums of ids that lie
-//     inside the chunk are final; the pieces of an id that crosses chunk
-//     boundaries go to a partials buffer.
-//  5. seg_combine: adds the pieces of each crossing id in chunk order
+//     gradient rows of its tokens in sorted order.  The sums of an id that
+//     crosses chunk boundaries inside the workgroup are added in LDS, in chunk
+//     order; only an id that crosses a boundary between workgroups leaves its
+//     pieces (one per workgroup) in a partials buffer.
+//  5. seg_combine: adds the pieces of each such id in workgroup order
 //     (16 waves per id, each summing a contiguous range of pieces, then the
 //     results in wave order); by owner, it also forms the per-owner counts.
 // The lookup requests of the row-wise forward exchange reuse kernels 1-3 on
@@ -609,6 +610,7 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     int32_t* __restrict__ span_list, int32_t* __restrict__ span_count, int nchunks) {
   __shared__ uint32_t wave_heads[kWaves];
   __shared__ uint32_t red[kWaves];
+  __shared__ uint32_t wave_flags[kWaves];
   const int tile = blockIdx.x;
   const int w = threadIdx.x / kWave;
   const int lane = static_cast<int>(lane_id());
@@ -642,7 +644,14 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
   const uint64_t heads = __ballot(head);
   const uint64_t brk = __ballot(starts_new);
   const int nv = __popcll(__ballot(in_chunk && valid));  // valid tokens of the chunk (a prefix of it)
-  if (lane == 0) wave_heads[w] = static_cast<uint32_t>(__popcll(heads));
+  const bool open_lo = ((brk >> 1) & 1ull) == 0;             // element a continues the id of a - 1
+  const bool open_hi = ((brk >> (kChunk + 1)) & 1ull) == 0;  // element a + kChunk continues the chunk's last id
+  const uint64_t inner = nv >= 1 ? (((1ull << (nv - 1)) - 1ull) << 2) : 0ull;
+  const bool one_run = nv >= 1 && (brk & inner) == 0;  // no head after the chunk's first token
+  if (lane == 0) {
+    wave_heads[w] = static_cast<uint32_t>(__popcll(heads));
+    wave_flags[w] = (open_hi ? 1u : 0u) | (one_run ? 2u : 0u);
+  }
   // The rows do not depend on the unique indices: the loads of the first
   // column block of all kChunk rows are issued before the workgroup combines
   // its counts.  Loads are unconditional, from clamped rows (a chunk with
@@ -699,12 +708,22 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     if (owner_offsets != nullptr)
       for (int p = 0; p <= ks.G; ++p) owner_offsets[p] = 0;
   }
-  if (nv == 0) return;
+  // from here on the waves of the workgroup meet at one barrier per column
+  // block, so only a whole workgroup may leave early
+  if (tile * kRedTile >= tv) return;
 
-  // sum the rows of the chunk's tokens in sorted order, one run of equal ids at a time
+  // sum the rows of the chunk's tokens in sorted order, one run of equal ids
+  // at a time.  A run that crosses chunk boundaries inside the workgroup is
+  // finished by the wave where it starts (wave 0 for one that began before the
+  // workgroup): it adds the first-run sums the later waves leave in LDS, in
+  // chunk order.  Only runs that cross the workgroup's ends leave pieces for
+  // seg_combine: slot 0 holds the run through the workgroup's first token,
+  // slot 1 a run that starts later and goes on into the next workgroup.
+  __shared__ Acc lds_piece[2][kWaves - 1][kWave];
   Acc* out_rows = reinterpret_cast<Acc*>(uniq_grad);
   Acc* part_rows = reinterpret_cast<Acc*>(partial);
-  for (int cb = cb0; cb < Dv; cb += cstep) {
+  int buf = 0;
+  for (int cb = cb0; cb < Dv; cb += cstep, buf ^= 1) {
     const int c = cb + lane;
     const bool colok = c < Dv;
     const int cc = min(c, Dv - 1);
@@ -717,31 +736,53 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     int rs = 0;
     int cur = __builtin_amdgcn_readlane(u, 1);
     auto flush = [&](int uu, int s, int t) {  // run of chunk tokens [s, t)
-      const bool whole = ((brk >> (s + 1)) & 1ull) && ((brk >> (t + 1)) & 1ull);
-      if (whole) {
+      const bool lo = s == 0 && open_lo;
+      const bool hi = t == kChunk && open_hi;
+      if (hi && (w == 0 || !lo)) return;  // this wave finishes it after the barrier
+      if (!lo) {
         if (colok && uu >= 0 && uu < T) out_rows[static_cast<size_t>(uu) * Dv + c] = acc;
-      } else {
-        const int slot = (s == 0) ? 0 : 1;
-        if (colok) part_rows[(static_cast<size_t>(chunk) * 2 + slot) * Dv + c] = acc;
-        if (((brk >> (s + 1)) & 1ull) && cb == 0 && lane == 0) {
-          const int k = atomicAdd(span_count, 1);  // at most one per chunk
-          if (k < nchunks) span_list[k] = uu;
-        }
+      } else if (w > 0) {
+        lds_piece[buf][w - 1][lane] = acc;
+      } else if (colok) {  // the end of a run that began before the workgroup
+        part_rows[(static_cast<size_t>(tile) * 2) * Dv + c] = acc;
       }
     };
+    if (nv > 0) {
 #pragma unroll
-    for (int j = 0; j < kChunk; ++j) {
-      if (j < nv) {
-        if (j > rs && ((brk >> (j + 1)) & 1ull)) {
-          flush(cur, rs, j);
-          acc = Acc{};
-          rs = j;
-          cur = __builtin_amdgcn_readlane(u, j + 1);
+      for (int j = 0; j < kChunk; ++j) {
+        if (j < nv) {
+          if (j > rs && ((brk >> (j + 1)) & 1ull)) {
+            flush(cur, rs, j);
+            acc = Acc{};
+            rs = j;
+            cur = __builtin_amdgcn_readlane(u, j + 1);
+          }
+          acc += g[j];
         }
-        acc += g[j];
+      }
+      flush(cur, rs, nv);
+    }
+    __syncthreads();
+    if (nv == kChunk && open_hi && (w == 0 || rs > 0 || !open_lo)) {
+      int w1 = w;
+      bool more = true;  // the run goes on past chunk w1
+      while (more && w1 + 1 < kWaves) {
+        ++w1;
+        acc += lds_piece[buf][w1 - 1][lane];
+        more = wave_flags[w1] == 3u;
+      }
+      const bool from_before = w == 0 && rs == 0 && open_lo;
+      if (!more && !from_before) {
+        if (colok && cur >= 0 && cur < T) out_rows[static_cast<size_t>(cur) * Dv + c] = acc;
+      } else {
+        const int slot = (w == 0 && rs == 0) ? 0 : 1;
+        if (colok) part_rows[(static_cast<size_t>(tile) * 2 + slot) * Dv + c] = acc;
+        if (more && !from_before && cb == 0 && lane == 0) {
+          const int k = atomicAdd(span_count, 1);  // at most one per workgroup
+          if (k < nchunks) span_list[k] = cur;
+        }
       }
     }
-    flush(cur, rs, nv);
   }
 }
 
@@ -768,9 +809,9 @@ __global__ __launch_bounds__(kCombineThreads) void seg_combine_kernel(const floa
     if (u < 0 || u >= T) continue;
     const int S = min(max(seg_offsets[u], 0), T);
     const int E = min(max(seg_offsets[u + 1], S), T);
-    const int c0 = S / kChunk;
-    const int np = (E - 1) / kChunk - c0 + 1;
-    const int first_slot = (S == c0 * kChunk) ? 0 : 1;
+    const int c0 = S / kRedTile;
+    const int np = (E - 1) / kRedTile - c0 + 1;
+    const int first_slot = (S == c0 * kRedTile) ? 0 : 1;
     const int p_beg = static_cast<int>((static_cast<long long>(w) * np) / kCombineWaves);
     const int p_end = static_cast<int>((static_cast<long long>(w + 1) * np) / kCombineWaves);
     // column blocks of kWave vectors, split over gridDim.y workgroups as in seg_reduce
@@ -1299,7 +1340,7 @@ hipError_t launch_coalesce_reduce(const int32_t* ids, int T, const void* grad, b
   // 5. segments and per-chunk sums; 6. pieces of ids that cross chunks
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(grad) % (grad_bf16 ? 8 : 16) == 0) &&
                     (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
-  const dim3 cgrid(grid_for(nchunks, 256), grid_for((D / (vec4 ? 4 : 1) + kWave - 1) / kWave, 8));
+  const dim3 cgrid(grid_for(nred, 256), grid_for((D / (vec4 ? 4 : 1) + kWave - 1) / kWave, 8));
 #define EMB_REDUCE(BF, VC)                                                                                          \
   hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred, reduce_col_split(nred, D / (VC))), dim3(kThreads), 0,   \
                      stream, kin, vin, ws.n_valid, T,                                                                \
