@@ -26,6 +26,13 @@ constexpr int kThreads = 256;
 // 138.3 us with two-row tiles and four (eight, sixteen or three-row variants
 // in between); the shared-vocabulary workload (7.1k rows of 2 KB) 56.1 -> 53.7
 // us with two-row tiles for wide rows too, the 4 KB-row workloads unchanged.
+//
+// The grid is sized for the row capacity; the rows actually listed (known
+// only on the device) are spread over enough waves that each takes at most
+// four tiles, and over no fewer than the resident waves: a short list (6.3k
+// rows of 1 KB) then runs in one round of resident workgroups instead of
+// being packed into the first of several (update alone 15.0 -> 13.5 us, its
+// overlapped step 47.3 -> 45.7 us; 63.5k rows unchanged).
 constexpr int kRowsInFlight = 2;
 constexpr int kNarrowTilesPerWave = 4;
 
@@ -105,6 +112,9 @@ __global__ __launch_bounds__(kThreads) void adam_kernel(VecT* __restrict__ W, Ve
     part = wave_all - wave * cs;
     nwaves = all_waves / cs;
   }
+  if (!kWide)  // the listed rows over at least the resident waves, at most kNarrowTilesPerWave tiles each
+    nwaves = min(all_waves, max(kResidentWaves, (hi - lo + kNarrowTilesPerWave * step_rows - 1) /
+                                                    (kNarrowTilesPerWave * step_rows)));
   int per = (hi - lo + nwaves - 1) / nwaves;
   per = (per + step_rows - 1) / step_rows * step_rows;
   const long long r0 = lo + static_cast<long long>(wave) * per;
