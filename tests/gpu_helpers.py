@@ -191,3 +191,23 @@ def check_steps_against_oracle(wl, tbs, W0s, owns, host_batches, steps, split, l
         un_dev = torch.from_numpy(untouched.astype(np.int64)).to(tb.W.device)
         assert np.array_equal(host(tb.W[un_dev]).view(np.uint32), W0[untouched].view(np.uint32))
         assert not host(tb.M[un_dev]).any() and not host(tb.S[un_dev]).any()
+
+
+# run lengths around the reduction's 32-token chunks and 128-token workgroups
+RUN_LENGTHS = [1, 2, 3, 30, 31, 32, 33, 34, 62, 63, 64, 65, 66, 95, 96, 97, 126, 127, 128, 129, 130, 160, 255, 256,
+               257, 300, 511, 512, 513]
+
+
+def runs_ids(seed, n_runs, V, bad_frac=0.0):
+    """Ids in runs of the lengths above (each run one id, ids ascending with gaps), tokens shuffled:
+    the sorted sequence is the runs in order, so their ends fall at every offset from the chunk and
+    workgroup boundaries.  bad_frac of the tokens get an id past V (left out of the sort)."""
+    rng = np.random.default_rng(seed)
+    lengths = rng.choice(RUN_LENGTHS, n_runs)
+    vals = np.cumsum(rng.integers(1, 40, n_runs))
+    assert vals[-1] < V
+    ids = np.repeat(vals, lengths).astype(np.int32)
+    bad = rng.random(ids.size) < bad_frac
+    ids[bad] = V + rng.integers(0, 1000, int(bad.sum()))
+    rng.shuffle(ids)
+    return ids

@@ -14,7 +14,7 @@ import torch
 import oracle
 import paper_2110_09132_amd as emb
 import tolerance
-from gpu_helpers import host, to_dev
+from gpu_helpers import host, runs_ids, to_dev
 from workloads import configs, gen
 
 pytestmark = pytest.mark.gpu
@@ -126,6 +126,16 @@ def test_by_owner_hot_row_spans_many_chunks():
     T, V, D, P = 20000, 5000, 256, 4
     ids = ids_for("zipf", 77, T, V, 2.5)
     check_by_owner(ids, grads_for(78, T, D, 0.01), V, gen.owner_mod(V, P), P)
+
+
+@pytest.mark.parametrize("seed,rule,bad_frac", [(5, "range", 0.0), (6, "range", 0.01), (7, "mod", 0.0)])
+def test_by_owner_runs_around_chunk_and_workgroup_boundaries(seed, rule, bad_frac):
+    # with contiguous owners the sorted sequence is the runs in order (as for the plain call); with
+    # id mod P each owner's runs follow one another
+    V, P = 1 << 16, 4
+    ids = runs_ids(seed, 300, V, bad_frac)
+    G = grads_for(seed + 20, ids.size, 64)
+    check_by_owner(ids, G, V, owners(rule, V, P), P)
 
 
 def test_by_owner_lowdup_full_size():

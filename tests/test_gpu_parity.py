@@ -10,7 +10,7 @@ import oracle
 import paper_2110_09132_amd as emb
 import tolerance
 from adam_inputs import eps_regime_grads
-from gpu_helpers import (check_adam, check_coalesce, check_pack, gpu_coalesce, gpu_gather, host, to_dev)
+from gpu_helpers import (check_adam, check_coalesce, check_pack, gpu_coalesce, gpu_gather, host, runs_ids, to_dev)
 from workloads import gen
 
 pytestmark = pytest.mark.gpu
@@ -115,6 +115,16 @@ def test_coalesce_hot_row_spans_many_chunks():
     T, V, D = 20000, 5000, 256
     ids = ids_for("zipf", 77, T, V, 2.5)
     G = grads_for(78, T, D, 0.01)
+    check_coalesce(ids, G, V)
+
+
+@pytest.mark.parametrize("seed,n_runs,bad_frac", [(1, 300, 0.0), (2, 300, 0.0), (3, 250, 0.01), (4, 40, 0.0)])
+def test_coalesce_runs_around_chunk_and_workgroup_boundaries(seed, n_runs, bad_frac):
+    # ids that cross chunk boundaries inside a reduction workgroup are summed there, ids that
+    # cross workgroups in pieces: every placement of a run's ends against both boundaries
+    V = 1 << 16
+    ids = runs_ids(seed, n_runs, V, bad_frac)
+    G = grads_for(seed + 10, ids.size, 64)
     check_coalesce(ids, G, V)
 
 
