@@ -980,6 +980,15 @@ __global__ __launch_bounds__(kSmallThreads) void small_coalesce_kernel(
       if (c >= Dv) continue;
       Acc acc = Acc{};
       int i = S;
+      // eight rows in flight, added in order (a hot segment's chain of round trips is the
+      // longest part of the kernel: 512 Zipf tokens, 14.2 -> 12.8 us with eight instead of four)
+      for (; i + 8 <= E; i += 8) {
+        Acc g[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) g[k] = Row::load(grad, static_cast<size_t>(sp[i + k]), Dv, c);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc += g[k];
+      }
       for (; i + 4 <= E; i += 4) {  // four rows in flight, added in order
         const Acc g0 = Row::load(grad, static_cast<size_t>(sp[i]), Dv, c);
         const Acc g1 = Row::load(grad, static_cast<size_t>(sp[i + 1]), Dv, c);
