@@ -191,8 +191,8 @@ int emb_grad_coalesce_by_owner(const int32_t *ids, int32_t T,
  * once per device, at the first call on it).
  * Returns EMB_ERR_WORKSPACE, before anything touches the device, when
  * emb_grad_coalesce_workspace_bytes(T, V, D, grad_dtype) exceeds
- * EMB_NOALLOC_SCRATCH_BYTES (e.g. more than about 180k tokens of 256 floats, or
- * 59k of 1024).  Every call on one device shares the array, which keeps the
+ * EMB_NOALLOC_SCRATCH_BYTES (e.g. more than about 380k tokens of 256 floats, or
+ * 182k of 1024).  Every call on one device shares the array, which keeps the
  * last call's contents (the call clears what must start at zero itself): calls
  * in order on one stream are safe; calls that can overlap on one device
  * (different streams, nothing ordering them) race on it.

@@ -607,7 +607,7 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
     const void* __restrict__ grad, int D, const uint32_t* __restrict__ tile_heads, KeySpec ks,
     int32_t* __restrict__ uniq_ids, int32_t* __restrict__ seg_offsets, int32_t* __restrict__ num_unique,
     float* __restrict__ uniq_grad, int32_t* __restrict__ owner_offsets, float* __restrict__ partial,
-    int32_t* __restrict__ span_list, int32_t* __restrict__ span_count, int nchunks) {
+    int32_t* __restrict__ span_list, int32_t* __restrict__ span_count, int max_spans) {
   __shared__ uint32_t wave_heads[kWaves];
   __shared__ uint32_t red[kWaves];
   __shared__ uint32_t wave_flags[kWaves];
@@ -779,7 +779,7 @@ __global__ __launch_bounds__(kThreads) void seg_reduce_kernel(
         if (colok) part_rows[(static_cast<size_t>(tile) * 2 + slot) * Dv + c] = acc;
         if (more && !from_before && cb == 0 && lane == 0) {
           const int k = atomicAdd(span_count, 1);  // at most one per workgroup
-          if (k < nchunks) span_list[k] = cur;
+          if (k < max_spans) span_list[k] = cur;
         }
       }
     }
@@ -794,12 +794,12 @@ __global__ __launch_bounds__(kCombineThreads) void seg_combine_kernel(const floa
                                                                float* __restrict__ uniq_grad,
                                                                const int32_t* __restrict__ owner_offsets,
                                                                int32_t* __restrict__ owner_counts, int P, int T,
-                                                               int nchunks) {
+                                                               int max_spans) {
   using Acc = typename GradRow<false, VEC>::Acc;
   __shared__ Acc red[kCombineWaves][kWave];
   if (owner_counts != nullptr && blockIdx.x == 0 && blockIdx.y == 0)
     for (int p = threadIdx.x; p < P; p += kCombineThreads) owner_counts[p] = owner_offsets[p + 1] - owner_offsets[p];
-  const int n = min(span_count[0], nchunks);
+  const int n = min(span_count[0], max_spans);
   const int Dv = D / VEC;
   const int w = threadIdx.x / kWave;
   const Acc* part_rows = reinterpret_cast<const Acc*>(partial);
@@ -1142,7 +1142,6 @@ CoalesceWs carve_with(void* base, int T, int D, int T_next, int64_t V) {
   const size_t ntiles = (n + C::kTile - 1) / C::kTile;
   const size_t nup = (n + C::kUpTile - 1) / C::kUpTile;
   const size_t nred = (n + kRedTile - 1) / kRedTile;
-  const size_t nchunks = (n + kChunk - 1) / kChunk;
   CoalesceWs w;
   w.keys_a = cv.take<uint32_t>(n);
   w.keys_b = cv.take<uint32_t>(n);
@@ -1154,9 +1153,9 @@ CoalesceWs carve_with(void* base, int T, int D, int T_next, int64_t V) {
   w.sort_lb = cv.take<uint32_t>(static_cast<size_t>(kHistPerTile) * ntiles);
   w.n_valid = cv.take<uint32_t>(1);
   w.starts = cv.take<uint32_t>(static_cast<size_t>(kMaxPasses) * Wide9::kBins);
-  w.span_list = cv.take<int32_t>(nchunks);
+  w.span_list = cv.take<int32_t>(nred);  // at most one crossing id starts in each reduction workgroup
   w.tile_heads = cv.take<uint32_t>(nred);
-  w.partial = cv.take<float>(nchunks * 2 * static_cast<size_t>(D));
+  w.partial = cv.take<float>(nred * 2 * static_cast<size_t>(D));
   w.next_tab = nullptr;
   w.tab_words = 0;
   w.tab_bytemap = false;
@@ -1342,11 +1341,10 @@ hipError_t launch_coalesce_reduce(const int32_t* ids, int T, const void* grad, b
   CoalesceWs ws = carve(workspace, T, D, -1, V);  // the next-id set, if any, lies past everything used here
   const RadixPlan plan = plan_for_call(V, var);
   const int nred = (T + kRedTile - 1) / kRedTile;
-  const int nchunks = (T + kChunk - 1) / kChunk;
   const uint32_t* kin = nullptr;
   const int32_t* vin = nullptr;
   sorted_arrays(ws, plan, &kin, &vin);
-  // 5. segments and per-chunk sums; 6. pieces of ids that cross chunks
+  // 5. segments and their sums; 6. ids that cross reduction workgroups
   const bool vec4 = (D % 4 == 0) && (reinterpret_cast<uintptr_t>(grad) % (grad_bf16 ? 8 : 16) == 0) &&
                     (reinterpret_cast<uintptr_t>(uniq_grad) % 16 == 0);
   const dim3 cgrid(grid_for(nred, 256), grid_for((D / (vec4 ? 4 : 1) + kWave - 1) / kWave, 8));
@@ -1354,12 +1352,12 @@ hipError_t launch_coalesce_reduce(const int32_t* ids, int T, const void* grad, b
   hipLaunchKernelGGL((seg_reduce_kernel<BF, VC>), dim3(nred, reduce_col_split(nred, D / (VC))), dim3(kThreads), 0,   \
                      stream, kin, vin, ws.n_valid, T,                                                                \
                      grad, D, ws.tile_heads, ks, uniq_ids, seg_offsets, num_unique, uniq_grad, group_offsets,        \
-                     ws.partial, ws.span_list, ws.span_count, nchunks)
+                     ws.partial, ws.span_list, ws.span_count, nred)
 #define EMB_COMBINE(VC)                                                                                             \
   hipExtLaunchKernelGGL(seg_combine_kernel<VC>, cgrid, dim3(kCombineThreads), 0, stream, nullptr, done, 0,         \
                         ws.partial, D,                                                                               \
                         seg_offsets, ws.span_list, ws.span_count, uniq_grad, group_offsets, group_counts, ks.G, T,  \
-                        nchunks)
+                        nred)
   if (vec4) {
     if (grad_bf16)
       EMB_REDUCE(true, 4);
