@@ -17,6 +17,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import platform
 import sys
@@ -30,6 +31,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
 TUNE_FINALISTS = 3  # schedule candidates timed a second time
+TUNE_TRIAL_MS = 15.0  # the shortest trial of a schedule candidate
 
 
 def log(*a):
@@ -145,15 +147,16 @@ def _find(directory, suffix):
     raise FileNotFoundError(f"no *{suffix} under {directory}")
 
 
-def summarize_trace(directory, command, skip=20, steps=200, every=20):
+def summarize_trace(directory, command, skip=20, steps=200, every=20, tables=1):
     """Text summary of a rocprofv3 --kernel-trace --stats run (kernel_stats.csv), plus the
-    average duration of the update kernel over the steps of the bench run's roofline window (its
-    dispatches skip+1 .. skip+steps in launch order, from kernel_trace.csv; skip counts the
-    steps before them: the order tuning, the warm-up and the timed steps), every `every`-th of
-    which the bench times with events."""
+    average duration of the first table's update kernel over the steps of the bench run's roofline
+    window (steps skip+1 .. skip+steps in launch order, one update dispatch per table each, from
+    kernel_trace.csv; skip counts the steps before them: the order tuning, the warm-up and the
+    timed steps), every `every`-th of which the bench times with events."""
     trace = [r for r in _read_csv(_find(directory, "kernel_trace.csv")) if ADAM_KERNEL in r["Kernel_Name"]]
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
-    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in trace[skip:skip + steps]]
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            for r in trace[skip * tables:(skip + steps) * tables:tables]]
     sampled = durs[::every]  # the launches the bench times with events (every `every`-th timed step)
     rows = _read_csv(_find(directory, "kernel_stats.csv"))
     out = [f"command: {command}", "", f"{'kernel':64s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} "
@@ -612,24 +615,27 @@ class WorkloadRun:
         if len(cands) == 1:
             return cands[0], tune_ms
 
-        def trial_ms(c):
+        def trial_ms(c, n):
             trial = self.make_pipe(c)
-            for k in range(5 + tune_steps):
+            for k in range(5 + n):
                 if k == 5:
                     self.settle(trial)
                     t_start = time.perf_counter()
                 self.step(trial)
             self.settle(trial)
-            ms = (time.perf_counter() - t_start) * 1e3 / tune_steps
+            ms = (time.perf_counter() - t_start) * 1e3 / n
             del trial
             return ms
 
+        # each trial runs for at least TUNE_TRIAL_MS, so that host jitter does not pick the schedule
+        # of a short-stepped workload (a 30-step trial of 50 us steps lasts 1.5 ms)
+        tune_steps = max(tune_steps, math.ceil(TUNE_TRIAL_MS / trial_ms(cands[0], tune_steps)))
         for c in cands:
-            tune_ms[cand_name(c)] = trial_ms(c)
+            tune_ms[cand_name(c)] = trial_ms(c, tune_steps)
         order = sorted(range(len(cands)), key=lambda i: tune_ms[cand_name(cands[i])])
         for i in reversed(order[:TUNE_FINALISTS]):
             name = cand_name(cands[i])
-            tune_ms[name] = min(tune_ms[name], trial_ms(cands[i]))
+            tune_ms[name] = min(tune_ms[name], trial_ms(cands[i], tune_steps))
         best = min(range(len(cands)), key=lambda i: tune_ms[cand_name(cands[i])])
         return cands[best], tune_ms
 
@@ -746,6 +752,7 @@ def pipelined_report(run, args, K):
         run.step(pipe)
     run.settle(pipe)
     r = run.timed(pipe, K, 0)
+    steps_before_window = run.t  # every step enqueued so far on this workload: tuning, warm-up, timed
     w = run.timed(pipe, args.roofline_steps, args.roofline_every)
     ms_step = r["ms_total"] / K
     bytes_step = run.step_bytes(r["used"])
@@ -757,7 +764,8 @@ def pipelined_report(run, args, K):
                 rows=r["rows"], used=r["used"], bytes_step=bytes_step, total_bytes=total,
                 step_gbps=total / (ms_step * 1e-3) / 1e9, adam_us=adam_us, adam_us_all=w["adam_us"],
                 adam_bytes=adam_bytes, adam_gbps=adam_bytes / (adam_us * 1e-6) / 1e9,
-                window_ms_step=w["ms_total"] / args.roofline_steps, host_enqueue_ms=r["host_enqueue_ms"])
+                window_ms_step=w["ms_total"] / args.roofline_steps, host_enqueue_ms=r["host_enqueue_ms"],
+                steps_before_window=steps_before_window)
 
 
 def config_report(torch, emb, name, args, K, run=None, pl=None):
@@ -832,14 +840,24 @@ def main():
                     help="print the scaled HBM traffic of every kernel from two rocprofv3 --pmc runs")
     ap.add_argument("--summarize-counters", nargs="+", metavar="DIR",
                     help="print per-kernel occupancy, VALU, LDS and L2 figures from rocprofv3 --pmc runs")
+    ap.add_argument("--bench-line", metavar="JSON", default="",
+                    help="with --summarize-trace: the traced run's bench line, for the number of steps before "
+                         "its roofline window (else counted from the options, with trials of --tune-steps)")
     ap.add_argument("--command", default="", help="the command recorded in a summary")
     ap.add_argument("--command2", default="", help="the second command recorded in a summary")
     args = ap.parse_args()
     if args.summarize_trace:
-        n = len(schedule_candidates(args))
-        tuned = (n + min(n, TUNE_FINALISTS)) * (5 + args.tune_steps) if n > 1 else 0
-        print(summarize_trace(args.summarize_trace, args.command, tuned + args.warmup + args.steps,
-                              args.roofline_steps, args.roofline_every), end="")
+        from workloads import configs
+        tables = len(configs.WORKLOADS[args.workload].tables)
+        if args.bench_line:  # the traced run's own count of the steps before its roofline window
+            with open(args.bench_line) as f:
+                skip = json.loads(f.read().strip().splitlines()[-1])["roofline"]["steps_before_window"]
+        else:
+            n = len(schedule_candidates(args))
+            tuned = (n + 1 + min(n, TUNE_FINALISTS)) * (5 + args.tune_steps) if n > 1 else 0
+            skip = tuned + args.warmup + args.steps
+        print(summarize_trace(args.summarize_trace, args.command, skip, args.roofline_steps, args.roofline_every,
+                              tables), end="")
         return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc, args.command, args.command2), indent=1))
@@ -943,7 +961,8 @@ def main():
                      "launch_us_spread": spread(pl["adam_us_all"]),
                      "window": f"{args.roofline_steps} steps after the timed ones, same schedule, the update "
                                f"timed on every {args.roofline_every}th",
-                     "window_ms_per_step": pl["window_ms_step"]},
+                     "window_ms_per_step": pl["window_ms_step"],
+                     "steps_before_window": pl["steps_before_window"]},
         "gradient_sizes_table3": table3,
         "host": host_info(),
     }
