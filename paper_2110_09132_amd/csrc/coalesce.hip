@@ -102,9 +102,10 @@ static_assert(Narrow::kUpTile == Wide9::kUpTile && Narrow::kUpTile == NarrowBig:
 constexpr int kChunk = 32;                    // sorted tokens per reduction wave
 constexpr int kRedTile = kChunk * kWaves;     // sorted tokens per reduction workgroup
 constexpr int kLoadsInFlight = 8;
-// The combine of ids that cross chunks: one workgroup per such id, its waves
-// splitting the id's chunk pieces; wide, so that a hot id's hundreds of pieces
-// are summed by many waves at once.
+// The combine of ids that cross reduction workgroups: one workgroup per such
+// id, its waves splitting the id's pieces (one per reduction workgroup it
+// touches); wide, so that a hot id's many pieces are summed by many waves at
+// once.
 constexpr int kCombineThreads = 1024;
 constexpr int kCombineWaves = kCombineThreads / kWave;
 constexpr uint32_t kSpinLimit = 1u << 22;
