@@ -118,14 +118,19 @@ def test_coalesce_hot_row_spans_many_chunks():
     check_coalesce(ids, G, V)
 
 
-@pytest.mark.parametrize("seed,n_runs,bad_frac", [(1, 300, 0.0), (2, 300, 0.0), (3, 250, 0.01), (4, 40, 0.0)])
-def test_coalesce_runs_around_chunk_and_workgroup_boundaries(seed, n_runs, bad_frac):
+@pytest.mark.parametrize("seed,n_runs,bad_frac,D,bf16", [(1, 300, 0.0, 64, False), (2, 300, 0.0, 64, False),
+                                                         (3, 250, 0.01, 64, False), (4, 40, 0.0, 64, False),
+                                                         (5, 80, 0.0, 1024, False), (6, 120, 0.0, 256, True),
+                                                         (7, 480, 0.0, 129, False), (8, 320, 0.0, 1024, False)])
+def test_coalesce_runs_around_chunk_and_workgroup_boundaries(seed, n_runs, bad_frac, D, bf16):
     # ids that cross chunk boundaries inside a reduction workgroup are summed there, ids that
-    # cross workgroups in pieces: every placement of a run's ends against both boundaries
+    # cross workgroups in pieces: every placement of a run's ends against both boundaries (with
+    # rows of 1024 floats the columns are split over several workgroups per token range; the last
+    # two cases leave each workgroup two column blocks in turn, scalar and float4)
     V = 1 << 16
     ids = runs_ids(seed, n_runs, V, bad_frac)
-    G = grads_for(seed + 10, ids.size, 64)
-    check_coalesce(ids, G, V)
+    G = grads_for(seed + 10, ids.size, D, 0.01, bf16=bf16)
+    check_coalesce(ids, G, V, bf16=bf16)
 
 
 def test_coalesce_all_one_id():
