@@ -264,3 +264,62 @@ def test_bench_refuses_more_than_one_gpu():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def _step_structs():
+    """A schedule and arguments that pass every host check up to the first HIP call (pointers never
+    dereferenced: each case below is refused before that)."""
+    a = emb.StepArgs(V=1000, D=8, P=2, T=100, cap_rows=100, grad_dtype=emb.EMB_F32, lr=1e-3, beta1=0.9,
+                     beta2=0.999, eps=1e-8, step=1)
+    s = emb.StepSchedule(lookup_update=1, coalesce=2, pack=3, delayed=1, sorted=4096, coalesced=4096, packed=4096,
+                         updated=4096, by_owner=1, sets=2)
+    return a, s
+
+
+def test_train_step_validation():
+    L = emb.lib
+    a, s = _step_structs()
+    assert L.emb_train_step(None, ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    a.T = 101  # more tokens than the buffers hold
+    assert L.emb_train_step(ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    a, s = _step_structs()
+    s.updated = None  # events without the update's end event
+    assert L.emb_train_step(ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    a, s = _step_structs()
+    s.by_owner, s.split = 0, 1  # the split is owner-major
+    assert L.emb_train_step(ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    a, s = _step_structs()
+    s.sets = 65
+    assert L.emb_train_step(ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+
+
+def test_train_step_queued_validation():
+    # refusals of the two-thread enqueue, all before any HIP call; the queue itself needs no GPU
+    L = emb.lib
+    q = emb.StepQueue()
+    a, s = _step_structs()
+    assert L.emb_train_step_queued(None, ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    for field, value in (("signals", 4096), ("by_owner", 0), ("split", 1)):
+        a, s = _step_structs()
+        setattr(s, field, value)
+        assert L.emb_train_step_queued(q.handle, ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_UNSUPPORTED, field
+    a, s = _step_structs()
+    s.coalesce = s.lookup_update  # the sort on the stream the worker feeds
+    assert L.emb_train_step_queued(q.handle, ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_UNSUPPORTED
+    a, s = _step_structs()
+    s.pack = s.lookup_update
+    assert L.emb_train_step_queued(q.handle, ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_UNSUPPORTED
+    a, s = _step_structs()
+    a.T = 101
+    assert L.emb_train_step_queued(q.handle, ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    a, s = _step_structs()
+    s.sorted = None
+    assert L.emb_train_step_queued(q.handle, ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    a, s = _step_structs()
+    s.sets = 65
+    assert L.emb_train_step_queued(q.handle, ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    a, s = _step_structs()  # the owner-major call's own argument checks (no ids)
+    assert L.emb_train_step_queued(q.handle, ctypes.byref(a), ctypes.byref(s)) == emb.EMB_ERR_INVALID_ARG
+    q.flush()  # nothing was handed to the worker
+    assert L.emb_step_queue_flush(None) == emb.EMB_ERR_INVALID_ARG
+    del q
