@@ -75,6 +75,39 @@ def test_noalloc_equals_workspace_call():
                                       b.view(np.uint32) if b.dtype == np.float32 else b)
 
 
+def largest_batch(V, D):
+    """The most tokens whose workspace fits the static array (bisection on the library's query)."""
+    lo, hi = 1, 1 << 24
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        if emb.lib.emb_grad_coalesce_workspace_bytes(mid, V, D, emb.EMB_F32) <= emb.NOALLOC_SCRATCH_BYTES:
+            lo = mid
+        else:
+            hi = mid - 1
+    return lo
+
+
+def test_noalloc_at_its_largest_batch():
+    # the largest batch of 256-float rows the array holds, against the workspace call; one token more
+    # is refused on the host
+    V, D, P = 1 << 20, 256, 16
+    T = largest_batch(V, D)
+    print(f"noalloc largest batch T={T} D={D}", flush=True)
+    assert T > 65536
+    ids = torch.from_numpy(gen.uniform_ids(gen.stream_key(T, 1, gen.PURPOSE_IDS), T, V)).cuda()
+    G = torch.from_numpy(gen.normal_f32(gen.stream_key(T, 1, gen.PURPOSE_GRADS), T * D, 0.01).reshape(T, D)).cuda()
+    own = torch.from_numpy(gen.owner_mod(V, P)).cuda()
+    U0, want = call(ids, G, V, own, P, noalloc=False)
+    U1, got = call(ids, G, V, own, P, noalloc=True)
+    assert U1 == U0 and U1 > 0
+    for a, b in zip(got, want):
+        assert np.array_equal(a.view(np.uint32) if a.dtype == np.float32 else a,
+                              b.view(np.uint32) if b.dtype == np.float32 else b)
+    fake = ctypes.c_void_p(256)
+    assert emb.lib.emb_grad_coalesce_by_owner_noalloc(fake, T + 1, fake, emb.EMB_F32, D, V, fake, P, fake, fake,
+                                                      fake, fake, fake, fake, None, None) == emb.EMB_ERR_WORKSPACE
+
+
 def test_noalloc_rejects_sizes_beyond_its_array():
     # 65536 tokens of 4096 floats need more than the 16 MiB array: refused on the host, nothing launched
     T, D, V, P = 65536, 4096, 1 << 20, 16
