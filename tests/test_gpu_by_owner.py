@@ -93,6 +93,7 @@ def check_by_owner(ids_np, grad_np, V, own_np, P, bf16=False, grad_dev=None):
     ("zipf", 1 << 16, 40001, 8, 4, "range"),        # 16 + 2 = 18 key bits: two 9-bit passes
     ("uniform", 1 << 20, 33000, 8, 64, "rand"),     # 20 + 6 = 26 key bits: three 9-bit passes
     ("uniform", (1 << 22) - 1, 50000, 4, 1024, "rand"),  # 32 key bits: four 8-bit passes
+    ("uniform", 1 << 20, 1 << 21, 4, 16, "mod"),   # two million tokens: 1366 sort tiles, 16384 reduction workgroups
     # the one-workgroup path (at most 2048 tokens): the most owners, 32 key bits, a device-side count
     ("uniform", 50000, 2048, 20, 1024, "rand"),
     ("uniform", (1 << 22) - 1, 1500, 4, 1024, "rand"),

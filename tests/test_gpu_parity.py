@@ -94,6 +94,9 @@ def test_gather_empty():
     # more than 1024 reduction workgroups: the head counts are scanned once by their own kernel
     ("zipf", 1 << 20, 200000, 8),
     ("uniform", 1 << 18, 131073, 4),
+    # two million tokens: 1366 sort tiles to look back over, 16384 reduction workgroups
+    ("uniform", 1 << 22, 1 << 21, 4),
+    ("zipf", 1 << 20, (1 << 21) + 77, 4),
 ])
 def test_coalesce_parity_fp32(law, V, T, D):
     ids = ids_for(law, V + T + D, T, V)
